@@ -1,0 +1,271 @@
+/*
+ * via.h — C ABI of the VIA-SD verification step on gfx950 (MI355X).
+ *
+ * The verification step of "VIA-SD: Verification via Intra-Model Routing
+ * for Speculative Decoding" (arXiv 2606.12243): one batched forward of a
+ * decoder-only verifier over a k-token draft window against its KV cache,
+ * run as the full verifier q or as the slim-verifier q' = Pi_z(q) (the layers
+ * the routing mask z retains, sharing q's weights, embedding and head;
+ * Sec. 3.3 and Sec. 3.2), then a per-position confidence and a three-tier
+ * decision (accept / slim rewrite / escalate to q; regions B.1-B.3 of
+ * App. B.2), the gate walk and longest accepted prefix (Alg. 1, App. B.1,
+ * Sec. 3.4 Steps 3-4), and the KV commit/rollback of the accepted positions.
+ *
+ * Conventions
+ *  - Every pointer documented "device" is caller-owned device memory that
+ *    must outlive the handle using it; the library never allocates or frees
+ *    device memory.  "host" pointers are read (or written) before the call
+ *    returns unless stated otherwise; "pinned host" pointers are written by
+ *    an asynchronous copy and are valid once the caller has synchronised the
+ *    stream.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Calls enqueue work and return; the library never synchronises.
+ *  - Handles are single-stream and not thread-safe.
+ *  - Every argument is validated before any work is enqueued.  A non-OK
+ *    return leaves model and KV state unchanged; via_last_error() gives a
+ *    thread-local message.
+ *  - Token ids are int32 in [0, vocab).  Weights are row-major
+ *    [out_features, in_features] in the model dtype (fp32 or bf16).
+ */
+#ifndef VIA_H
+#define VIA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t via_status;
+#define VIA_OK 0
+#define VIA_EINVAL (-1)       /* bad argument: null pointer, size, id, ordering */
+#define VIA_ENOMEM (-2)       /* KV block pool (or workspace sizing) exhausted */
+#define VIA_EDEVICE (-3)      /* a HIP call failed; sticky for the handle */
+#define VIA_ESTATE (-4)       /* call out of order or inconsistent with KV state */
+#define VIA_EUNSUPPORTED (-5) /* shape/dtype this build does not run */
+
+#define VIA_DTYPE_F32 0
+#define VIA_DTYPE_BF16 1
+
+#define VIA_CACHE_FULL 0
+#define VIA_CACHE_SLIM 1
+
+#define VIA_TIER_ACCEPT 0 /* region A: c >= tau_acc */
+#define VIA_TIER_SLIM 1   /* region B: tau_full <= c < tau_acc */
+#define VIA_TIER_FULL 2   /* region C: c < tau_full (also a non-finite c) */
+
+#define VIA_FORCED_NONE (-1)
+#define VIA_FORCED_ACCEPT 0
+#define VIA_FORCED_SLIM 1
+#define VIA_FORCED_FULL 2
+
+/* Largest draft block / tree (rows with a tree mask, drafts per window). */
+#define VIA_MAX_TREE_ROWS 64
+#define VIA_MAX_DRAFTS 64
+#define VIA_MAX_CHILDREN 8
+
+typedef struct via_model via_model; /* opaque, library-owned host object */
+typedef struct via_kv via_kv;       /* opaque, library-owned host object */
+
+/* Verifier architecture.  Supported: head_dim 64 or 128, n_heads a multiple
+ * of n_kv_heads, d_model and d_ffn multiples of 64, vocab >= 1.  The layer
+ * is RMSNorm -> QKV -> rotate-half RoPE (rope_theta) -> GQA attention -> O,
+ * RMSNorm -> SwiGLU FFN, each with a residual add; a final RMSNorm precedes
+ * the untied output head. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  float rms_eps, rope_theta;
+  int32_t dtype; /* VIA_DTYPE_F32 or VIA_DTYPE_BF16 */
+} via_model_desc;
+
+/* Weight pointers (device, caller-owned, model dtype).  Per-layer entries
+ * are HOST arrays of n_layers device pointers, copied at via_model_create.
+ *   embed     [vocab, d]          lm_head [vocab, d]      final_norm [d]
+ *   attn_norm [d]                 ffn_norm [d]
+ *   w_qkv     [(H + 2 KVH) hd, d]  rows: Q heads, then K heads, then V heads
+ *   w_o       [d, H hd]
+ *   w_gate_up [2 F, d]            rows: gate (F), then up (F)
+ *   w_down    [d, F]
+ * The slim-verifier reads the same pointers for its retained layers: no
+ * weight is copied (Sec. 3.3). */
+typedef struct {
+  const void *embed, *lm_head, *final_norm;
+  const void *const *attn_norm, *const *w_qkv, *const *w_o;
+  const void *const *ffn_norm, *const *w_gate_up, *const *w_down;
+} via_weights;
+
+/* Tier parameters.  Confidence of draft d verified by row r is the ratio
+ * c = q'_r(d) / max_u q'_r(u) = exp((l'_r(d) - max_u l'_r(u)) / T)
+ * (App. B.2 gates q'(v) against fractions of M' = max_u q'(u));
+ * tau_acc and tau_full stand for 1 - alpha_1 and 1 - alpha_2.
+ * Requires 0 <= tau_full <= tau_acc (tau_acc may exceed 1) and T > 0. */
+typedef struct {
+  float tau_acc, tau_full, temperature;
+  int32_t forced; /* VIA_FORCED_*: every tier forced (tests, baselines) */
+} via_tier_params;
+
+/* KV handle description.  Two paged caches: the full verifier's (n_layers
+ * layer slots) and the slim-verifier's (one slot per retained layer, in
+ * route order).  Pool layout, element type = model dtype, block_size = 16:
+ *   pool[slot][block][K|V][kv_head][...]
+ *   K page: [16 tokens][head_dim]         (token-major)
+ *   V page: [head_dim][16 tokens]         (transposed)
+ * Cache slot p of a sequence lives in block table[p / 16], row p % 16.
+ * Sizes: via_pool_bytes() and via_workspace_bytes(). */
+typedef struct {
+  int32_t block_size;         /* must be 16 */
+  int32_t max_seqs;           /* sequence ids are in [0, max_seqs) */
+  int32_t max_blocks_per_seq; /* block-table capacity per sequence */
+  int32_t blocks_full, blocks_slim;
+  void *pool_full, *pool_slim; /* device */
+  int32_t max_rows;   /* rows per forward (lag + window, summed over batch) */
+  int32_t max_batch;  /* sequences per window */
+  int32_t max_drafts; /* drafts per sequence per window, 1..VIA_MAX_DRAFTS */
+  void *workspace;    /* device, >= via_workspace_bytes(...) */
+  size_t workspace_bytes;
+  void *pinned_staging; /* pinned host, >= via_staging_bytes(...) */
+  size_t staging_bytes;
+} via_kv_desc;
+
+/* One draft window for a batch of sequences (HOST arrays, copied).
+ * Row 0 of each sequence is its pending token x[n-1] (the last committed
+ * token, whose K/V are not cached yet).  Chain: rows are
+ * [x[n-1], d_0 .. d_{k-2}] and draft j is verified by row j (App. B.1 runs q'
+ * on the prefixes x_<t .. x_<t+gamma-1).  Tree: rows are the root and every
+ * draft node that has children, in node order; draft j is verified by its
+ * parent's row.
+ *   row_depth NULL: row r sits at RoPE position n-1+r.  Else n-1+row_depth[r].
+ *   row_mask  NULL: causal over the window.  Else bit r' of row_mask[r] set
+ *             iff row r attends row r' (ancestors and itself; r' <= r; at
+ *             most VIA_MAX_TREE_ROWS rows).
+ *   draft_parent NULL: chain (parent of draft j is j-1).  Else parent draft
+ *             index (< j) or -1 for children of the root; at most
+ *             VIA_MAX_CHILDREN children per node.
+ *   n_lag / lag_tok: committed tokens the full cache is missing
+ *             (x[valid_full .. n-2]); required by via_verify_full when the
+ *             full cache lags, ignored by via_verify_slim.
+ * Strides: 1 <= max_drafts <= the KV handle's max_drafts. */
+typedef struct {
+  int32_t batch, max_rows, max_drafts, max_lag; /* strides */
+  const int32_t *seq_id;       /* [batch] distinct, attached */
+  const int32_t *n_rows;       /* [batch] >= 1 */
+  const int32_t *row_tok;      /* [batch * max_rows] */
+  const int32_t *row_depth;    /* [batch * max_rows] or NULL */
+  const uint64_t *row_mask;    /* [batch * max_rows] or NULL */
+  const int32_t *n_drafts;     /* [batch] */
+  const int32_t *draft_tok;    /* [batch * max_drafts] */
+  const int32_t *draft_row;    /* [batch * max_drafts] */
+  const int32_t *draft_parent; /* [batch * max_drafts] or NULL */
+  const int32_t *n_lag;        /* [batch] or NULL (no lag rows) */
+  const int32_t *lag_tok;      /* [batch * max_lag] */
+} via_window;
+
+/* Per-row statistics of one forward (device arrays written by the call).
+ * Indexed by b * window.max_rows + r (window rows; lag rows produce none)
+ * and b * window.max_drafts + j. */
+typedef struct {
+  int32_t *row_argmax; /* lowest token id among the maxima */
+  float *row_max;      /* max_u l(u) */
+  float *row_sumexp;   /* sum_u exp((l(u) - max) / T) */
+  float *row_gap;      /* max minus the largest other logit (0 on ties); nullable */
+  float *draft_logit;  /* l_{draft_row[j]}(draft_tok[j]) */
+  float *logits;       /* nullable fp32 [batch * max_rows * vocab] (debug/parity) */
+} via_verify_out;
+
+/* Decision of one window.  `packed` (device) and `h_packed` (pinned host)
+ * hold, for B = window.batch and D = window.max_drafts:
+ *   [0, B)        status  0 resolved, 1 needs the full verifier,
+ *                         2 non-finite full logits (sequence not advanced)
+ *   [B, 2B)       kappa   accepted draft count
+ *   [2B, 3B)      emit    token appended after the accepted drafts, -1 none
+ *   [3B, 4B)      new_len committed length n' = n + kappa + (emit >= 0)
+ *   [4B, 4B+B*D)  path    accepted draft indices in order (kappa entries)
+ * `tier` and `conf` (device [B * D]) give every draft's tier (VIA_TIER_*)
+ * and ratio confidence. */
+typedef struct {
+  int8_t *tier;
+  float *conf;
+  int32_t *packed;
+  int32_t *h_packed;
+} via_decision;
+
+/* ---- sizes -------------------------------------------------------------- */
+size_t via_pool_bytes(const via_model_desc *desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size);
+size_t via_workspace_bytes(const via_model_desc *desc, int32_t max_rows, int32_t max_batch,
+                           int32_t max_blocks_per_seq, int32_t max_drafts);
+size_t via_staging_bytes(const via_model_desc *desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
+                         int32_t max_drafts);
+
+/* ---- model -------------------------------------------------------------- */
+/* Validates the shapes and copies the pointer tables.  The slim route
+ * defaults to all layers. */
+via_status via_model_create(const via_model_desc *desc, const via_weights *w, via_model **out);
+/* Routing mask z as the sorted list of retained layer ids (Sec. 3.3);
+ * 1 <= n <= n_layers.  Must be set before via_kv_create. */
+via_status via_model_set_route(via_model *m, const int32_t *layers, int32_t n);
+via_status via_model_destroy(via_model *m);
+
+/* ---- KV handle and sequences ------------------------------------------- */
+via_status via_kv_create(via_model *m, const via_kv_desc *desc, via_kv **out);
+via_status via_kv_destroy(via_kv *kv);
+/* Attach sequence `seq_id` with n_ctx already-cached positions in both
+ * caches (blocks allocated, lowest ids first, full cache then slim cache;
+ * contents are whatever the caller writes at those slots). */
+via_status via_kv_seq_reserve(via_kv *kv, int32_t seq_id, int32_t n_ctx);
+/* Attach `seq_id` and cache tokens[0..n) in both caches (full forward and
+ * slim forward, causal; RoPE positions 0..n-1). */
+via_status via_prefill(via_model *m, via_kv *kv, int32_t seq_id, const int32_t *tokens, int32_t n,
+                       void *stream);
+/* Detach a sequence and free its blocks.  Not during a step. */
+via_status via_kv_seq_release(via_kv *kv, int32_t seq_id);
+/* Valid lengths and block table of one cache (host outputs; table may be
+ * NULL).  *n_blocks receives the table length. */
+via_status via_kv_seq_info(const via_kv *kv, int32_t seq_id, int32_t cache, int32_t *valid,
+                           int32_t *table, int32_t cap, int32_t *n_blocks);
+
+/* ---- the verification step ---------------------------------------------
+ * Order per step: via_verify_slim -> via_tier_decide(full = NULL) ->
+ * [synchronise; if any status == 1: via_verify_full (those sequences) ->
+ * via_tier_decide(full)] -> synchronise -> via_kv_commit_rollback. */
+
+/* Slim-verifier forward (route of via_model_set_route, slim cache) over the
+ * window rows, then the fused head: per-row max/argmax/sum-exp and the
+ * logit of every draft token.  Allocates cache blocks for the rows (ENOMEM
+ * leaves state unchanged) and starts a step.  ESTATE if a step is open. */
+via_status via_verify_slim(via_model *m, via_kv *kv, const via_window *win, const via_tier_params *p,
+                           via_verify_out *out, void *stream);
+/* Full-verifier forward (all layers, full cache) for the sequences with
+ * run[b] != 0 (host [batch]; NULL = all), over lag rows + window rows.
+ * win must be the window of the open step; n_lag[b] must equal the full
+ * cache's lag for each run sequence (ESTATE otherwise). */
+via_status via_verify_full(via_model *m, via_kv *kv, const via_window *win, const int32_t *run,
+                           const via_tier_params *p, via_verify_out *out, void *stream);
+/* Forward of either verifier (cache = VIA_CACHE_*) that leaves the logical
+ * KV state untouched: rows are written past the valid length and any block
+ * it needs is returned to the pool on exit.  For drafters and probes. */
+via_status via_verify_probe(via_model *m, via_kv *kv, int32_t cache, const via_window *win,
+                            const via_tier_params *p, via_verify_out *out, void *stream);
+/* Confidence, tier, gate walk of the open step (App. B.1).  With full ==
+ * NULL, sequences whose walk reaches an escalated position get status 1.
+ * With full, sequences that ran the full forward are resolved.  Writes the
+ * decision and copies `packed` to `h_packed`. */
+via_status via_tier_decide(via_kv *kv, const via_tier_params *p, const via_verify_out *slim,
+                           const via_verify_out *full, via_decision *dec, void *stream);
+/* Commit the open step from dec->h_packed (read on the host: synchronise
+ * first).  Appends kappa drafts (+ emit) per sequence: slim valid length
+ * becomes n'-1; full valid length becomes n'-1 if the full verifier ran
+ * for that sequence this step, else it keeps lagging; blocks wholly past a
+ * valid length are freed; tree steps move the accepted nodes' K/V to
+ * contiguous slots (kernel on `stream`).  All-or-nothing: ESTATE (nothing
+ * changed) if any status is 1 or no step is open. */
+via_status via_kv_commit_rollback(via_kv *kv, const via_decision *dec, void *stream);
+
+const char *via_last_error(void);
+/* Library version string. */
+const char *via_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VIA_H */

@@ -297,15 +297,17 @@ class Verifier:
             conf = [confidence(float(lg[draft_row[j], d.tok[j]]), stt["max"][draft_row[j]], T)
                     for j in range(len(d.tok))]
             tiers = [tier_of(c, p) for c in conf]
-            dec[b] = dict(conf=conf, tiers=tiers, slim_stats=stt, draft_row=draft_row,
+            dec[b] = dict(conf=conf, tiers=tiers, slim_stats=stt, draft_row=draft_row, slim_logits=lg,
                           slim_draft_logit=[float(lg[draft_row[j], d.tok[j]]) for j in range(len(d.tok))])
             dec[b].update(self._walk(d, tiers, conf, stt, None))
+            dec[b]["first_status"] = dec[b]["status"]
         full = {}
         for b in order:                               # escalation to q
             if dec[b]["needs_full"]:
                 lg = self._full_forward(b, drafts[b])
                 full[b] = (lg, row_stats(lg, 1.0))
                 dec[b]["full_stats"] = full[b][1]
+                dec[b]["full_logits"] = lg
                 d = drafts[b]
                 dec[b]["full_draft_logit"] = [float(lg[dec[b]["draft_row"][j], d.tok[j]])
                                               for j in range(len(d.tok))]

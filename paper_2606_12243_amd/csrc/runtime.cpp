@@ -1,0 +1,1069 @@
+// Host runtime of the C ABI (include/via.h): handles, argument validation,
+// the paged block allocator, per-call row plans and kernel sequencing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "../../include/via.h"
+#include "kernels.h"
+
+using namespace via;
+
+namespace {
+
+thread_local std::string g_err;
+
+via_status fail(via_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+constexpr size_t kAlign = 256;
+constexpr int kRing = 4;
+constexpr int kCounters = 1 << 16;
+
+size_t al(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int esize_of(const via_model_desc* d) { return d->dtype == VIA_DTYPE_BF16 ? 2 : 4; }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Split-K policy: enough work-groups to cover the chip several times, at
+// least two 64-wide K steps per wave.  Depends only on the GEMM shape.
+int choose_ksplit(int ntiles, int K) {
+  int ksteps = K / 64;
+  int cap = std::max(1, ksteps / 8);
+  int ks = ceil_div(1024, ntiles);
+  return std::max(1, std::min(ks, cap));
+}
+
+struct GemmShape {
+  int ntiles, K, ks;
+};
+
+struct Dims {
+  int L, d, H, KVH, hd, F, V, qkv, G;
+  GemmShape g_qkv, g_o, g_gu, g_down, g_lm;
+};
+
+Dims dims_of(const via_model_desc* d) {
+  Dims r;
+  r.L = d->n_layers;
+  r.d = d->d_model;
+  r.H = d->n_heads;
+  r.KVH = d->n_kv_heads;
+  r.hd = d->head_dim;
+  r.F = d->d_ffn;
+  r.V = d->vocab;
+  r.qkv = (r.H + 2 * r.KVH) * r.hd;
+  r.G = r.H / std::max(1, r.KVH);
+  r.g_qkv = {r.qkv / 64, r.d, choose_ksplit(r.qkv / 64, r.d)};
+  r.g_o = {r.d / 64, r.H * r.hd, choose_ksplit(r.d / 64, r.H * r.hd)};
+  r.g_gu = {r.F / 32, r.d, choose_ksplit(r.F / 32, r.d)};
+  r.g_down = {r.d / 64, r.F, choose_ksplit(r.d / 64, r.F)};
+  r.g_lm = {ceil_div(r.V, 64), r.d, 1};
+  return r;
+}
+
+struct Layout {
+  size_t X, Y, Q, A, Hb, Yl, part, counters, att_o, att_ml, lm_part;
+  size_t rows, seqs, btab, items, lm;  // plan region
+  size_t step_seqs, dtok, drow, dpar;  // step region
+  size_t c_btab, c_moves;              // commit region
+  size_t plan_bytes, step_bytes, commit_bytes;
+  size_t total;
+  int max_chunks, max_items;
+};
+
+Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int max_blocks, int max_drafts) {
+  Dims D = dims_of(desc);
+  const size_t es = esize_of(desc);
+  Layout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t r = o;
+    o += al(bytes);
+    return r;
+  };
+  const size_t R = max_rows;
+  L.X = take(R * D.d * 4);
+  L.Y = take(R * D.d * es);
+  L.Q = take(R * D.H * D.hd * es);
+  L.A = take(R * D.H * D.hd * es);
+  L.Hb = take(R * D.F * es);
+  L.Yl = take(R * D.d * es);
+  size_t part = 0;
+  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down})
+    part = std::max(part, (size_t)g.ks * R * g.ntiles * 64 * 4);
+  L.part = take(part);
+  L.counters = take((size_t)kCounters * 4);
+  L.max_chunks = ceil_div(max_blocks * kBlock, kAttnChunk);
+  L.att_o = take((size_t)L.max_chunks * R * D.H * D.hd * 4);
+  L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
+  L.lm_part = take((size_t)D.g_lm.ntiles * R * 4 * 4);
+  L.max_items = ceil_div(max_rows * D.G, 32) + max_batch;
+  // plan region (one upload per forward)
+  size_t p0 = o;
+  L.rows = take(R * sizeof(RowInfo));
+  L.seqs = take((size_t)max_batch * sizeof(SeqInfo));
+  L.btab = take((size_t)max_batch * max_blocks * 4);
+  L.items = take((size_t)L.max_items * sizeof(AttnItem));
+  L.lm = take(R * sizeof(LmRow));
+  L.plan_bytes = o - p0;
+  size_t s0 = o;
+  L.step_seqs = take((size_t)max_batch * sizeof(StepSeq));
+  L.dtok = take((size_t)max_batch * max_drafts * 4);
+  L.drow = take((size_t)max_batch * max_drafts * 4);
+  L.dpar = take((size_t)max_batch * max_drafts * 4);
+  L.step_bytes = o - s0;
+  size_t c0 = o;
+  L.c_btab = take((size_t)2 * max_batch * max_blocks * 4);
+  L.c_moves = take((size_t)2 * max_batch * max_drafts * sizeof(KvMove));
+  L.commit_bytes = o - c0;
+  L.total = o;
+  return L;
+}
+
+size_t staging_slot_bytes(const Layout& L) { return std::max({L.plan_bytes, L.step_bytes, L.commit_bytes}); }
+
+}  // namespace
+
+struct via_model {
+  via_model_desc d;
+  Dims D;
+  const void *embed, *lm_head, *final_norm;
+  std::vector<const void*> attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
+  std::vector<int> route;
+  bool bf16;
+  int n_kv = 0;
+};
+
+namespace {
+
+struct SeqSt {
+  bool on = false;
+  int valid[2] = {0, 0};
+  std::vector<int> table[2];
+  bool full_ran = false;
+};
+
+struct WinCopy {
+  int batch = 0, max_rows = 0, max_drafts = 0;
+  bool tree = false;
+  std::vector<int> seq, n_rows, row_tok, row_depth, n_drafts, draft_tok, draft_row, draft_parent;
+  std::vector<uint64_t> row_mask;
+};
+
+}  // namespace
+
+struct via_kv {
+  via_model* m;
+  via_kv_desc d;
+  Layout L;
+  char* ws;
+  char* stage;
+  size_t slot_bytes;
+  std::vector<SeqSt> seqs;
+  std::set<int> free_[2];
+  bool step_open = false;
+  WinCopy win;
+  std::vector<int> step_n;  // committed length n per batch entry at step start
+  bool sticky = false;
+  hipEvent_t ev[kRing];
+  bool ev_used[kRing];
+  int ring = 0;
+};
+
+namespace {
+
+via_status hip_check(via_kv* kv, hipError_t e, const char* what) {
+  if (e == hipSuccess) return VIA_OK;
+  if (kv) kv->sticky = true;
+  return fail(VIA_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Copy host bytes to device through the next pinned staging slot.
+via_status upload(via_kv* kv, void* dst, const void* src, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return VIA_OK;
+  if (bytes > kv->slot_bytes) return fail(VIA_EINVAL, "upload of %zu bytes exceeds staging slot", bytes);
+  int r = kv->ring;
+  kv->ring = (kv->ring + 1) % kRing;
+  if (kv->ev_used[r]) {
+    via_status st = hip_check(kv, hipEventSynchronize(kv->ev[r]), "hipEventSynchronize");
+    if (st) return st;
+  }
+  char* slot = kv->stage + (size_t)r * kv->slot_bytes;
+  memcpy(slot, src, bytes);
+  via_status st = hip_check(kv, hipMemcpyAsync(dst, slot, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
+  if (st) return st;
+  st = hip_check(kv, hipEventRecord(kv->ev[r], s), "hipEventRecord");
+  kv->ev_used[r] = true;
+  return st;
+}
+
+struct Plan {
+  std::vector<RowInfo> rows;
+  std::vector<SeqInfo> seqs;
+  std::vector<int32_t> btab;
+  std::vector<AttnItem> items;
+  std::vector<LmRow> lm;
+  std::vector<char> blob;
+};
+
+// Blocks a sequence needs to hold `slots` cache slots.
+int blocks_for(int slots) { return ceil_div(slots, kBlock); }
+
+// All-or-nothing allocation of the missing blocks of several sequences of
+// one cache, lowest free block id first, in the given order.
+via_status alloc_blocks(via_kv* kv, int cache, const std::vector<std::pair<int, int>>& need /*seq, slots*/,
+                        std::vector<std::pair<int, int>>* taken) {
+  size_t missing = 0;
+  for (auto& pr : need) {
+    const SeqSt& S = kv->seqs[pr.first];
+    int want = blocks_for(pr.second);
+    if (want > kv->d.max_blocks_per_seq)
+      return fail(VIA_ENOMEM, "sequence %d needs %d blocks > max_blocks_per_seq %d", pr.first, want,
+                  kv->d.max_blocks_per_seq);
+    if (want > (int)S.table[cache].size()) missing += want - S.table[cache].size();
+  }
+  if (missing > kv->free_[cache].size())
+    return fail(VIA_ENOMEM, "%s KV pool exhausted: need %zu blocks, %zu free", cache == 0 ? "full" : "slim", missing,
+                kv->free_[cache].size());
+  for (auto& pr : need) {
+    SeqSt& S = kv->seqs[pr.first];
+    int want = blocks_for(pr.second);
+    while ((int)S.table[cache].size() < want) {
+      int blk = *kv->free_[cache].begin();
+      kv->free_[cache].erase(kv->free_[cache].begin());
+      S.table[cache].push_back(blk);
+      if (taken) taken->push_back({pr.first, blk});
+    }
+  }
+  return VIA_OK;
+}
+
+void trim_blocks(via_kv* kv, int cache, int seq, int valid) {
+  SeqSt& S = kv->seqs[seq];
+  size_t keep = blocks_for(valid);
+  while (S.table[cache].size() > keep) {
+    kv->free_[cache].insert(S.table[cache].back());
+    S.table[cache].pop_back();
+  }
+}
+
+template <typename T>
+void put(std::vector<char>& blob, size_t& off, const std::vector<T>& v) {
+  if (!v.empty()) memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
+}
+
+// Forward of one route over the planned rows; optional fused head.
+via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head, const via_verify_out* out,
+                        float inv_T, hipStream_t s) {
+  const Layout& L = kv->L;
+  const Dims& D = m->D;
+  const int M = (int)P.rows.size();
+  if (M == 0) return VIA_OK;
+  if (M > kv->d.max_rows) return fail(VIA_EINVAL, "forward of %d rows exceeds max_rows %d", M, kv->d.max_rows);
+  if ((int)P.items.size() > L.max_items) return fail(VIA_EINVAL, "too many attention tiles");
+  // one upload of the whole plan region
+  std::vector<char> blob(L.plan_bytes);
+  size_t o0 = 0;
+  memcpy(blob.data() + (L.rows - L.rows), P.rows.data(), P.rows.size() * sizeof(RowInfo));
+  memcpy(blob.data() + (L.seqs - L.rows), P.seqs.data(), P.seqs.size() * sizeof(SeqInfo));
+  if (!P.btab.empty()) memcpy(blob.data() + (L.btab - L.rows), P.btab.data(), P.btab.size() * 4);
+  if (!P.items.empty()) memcpy(blob.data() + (L.items - L.rows), P.items.data(), P.items.size() * sizeof(AttnItem));
+  if (!P.lm.empty()) memcpy(blob.data() + (L.lm - L.rows), P.lm.data(), P.lm.size() * sizeof(LmRow));
+  (void)o0;
+  char* ws = kv->ws;
+  via_status st = upload(kv, ws + L.rows, blob.data(), L.plan_bytes, s);
+  if (st) return st;
+
+  const bool bf = m->bf16;
+  const RowInfo* d_rows = (const RowInfo*)(ws + L.rows);
+  const SeqInfo* d_seqs = (const SeqInfo*)(ws + L.seqs);
+  const int32_t* d_btab = (const int32_t*)(ws + L.btab);
+  float* X = (float*)(ws + L.X);
+  void* Y = ws + L.Y;
+  void* Q = ws + L.Q;
+  void* A = ws + L.A;
+  void* Hb = ws + L.Hb;
+  void* pool = cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim;
+  const int pool_blocks = cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim;
+  std::vector<int> route;
+  if (cache == VIA_CACHE_FULL)
+    for (int l = 0; l < D.L; ++l) route.push_back(l);
+  else
+    route = m->route;
+
+  launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
+  GemmArgs g{};
+  g.M = M;
+  g.part = (float*)(ws + L.part);
+  g.counters = (int*)(ws + L.counters);
+  g.rows = d_rows;
+  g.seqs = d_seqs;
+  g.btab = d_btab;
+  AttnArgs at{};
+  at.q = Q;
+  at.pool = pool;
+  at.pool_blocks = pool_blocks;
+  at.rows = d_rows;
+  at.seqs = d_seqs;
+  at.btab = d_btab;
+  at.items = (const AttnItem*)(ws + L.items);
+  at.n_items = (int)P.items.size();
+  at.max_chunks = 0;
+  for (const AttnItem& it : P.items) at.max_chunks = std::max(at.max_chunks, it.n_chunks);
+  at.M = M;
+  at.H = D.H;
+  at.KVH = D.KVH;
+  at.hd = D.hd;
+  at.scale = (float)(1.0 / std::sqrt((double)D.hd));
+  at.part_o = (float*)(ws + L.att_o);
+  at.part_ml = (float*)(ws + L.att_ml);
+  at.out = A;
+  for (size_t si = 0; si < route.size(); ++si) {
+    const int l = route[si];
+    launch_rmsnorm(bf, X, m->attn_norm[l], M, D.d, m->d.rms_eps, Y, nullptr, s);
+    // QKV + RoPE + paged K/V write
+    g.X = Y;
+    g.ldx = D.d;
+    g.W = m->w_qkv[l];
+    g.K = D.d;
+    g.N = D.qkv;
+    g.ntiles = D.g_qkv.ntiles;
+    g.ksplit = D.g_qkv.ks;
+    g.q_out = Q;
+    g.pool = pool;
+    g.pool_blocks = pool_blocks;
+    g.layer_slot = (int)si;
+    g.H = D.H;
+    g.KVH = D.KVH;
+    g.hd = D.hd;
+    g.theta = m->d.rope_theta;
+    launch_gemm(EPI_QKV, bf, g, s);
+    at.layer_slot = (int)si;
+    launch_attention(bf, at, s);
+    // O projection + residual
+    g.X = A;
+    g.ldx = D.H * D.hd;
+    g.W = m->w_o[l];
+    g.K = D.H * D.hd;
+    g.N = D.d;
+    g.ntiles = D.g_o.ntiles;
+    g.ksplit = D.g_o.ks;
+    g.resid = X;
+    launch_gemm(EPI_RESID, bf, g, s);
+    launch_rmsnorm(bf, X, m->ffn_norm[l], M, D.d, m->d.rms_eps, Y, nullptr, s);
+    // gate/up + SwiGLU
+    g.X = Y;
+    g.ldx = D.d;
+    g.W = m->w_gate_up[l];
+    g.K = D.d;
+    g.N = 2 * D.F;
+    g.F = D.F;
+    g.ntiles = D.g_gu.ntiles;
+    g.ksplit = D.g_gu.ks;
+    g.h_out = Hb;
+    launch_gemm(EPI_SWIGLU, bf, g, s);
+    // down + residual
+    g.X = Hb;
+    g.ldx = D.F;
+    g.W = m->w_down[l];
+    g.K = D.F;
+    g.N = D.d;
+    g.ntiles = D.g_down.ntiles;
+    g.ksplit = D.g_down.ks;
+    g.resid = X;
+    launch_gemm(EPI_RESID, bf, g, s);
+  }
+  if (head && !P.lm.empty()) {
+    const int nlm = (int)P.lm.size();
+    const LmRow* d_lm = (const LmRow*)(ws + L.lm);
+    void* Yl = ws + L.Yl;
+    launch_rmsnorm(bf, X, m->final_norm, nlm, D.d, m->d.rms_eps, Yl, d_lm, s);
+    GemmArgs h{};
+    h.X = Yl;
+    h.ldx = D.d;
+    h.W = m->lm_head;
+    h.M = nlm;
+    h.K = D.d;
+    h.N = D.V;
+    h.ntiles = D.g_lm.ntiles;
+    h.ksplit = 1;
+    h.part = g.part;
+    h.counters = g.counters;
+    h.lm = d_lm;
+    h.lm_part = (float*)(ws + L.lm_part);
+    h.inv_T = inv_T;
+    h.logits = out->logits;
+    h.draft_logit = out->draft_logit;
+    launch_gemm(EPI_STATS, bf, h, s);
+    launch_lm_finalize(d_lm, h.lm_part, nlm, h.ntiles, inv_T, out->row_argmax, out->row_max, out->row_sumexp,
+                       out->row_gap, s);
+  }
+  return hip_check(kv, hipGetLastError(), "kernel launch");
+}
+
+via_status check_params(const via_tier_params* p) {
+  if (!p) return fail(VIA_EINVAL, "null tier params");
+  if (!(p->temperature > 0.f) || !std::isfinite(p->temperature)) return fail(VIA_EINVAL, "temperature must be > 0");
+  if (!(p->tau_full >= 0.f) || !(p->tau_acc >= p->tau_full))
+    return fail(VIA_EINVAL, "thresholds must satisfy 0 <= tau_full <= tau_acc");
+  if (p->forced < -1 || p->forced > 2) return fail(VIA_EINVAL, "forced must be -1..2");
+  return VIA_OK;
+}
+
+via_status check_out(const via_verify_out* o) {
+  if (!o || !o->row_argmax || !o->row_max || !o->row_sumexp || !o->draft_logit)
+    return fail(VIA_EINVAL, "verify_out: row_argmax, row_max, row_sumexp and draft_logit are required");
+  return VIA_OK;
+}
+
+// Validate and copy a window.
+via_status copy_window(via_kv* kv, const via_window* w, WinCopy& c) {
+  const via_model* m = kv->m;
+  if (!w) return fail(VIA_EINVAL, "null window");
+  if (w->batch < 1 || w->batch > kv->d.max_batch) return fail(VIA_EINVAL, "batch %d not in [1, %d]", w->batch, kv->d.max_batch);
+  if (w->max_rows < 1 || w->max_drafts < 1 || w->max_drafts > kv->d.max_drafts)
+    return fail(VIA_EINVAL, "window strides out of range (1 <= max_drafts <= %d)", kv->d.max_drafts);
+  if (!w->seq_id || !w->n_rows || !w->row_tok || !w->n_drafts || (w->max_drafts > 0 && (!w->draft_tok || !w->draft_row)))
+    return fail(VIA_EINVAL, "window arrays missing");
+  const int V = m->d.vocab;
+  c = WinCopy();
+  c.batch = w->batch;
+  c.max_rows = w->max_rows;
+  c.max_drafts = w->max_drafts;
+  c.tree = w->row_mask != nullptr || w->draft_parent != nullptr;
+  if ((w->row_mask != nullptr) != (w->draft_parent != nullptr))
+    return fail(VIA_EINVAL, "tree windows need both row_mask and draft_parent");
+  std::set<int> seen;
+  for (int b = 0; b < w->batch; ++b) {
+    int sid = w->seq_id[b];
+    if (sid < 0 || sid >= kv->d.max_seqs || !kv->seqs[sid].on) return fail(VIA_EINVAL, "sequence %d not attached", sid);
+    if (!seen.insert(sid).second) return fail(VIA_EINVAL, "sequence %d appears twice", sid);
+    int R = w->n_rows[b], nd = w->n_drafts[b];
+    if (R < 1 || R > w->max_rows) return fail(VIA_EINVAL, "n_rows[%d]=%d out of range", b, R);
+    if (nd < 0 || nd > w->max_drafts) return fail(VIA_EINVAL, "n_drafts[%d]=%d out of range", b, nd);
+    if (c.tree && R > VIA_MAX_TREE_ROWS) return fail(VIA_EINVAL, "tree windows hold at most %d rows", VIA_MAX_TREE_ROWS);
+    c.seq.push_back(sid);
+    c.n_rows.push_back(R);
+    c.n_drafts.push_back(nd);
+  }
+  c.row_tok.assign((size_t)w->batch * w->max_rows, 0);
+  c.row_depth.assign((size_t)w->batch * w->max_rows, 0);
+  c.row_mask.assign((size_t)w->batch * w->max_rows, 0);
+  c.draft_tok.assign((size_t)w->batch * std::max(1, w->max_drafts), 0);
+  c.draft_row.assign((size_t)w->batch * std::max(1, w->max_drafts), 0);
+  c.draft_parent.assign((size_t)w->batch * std::max(1, w->max_drafts), -1);
+  for (int b = 0; b < w->batch; ++b) {
+    int R = c.n_rows[b], nd = c.n_drafts[b];
+    for (int r = 0; r < R; ++r) {
+      size_t i = (size_t)b * w->max_rows + r;
+      int t = w->row_tok[i];
+      if (t < 0 || t >= V) return fail(VIA_EINVAL, "row token %d out of range", t);
+      c.row_tok[i] = t;
+      int dep = w->row_depth ? w->row_depth[i] : r;
+      if (dep < 0 || (r == 0 && dep != 0)) return fail(VIA_EINVAL, "row depth must be >= 0 and 0 for row 0");
+      c.row_depth[i] = dep;
+      if (w->row_mask) {
+        uint64_t mk = w->row_mask[i];
+        if (!((mk >> r) & 1) || !(mk & 1) || (r < 63 && (mk >> (r + 1))))
+          return fail(VIA_EINVAL, "row_mask[%d][%d] must contain row 0, itself and no later row", b, r);
+        c.row_mask[i] = mk;
+      }
+    }
+    std::vector<int> node_row(nd, -1);
+    for (int j = 0; j < nd; ++j) {
+      size_t i = (size_t)b * w->max_drafts + j;
+      int t = w->draft_tok[i], row = w->draft_row[i];
+      int par = w->draft_parent ? w->draft_parent[i] : j - 1;
+      if (t < 0 || t >= V) return fail(VIA_EINVAL, "draft token %d out of range", t);
+      if (row < 0 || row >= R) return fail(VIA_EINVAL, "draft_row[%d][%d]=%d out of range", b, j, row);
+      if (par < -1 || par >= j) return fail(VIA_EINVAL, "draft_parent[%d][%d] must be -1 or < j", b, j);
+      // the row verifying draft j is its parent's row (root row 0)
+      if (par == -1 ? row != 0 : (node_row[par] >= 0 && node_row[par] != row))
+        return fail(VIA_EINVAL, "draft_row[%d][%d] inconsistent with its parent", b, j);
+      if (par >= 0) node_row[par] = row;
+      if (!w->draft_parent && row != j) return fail(VIA_EINVAL, "chain draft j must be verified by row j");
+      c.draft_tok[i] = t;
+      c.draft_row[i] = row;
+      c.draft_parent[i] = par;
+    }
+    // children per row bounded (head rows carry at most kMaxChildren drafts)
+    std::vector<int> per_row(R, 0);
+    for (int j = 0; j < nd; ++j)
+      if (++per_row[c.draft_row[(size_t)b * w->max_drafts + j]] > kMaxChildren)
+        return fail(VIA_EINVAL, "a row verifies more than %d drafts", kMaxChildren);
+  }
+  return VIA_OK;
+}
+
+// Rows of one verify forward; `run` selects batch entries.
+via_status build_verify_plan(via_kv* kv, int cache, const WinCopy& w, const std::vector<int>& run,
+                             const via_window* raw, bool head, Plan& P, std::vector<std::pair<int, int>>* taken) {
+  const Dims& D = kv->m->D;
+  std::vector<std::pair<int, int>> need;
+  for (int b : run) {
+    const SeqSt& S = kv->seqs[w.seq[b]];
+    int n_lag = 0;
+    if (cache == VIA_CACHE_FULL) {
+      int lag = S.valid[VIA_CACHE_SLIM] - S.valid[VIA_CACHE_FULL];
+      n_lag = (raw && raw->n_lag) ? raw->n_lag[b] : 0;
+      if (n_lag != lag) return fail(VIA_ESTATE, "sequence %d: full cache lags %d tokens, window gives %d", w.seq[b], lag, n_lag);
+      if (n_lag > 0 && (!raw->lag_tok || n_lag > raw->max_lag)) return fail(VIA_EINVAL, "lag_tok missing or max_lag too small");
+    }
+    need.push_back({w.seq[b], S.valid[cache] + n_lag + w.n_rows[b]});
+  }
+  via_status st = alloc_blocks(kv, cache, need, taken);
+  if (st) return st;
+  int lm_i = 0;
+  for (size_t q = 0; q < run.size(); ++q) {
+    const int b = run[q];
+    const SeqSt& S = kv->seqs[w.seq[b]];
+    const int valid = S.valid[cache];
+    const int n_lag = need[q].second - valid - w.n_rows[b];
+    const int R = w.n_rows[b];
+    const int win_base = valid + n_lag;
+    const int npos = S.valid[VIA_CACHE_SLIM];  // position of the pending token, n - 1
+    SeqInfo si{};
+    si.row_start = (int)P.rows.size();
+    si.n_rows = n_lag + R;
+    si.kv_len = valid + n_lag + R;
+    si.win_base = win_base;
+    si.bt = (int)P.btab.size();
+    si.n_blocks = (int)S.table[cache].size();
+    for (int blk : S.table[cache]) P.btab.push_back(blk);
+    const int sidx = (int)P.seqs.size();
+    for (int i = 0; i < n_lag; ++i) {
+      RowInfo r{};
+      r.tok = raw->lag_tok[(size_t)b * raw->max_lag + i];
+      if (r.tok < 0 || r.tok >= D.V) return fail(VIA_EINVAL, "lag token out of range");
+      r.pos = valid + i;
+      r.seq = sidx;
+      r.slot = valid + i;
+      r.vis_len = valid + i + 1;
+      r.lm = -1;
+      P.rows.push_back(r);
+    }
+    for (int rr = 0; rr < R; ++rr) {
+      size_t i = (size_t)b * w.max_rows + rr;
+      RowInfo r{};
+      r.tok = w.row_tok[i];
+      r.pos = npos + w.row_depth[i];
+      r.seq = sidx;
+      r.slot = win_base + rr;
+      r.vis_len = w.tree ? win_base : win_base + rr + 1;
+      r.mask = w.tree ? w.row_mask[i] : 0;
+      r.lm = -1;
+      if (head) {
+        LmRow lr{};
+        lr.row = (int)P.rows.size();
+        lr.out = b * w.max_rows + rr;
+        for (int j = 0; j < w.n_drafts[b]; ++j) {
+          size_t di = (size_t)b * w.max_drafts + j;
+          if (w.draft_row[di] == rr) {
+            lr.draft_idx[lr.n_drafts] = (int)di;
+            lr.draft_tok[lr.n_drafts] = w.draft_tok[di];
+            lr.n_drafts++;
+          }
+        }
+        r.lm = lm_i++;
+        P.lm.push_back(lr);
+      }
+      P.rows.push_back(r);
+    }
+    P.seqs.push_back(si);
+    const int nq = si.n_rows * D.G;
+    for (int q0 = 0; q0 < nq; q0 += 32) P.items.push_back(AttnItem{sidx, q0, ceil_div(si.kv_len, kAttnChunk), 0});
+  }
+  return VIA_OK;
+}
+
+via_status common_checks(via_model* m, via_kv* kv) {
+  if (!m || !kv) return fail(VIA_EINVAL, "null handle");
+  if (kv->m != m) return fail(VIA_EINVAL, "KV handle belongs to another model");
+  if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
+  return VIA_OK;
+}
+
+void release_taken(via_kv* kv, int cache, const std::vector<std::pair<int, int>>& taken) {
+  for (auto it = taken.rbegin(); it != taken.rend(); ++it) {
+    SeqSt& S = kv->seqs[it->first];
+    if (!S.table[cache].empty() && S.table[cache].back() == it->second) S.table[cache].pop_back();
+    kv->free_[cache].insert(it->second);
+  }
+}
+
+via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* win, const int32_t* run_mask,
+                       const via_tier_params* p, via_verify_out* out, hipStream_t s, bool probe) {
+  via_status st = common_checks(m, kv);
+  if (st) return st;
+  if ((st = check_params(p)) || (st = check_out(out))) return st;
+  WinCopy w;
+  const WinCopy* wp = &w;
+  if (probe || cache == VIA_CACHE_SLIM) {
+    if ((st = copy_window(kv, win, w))) return st;
+  } else {
+    if (!kv->step_open) return fail(VIA_ESTATE, "via_verify_full needs an open step (call via_verify_slim first)");
+    if (!win || win->batch != kv->win.batch) return fail(VIA_EINVAL, "window batch differs from the open step");
+    for (int b = 0; b < win->batch; ++b)
+      if (win->seq_id[b] != kv->win.seq[b] || win->n_rows[b] != kv->win.n_rows[b])
+        return fail(VIA_EINVAL, "window differs from the open step");
+    wp = &kv->win;
+  }
+  if (!probe && cache == VIA_CACHE_SLIM && kv->step_open) return fail(VIA_ESTATE, "a step is already open");
+  std::vector<int> run;
+  for (int b = 0; b < wp->batch; ++b)
+    if (!run_mask || run_mask[b]) run.push_back(b);
+  Plan P;
+  std::vector<std::pair<int, int>> taken;
+  if ((st = build_verify_plan(kv, cache, *wp, run, win, true, P, &taken))) return st;
+  st = exec_forward(m, kv, cache, P, true, out, 1.0f / p->temperature, s);
+  if (probe) {
+    release_taken(kv, cache, taken);
+    return st;
+  }
+  if (st) {
+    release_taken(kv, cache, taken);
+    return st;
+  }
+  if (cache == VIA_CACHE_SLIM) {
+    kv->win = w;
+    kv->step_open = true;
+    kv->step_n.assign(w.batch, 0);
+    for (int b = 0; b < w.batch; ++b) {
+      kv->step_n[b] = kv->seqs[w.seq[b]].valid[VIA_CACHE_SLIM] + 1;
+      kv->seqs[w.seq[b]].full_ran = false;
+    }
+  } else {
+    for (int b : run) kv->seqs[wp->seq[b]].full_ran = true;
+  }
+  return VIA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* via_last_error(void) { return g_err.c_str(); }
+const char* via_version(void) { return "via-gfx950 0.1"; }
+
+size_t via_pool_bytes(const via_model_desc* desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size) {
+  if (!desc) return 0;
+  return (size_t)n_layer_slots * n_blocks * 2 * desc->n_kv_heads * block_size * desc->head_dim * esize_of(desc);
+}
+
+size_t via_workspace_bytes(const via_model_desc* desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
+                           int32_t max_drafts) {
+  if (!desc || max_rows < 1 || max_batch < 1 || max_blocks_per_seq < 1 || max_drafts < 1) return 0;
+  return layout_of(desc, max_rows, max_batch, max_blocks_per_seq, max_drafts).total;
+}
+
+size_t via_staging_bytes(const via_model_desc* desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
+                         int32_t max_drafts) {
+  if (!desc || max_rows < 1 || max_batch < 1 || max_blocks_per_seq < 1 || max_drafts < 1) return 0;
+  Layout L = layout_of(desc, max_rows, max_batch, max_blocks_per_seq, max_drafts);
+  return staging_slot_bytes(L) * kRing;
+}
+
+via_status via_model_create(const via_model_desc* desc, const via_weights* w, via_model** out) {
+  if (!desc || !w || !out) return fail(VIA_EINVAL, "null argument");
+  *out = nullptr;
+  const via_model_desc& d = *desc;
+  if (d.n_layers < 1 || d.d_model < 1 || d.n_heads < 1 || d.n_kv_heads < 1 || d.head_dim < 1 || d.d_ffn < 1 ||
+      d.vocab < 1)
+    return fail(VIA_EINVAL, "model dimensions must be positive");
+  if (d.dtype != VIA_DTYPE_F32 && d.dtype != VIA_DTYPE_BF16) return fail(VIA_EINVAL, "dtype must be f32 or bf16");
+  if (d.head_dim != 64 && d.head_dim != 128) return fail(VIA_EUNSUPPORTED, "head_dim must be 64 or 128");
+  if (d.n_heads % d.n_kv_heads) return fail(VIA_EUNSUPPORTED, "n_heads must be a multiple of n_kv_heads");
+  if (d.d_model % 64 || d.d_ffn % 64 || (d.n_heads * d.head_dim) % 64)
+    return fail(VIA_EUNSUPPORTED, "d_model, d_ffn and n_heads*head_dim must be multiples of 64");
+  if (!(d.rms_eps > 0.f) || !(d.rope_theta > 0.f)) return fail(VIA_EINVAL, "rms_eps and rope_theta must be > 0");
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->w_qkv || !w->w_o || !w->ffn_norm ||
+      !w->w_gate_up || !w->w_down)
+    return fail(VIA_EINVAL, "weight pointer missing");
+  via_model* m = new via_model();
+  m->d = d;
+  m->D = dims_of(&d);
+  m->bf16 = d.dtype == VIA_DTYPE_BF16;
+  m->embed = w->embed;
+  m->lm_head = w->lm_head;
+  m->final_norm = w->final_norm;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const void* ptrs[6] = {w->attn_norm[l], w->w_qkv[l], w->w_o[l], w->ffn_norm[l], w->w_gate_up[l], w->w_down[l]};
+    for (const void* p : ptrs)
+      if (!p) {
+        delete m;
+        return fail(VIA_EINVAL, "layer %d weight pointer missing", l);
+      }
+    m->attn_norm.push_back(w->attn_norm[l]);
+    m->w_qkv.push_back(w->w_qkv[l]);
+    m->w_o.push_back(w->w_o[l]);
+    m->ffn_norm.push_back(w->ffn_norm[l]);
+    m->w_gate_up.push_back(w->w_gate_up[l]);
+    m->w_down.push_back(w->w_down[l]);
+    m->route.push_back(l);
+  }
+  *out = m;
+  return VIA_OK;
+}
+
+via_status via_model_set_route(via_model* m, const int32_t* layers, int32_t n) {
+  if (!m || !layers) return fail(VIA_EINVAL, "null argument");
+  if (m->n_kv > 0) return fail(VIA_ESTATE, "route is fixed while KV handles exist");
+  if (n < 1 || n > m->d.n_layers) return fail(VIA_EINVAL, "route length %d not in [1, %d]", n, m->d.n_layers);
+  for (int i = 0; i < n; ++i) {
+    if (layers[i] < 0 || layers[i] >= m->d.n_layers) return fail(VIA_EINVAL, "route layer %d out of range", layers[i]);
+    if (i && layers[i] <= layers[i - 1]) return fail(VIA_EINVAL, "route must be strictly increasing");
+  }
+  m->route.assign(layers, layers + n);
+  return VIA_OK;
+}
+
+via_status via_model_destroy(via_model* m) {
+  if (!m) return fail(VIA_EINVAL, "null model");
+  if (m->n_kv > 0) return fail(VIA_ESTATE, "destroy the KV handles first");
+  delete m;
+  return VIA_OK;
+}
+
+via_status via_kv_create(via_model* m, const via_kv_desc* d, via_kv** out) {
+  if (!m || !d || !out) return fail(VIA_EINVAL, "null argument");
+  *out = nullptr;
+  if (d->block_size != kBlock) return fail(VIA_EUNSUPPORTED, "block_size must be %d", kBlock);
+  if (d->max_seqs < 1 || d->max_blocks_per_seq < 1 || d->blocks_full < 1 || d->blocks_slim < 1 || d->max_rows < 1 ||
+      d->max_batch < 1 || d->max_drafts < 1 || d->max_drafts > VIA_MAX_DRAFTS)
+    return fail(VIA_EINVAL, "KV description sizes out of range");
+  if (!d->pool_full || !d->pool_slim || !d->workspace || !d->pinned_staging)
+    return fail(VIA_EINVAL, "pools, workspace and staging are required");
+  Layout L = layout_of(&m->d, d->max_rows, d->max_batch, d->max_blocks_per_seq, std::max(1, (int)d->max_drafts));
+  if (d->workspace_bytes < L.total)
+    return fail(VIA_ENOMEM, "workspace %zu bytes < required %zu", d->workspace_bytes, L.total);
+  size_t slot = staging_slot_bytes(L);
+  if (d->staging_bytes < slot * kRing)
+    return fail(VIA_ENOMEM, "staging %zu bytes < required %zu", d->staging_bytes, slot * kRing);
+  via_kv* kv = new via_kv();
+  kv->m = m;
+  kv->d = *d;
+  kv->L = L;
+  kv->ws = (char*)d->workspace;
+  kv->stage = (char*)d->pinned_staging;
+  kv->slot_bytes = slot;
+  kv->seqs.resize(d->max_seqs);
+  for (int c = 0; c < 2; ++c) {
+    int nb = c == 0 ? d->blocks_full : d->blocks_slim;
+    for (int i = 0; i < nb; ++i) kv->free_[c].insert(kv->free_[c].end(), i);
+  }
+  for (int r = 0; r < kRing; ++r) {
+    kv->ev_used[r] = false;
+    if (hipEventCreateWithFlags(&kv->ev[r], hipEventDisableTiming) != hipSuccess) {
+      for (int q = 0; q < r; ++q) (void)hipEventDestroy(kv->ev[q]);
+      delete kv;
+      return fail(VIA_EDEVICE, "hipEventCreate failed");
+    }
+  }
+  // split-K counters start at zero and reset themselves after each use
+  if (hipMemset(kv->ws + L.counters, 0, (size_t)kCounters * 4) != hipSuccess) {
+    for (int r = 0; r < kRing; ++r) (void)hipEventDestroy(kv->ev[r]);
+    delete kv;
+    return fail(VIA_EDEVICE, "hipMemset of the workspace failed");
+  }
+  m->n_kv++;
+  *out = kv;
+  return VIA_OK;
+}
+
+via_status via_kv_destroy(via_kv* kv) {
+  if (!kv) return fail(VIA_EINVAL, "null KV handle");
+  for (int r = 0; r < kRing; ++r) {
+    if (kv->ev_used[r]) (void)hipEventSynchronize(kv->ev[r]);
+    (void)hipEventDestroy(kv->ev[r]);
+  }
+  kv->m->n_kv--;
+  delete kv;
+  return VIA_OK;
+}
+
+static via_status attach_checks(via_kv* kv, int32_t seq_id, int32_t n) {
+  if (!kv) return fail(VIA_EINVAL, "null KV handle");
+  if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
+  if (kv->step_open) return fail(VIA_ESTATE, "a step is open");
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs) return fail(VIA_EINVAL, "seq_id %d out of range", seq_id);
+  if (kv->seqs[seq_id].on) return fail(VIA_ESTATE, "sequence %d already attached", seq_id);
+  if (n < 0) return fail(VIA_EINVAL, "negative length");
+  return VIA_OK;
+}
+
+via_status via_kv_seq_reserve(via_kv* kv, int32_t seq_id, int32_t n_ctx) {
+  via_status st = attach_checks(kv, seq_id, n_ctx);
+  if (st) return st;
+  if (blocks_for(n_ctx) > (int)kv->free_[0].size() || blocks_for(n_ctx) > (int)kv->free_[1].size() ||
+      blocks_for(n_ctx) > kv->d.max_blocks_per_seq)
+    return fail(VIA_ENOMEM, "not enough KV blocks for %d slots", n_ctx);
+  kv->seqs[seq_id] = SeqSt();
+  kv->seqs[seq_id].on = true;
+  alloc_blocks(kv, 0, {{seq_id, n_ctx}}, nullptr);
+  alloc_blocks(kv, 1, {{seq_id, n_ctx}}, nullptr);
+  kv->seqs[seq_id].valid[0] = kv->seqs[seq_id].valid[1] = n_ctx;
+  return VIA_OK;
+}
+
+via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* tokens, int32_t n, void* stream) {
+  via_status st = attach_checks(kv, seq_id, n);
+  if (st) return st;
+  if ((st = common_checks(m, kv))) return st;
+  if (n > 0 && !tokens) return fail(VIA_EINVAL, "null tokens");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= m->d.vocab) return fail(VIA_EINVAL, "token %d out of range", tokens[i]);
+  if (blocks_for(n) > (int)kv->free_[0].size() || blocks_for(n) > (int)kv->free_[1].size() ||
+      blocks_for(n) > kv->d.max_blocks_per_seq)
+    return fail(VIA_ENOMEM, "not enough KV blocks for %d slots", n);
+  kv->seqs[seq_id] = SeqSt();
+  kv->seqs[seq_id].on = true;
+  SeqSt& S = kv->seqs[seq_id];
+  hipStream_t s = (hipStream_t)stream;
+  const int G = m->D.G;
+  for (int cache = 0; cache < 2; ++cache) {
+    alloc_blocks(kv, cache, {{seq_id, n}}, nullptr);
+    for (int c0 = 0; c0 < n; c0 += kv->d.max_rows) {
+      int c1 = std::min(n, c0 + kv->d.max_rows);
+      Plan P;
+      SeqInfo si{};
+      si.row_start = 0;
+      si.n_rows = c1 - c0;
+      si.kv_len = c1;
+      si.win_base = c0;
+      si.bt = 0;
+      si.n_blocks = (int)S.table[cache].size();
+      for (int blk : S.table[cache]) P.btab.push_back(blk);
+      for (int i = c0; i < c1; ++i) {
+        RowInfo r{};
+        r.tok = tokens[i];
+        r.pos = i;
+        r.seq = 0;
+        r.slot = i;
+        r.vis_len = i + 1;
+        r.lm = -1;
+        P.rows.push_back(r);
+      }
+      P.seqs.push_back(si);
+      for (int q0 = 0; q0 < si.n_rows * G; q0 += 32) P.items.push_back(AttnItem{0, q0, ceil_div(c1, kAttnChunk), 0});
+      if ((st = exec_forward(m, kv, cache, P, false, nullptr, 1.f, s))) {
+        trim_blocks(kv, 0, seq_id, 0);
+        trim_blocks(kv, 1, seq_id, 0);
+        S = SeqSt();
+        return st;
+      }
+    }
+    S.valid[cache] = n;
+  }
+  return VIA_OK;
+}
+
+via_status via_kv_seq_release(via_kv* kv, int32_t seq_id) {
+  if (!kv) return fail(VIA_EINVAL, "null KV handle");
+  if (kv->step_open) return fail(VIA_ESTATE, "a step is open");
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
+  trim_blocks(kv, 0, seq_id, 0);
+  trim_blocks(kv, 1, seq_id, 0);
+  kv->seqs[seq_id] = SeqSt();
+  return VIA_OK;
+}
+
+via_status via_kv_seq_info(const via_kv* kv, int32_t seq_id, int32_t cache, int32_t* valid, int32_t* table,
+                           int32_t cap, int32_t* n_blocks) {
+  if (!kv || !valid || !n_blocks) return fail(VIA_EINVAL, "null argument");
+  if (cache != 0 && cache != 1) return fail(VIA_EINVAL, "cache must be VIA_CACHE_FULL or VIA_CACHE_SLIM");
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
+  const SeqSt& S = kv->seqs[seq_id];
+  *valid = S.valid[cache];
+  *n_blocks = (int)S.table[cache].size();
+  if (table) {
+    if (cap < *n_blocks) return fail(VIA_EINVAL, "table capacity %d < %d", cap, *n_blocks);
+    for (int i = 0; i < *n_blocks; ++i) table[i] = S.table[cache][i];
+  }
+  return VIA_OK;
+}
+
+via_status via_verify_slim(via_model* m, via_kv* kv, const via_window* win, const via_tier_params* p,
+                           via_verify_out* out, void* stream) {
+  return verify_impl(m, kv, VIA_CACHE_SLIM, win, nullptr, p, out, (hipStream_t)stream, false);
+}
+
+via_status via_verify_full(via_model* m, via_kv* kv, const via_window* win, const int32_t* run,
+                           const via_tier_params* p, via_verify_out* out, void* stream) {
+  return verify_impl(m, kv, VIA_CACHE_FULL, win, run, p, out, (hipStream_t)stream, false);
+}
+
+via_status via_verify_probe(via_model* m, via_kv* kv, int32_t cache, const via_window* win,
+                            const via_tier_params* p, via_verify_out* out, void* stream) {
+  if (cache != 0 && cache != 1) return fail(VIA_EINVAL, "cache must be VIA_CACHE_FULL or VIA_CACHE_SLIM");
+  if (kv && kv->step_open) return fail(VIA_ESTATE, "no probe while a step is open (it would overwrite the window rows)");
+  return verify_impl(m, kv, cache, win, nullptr, p, out, (hipStream_t)stream, true);
+}
+
+via_status via_tier_decide(via_kv* kv, const via_tier_params* p, const via_verify_out* slim,
+                           const via_verify_out* full, via_decision* dec, void* stream) {
+  if (!kv || !dec) return fail(VIA_EINVAL, "null argument");
+  if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
+  via_status st = check_params(p);
+  if (st) return st;
+  if ((st = check_out(slim))) return st;
+  if (full && (st = check_out(full))) return st;
+  if (!dec->tier || !dec->conf || !dec->packed || !dec->h_packed) return fail(VIA_EINVAL, "decision arrays missing");
+  if (!kv->step_open) return fail(VIA_ESTATE, "no open step");
+  const WinCopy& w = kv->win;
+  const Layout& L = kv->L;
+  hipStream_t s = (hipStream_t)stream;
+  const int B = w.batch, Dd = std::max(1, w.max_drafts);
+  // step region: per-sequence state + draft arrays
+  std::vector<char> blob(L.step_bytes);
+  std::vector<StepSeq> ss(B);
+  for (int b = 0; b < B; ++b) {
+    ss[b].n = kv->step_n[b];
+    ss[b].n_drafts = w.n_drafts[b];
+    ss[b].full_ran = kv->seqs[w.seq[b]].full_ran ? 1 : 0;
+  }
+  memcpy(blob.data(), ss.data(), B * sizeof(StepSeq));
+  memcpy(blob.data() + (L.dtok - L.step_seqs), w.draft_tok.data(), (size_t)B * Dd * 4);
+  memcpy(blob.data() + (L.drow - L.step_seqs), w.draft_row.data(), (size_t)B * Dd * 4);
+  memcpy(blob.data() + (L.dpar - L.step_seqs), w.draft_parent.data(), (size_t)B * Dd * 4);
+  if ((st = upload(kv, kv->ws + L.step_seqs, blob.data(), L.step_bytes, s))) return st;
+  DecideArgs a{};
+  a.seqs = (const StepSeq*)(kv->ws + L.step_seqs);
+  a.batch = B;
+  a.max_rows = w.max_rows;
+  a.max_drafts = Dd;
+  a.draft_tok = (const int32_t*)(kv->ws + L.dtok);
+  a.draft_row = (const int32_t*)(kv->ws + L.drow);
+  a.draft_parent = (const int32_t*)(kv->ws + L.dpar);
+  a.s_row_max = slim->row_max;
+  a.s_row_argmax = slim->row_argmax;
+  a.s_draft_logit = slim->draft_logit;
+  if (full) {
+    a.f_row_max = full->row_max;
+    a.f_row_argmax = full->row_argmax;
+    a.f_draft_logit = full->draft_logit;
+  }
+  a.tau_acc = p->tau_acc;
+  a.tau_full = p->tau_full;
+  a.inv_T = 1.0f / p->temperature;
+  a.forced = p->forced;
+  a.tier = dec->tier;
+  a.conf = dec->conf;
+  a.packed = dec->packed;
+  launch_decide(a, s);
+  if ((st = hip_check(kv, hipGetLastError(), "decide launch"))) return st;
+  size_t bytes = (size_t)(4 * B + B * Dd) * 4;
+  return hip_check(kv, hipMemcpyAsync(dec->h_packed, dec->packed, bytes, hipMemcpyDeviceToHost, s), "decision copy");
+}
+
+via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* stream) {
+  if (!kv || !dec || !dec->h_packed) return fail(VIA_EINVAL, "null argument");
+  if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
+  if (!kv->step_open) return fail(VIA_ESTATE, "no open step to commit");
+  const WinCopy& w = kv->win;
+  const int B = w.batch, Dd = std::max(1, w.max_drafts), V = kv->m->d.vocab;
+  const int32_t* hp = dec->h_packed;
+  // validate everything before touching state
+  std::vector<std::vector<int>> new_tokens_rows(B);
+  for (int b = 0; b < B; ++b) {
+    int status = hp[b], kappa = hp[B + b], emit = hp[2 * B + b], nl = hp[3 * B + b];
+    const int* path = hp + 4 * B + b * Dd;
+    const int n = kv->step_n[b];
+    if (status == 1) return fail(VIA_ESTATE, "sequence %d still needs the full verifier", w.seq[b]);
+    if (status != 0 && status != 2) return fail(VIA_EINVAL, "bad status %d", status);
+    if (kappa < 0 || kappa > w.n_drafts[b]) return fail(VIA_EINVAL, "kappa %d out of range", kappa);
+    if (emit < -1 || emit >= V) return fail(VIA_EINVAL, "emit %d out of range", emit);
+    if (status == 2) {
+      if (nl != n) return fail(VIA_EINVAL, "new_len must equal n when the sequence is not advanced");
+      continue;
+    }
+    if (nl != n + kappa + (emit >= 0 ? 1 : 0)) return fail(VIA_EINVAL, "new_len inconsistent with kappa/emit");
+    int prev = -1;
+    for (int i = 0; i < kappa; ++i) {
+      int j = path[i];
+      if (j < 0 || j >= w.n_drafts[b] || w.draft_parent[(size_t)b * w.max_drafts + j] != prev)
+        return fail(VIA_EINVAL, "accepted path of sequence %d is not a root path", w.seq[b]);
+      prev = j;
+    }
+    // window rows that stay valid: root + the first (kept - 1) path nodes
+    int kept = kappa + (emit >= 0 ? 1 : 0);
+    for (int i = 1; i < kept; ++i) {
+      int node = path[i - 1], row = -1;
+      for (int j = 0; j < w.n_drafts[b]; ++j)
+        if (w.draft_parent[(size_t)b * w.max_drafts + j] == node) {
+          row = w.draft_row[(size_t)b * w.max_drafts + j];
+          break;
+        }
+      if (row < 0) return fail(VIA_EINVAL, "accepted node %d has no fed row", node);
+      new_tokens_rows[b].push_back(row);
+    }
+  }
+  // tree compaction moves (slim cache always, full cache where it ran)
+  hipStream_t s = (hipStream_t)stream;
+  if (w.tree) {
+    for (int cache = 0; cache < 2; ++cache) {
+      std::vector<int32_t> bt;
+      std::vector<KvMove> mv;
+      for (int b = 0; b < B; ++b) {
+        const SeqSt& S = kv->seqs[w.seq[b]];
+        if (hp[b] != 0) continue;
+        if (cache == VIA_CACHE_FULL && !S.full_ran) continue;
+        int base = kv->step_n[b] - 1;
+        int off = (int)bt.size();
+        bool any = false;
+        for (size_t i = 0; i < new_tokens_rows[b].size(); ++i) {
+          int src = base + new_tokens_rows[b][i], dst = base + (int)i + 1;
+          if (src != dst) {
+            mv.push_back(KvMove{off, src, dst, 0});
+            any = true;
+          }
+        }
+        if (any)
+          for (int blk : S.table[cache]) bt.push_back(blk);
+      }
+      if (mv.empty()) continue;
+      const Layout& L = kv->L;
+      std::vector<char> blob(L.commit_bytes);
+      memcpy(blob.data(), bt.data(), bt.size() * 4);
+      memcpy(blob.data() + (L.c_moves - L.c_btab), mv.data(), mv.size() * sizeof(KvMove));
+      via_status st = upload(kv, kv->ws + L.c_btab, blob.data(), L.commit_bytes, s);
+      if (st) return st;
+      int slots = cache == VIA_CACHE_FULL ? kv->m->d.n_layers : (int)kv->m->route.size();
+      launch_kv_moves(kv->m->bf16, cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim,
+                      cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim, slots, kv->m->d.n_kv_heads,
+                      kv->m->d.head_dim, (const int32_t*)(kv->ws + L.c_btab), (const KvMove*)(kv->ws + L.c_moves),
+                      (int)mv.size(), s);
+      if ((st = hip_check(kv, hipGetLastError(), "compaction launch"))) return st;
+    }
+  }
+  for (int b = 0; b < B; ++b) {
+    SeqSt& S = kv->seqs[w.seq[b]];
+    if (hp[b] == 0) {
+      int nv = hp[3 * B + b] - 1;
+      S.valid[VIA_CACHE_SLIM] = nv;
+      if (S.full_ran) S.valid[VIA_CACHE_FULL] = nv;
+    }
+    trim_blocks(kv, VIA_CACHE_SLIM, w.seq[b], S.valid[VIA_CACHE_SLIM]);
+    trim_blocks(kv, VIA_CACHE_FULL, w.seq[b], S.valid[VIA_CACHE_FULL]);
+    S.full_ran = false;
+  }
+  kv->step_open = false;
+  return VIA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,217 @@
+"""Host-side step loop over the C ABI (Alg. 1 of the paper, App. B.1 form).
+
+Per verification step: slim-verifier forward + fused head over the draft
+window, tier decision, one small device->host read; if any sequence
+escalates, the full-verifier forward (with the lag rows its cache misses)
+and a second decision; then the KV commit.  The library keeps cache state
+(valid lengths, block tables); this object keeps the committed tokens the
+caller owns (pending token, lag rows) and builds windows.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import via
+
+
+def tree_layout(tok, parent):
+    """Fed rows of a token tree: root + every node with children, node order.
+
+    Returns (row_nodes, draft_row, row_depth, row_mask)."""
+    has_child = set(p for p in parent if p >= 0)
+    row_nodes = [-1] + [j for j in range(len(tok)) if j in has_child]
+    row_of = {u: r for r, u in enumerate(row_nodes)}
+    depth = {}
+    for j in range(len(tok)):
+        depth[j] = 1 if parent[j] < 0 else depth[parent[j]] + 1
+    draft_row = [row_of[p] for p in parent]
+    row_depth = [0] + [depth[u] for u in row_nodes[1:]]
+    masks = []
+    for r, u in enumerate(row_nodes):
+        m = 1 | (1 << r)
+        while u >= 0:
+            m |= 1 << row_of[u]
+            u = parent[u]
+        masks.append(m)
+    return row_nodes, draft_row, row_depth, masks
+
+
+class Session:
+    def __init__(self, model: via.Model, kv: via.KV, params: via.TierParams, logits=False):
+        self.m, self.kv, self.p = model, kv, params
+        self.tokens = {}
+        self.want_logits = logits
+        B, R, D, V = kv.max_batch, kv.max_rows, kv.max_drafts, model.desc["vocab"]
+        # window rows per sequence are bounded by max_rows / batch at call time
+        self.out_slim = via.Out(B, R, D, V, logits)
+        self.out_full = via.Out(B, R, D, V, logits)
+        self.dec = via.Dec(B, D)
+        self.stream = torch.cuda.current_stream()
+
+    # ----------------------------------------------------------- sequences
+    def sp(self):
+        return C.c_void_p(self.stream.cuda_stream)
+
+    def prefill(self, seq, tokens):
+        """Cache tokens[0..n-2]; tokens[-1] becomes the pending token."""
+        t, tp = via._i32(tokens[:-1])
+        via.check(via.via_prefill(self.m.h, self.kv.h, seq, tp, len(tokens) - 1, self.sp()))
+        self.tokens[seq] = list(tokens)
+
+    def reserve(self, seq, tokens, kv_values=None):
+        """Attach with n-1 context slots whose K/V are supplied by the caller.
+
+        kv_values(cache, layer_slot) -> (K, V) tensors [n-1, KVH, hd] in the
+        model dtype (host or device); written into the paged pools."""
+        n1 = len(tokens) - 1
+        via.check(via.via_kv_seq_reserve(self.kv.h, seq, n1))
+        self.tokens[seq] = list(tokens)
+        if kv_values is not None:
+            self.write_context(seq, n1, kv_values)
+
+    def write_context(self, seq, n1, kv_values):
+        md = self.m.desc
+        KVH, hd = md["n_kv_heads"], md["head_dim"]
+        for cache in (via.CACHE_FULL, via.CACHE_SLIM):
+            _, table = self.kv.seq_info(seq, cache)
+            pv = self.kv.pool_view(cache)
+            nb = (n1 + via.BLOCK - 1) // via.BLOCK
+            idx = torch.as_tensor(table[:nb], dtype=torch.long, device=pv.device)
+            slots = pv.shape[0]
+            for s in range(slots):
+                K, V = kv_values(cache, s)
+                K = torch.as_tensor(K).to(pv.device).view(pv.dtype) if K.dtype != pv.dtype else K.to(pv.device)
+                V = torch.as_tensor(V).to(pv.device).view(pv.dtype) if V.dtype != pv.dtype else V.to(pv.device)
+                pad = nb * via.BLOCK - n1
+                if pad:
+                    K = torch.cat([K, torch.zeros((pad, KVH, hd), dtype=K.dtype, device=K.device)])
+                    V = torch.cat([V, torch.zeros((pad, KVH, hd), dtype=V.dtype, device=V.device)])
+                Kp = K.view(nb, via.BLOCK, KVH, hd).permute(0, 2, 1, 3).reshape(nb, KVH, via.BLOCK * hd)
+                Vp = V.view(nb, via.BLOCK, KVH, hd).permute(0, 2, 3, 1).reshape(nb, KVH, via.BLOCK * hd)
+                pv[s, :, 0].index_copy_(0, idx, Kp.contiguous())
+                pv[s, :, 1].index_copy_(0, idx, Vp.contiguous())
+
+    def release(self, seq):
+        via.check(via.via_kv_seq_release(self.kv.h, seq))
+        self.tokens.pop(seq, None)
+
+    def lag(self, seq):
+        vf, _ = self.kv.seq_info(seq, via.CACHE_FULL)
+        n = len(self.tokens[seq])
+        return self.tokens[seq][vf:n - 1]
+
+    # --------------------------------------------------------------- windows
+    def window(self, drafts: dict, with_lag=False):
+        """drafts: {seq: (tokens, parents or None)} -> WindowBuf."""
+        seqs = list(drafts)
+        rows, dtoks, drows, parents, depths, masks, lags = [], [], [], [], [], [], []
+        tree = any(drafts[s][1] is not None for s in seqs)
+        for s in seqs:
+            tok, par = drafts[s]
+            pend = self.tokens[s][-1]
+            if par is None and not tree:
+                rows.append([pend] + list(tok[:-1]))
+                dtoks.append(list(tok))
+                drows.append(list(range(len(tok))))
+            else:
+                par = list(par) if par is not None else [j - 1 for j in range(len(tok))]
+                rn, dr, rd, mk = tree_layout(tok, par)
+                rows.append([pend] + [tok[u] for u in rn[1:]])
+                dtoks.append(list(tok))
+                drows.append(dr)
+                parents.append(par)
+                depths.append(rd)
+                masks.append(mk)
+            if with_lag:
+                lags.append(self.lag(s))
+        return via.WindowBuf(seqs, rows, dtoks, drows, parents if tree else None, depths if tree else None,
+                             masks if tree else None, lags if with_lag else None,
+                             max_rows=max(len(r) for r in rows), max_drafts=max(1, max(len(d) for d in dtoks)))
+
+    # ------------------------------------------------------------------ step
+    def begin(self, drafts: dict):
+        """Slim forward, decision, and the full forward where needed.
+        Returns (window, host decision, full ran per batch entry)."""
+        w = self.window(drafts, with_lag=True)
+        self._w = w
+        via.check(via.via_verify_slim(self.m.h, self.kv.h, C.byref(w.c), C.byref(self.p),
+                                      C.byref(self.out_slim.c), self.sp()))
+        via.check(via.via_tier_decide(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c), None,
+                                      C.byref(self.dec.c), self.sp()))
+        self.stream.synchronize()
+        h = self._host(w)
+        run = (h["status"] == 1).astype(np.int32)
+        if run.any():
+            r, rp = via._i32(run)
+            via.check(via.via_verify_full(self.m.h, self.kv.h, C.byref(w.c), rp, C.byref(self.p),
+                                          C.byref(self.out_full.c), self.sp()))
+            via.check(via.via_tier_decide(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c),
+                                          C.byref(self.out_full.c), C.byref(self.dec.c), self.sp()))
+            self.stream.synchronize()
+            h = self._host(w)
+        return w, h, run
+
+    def _host(self, w):
+        B, D = w.B, w.max_drafts
+        hp = self.dec.h_packed.numpy()
+        return dict(status=hp[:B].copy(), kappa=hp[B:2 * B].copy(), emit=hp[2 * B:3 * B].copy(),
+                    new_len=hp[3 * B:4 * B].copy(), path=hp[4 * B:4 * B + B * D].reshape(B, D).copy())
+
+    def commit(self, w, drafts: dict, h=None):
+        """Commit the open step; ``h`` (host decision) may replace the
+        device's (lock-step parity re-sync)."""
+        B, D = w.B, w.max_drafts
+        if h is not None:
+            hp = self.dec.h_packed.numpy()
+            hp[:B], hp[B:2 * B], hp[2 * B:3 * B], hp[3 * B:4 * B] = h["status"], h["kappa"], h["emit"], h["new_len"]
+            hp[4 * B:4 * B + B * D] = np.asarray(h["path"], np.int32).reshape(-1)
+        else:
+            h = self._host(w)
+        via.check(via.via_kv_commit_rollback(self.kv.h, C.byref(self.dec.c), self.sp()))
+        for b, s in enumerate(w.a["seq"].tolist()):
+            if h["status"][b] != 0:
+                continue
+            tok = drafts[s][0]
+            k = int(h["kappa"][b])
+            new = [tok[j] for j in h["path"][b][:k]]
+            if h["emit"][b] >= 0:
+                new.append(int(h["emit"][b]))
+            self.tokens[s].extend(new)
+        return h
+
+    def step(self, drafts: dict):
+        w, h, run = self.begin(drafts)
+        self.commit(w, drafts)
+        return h, run
+
+
+class GreedyDrafter:
+    """Synthetic drafter on the GPU: the full verifier's greedy token on the
+    draft's own prefix (probe forwards, no change to the KV state), with
+    positions replaced by the workload's corruption draws."""
+
+    def __init__(self, sess: Session, corrupt_fn):
+        self.s = sess
+        self.corrupt = corrupt_fn
+        kv = sess.kv
+        self.out = via.Out(kv.max_batch, kv.max_rows, kv.max_drafts, sess.m.desc["vocab"], logits=False)
+
+    def chain(self, seqs, k, step):
+        s = self.s
+        drafts = {q: [] for q in seqs}
+        for j in range(k):
+            rows = {q: [s.tokens[q][-1]] + drafts[q] for q in seqs}
+            lags = [s.lag(q) for q in seqs]
+            w = via.WindowBuf(seqs, [rows[q] for q in seqs], [[] for _ in seqs], [[] for _ in seqs],
+                              lags=lags, max_drafts=1)
+            via.check(via.via_verify_probe(s.m.h, s.kv.h, via.CACHE_FULL, C.byref(w.c), C.byref(s.p),
+                                           C.byref(self.out.c), s.sp()))
+            am = self.out.row_argmax.cpu().numpy()
+            for b, q in enumerate(seqs):
+                g = int(am[b * w.max_rows + len(rows[q]) - 1])
+                rep, tok = self.corrupt(q, step, j)
+                drafts[q].append(tok if rep else g)
+        return drafts

@@ -1,0 +1,319 @@
+"""ctypes binding of libvia.so (include/via.h), names as in the C ABI.
+
+Argument marshalling only: every step of the verification path runs in the
+library's HIP kernels.  torch supplies device memory (weights, KV pools,
+workspace, outputs), pinned host buffers and the stream.  Importing this
+module fails loudly if the built library is missing.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvia.so")
+
+OK, EINVAL, ENOMEM, EDEVICE, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+DTYPE_F32, DTYPE_BF16 = 0, 1
+CACHE_FULL, CACHE_SLIM = 0, 1
+TIER_ACCEPT, TIER_SLIM, TIER_FULL = 0, 1, 2
+FORCED_NONE, FORCED_ACCEPT, FORCED_SLIM, FORCED_FULL = -1, 0, 1, 2
+BLOCK = 16
+MAX_TREE_ROWS = 64
+MAX_DRAFTS = 64
+
+
+class ViaError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"via status {status}: {msg}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_12243_amd.build`")
+    return C.CDLL(LIB_PATH)
+
+
+lib = _load()
+
+P = C.c_void_p
+I32 = C.c_int32
+PI32 = C.POINTER(C.c_int32)
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [("n_layers", I32), ("d_model", I32), ("n_heads", I32), ("n_kv_heads", I32),
+                ("head_dim", I32), ("d_ffn", I32), ("vocab", I32), ("rms_eps", C.c_float),
+                ("rope_theta", C.c_float), ("dtype", I32)]
+
+
+class Weights(C.Structure):
+    _fields_ = [("embed", P), ("lm_head", P), ("final_norm", P), ("attn_norm", C.POINTER(P)),
+                ("w_qkv", C.POINTER(P)), ("w_o", C.POINTER(P)), ("ffn_norm", C.POINTER(P)),
+                ("w_gate_up", C.POINTER(P)), ("w_down", C.POINTER(P))]
+
+
+class TierParams(C.Structure):
+    _fields_ = [("tau_acc", C.c_float), ("tau_full", C.c_float), ("temperature", C.c_float), ("forced", I32)]
+
+
+class KvDesc(C.Structure):
+    _fields_ = [("block_size", I32), ("max_seqs", I32), ("max_blocks_per_seq", I32), ("blocks_full", I32),
+                ("blocks_slim", I32), ("pool_full", P), ("pool_slim", P), ("max_rows", I32),
+                ("max_batch", I32), ("max_drafts", I32), ("workspace", P), ("workspace_bytes", C.c_size_t),
+                ("pinned_staging", P), ("staging_bytes", C.c_size_t)]
+
+
+class Window(C.Structure):
+    _fields_ = [("batch", I32), ("max_rows", I32), ("max_drafts", I32), ("max_lag", I32),
+                ("seq_id", PI32), ("n_rows", PI32), ("row_tok", PI32), ("row_depth", PI32),
+                ("row_mask", C.POINTER(C.c_uint64)), ("n_drafts", PI32), ("draft_tok", PI32),
+                ("draft_row", PI32), ("draft_parent", PI32), ("n_lag", PI32), ("lag_tok", PI32)]
+
+
+class VerifyOut(C.Structure):
+    _fields_ = [("row_argmax", P), ("row_max", P), ("row_sumexp", P), ("row_gap", P),
+                ("draft_logit", P), ("logits", P)]
+
+
+class Decision(C.Structure):
+    _fields_ = [("tier", P), ("conf", P), ("packed", P), ("h_packed", P)]
+
+
+def _sig(name, res, *args):
+    f = getattr(lib, name)
+    f.restype = res
+    f.argtypes = list(args)
+    return f
+
+
+via_pool_bytes = _sig("via_pool_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32)
+via_workspace_bytes = _sig("via_workspace_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
+via_staging_bytes = _sig("via_staging_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
+via_model_create = _sig("via_model_create", I32, C.POINTER(ModelDesc), C.POINTER(Weights), C.POINTER(P))
+via_model_set_route = _sig("via_model_set_route", I32, P, PI32, I32)
+via_model_destroy = _sig("via_model_destroy", I32, P)
+via_kv_create = _sig("via_kv_create", I32, P, C.POINTER(KvDesc), C.POINTER(P))
+via_kv_destroy = _sig("via_kv_destroy", I32, P)
+via_kv_seq_reserve = _sig("via_kv_seq_reserve", I32, P, I32, I32)
+via_prefill = _sig("via_prefill", I32, P, P, I32, PI32, I32, P)
+via_kv_seq_release = _sig("via_kv_seq_release", I32, P, I32)
+via_kv_seq_info = _sig("via_kv_seq_info", I32, P, I32, I32, PI32, PI32, I32, PI32)
+via_verify_slim = _sig("via_verify_slim", I32, P, P, C.POINTER(Window), C.POINTER(TierParams),
+                       C.POINTER(VerifyOut), P)
+via_verify_full = _sig("via_verify_full", I32, P, P, C.POINTER(Window), PI32, C.POINTER(TierParams),
+                       C.POINTER(VerifyOut), P)
+via_verify_probe = _sig("via_verify_probe", I32, P, P, I32, C.POINTER(Window), C.POINTER(TierParams),
+                        C.POINTER(VerifyOut), P)
+via_tier_decide = _sig("via_tier_decide", I32, P, C.POINTER(TierParams), C.POINTER(VerifyOut),
+                       C.POINTER(VerifyOut), C.POINTER(Decision), P)
+via_kv_commit_rollback = _sig("via_kv_commit_rollback", I32, P, C.POINTER(Decision), P)
+via_last_error = _sig("via_last_error", C.c_char_p)
+via_version = _sig("via_version", C.c_char_p)
+
+EXPORTS = ["via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
+           "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
+           "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
+           "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide",
+           "via_kv_commit_rollback", "via_last_error", "via_version"]
+
+
+def check(status):
+    if status != OK:
+        raise ViaError(status, via_last_error().decode())
+    return status
+
+
+def _ptr(t: torch.Tensor):
+    return C.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _i32(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return a, a.ctypes.data_as(PI32)
+
+
+def model_desc(m: dict) -> ModelDesc:
+    return ModelDesc(m["n_layers"], m["d_model"], m["n_heads"], m["n_kv_heads"], m["head_dim"], m["d_ffn"],
+                     m["vocab"], float(m["rms_eps"]), float(m["rope_theta"]),
+                     DTYPE_BF16 if m["dtype"] == "bf16" else DTYPE_F32)
+
+
+def stream_ptr(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+class Model:
+    """Device weights + via_model handle.  ``weights`` as produced by the
+    workload generator (numpy uint16 bf16 bits or float32)."""
+
+    def __init__(self, desc: dict, weights: dict, route, device="cuda"):
+        self.desc = dict(desc)
+        self.cdesc = model_desc(desc)
+        bf16 = desc["dtype"] == "bf16"
+
+        def dev(a):
+            if isinstance(a, torch.Tensor):
+                return a.to(device).contiguous()
+            t = torch.from_numpy(a.view(np.int16) if bf16 else a)
+            t = t.view(torch.bfloat16) if bf16 else t
+            return t.to(device).contiguous()
+
+        self.t = {}
+        for k, v in weights.items():
+            self.t[k] = [dev(x) for x in v] if isinstance(v, list) else dev(v)
+        L = desc["n_layers"]
+        arr = lambda k: (P * L)(*[x.data_ptr() for x in self.t[k]])
+        self._arrs = {k: arr(k) for k in ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")}
+        w = Weights(self.t["embed"].data_ptr(), self.t["lm_head"].data_ptr(), self.t["final_norm"].data_ptr(),
+                    self._arrs["attn_norm"], self._arrs["w_qkv"], self._arrs["w_o"], self._arrs["ffn_norm"],
+                    self._arrs["w_gate_up"], self._arrs["w_down"])
+        h = P()
+        check(via_model_create(C.byref(self.cdesc), C.byref(w), C.byref(h)))
+        self.h = h
+        self.route = list(route)
+        r, rp = _i32(self.route)
+        check(via_model_set_route(self.h, rp, len(self.route)))
+
+    def close(self):
+        if self.h:
+            check(via_model_destroy(self.h))
+            self.h = None
+
+
+class KV:
+    """Paged full/slim KV pools, workspace and pinned staging of one handle."""
+
+    def __init__(self, model: Model, max_seqs, max_blocks_per_seq, blocks_full, blocks_slim, max_rows,
+                 max_batch, max_drafts, device="cuda", zero_pools=True):
+        self.model = model
+        d = model.cdesc
+        esz = 2 if model.desc["dtype"] == "bf16" else 4
+        nb_full = via_pool_bytes(C.byref(d), model.desc["n_layers"], blocks_full, BLOCK)
+        nb_slim = via_pool_bytes(C.byref(d), len(model.route), blocks_slim, BLOCK)
+        mk = torch.zeros if zero_pools else torch.empty
+        dt = torch.bfloat16 if esz == 2 else torch.float32
+        self.pool_full = mk(nb_full // esz, dtype=dt, device=device)
+        self.pool_slim = mk(nb_slim // esz, dtype=dt, device=device)
+        wsb = via_workspace_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts)
+        stb = via_staging_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts)
+        self.workspace = torch.empty(wsb, dtype=torch.uint8, device=device)
+        self.staging = torch.empty(stb, dtype=torch.uint8, pin_memory=True)
+        self.cd = KvDesc(BLOCK, max_seqs, max_blocks_per_seq, blocks_full, blocks_slim,
+                         self.pool_full.data_ptr(), self.pool_slim.data_ptr(), max_rows, max_batch,
+                         max_drafts, self.workspace.data_ptr(), wsb, self.staging.data_ptr(), stb)
+        h = P()
+        check(via_kv_create(model.h, C.byref(self.cd), C.byref(h)))
+        self.h = h
+        self.max_batch, self.max_drafts, self.max_rows = max_batch, max_drafts, max_rows
+
+    def close(self):
+        if self.h:
+            check(via_kv_destroy(self.h))
+            self.h = None
+
+    def seq_info(self, seq, cache):
+        valid, nb = C.c_int32(), C.c_int32()
+        check(via_kv_seq_info(self.h, seq, cache, C.byref(valid), None, 0, C.byref(nb)))
+        tab = np.zeros(max(1, nb.value), dtype=np.int32)
+        check(via_kv_seq_info(self.h, seq, cache, C.byref(valid), tab.ctypes.data_as(PI32), len(tab),
+                              C.byref(nb)))
+        return valid.value, tab[:nb.value].tolist()
+
+    def pool_view(self, cache):
+        """Pool as [slots, blocks, 2, KVH, 16*hd] (K page token-major, V page transposed)."""
+        m = self.model.desc
+        slots = m["n_layers"] if cache == CACHE_FULL else len(self.model.route)
+        nb = self.cd.blocks_full if cache == CACHE_FULL else self.cd.blocks_slim
+        t = self.pool_full if cache == CACHE_FULL else self.pool_slim
+        return t.view(slots, nb, 2, m["n_kv_heads"], BLOCK * m["head_dim"])
+
+
+class WindowBuf:
+    """Host arrays of a via_window (kept alive with the struct)."""
+
+    def __init__(self, seq_ids, rows, drafts, draft_rows, parents=None, depths=None, masks=None,
+                 lags=None, max_rows=None, max_drafts=None):
+        B = len(seq_ids)
+        self.B = B
+        self.max_rows = max_rows or max(len(r) for r in rows)
+        self.max_drafts = max_drafts or max(1, max(len(d) for d in drafts))
+        self.max_lag = max(1, max((len(l) for l in lags), default=1)) if lags else 1
+        R, D, Lg = self.max_rows, self.max_drafts, self.max_lag
+        self.a = {}
+
+        def grid(lists, width, fill=0, dtype=np.int32):
+            g = np.full((B, width), fill, dtype=dtype)
+            for b, l in enumerate(lists):
+                g[b, :len(l)] = l
+            return g.reshape(-1)
+
+        self.a["seq"] = np.asarray(seq_ids, np.int32)
+        self.a["n_rows"] = np.asarray([len(r) for r in rows], np.int32)
+        self.a["row_tok"] = grid(rows, R)
+        self.a["n_drafts"] = np.asarray([len(d) for d in drafts], np.int32)
+        self.a["draft_tok"] = grid(drafts, D)
+        self.a["draft_row"] = grid(draft_rows, D)
+        tree = parents is not None
+        if tree:
+            self.a["draft_parent"] = grid(parents, D, -1)
+            self.a["row_depth"] = grid(depths, R)
+            self.a["row_mask"] = grid(masks, R, 0, np.uint64)
+        if lags is not None:
+            self.a["n_lag"] = np.asarray([len(l) for l in lags], np.int32)
+            self.a["lag_tok"] = grid(lags, Lg)
+        g = lambda k: self.a[k].ctypes.data_as(PI32) if k in self.a else None
+        self.c = Window(B, R, D, Lg, g("seq"), g("n_rows"), g("row_tok"), g("row_depth"),
+                        self.a["row_mask"].ctypes.data_as(C.POINTER(C.c_uint64)) if tree else None,
+                        g("n_drafts"), g("draft_tok"), g("draft_row"), g("draft_parent"), g("n_lag"),
+                        g("lag_tok"))
+
+
+class Out:
+    """Device outputs of one verify forward."""
+
+    def __init__(self, B, max_rows, max_drafts, vocab=None, logits=False, device="cuda"):
+        n = B * max_rows
+        self.row_argmax = torch.empty(n, dtype=torch.int32, device=device)
+        self.row_max = torch.empty(n, dtype=torch.float32, device=device)
+        self.row_sumexp = torch.empty(n, dtype=torch.float32, device=device)
+        self.row_gap = torch.empty(n, dtype=torch.float32, device=device)
+        self.draft_logit = torch.empty(B * max_drafts, dtype=torch.float32, device=device)
+        self.logits = torch.empty(n * vocab, dtype=torch.float32, device=device) if logits else None
+        self.c = VerifyOut(self.row_argmax.data_ptr(), self.row_max.data_ptr(), self.row_sumexp.data_ptr(),
+                           self.row_gap.data_ptr(), self.draft_logit.data_ptr(),
+                           self.logits.data_ptr() if logits else None)
+
+
+class Dec:
+    """Decision arrays (device) + pinned host mirror of the packed block."""
+
+    def __init__(self, B, max_drafts, device="cuda"):
+        self.B, self.D = B, max_drafts
+        self.tier = torch.empty(B * max_drafts, dtype=torch.int8, device=device)
+        self.conf = torch.empty(B * max_drafts, dtype=torch.float32, device=device)
+        self.packed = torch.empty(4 * B + B * max_drafts, dtype=torch.int32, device=device)
+        self.h_packed = torch.empty(4 * B + B * max_drafts, dtype=torch.int32, pin_memory=True)
+        self.c = Decision(self.tier.data_ptr(), self.conf.data_ptr(), self.packed.data_ptr(),
+                          self.h_packed.data_ptr())
+
+    def host(self):
+        h = self.h_packed.numpy()
+        B = self.B
+        return dict(status=h[:B].copy(), kappa=h[B:2 * B].copy(), emit=h[2 * B:3 * B].copy(),
+                    new_len=h[3 * B:4 * B].copy(), path=h[4 * B:].reshape(B, self.D).copy())
+
+    def set_host(self, status, kappa, emit, new_len, path):
+        h = self.h_packed.numpy()
+        B = self.B
+        h[:B], h[B:2 * B], h[2 * B:3 * B], h[3 * B:4 * B] = status, kappa, emit, new_len
+        h[4 * B:] = np.asarray(path, np.int32).reshape(-1)
+
+
+def tier_params(tau_acc=0.9, tau_full=0.5, temperature=1.0, forced=FORCED_NONE):
+    return TierParams(tau_acc, tau_full, temperature, forced)

@@ -1,0 +1,180 @@
+"""Lock-step parity runner: the HIP path (through the C ABI) and the oracle
+decode the same sequences from the same drafts, step by step.
+
+Each step both sides start from the same committed state.  Compared per
+step: slim/full logits (fp32 dump; tolerance 2e-2 for bf16 models, 1e-4 for
+fp32), row argmaxes, every draft's tier, which sequences escalate, the
+accepted length, the emitted token, the new length, and both caches' valid
+lengths and block tables.  A difference is allowed only where the oracle
+itself is within 1e-3 of a decision boundary: a top-2 logit gap below 1e-3
+(argmax / full-tier check) or a draft logit within 1e-3 of a threshold
+(l'(d) - max l' vs T ln tau).  After such an exempt difference the GPU is
+re-synchronised to the oracle's decision (its commit takes the oracle's
+kappa/emit) and the step is logged.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from oracle.decode import (FORCED_NONE, Draft, GreedyDrafter, TierParams, Verifier)
+from oracle.model import OracleModel, round_bf16
+from paper_2606_12243_amd import via
+from paper_2606_12243_amd.session import Session
+from workload import gen
+
+GAP_EXEMPT = 1e-3
+TIER_CODE = {"A": 0, "S": 1, "F": 2}
+
+
+def logit_tol(desc):
+    return 2e-2 if desc["dtype"] == "bf16" else 1e-4
+
+
+class Lockstep:
+    def __init__(self, cfg, weights=None, max_rows=None, max_batch=None, max_drafts=None, max_blocks=None,
+                 blocks=None, params=None, oracle_model=None):
+        self.cfg = cfg
+        md = cfg["model"]
+        self.md = md
+        W = weights if weights is not None else gen.model_weights(cfg)
+        self.om = oracle_model or OracleModel(md, W)
+        self.p = params or TierParams(0.9, 0.5, cfg.get("temperature", 1.0))
+        self.ver = Verifier(self.om, cfg["route"], block_size=16)
+        V = md["vocab"]
+        self.drafter = GreedyDrafter(self.om, lambda b, step, j: gen.corruption(
+            cfg["seed_d"], b, step, j, cfg.get("corrupt", 0.3), V))
+        B = max_batch or cfg.get("batch", 1)
+        self.gm = via.Model(md, W, cfg["route"])
+        self.kv = via.KV(self.gm, max_seqs=B, max_blocks_per_seq=max_blocks or 64, blocks_full=blocks or 256,
+                         blocks_slim=blocks or 256, max_rows=max_rows or 128, max_batch=B,
+                         max_drafts=max_drafts or 16)
+        self.sess = Session(self.gm, self.kv, via.tier_params(self.p.tau_acc, self.p.tau_full, self.p.temperature,
+                                                             self.p.forced), logits=True)
+        self.log = []
+        self.seen_tiers = set()
+        self.max_logit_err = 0.0
+
+    def close(self):
+        self.kv.close()
+        self.gm.close()
+
+    # ------------------------------------------------------------ setup
+    def add_prompt(self, b, tokens):
+        self.ver.prefill(tokens)
+        self.drafter.attach(b)
+        self.sess.prefill(b, tokens)
+
+    # ------------------------------------------------------------ checks
+    def _cmp_logits(self, w, out, o_logits, b, what):
+        R = w.max_rows
+        V = self.md["vocab"]
+        n = int(w.a["n_rows"][b])
+        g = out.logits[b * R * V:(b * R + n) * V].view(n, V).double().cpu()
+        err = float((g - o_logits).abs().max())
+        self.max_logit_err = max(self.max_logit_err, err)
+        assert err <= logit_tol(self.md), f"{what} logits of seq {b}: max |diff| {err}"
+        am = out.row_argmax[b * R:b * R + n].cpu().numpy()
+        return am
+
+    def step(self, drafts: dict, step_idx: int):
+        """drafts: {b: Draft}; runs both sides, compares, commits."""
+        p = self.p
+        order = sorted(drafts)
+        dec_o = self.ver.step(drafts, p)          # oracle decides and commits
+        gd = {b: (drafts[b].tok, None if self._is_chain(drafts[b]) else drafts[b].parent) for b in order}
+        s = self.sess
+        w = s.window(gd, with_lag=True)
+        via.check(via.via_verify_slim(s.m.h, s.kv.h, w.c, s.p, s.out_slim.c, s.sp()))
+        via.check(via.via_tier_decide(s.kv.h, s.p, s.out_slim.c, None, s.dec.c, s.sp()))
+        s.stream.synchronize()
+        h1 = s._host(w)
+        exempt = False
+        T = p.temperature
+        for i, b in enumerate(order):
+            do = dec_o[b]
+            am = self._cmp_logits(w, s.out_slim, do["slim_logits"], i, "slim")
+            st = do["slim_stats"]
+            for r in range(len(am)):
+                if am[r] != st["argmax"][r]:
+                    assert st["gap"][r] < GAP_EXEMPT, f"slim argmax differs at gap {st['gap'][r]}"
+                    exempt = True
+            D = w.max_drafts
+            tier_g = s.dec.tier[i * D:i * D + len(drafts[b].tok)].cpu().numpy()
+            for j, t in enumerate(do["tiers"]):
+                self.seen_tiers.add(t)
+                if tier_g[j] != TIER_CODE[t]:
+                    dl = do["slim_draft_logit"][j] - st["max"][do["draft_row"][j]]
+                    near = min(abs(dl - T * math.log(p.tau_acc)) if p.tau_acc > 0 else 1e9,
+                               abs(dl - T * math.log(p.tau_full)) if p.tau_full > 0 else 1e9)
+                    assert near < GAP_EXEMPT, f"tier of draft {j} differs ({tier_g[j]} vs {t}), margin {near}"
+                    exempt = True
+            if (h1["status"][i] == 1) != (do["first_status"] == 1):
+                assert exempt, f"escalation differs for seq {b}"
+        # full forward for the sequences the oracle escalated (keeps cache state in step)
+        run = np.array([1 if dec_o[b]["full_ran"] else 0 for b in order], np.int32)
+        if run.any():
+            r, rp = via._i32(run)
+            via.check(via.via_verify_full(s.m.h, s.kv.h, w.c, rp, s.p, s.out_full.c, s.sp()))
+            via.check(via.via_tier_decide(s.kv.h, s.p, s.out_slim.c, s.out_full.c, s.dec.c, s.sp()))
+            s.stream.synchronize()
+            for i, b in enumerate(order):
+                if not run[i]:
+                    continue
+                do = dec_o[b]
+                am = self._cmp_logits(w, s.out_full, do["full_logits"], i, "full")
+                st = do["full_stats"]
+                for rr in range(len(am)):
+                    if am[rr] != st["argmax"][rr]:
+                        assert st["gap"][rr] < GAP_EXEMPT, f"full argmax differs at gap {st['gap'][rr]}"
+                        exempt = True
+        h = s._host(w)
+        same = True
+        for i, b in enumerate(order):
+            do = dec_o[b]
+            got = (int(h["status"][i]), int(h["kappa"][i]), int(h["emit"][i]), int(h["new_len"][i]))
+            want = (do["status"], do["kappa"], do["emit"], do["new_len"])
+            if got != want:
+                assert exempt, f"step {step_idx} seq {b}: GPU {got} oracle {want}"
+                same = False
+        if not same:
+            self.log.append(dict(step=step_idx, kind="resync"))
+            D = w.max_drafts
+            path = np.full((w.B, D), -1, np.int32)
+            for i, b in enumerate(order):
+                pp = dec_o[b]["path"]
+                path[i, :len(pp)] = pp
+            h = dict(status=np.array([dec_o[b]["status"] for b in order], np.int32),
+                     kappa=np.array([dec_o[b]["kappa"] for b in order], np.int32),
+                     emit=np.array([dec_o[b]["emit"] for b in order], np.int32),
+                     new_len=np.array([dec_o[b]["new_len"] for b in order], np.int32), path=path)
+            s.commit(w, gd, h)
+        else:
+            s.commit(w, gd)
+        # committed tokens, valid lengths and block tables
+        for b in order:
+            st = self.ver.seqs[b]
+            assert s.tokens[b] == st.tokens, f"seq {b} token streams differ"
+            for cache, oc, which in ((via.CACHE_FULL, st.full, "full"), (via.CACHE_SLIM, st.slim, "slim")):
+                valid, table = self.kv.seq_info(b, cache)
+                assert valid == oc.valid, f"seq {b} {which} valid {valid} vs {oc.valid}"
+                assert table == self.ver.block_table(which, b), f"seq {b} {which} block table differs"
+        return dec_o, h
+
+    @staticmethod
+    def _is_chain(d: Draft):
+        return all(p == j - 1 for j, p in enumerate(d.parent))
+
+    def run_chain(self, seqs, G, k):
+        n0 = {b: len(self.ver.seqs[b].tokens) for b in seqs}
+        step = 0
+        while True:
+            active = [b for b in seqs if len(self.ver.seqs[b].tokens) - n0[b] < G]
+            if not active:
+                break
+            drafts = {b: self.drafter.chain(b, self.ver.seqs[b].tokens, k, step) for b in active}
+            self.step(drafts, step)
+            step += 1
+        return step
