@@ -1,0 +1,279 @@
+#!/usr/bin/env python
+"""Benchmark of the VIA-SD verification step on one MI355X (gfx950).
+
+A step is one pass of the whole verification hot path over a batch:
+slim-verifier forward + fused head, tier decision (device->host read),
+the full-verifier forward with its lag rows when any sequence escalates,
+the second decision, and the KV commit/rollback.  Drafts come from a
+synthetic drafter (the full verifier's greedy token with random
+replacements) run beforehand: an untimed reference decode records every
+step's drafts, then the KV state is reset and the recorded steps are
+replayed; W replayed steps warm up, the next K are timed.
+
+value = accepted (committed) tokens summed over the batch / timed seconds.
+The JSON line adds the verify-step latency percentiles, the roofline of the
+dominant kernel (HIP events on the library's stream during the timed
+region) and the oracle's rate on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--config 8b_bf16_chain]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "accepted tokens/s + verify-step latency, 8B-shape bf16 k=8; % HBM/MFMA roofline"
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def build_session(cfg, W, pools=None, n_steps=64):
+    import torch
+    from paper_2606_12243_amd import via
+    from paper_2606_12243_amd.session import Session
+    md = cfg["model"]
+    B = cfg["batch"]
+    ctx = cfg["ctx_lens"]
+    k = cfg.get("k", 8)
+    rows_per_seq = 64 if cfg["draft"] == "tree" else k * 8
+    max_rows = B * rows_per_seq
+    grow = n_steps * ((k + 1) if cfg["draft"] != "tree" else len(cfg["tree_budget"]) + 1)
+    max_blocks = (max(ctx) + grow + rows_per_seq + 16) // 16 + 1
+    blocks = B * max_blocks
+    model = cfg.get("_model")
+    kv = via.KV(model, max_seqs=B, max_blocks_per_seq=max_blocks, blocks_full=blocks, blocks_slim=blocks,
+                max_rows=max_rows, max_batch=B, max_drafts=64, zero_pools=False, pools=pools)
+    p = via.tier_params(0.9, 0.5, cfg["temperature"])
+    return Session(model, kv, p)
+
+
+def attach_context(cfg, sess, synthetic):
+    from workload import gen
+    import torch
+    B = cfg["batch"]
+    for b, n in enumerate(cfg["ctx_lens"]):
+        toks = gen.context_tokens(cfg, b, n + 1)
+        if synthetic:
+            def kvv(cache, slot, b=b, n=n):
+                K, V = gen.synthetic_kv(cfg, cache, slot, b, n)
+                return (torch.from_numpy(K.view(np.int16)).view(torch.bfloat16),
+                        torch.from_numpy(V.view(np.int16)).view(torch.bfloat16))
+            sess.reserve(b, toks, kvv)
+        else:
+            sess.prefill(b, toks)
+
+
+def step_bytes(cfg, h, rows_slim, rows_full):
+    """Algorithmic HBM bytes of one step: weights of the routed layers +
+    head for the slim forward, the same for all layers when q ran, plus the
+    cached K/V each forward reads."""
+    from workload.configs import model_bytes
+    md = cfg["model"]
+    slim = model_bytes(md, cfg["route"])
+    full = model_bytes(md)
+    kvb = slim["kv_per_token_layer"]
+    tot = slim["layers"] + slim["head"] + kvb * len(cfg["route"]) * rows_slim["ctx"]
+    if rows_full["n"] > 0:
+        tot += full["layers"] + full["head"] + kvb * md["n_layers"] * rows_full["ctx"]
+    return tot
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="8b_bf16_chain")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the verification step of a batch "
+                                   "is measured on a single MI355X (--gpus 1)", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    from paper_2606_12243_amd import via
+    from paper_2606_12243_amd.session import GreedyDrafter
+    from workload import configs, gen
+
+    cfg = configs.get(args.config)
+    md = cfg["model"]
+    cfg["ctx_lens"] = gen.context_lengths(cfg)
+    synthetic = cfg.get("seed_kv") is not None
+    t0 = time.time()
+    W = gen.model_weights(cfg)
+    log(f"weights generated in {time.time() - t0:.1f}s")
+    t0 = time.time()
+    cfg["_model"] = via.Model(md, W, cfg["route"])
+    torch.cuda.synchronize()
+    log(f"weights on device in {time.time() - t0:.1f}s")
+    n_steps = args.warmup + args.steps
+    sess = build_session(cfg, W, n_steps=n_steps)
+    t0 = time.time()
+    attach_context(cfg, sess, synthetic)
+    torch.cuda.synchronize()
+    log(f"context attached ({'synthetic K/V' if synthetic else 'prefill'}) in {time.time() - t0:.1f}s")
+    V = md["vocab"]
+    drafter = GreedyDrafter(sess, lambda b, step, j: gen.corruption(cfg["seed_d"], b, step, j, cfg["corrupt"], V))
+    B = cfg["batch"]
+
+    # ---- reference decode: record drafts and decisions
+    recorded, t_draft = [], 0.0
+    init_tokens = {b: list(sess.tokens[b]) for b in range(B)}
+    for i in range(n_steps):
+        ts = time.time()
+        if cfg["draft"] == "tree":
+            drafts = drafter.tree(list(range(B)), cfg["tree_budget"], cfg["tree_branch"], i)
+        else:
+            d = drafter.chain(list(range(B)), cfg["k"], i)
+            drafts = {b: (d[b], None) for b in range(B)}
+        torch.cuda.synchronize()
+        t_draft += time.time() - ts
+        h, run = sess.step(drafts)
+        recorded.append((drafts, h["new_len"].copy(), run.copy()))
+    log(f"reference decode: {n_steps} steps, drafting {t_draft:.2f}s")
+
+    # ---- reset: fresh handle on the same pools (context slots untouched)
+    pools = (sess.kv.pool_full, sess.kv.pool_slim)
+    sess.kv.close()
+
+    def fresh():
+        s2 = build_session(cfg, W, pools=pools, n_steps=n_steps)
+        if synthetic:
+            for b in range(B):
+                s2.reserve(b, init_tokens[b], None)
+        else:
+            for b in range(B):
+                s2.prefill(b, init_tokens[b])
+        torch.cuda.synchronize()
+        return s2
+
+    kinds = {"qkv": via.KERNEL_QKV, "attn": via.KERNEL_ATTN, "o": via.KERNEL_O, "gateup": via.KERNEL_GATEUP,
+             "down": via.KERNEL_DOWN, "head": via.KERNEL_HEAD}
+    DOM = "gateup"
+    sess = fresh()
+    mism = 0
+    for i in range(args.warmup):
+        h, run = sess.step(recorded[i][0])
+        mism += int((h["new_len"] != recorded[i][1]).any())
+    torch.cuda.synchronize()
+    sess.kv.timer_enable(1 << kinds[DOM])
+    sess.kv.timer_read(kinds[DOM])
+    lat, accepted, n_full_steps, bytes_tot = [], 0, 0, 0
+    rows_gateup = []
+    tier_counts = np.zeros(3, np.int64)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.warmup, n_steps):
+        drafts = recorded[i][0]
+        n_before = np.array([len(sess.tokens[b]) for b in range(B)])
+        ts = time.perf_counter()
+        w, h, run = sess.begin(drafts)
+        sess.commit(w, drafts)
+        torch.cuda.synchronize()
+        lat.append(time.perf_counter() - ts)
+        accepted += int((h["new_len"] - n_before).sum())
+        mism += int((h["new_len"] != recorded[i][1]).any())
+        n_full_steps += int(run.any())
+    t_total = time.perf_counter() - t_start
+    n_launch, ms_dom = sess.kv.timer_read(kinds[DOM])
+    sess.kv.timer_enable(0)
+
+    value = accepted / t_total
+    lat_ms = np.array(lat) * 1e3
+    # algorithmic bytes of the dominant kernel per launch: gate/up weights of one layer
+    F, d = md["d_ffn"], md["d_model"]
+    esz = 2 if md["dtype"] == "bf16" else 4
+    dom_bytes = 2 * F * d * esz
+    avg_ms = ms_dom / max(1, n_launch)
+    achieved = dom_bytes / (avg_ms * 1e-3) / 1e9 if n_launch else None
+    roof = {"kernel": "gemm gate/up + SwiGLU (one layer)", "bound": "hbm",
+            "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None, "traffic": None,
+            "bytes_per_launch": dom_bytes, "avg_launch_us": round(avg_ms * 1e3, 2), "launches": n_launch}
+
+    breakdown = None
+    if args.breakdown:
+        sess.kv.close()
+        sess = fresh()
+        sess.kv.timer_enable((1 << 6) - 1)
+        for i in range(n_steps):
+            sess.step(recorded[i][0])
+        torch.cuda.synchronize()
+        breakdown = {}
+        for nme, kd in kinds.items():
+            n, ms = sess.kv.timer_read(kd)
+            breakdown[nme] = {"launches": n, "total_ms": round(ms, 3), "avg_us": round(ms * 1e3 / max(1, n), 2)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, W, recorded, init_tokens)
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(float(lat_ms.mean()), 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": md["dtype"], "data": "synthetic",
+        "config": {"workload": args.config, "batch": B, "ctx": cfg["ctx"], "draft": cfg["draft"],
+                   "k": cfg.get("k"), "route_layers": len(cfg["route"]), "n_layers": md["n_layers"],
+                   "d_model": md["d_model"], "vocab": md["vocab"],
+                   "context_kv": "synthetic N(0, (0.02 sqrt d)^2)" if synthetic else "prefill"},
+        "latency_ms": {"p10": round(float(np.percentile(lat_ms, 10)), 3),
+                       "p50": round(float(np.percentile(lat_ms, 50)), 3),
+                       "p90": round(float(np.percentile(lat_ms, 90)), 3)},
+        "escalation_rate": round(n_full_steps / max(1, args.steps), 3),
+        "replay_mismatch_steps": mism,
+        "drafting_s_untimed": round(t_draft, 3),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    if breakdown:
+        out["kernels"] = breakdown
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, W, recorded, init_tokens):
+    """The oracle, as it stands, on a bounded sample: the first recorded step
+    of sequence 0 (slim forward, decision, full forward if escalated)."""
+    import torch
+    from oracle.decode import Draft, TierParams, Verifier
+    from oracle.model import OracleModel
+    from workload import gen
+    md = cfg["model"]
+    om = OracleModel(md, W)
+    ver = Verifier(om, cfg["route"])
+    toks = init_tokens[0]
+    if cfg.get("seed_kv") is not None:
+        n = len(toks) - 1
+        bits = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(torch.float64)
+        kvf = [tuple(bits(x) for x in gen.synthetic_kv(cfg, 0, s, 0, n)) for s in range(md["n_layers"])]
+        kvs = [tuple(bits(x) for x in gen.synthetic_kv(cfg, 1, s, 0, n)) for s in range(len(cfg["route"]))]
+        ver.attach_context(toks, kvf, kvs)
+    else:
+        ver.prefill(toks)
+    tok, par = recorded[0][0][0]
+    d = Draft.chain(tok) if par is None else Draft(list(tok), list(par))
+    t0 = time.perf_counter()
+    dec = ver.step({0: d}, TierParams(0.9, 0.5, cfg["temperature"]))
+    dt = time.perf_counter() - t0
+    acc = dec[0]["new_len"] - len(toks)
+    return {"value": round(acc / dt, 4), "unit": "tokens/s", "cores": torch.get_num_threads(), "kind": "oracle",
+            "sample": f"one verification step of sequence 0 of {cfg['name']} (slim forward, decision"
+                      f"{', full forward' if dec[0]['full_ran'] else ''}) in fp64: {acc} tokens in {dt:.2f}s",
+            "agrees_with_gpu_step": bool(dec[0]["new_len"] == int(recorded[0][1][0]))}
+
+
+if __name__ == "__main__":
+    main()

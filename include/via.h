@@ -261,6 +261,21 @@ via_status via_tier_decide(via_kv *kv, const via_tier_params *p, const via_verif
  * changed) if any status is 1 or no step is open. */
 via_status via_kv_commit_rollback(via_kv *kv, const via_decision *dec, void *stream);
 
+/* ---- kernel timing (profiling aid) --------------------------------------
+ * When a kind's bit is set, every launch of that kernel kind is bracketed by
+ * two HIP events on the call's stream.  via_kv_timer_read waits for the
+ * recorded events, returns the launch count and summed milliseconds of one
+ * kind since the last read of that kind, and forgets them. */
+#define VIA_KERNEL_QKV 0    /* QKV projection + RoPE + paged K/V write */
+#define VIA_KERNEL_ATTN 1   /* window attention (+ split-KV combine) */
+#define VIA_KERNEL_O 2      /* O projection + residual */
+#define VIA_KERNEL_GATEUP 3 /* gate/up projection + SwiGLU */
+#define VIA_KERNEL_DOWN 4   /* down projection + residual */
+#define VIA_KERNEL_HEAD 5   /* output head + row statistics */
+#define VIA_KERNEL_COUNT 6
+via_status via_kv_timer_enable(via_kv *kv, uint32_t kind_mask);
+via_status via_kv_timer_read(via_kv *kv, int32_t kind, int32_t *launches, double *total_ms);
+
 const char *via_last_error(void);
 /* Library version string. */
 const char *via_version(void);

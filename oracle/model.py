@@ -18,12 +18,12 @@ What it follows:
     by the workload (RMSNorm, rotate-half RoPE, GQA attention, SwiGLU, untied
     head) is written out here op by op, each from its textbook definition.
 
-Precision: every quantity is fp64.  For bf16 models the optional
-"storage" mode rounds to bf16 (nearest, ties to even) exactly at the points
-where a bf16 verifier stores activations: the normalised rows fed to a
-projection, Q/K/V after RoPE (K/V as cached), the attention output, the
-SwiGLU product and the final normalised row.  Accumulation, the residual
-stream, norms and softmax stay fp64.
+Precision: every quantity is fp64.  For bf16 models the "storage" mode
+(default on) rounds to bf16 (nearest, ties to even) the one activation a
+bf16 verifier stores in bf16: the key/value cache (K after RoPE, V), which
+later rows read back.  Weights are bf16 values already; every other
+activation (normalised rows, Q, attention output, SwiGLU product, residual
+stream, logits) stays fp64.
 
 Parity pins: see tests/test_oracle_model.py (library routines, RoPE
 closed-form properties, cached == cache-free == token-by-token, routed ==
@@ -102,7 +102,7 @@ class OracleModel:
         return t64
 
     def store(self, x: torch.Tensor) -> torch.Tensor:
-        """Apply the bf16 storage rounding when that mode is on."""
+        """Cache storage: round K/V to bf16 when that mode is on."""
         return round_bf16(x) if self.storage_bf16 else x
 
     # ---------------------------------------------------------------- ops
@@ -150,7 +150,7 @@ class OracleModel:
         q = p[:, : H * hd].reshape(R, H, hd)
         k = p[:, H * hd:(H + KVH) * hd].reshape(R, KVH, hd)
         v = p[:, (H + KVH) * hd:].reshape(R, KVH, hd)
-        q = self.store(self.rope(q, pos))
+        q = self.rope(q, pos)
         k = self.store(self.rope(k, pos))
         v = self.store(v)
         return q, k, v
@@ -173,15 +173,15 @@ class OracleModel:
         return o.permute(1, 0, 2).reshape(R, H * hd)
 
     def ffn(self, x: torch.Tensor, l: int) -> torch.Tensor:
-        y = self.store(self.rmsnorm(x, self.w("ffn_norm", l)))
+        y = self.rmsnorm(x, self.w("ffn_norm", l))
         g = self.linear(y, "w_gate_up", l, rows=(0, self.F))
         u = self.linear(y, "w_gate_up", l, rows=(self.F, 2 * self.F))
-        h = self.store(self.silu(g) * u)
+        h = self.silu(g) * u
         return self.linear(h, "w_down", l)
 
     def head(self, x: torch.Tensor, chunk=16384) -> torch.Tensor:
         """Final RMSNorm then the output head: logits [R, V]."""
-        y = self.store(self.rmsnorm(x, self.w("final_norm")))
+        y = self.rmsnorm(x, self.w("final_norm"))
         if self._keep:
             return self.linear(y, "lm_head")
         out = torch.empty((y.shape[0], self.V), dtype=F64)
@@ -209,9 +209,9 @@ class OracleModel:
         vis = torch.tril(torch.ones(T, T, dtype=torch.bool))
         x = self.embed(tokens)
         for l in route:
-            y = self.store(self.rmsnorm(x, self.w("attn_norm", l)))
+            y = self.rmsnorm(x, self.w("attn_norm", l))
             q, k, v = self.qkv(y, l, pos)
-            a = self.store(self.attend(q, k, v, vis))
+            a = self.attend(q, k, v, vis)
             x = x + self.linear(a, "w_o", l)
             x = x + self.ffn(x, l)
         return self.head(x)
@@ -271,12 +271,12 @@ def forward_window(model: OracleModel, route, cache: SeqCache, tokens, positions
     vis = torch.cat([torch.ones((R, base), dtype=torch.bool), wv], dim=1)
     x = model.embed(tokens)
     for s, l in enumerate(route):
-        y = model.store(model.rmsnorm(x, model.w("attn_norm", l)))
+        y = model.rmsnorm(x, model.w("attn_norm", l))
         q, k, v = model.qkv(y, l, pos)
         cache.write(s, base, k, v)
         K = cache.K[s][: base + R]
         V = cache.V[s][: base + R]
-        a = model.store(model.attend(q, K, V, vis))
+        a = model.attend(q, K, V, vis)
         x = x + model.linear(a, "w_o", l)
         x = x + model.ffn(x, l)
     return model.head(x)

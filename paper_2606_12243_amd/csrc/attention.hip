@@ -17,8 +17,9 @@
 //   A-row m of the K tile holds key pi(m) = (m/16)*16 + ((m/4)%2)*8 +
 //     ((m/8)%2)*4 + m%4, which makes register r of S^T hold key
 //     (r/8)*16 + (l/32)*8 + r%8: the 8-key groups the PV step consumes.
-//   P is fed to the MFMA as bf16 hi + bf16 lo (two products), so the
-//   weights keep ~16 significant bits.
+//   Q (fp32) and P are fed to the MFMA as bf16 hi + lo terms (two
+//   products each), so both keep ~16 significant bits; K and V are the
+//   cache's bf16 values, exact operands.
 // fp32 path: one wave per (row, head), keys streamed with an online softmax.
 #include "kernels.h"
 
@@ -53,14 +54,26 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   const int row = si.row_start + (qvalid ? rloc : 0);
   const int head = g * G + gq;
   const RowInfo ri = a.rows[row];
-  const uint16_t* Q = (const uint16_t*)a.q;
   const uint16_t* pool = (const uint16_t*)a.pool;
 
-  uint4 qv[NQ];
+  // Q (fp32) as bf16 hi + lo terms, in the B-operand layout of S^T = K Q^T
+  uint4 qh[NQ], ql[NQ];
   {
-    const uint4* qp = (const uint4*)(Q + ((size_t)row * a.H + head) * HD + hq * (HD / 2));
+    const float4* qp = (const float4*)(a.q + ((size_t)row * a.H + head) * HD + hq * (HD / 2));
 #pragma unroll
-    for (int i = 0; i < NQ; ++i) qv[i] = qvalid ? qp[i] : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < NQ; ++i) {
+      float4 u = qp[2 * i], w = qp[2 * i + 1];  // unconditional: row is a valid row of this sequence
+      float f[8] = {u.x, u.y, u.z, u.w, w.x, w.y, w.z, w.w};
+      uint16_t hi[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float v = qvalid ? f[e] : 0.f;
+        hi[e] = (uint16_t)(__float_as_uint(v) >> 16);
+        lo[e] = f2bf(v - bf2f(hi[e]));
+      }
+      __builtin_memcpy(&qh[i], hi, 16);
+      __builtin_memcpy(&ql[i], lo, 16);
+    }
   }
   // key pi(m) loaded by this lane as an A row of the K tile
   const int km = ((n >> 4) << 4) + (((n >> 2) & 1) << 3) + (((n >> 3) & 1) << 2) + (n & 3);
@@ -95,7 +108,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const uint4* vp = (const uint4*)(pool + v_off(a.layer_slot, vblk, a.pool_blocks, a.KVH, HD, g, hq * 8, db * 32 + n));
-        uint4 v = in ? *vp : make_uint4(0, 0, 0, 0);
+        uint4 v = *vp;  // page index is clamped to the table: always a valid address
+        if (!in) v = make_uint4(0, 0, 0, 0);
         // zero keys past the written slots (their page rows may hold anything)
         int valid8 = si.kv_len - (kh + hq * 8);
         if (in && valid8 < 8) {
@@ -113,7 +127,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.f;
 #pragma unroll
-    for (int i = 0; i < NQ; ++i) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[i]), as_bf16x8(qv[i]), s, 0, 0, 0);
+    for (int i = 0; i < NQ; ++i) {
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[i]), as_bf16x8(qh[i]), s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv[i]), as_bf16x8(ql[i]), s, 0, 0, 0);
+    }
     // ---- online softmax for this lane's query
     float sv[16];
     float bmax = -INFINITY;
@@ -180,7 +197,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   }
 }
 
-template <typename T>
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
   const int row = blockIdx.x, head = blockIdx.y, d = threadIdx.x;
   const RowInfo ri = a.rows[row];
@@ -195,7 +211,7 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
     L += pm[1] * w;
     if (d < a.hd) O += a.part_o[(((size_t)c * a.M + row) * a.H + head) * a.hd + d] * w;
   }
-  if (d < a.hd) ((T*)a.out)[((size_t)row * a.H + head) * a.hd + d] = from_f<T>(O / L);
+  if (d < a.hd) a.out[((size_t)row * a.H + head) * a.hd + d] = O / L;
 }
 
 // fp32: one wave per (row, head); lane holds head_dim/64 dims.
@@ -206,7 +222,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
   const RowInfo ri = a.rows[row];
   const SeqInfo si = a.seqs[ri.seq];
   const int G = a.H / a.KVH, g = head / G;
-  const float* Q = (const float*)a.q;
+  const float* Q = a.q;
   const float* pool = (const float*)a.pool;
   float q[PER], acc[PER];
 #pragma unroll
@@ -230,7 +246,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
       acc[e] = acc[e] * alpha + p * pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, HD, g, t, lane * PER + e)];
     m_run = m_new;
   }
-  float* out = (float*)a.out;
+  float* out = a.out;
 #pragma unroll
   for (int e = 0; e < PER; ++e) out[((size_t)row * a.H + head) * HD + lane * PER + e] = acc[e] / l_run;
 }
@@ -244,7 +260,7 @@ void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(64), 0, s, a);
     else
       hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(64), 0, s, a);
-    hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, dim3(a.M, a.H), dim3(128), 0, s, a);
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.M, a.H), dim3(128), 0, s, a);
   } else {
     dim3 grid(a.M, a.H);
     if (a.hd == 128)

@@ -7,6 +7,7 @@ namespace via {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;        // tokens per KV page
 constexpr int kMaxChildren = 8;   // drafts verified by one row

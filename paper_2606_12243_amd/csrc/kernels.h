@@ -7,43 +7,47 @@
 
 namespace via {
 
-enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_STATS = 3 };
-
-// Y = X W^T over one 64-column tile per work-group, K split across the
-// group's four waves and `ksplit` groups; the fused epilogue consumes the
-// reduced tile.
+// P[split] = X W^T (or, with `lm`, the head's per-tile row statistics).
 struct GemmArgs {
-  const void* X;       // [M, ldx] activations (model dtype)
+  const void* X;       // [M, ldx] fp32 activations
   int ldx;
-  const void* W;       // [rows, K] weights (model dtype)
-  int M, K, N;         // N: valid output columns of the plain column mapping
-  int ntiles;          // 64-column tiles
-  int ksplit;          // work-groups per tile along K
-  float* part;         // split-K partial tiles [ksplit][M][ntiles * 64]
-  int* counters;       // one per (m-group, tile); self-resetting
-  // QKV: RoPE, Q store, paged K/V write
-  const RowInfo* rows;
-  const SeqInfo* seqs;
-  const int32_t* btab;
-  void* q_out;         // [M, H, hd]
-  void* pool;          // cache pool base
-  int pool_blocks, layer_slot;
-  int H, KVH, hd;
-  float theta;
-  // RESID: resid[m, col] += y
-  float* resid;
-  // SWIGLU: h_out[m, f] = silu(gate) * up
-  void* h_out;
-  int F;
-  // STATS: per (tile, head row) partial max / second / sum-exp / argmax
+  const void* W;       // [N, K] weights (model dtype)
+  int M, K, N;
+  int ksplit;          // K slices, each written as its own partial tile
+  float* part;         // [ksplit][M][N] fp32 partial products
+  // head statistics (split 1)
   const LmRow* lm;
-  float* lm_part;      // [ntiles][M][4]
+  float* lm_part;      // [tiles][M][4]
   float inv_T;
   float* logits;       // nullable [*, V] fp32, row = LmRow::out
   float* draft_logit;
 };
 
-void launch_gemm(int epi, bool bf16, const GemmArgs& a, hipStream_t s);
+// terms: bf16 terms per fp32 activation (2 or 3); stats: head epilogue.
+void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s);
+// 64-column tiles of an N-column GEMM.
+int gemm_tiles(int N);
+
+// X[m] += sum_s P[s][m] (split order; P may be null); Y[.] = RMSNorm(X[m]) * g.
+// With `rows`, row m is written to Y[rows[m].lm] and skipped when lm < 0.
+void launch_resid_norm(bool bf16_gain, float* X, const float* P, int ksplit, int M, int d, const void* g, float eps,
+                       float* Y, const RowInfo* rows, hipStream_t s);
+// h[m, f] = silu(sum_s P[s][m][f]) * sum_s P[s][m][F + f]
+void launch_swiglu(const float* P, int ksplit, int M, int F, float* H, hipStream_t s);
+// Sum QKV partials, rotate-half RoPE at each row's position, Q -> fp32
+// buffer, K/V -> the paged cache (model dtype).
+struct QkvArgs {
+  const float* P;
+  int ksplit, M, H, KVH, hd;
+  float theta;
+  const RowInfo* rows;
+  const SeqInfo* seqs;
+  const int32_t* btab;
+  float* q;            // [M, H, hd]
+  void* pool;
+  int pool_blocks, layer_slot;
+};
+void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s);
 
 // Head statistics: combine the per-tile partials of every head row.
 void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int ntiles, float inv_T,
@@ -52,12 +56,9 @@ void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int nti
 
 // Embedding gather into the fp32 residual stream.
 void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, float* X, hipStream_t s);
-// RMSNorm of rows (optionally gathered through head rows) into the model dtype.
-void launch_rmsnorm(bool bf16, const float* X, const void* g, int M, int d, float eps, void* Y,
-                    const LmRow* gather, hipStream_t s);
 
 struct AttnArgs {
-  const void* q;           // [M, H, hd]
+  const float* q;          // [M, H, hd] fp32
   const void* pool;
   int pool_blocks, layer_slot;
   const RowInfo* rows;
@@ -69,7 +70,7 @@ struct AttnArgs {
   float scale;             // 1/sqrt(hd)
   float* part_o;           // [max_chunks][M][H][hd]
   float* part_ml;          // [max_chunks][M][H][2]
-  void* out;               // [M, H * hd] model dtype
+  float* out;              // [M, H * hd] fp32
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 

@@ -1,5 +1,7 @@
-// Small kernels of the verification step: embedding gather, RMSNorm, the
-// tier decision with its gate walk, and tree-path K/V compaction.
+// Small kernels of the verification step: embedding gather, the consumers
+// of the split-K GEMM partials (residual + RMSNorm, SwiGLU, QKV RoPE + paged
+// K/V write), the tier decision with its gate walk, and tree-path K/V
+// compaction.
 #include "kernels.h"
 
 namespace via {
@@ -13,24 +15,99 @@ __global__ __launch_bounds__(256) void embed_kernel(const T* E, const RowInfo* r
   for (int i = threadIdx.x; i < d; i += 256) X[(size_t)m * d + i] = to_f<T>(e[i]);
 }
 
-// y = x / sqrt(mean(x^2) + eps) * g; fixed-order block reduction.
-template <typename T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* X, const T* g, int d, float eps, T* Y,
-                                                      const LmRow* gather) {
+// x = X[m] + sum_s P[s][m] (split order); X[m] = x; y = x / sqrt(mean(x^2) + eps) * g.
+template <typename G>
+__global__ __launch_bounds__(256) void resid_norm_kernel(float* X, const float* P, int ksplit, int M, int d,
+                                                         const G* g, float eps, float* Y, const RowInfo* rows) {
   __shared__ float red[256];
   const int m = blockIdx.x;
-  const int src = gather ? gather[m].row : m;
-  const float* x = X + (size_t)src * d;
+  float* x = X + (size_t)m * d;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) ss += x[i] * x[i];
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = x[i];
+    if (P) {
+      float acc = 0.f;
+      for (int sp = 0; sp < ksplit; ++sp) acc += P[((size_t)sp * M + m) * d + i];
+      v = v + acc;
+      x[i] = v;
+    }
+    ss += v * v;
+  }
   red[threadIdx.x] = ss;
   __syncthreads();
   for (int o = 128; o > 0; o >>= 1) {
     if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
+  const int out = rows ? rows[m].lm : m;
+  if (out < 0) return;
   const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256) Y[(size_t)m * d + i] = from_f<T>(x[i] * inv * to_f<T>(g[i]));
+  for (int i = threadIdx.x; i < d; i += 256) Y[(size_t)out * d + i] = x[i] * inv * to_f<G>(g[i]);
+}
+
+// h = silu(gate) * up from the gate/up partial sums
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* P, int ksplit, int M, int F, float* H) {
+  const int m = blockIdx.x;
+  const size_t N = 2 * (size_t)F;
+  for (int f = threadIdx.x; f < F; f += 256) {
+    float gt = 0.f, up = 0.f;
+    for (int sp = 0; sp < ksplit; ++sp) {
+      const float* p = P + ((size_t)sp * M + m) * N;
+      gt += p[f];
+      up += p[F + f];
+    }
+    H[(size_t)m * F + f] = gt / (1.0f + expf(-gt)) * up;
+  }
+}
+
+// QKV partial sums -> rotate-half RoPE -> Q (fp32) and paged K/V (model dtype)
+template <typename T>
+__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
+  __shared__ double s_cos[64], s_sin[64];
+  const int m = blockIdx.x;
+  const int half = a.hd >> 1;
+  const RowInfo ri = a.rows[m];
+  if (threadIdx.x < half) {
+    // angle pos * theta^(-2i/hd) in fp64
+    const double inv = pow((double)a.theta, -2.0 * (double)threadIdx.x / (double)a.hd);
+    const double ang = (double)ri.pos * inv;
+    s_cos[threadIdx.x] = cos(ang);
+    s_sin[threadIdx.x] = sin(ang);
+  }
+  __syncthreads();
+  const SeqInfo si = a.seqs[ri.seq];
+  const int blk = a.btab[si.bt + ri.slot / kBlock], t = ri.slot % kBlock;
+  T* pool = (T*)a.pool;
+  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd;
+  const int pairs = (a.H + 2 * a.KVH) * half;
+  for (int e = threadIdx.x; e < pairs; e += 256) {
+    const int hh = e / half, i = e - hh * half;
+    const size_t c = (size_t)hh * a.hd + i;
+    float x1 = 0.f, x2 = 0.f;
+    for (int sp = 0; sp < a.ksplit; ++sp) {
+      const float* p = a.P + ((size_t)sp * a.M + m) * N;
+      x1 += p[c];
+      x2 += p[c + half];
+    }
+    float y1 = x1, y2 = x2;
+    if (hh < a.H + a.KVH) {
+      y1 = (float)((double)x1 * s_cos[i] - (double)x2 * s_sin[i]);
+      y2 = (float)((double)x2 * s_cos[i] + (double)x1 * s_sin[i]);
+    }
+    if (hh < a.H) {
+      float* q = a.q + ((size_t)m * a.H + hh) * a.hd;
+      q[i] = y1;
+      q[i + half] = y2;
+    } else if (hh < a.H + a.KVH) {
+      const int gk = hh - a.H;
+      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i)] = from_f<T>(y1);
+      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + half)] = from_f<T>(y2);
+    } else {
+      const int gv = hh - a.H - a.KVH;
+      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i)] = from_f<T>(y1);
+      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + half)] = from_f<T>(y2);
+    }
+  }
 }
 
 // Tier decision and gate walk for one sequence (App. B.1): every draft gets
@@ -97,7 +174,7 @@ __global__ __launch_bounds__(64) void decide_kernel(DecideArgs a) {
       break;
     }
     float fm = a.f_row_max[out];
-    if (!(fabsf(fm) <= 3.0e38f)) {  // non-finite logits of q
+    if (!isfinite(fm)) {  // non-finite logits of q
       st = 2;
       break;
     }
@@ -149,14 +226,25 @@ void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, f
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)E, rows, d, X);
 }
 
-void launch_rmsnorm(bool bf16, const float* X, const void* g, int M, int d, float eps, void* Y, const LmRow* gather,
-                    hipStream_t s) {
-  if (bf16)
-    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(M), dim3(256), 0, s, X, (const uint16_t*)g, d, eps,
-                       (uint16_t*)Y, gather);
+void launch_resid_norm(bool bf16_gain, float* X, const float* P, int ksplit, int M, int d, const void* g, float eps,
+                       float* Y, const RowInfo* rows, hipStream_t s) {
+  if (bf16_gain)
+    hipLaunchKernelGGL(resid_norm_kernel<uint16_t>, dim3(M), dim3(256), 0, s, X, P, ksplit, M, d, (const uint16_t*)g,
+                       eps, Y, rows);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(M), dim3(256), 0, s, X, (const float*)g, d, eps, (float*)Y,
-                       gather);
+    hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(M), dim3(256), 0, s, X, P, ksplit, M, d, (const float*)g, eps,
+                       Y, rows);
+}
+
+void launch_swiglu(const float* P, int ksplit, int M, int F, float* H, hipStream_t s) {
+  hipLaunchKernelGGL(swiglu_kernel, dim3(M), dim3(256), 0, s, P, ksplit, M, F, H);
+}
+
+void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
+  if (bf16)
+    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, dim3(a.M), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(qkv_finish_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
 }
 
 void launch_decide(const DecideArgs& a, hipStream_t s) {

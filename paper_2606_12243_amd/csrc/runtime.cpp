@@ -32,7 +32,6 @@ via_status fail(via_status s, const char* fmt, ...) {
 
 constexpr size_t kAlign = 256;
 constexpr int kRing = 4;
-constexpr int kCounters = 1 << 16;
 
 size_t al(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -40,22 +39,21 @@ int esize_of(const via_model_desc* d) { return d->dtype == VIA_DTYPE_BF16 ? 2 : 
 
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// Split-K policy: enough work-groups to cover the chip several times, at
-// least two 64-wide K steps per wave.  Depends only on the GEMM shape.
-int choose_ksplit(int ntiles, int K) {
-  int ksteps = K / 64;
-  int cap = std::max(1, ksteps / 8);
-  int ks = ceil_div(1024, ntiles);
-  return std::max(1, std::min(ks, cap));
+// Split-K policy: about two work-groups per CU, at least two 32-wide K steps
+// per wave (8 waves) in each slice.  Depends only on the GEMM shape.
+int choose_ksplit(int N, int K) {
+  const int tiles = gemm_tiles(N);
+  const int ks = ceil_div(512, tiles);
+  return std::max(1, std::min(ks, K / 512));
 }
 
 struct GemmShape {
-  int ntiles, K, ks;
+  int N, K, ks;
 };
 
 struct Dims {
   int L, d, H, KVH, hd, F, V, qkv, G;
-  GemmShape g_qkv, g_o, g_gu, g_down, g_lm;
+  GemmShape g_qkv, g_o, g_gu, g_down;
 };
 
 Dims dims_of(const via_model_desc* d) {
@@ -69,16 +67,17 @@ Dims dims_of(const via_model_desc* d) {
   r.V = d->vocab;
   r.qkv = (r.H + 2 * r.KVH) * r.hd;
   r.G = r.H / std::max(1, r.KVH);
-  r.g_qkv = {r.qkv / 64, r.d, choose_ksplit(r.qkv / 64, r.d)};
-  r.g_o = {r.d / 64, r.H * r.hd, choose_ksplit(r.d / 64, r.H * r.hd)};
-  r.g_gu = {r.F / 32, r.d, choose_ksplit(r.F / 32, r.d)};
-  r.g_down = {r.d / 64, r.F, choose_ksplit(r.d / 64, r.F)};
-  r.g_lm = {ceil_div(r.V, 64), r.d, 1};
+  const bool f32 = d->dtype != VIA_DTYPE_BF16;
+  auto shape = [&](int N, int K) { return GemmShape{N, K, f32 ? 1 : choose_ksplit(N, K)}; };
+  r.g_qkv = shape(r.qkv, r.d);
+  r.g_o = shape(r.d, r.H * r.hd);
+  r.g_gu = shape(2 * r.F, r.d);
+  r.g_down = shape(r.d, r.F);
   return r;
 }
 
 struct Layout {
-  size_t X, Y, Q, A, Hb, Yl, part, counters, att_o, att_ml, lm_part;
+  size_t X, Y, Q, A, Hb, Yl, part, att_o, att_ml, lm_part;
   size_t rows, seqs, btab, items, lm;  // plan region
   size_t step_seqs, dtok, drow, dpar;  // step region
   size_t c_btab, c_moves;              // commit region
@@ -98,21 +97,20 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
     return r;
   };
   const size_t R = max_rows;
+  (void)es;
   L.X = take(R * D.d * 4);
-  L.Y = take(R * D.d * es);
-  L.Q = take(R * D.H * D.hd * es);
-  L.A = take(R * D.H * D.hd * es);
-  L.Hb = take(R * D.F * es);
-  L.Yl = take(R * D.d * es);
+  L.Y = take(R * D.d * 4);
+  L.Q = take(R * D.H * D.hd * 4);
+  L.A = take(R * D.H * D.hd * 4);
+  L.Hb = take(R * D.F * 4);
+  L.Yl = take(R * D.d * 4);
   size_t part = 0;
-  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down})
-    part = std::max(part, (size_t)g.ks * R * g.ntiles * 64 * 4);
+  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down}) part = std::max(part, (size_t)g.ks * R * g.N * 4);
   L.part = take(part);
-  L.counters = take((size_t)kCounters * 4);
   L.max_chunks = ceil_div(max_blocks * kBlock, kAttnChunk);
   L.att_o = take((size_t)L.max_chunks * R * D.H * D.hd * 4);
   L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
-  L.lm_part = take((size_t)D.g_lm.ntiles * R * 4 * 4);
+  L.lm_part = take((size_t)gemm_tiles(D.V) * R * 4 * 4);
   L.max_items = ceil_div(max_rows * D.G, 32) + max_batch;
   // plan region (one upload per forward)
   size_t p0 = o;
@@ -184,6 +182,10 @@ struct via_kv {
   hipEvent_t ev[kRing];
   bool ev_used[kRing];
   int ring = 0;
+  // kernel timing
+  uint32_t timer_mask = 0;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> timed;
 };
 
 namespace {
@@ -211,6 +213,35 @@ via_status upload(via_kv* kv, void* dst, const void* src, size_t bytes, hipStrea
   st = hip_check(kv, hipEventRecord(kv->ev[r], s), "hipEventRecord");
   kv->ev_used[r] = true;
   return st;
+}
+
+hipEvent_t pool_event(via_kv* kv) {
+  if (!kv->ev_pool.empty()) {
+    hipEvent_t e = kv->ev_pool.back();
+    kv->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Run `launch` bracketed by events when its kind is being timed.
+template <typename F>
+void timed_launch(via_kv* kv, int kind, hipStream_t s, F&& launch) {
+  if (!(kv->timer_mask & (1u << kind))) {
+    launch();
+    return;
+  }
+  hipEvent_t a = pool_event(kv), b = pool_event(kv);
+  if (!a || !b) {
+    launch();
+    return;
+  }
+  (void)hipEventRecord(a, s);
+  launch();
+  (void)hipEventRecord(b, s);
+  kv->timed.push_back({kind, {a, b}});
 }
 
 struct Plan {
@@ -295,10 +326,11 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   const SeqInfo* d_seqs = (const SeqInfo*)(ws + L.seqs);
   const int32_t* d_btab = (const int32_t*)(ws + L.btab);
   float* X = (float*)(ws + L.X);
-  void* Y = ws + L.Y;
-  void* Q = ws + L.Q;
-  void* A = ws + L.A;
-  void* Hb = ws + L.Hb;
+  float* Y = (float*)(ws + L.Y);
+  float* Q = (float*)(ws + L.Q);
+  float* A = (float*)(ws + L.A);
+  float* Hb = (float*)(ws + L.Hb);
+  float* part = (float*)(ws + L.part);
   void* pool = cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim;
   const int pool_blocks = cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim;
   std::vector<int> route;
@@ -306,15 +338,23 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     for (int l = 0; l < D.L; ++l) route.push_back(l);
   else
     route = m->route;
+  const float eps = m->d.rms_eps;
+
+  auto gemm = [&](const float* Xin, int ldx, const void* W, const GemmShape& sh, int terms, int kind) {
+    GemmArgs g{};
+    g.X = Xin;
+    g.ldx = ldx;
+    g.W = W;
+    g.M = M;
+    g.K = sh.K;
+    g.N = sh.N;
+    g.ksplit = sh.ks;
+    g.part = part;
+    timed_launch(kv, kind, s, [&] { launch_gemm(bf, terms, false, g, s); });
+  };
 
   launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
-  GemmArgs g{};
-  g.M = M;
-  g.part = (float*)(ws + L.part);
-  g.counters = (int*)(ws + L.counters);
-  g.rows = d_rows;
-  g.seqs = d_seqs;
-  g.btab = d_btab;
+  launch_resid_norm(bf, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], eps, Y, nullptr, s);
   AttnArgs at{};
   at.q = Q;
   at.pool = pool;
@@ -334,66 +374,42 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   at.part_o = (float*)(ws + L.att_o);
   at.part_ml = (float*)(ws + L.att_ml);
   at.out = A;
+  QkvArgs qa{};
+  qa.P = part;
+  qa.ksplit = D.g_qkv.ks;
+  qa.M = M;
+  qa.H = D.H;
+  qa.KVH = D.KVH;
+  qa.hd = D.hd;
+  qa.theta = m->d.rope_theta;
+  qa.rows = d_rows;
+  qa.seqs = d_seqs;
+  qa.btab = d_btab;
+  qa.q = Q;
+  qa.pool = pool;
+  qa.pool_blocks = pool_blocks;
   for (size_t si = 0; si < route.size(); ++si) {
     const int l = route[si];
-    launch_rmsnorm(bf, X, m->attn_norm[l], M, D.d, m->d.rms_eps, Y, nullptr, s);
-    // QKV + RoPE + paged K/V write
-    g.X = Y;
-    g.ldx = D.d;
-    g.W = m->w_qkv[l];
-    g.K = D.d;
-    g.N = D.qkv;
-    g.ntiles = D.g_qkv.ntiles;
-    g.ksplit = D.g_qkv.ks;
-    g.q_out = Q;
-    g.pool = pool;
-    g.pool_blocks = pool_blocks;
-    g.layer_slot = (int)si;
-    g.H = D.H;
-    g.KVH = D.KVH;
-    g.hd = D.hd;
-    g.theta = m->d.rope_theta;
-    launch_gemm(EPI_QKV, bf, g, s);
+    // Q/K/V: three bf16 terms per activation (the K/V are rounded to the cache's bf16)
+    gemm(Y, D.d, m->w_qkv[l], D.g_qkv, 3, VIA_KERNEL_QKV);
+    qa.layer_slot = (int)si;
+    launch_qkv_finish(bf, qa, s);
     at.layer_slot = (int)si;
-    launch_attention(bf, at, s);
-    // O projection + residual
-    g.X = A;
-    g.ldx = D.H * D.hd;
-    g.W = m->w_o[l];
-    g.K = D.H * D.hd;
-    g.N = D.d;
-    g.ntiles = D.g_o.ntiles;
-    g.ksplit = D.g_o.ks;
-    g.resid = X;
-    launch_gemm(EPI_RESID, bf, g, s);
-    launch_rmsnorm(bf, X, m->ffn_norm[l], M, D.d, m->d.rms_eps, Y, nullptr, s);
-    // gate/up + SwiGLU
-    g.X = Y;
-    g.ldx = D.d;
-    g.W = m->w_gate_up[l];
-    g.K = D.d;
-    g.N = 2 * D.F;
-    g.F = D.F;
-    g.ntiles = D.g_gu.ntiles;
-    g.ksplit = D.g_gu.ks;
-    g.h_out = Hb;
-    launch_gemm(EPI_SWIGLU, bf, g, s);
-    // down + residual
-    g.X = Hb;
-    g.ldx = D.F;
-    g.W = m->w_down[l];
-    g.K = D.F;
-    g.N = D.d;
-    g.ntiles = D.g_down.ntiles;
-    g.ksplit = D.g_down.ks;
-    g.resid = X;
-    launch_gemm(EPI_RESID, bf, g, s);
+    timed_launch(kv, VIA_KERNEL_ATTN, s, [&] { launch_attention(bf, at, s); });
+    gemm(A, D.H * D.hd, m->w_o[l], D.g_o, 2, VIA_KERNEL_O);
+    launch_resid_norm(bf, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], eps, Y, nullptr, s);
+    gemm(Y, D.d, m->w_gate_up[l], D.g_gu, 2, VIA_KERNEL_GATEUP);
+    launch_swiglu(part, D.g_gu.ks, M, D.F, Hb, s);
+    gemm(Hb, D.F, m->w_down[l], D.g_down, 2, VIA_KERNEL_DOWN);
+    if (si + 1 < route.size())
+      launch_resid_norm(bf, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], eps, Y, nullptr, s);
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
     const LmRow* d_lm = (const LmRow*)(ws + L.lm);
-    void* Yl = ws + L.Yl;
-    launch_rmsnorm(bf, X, m->final_norm, nlm, D.d, m->d.rms_eps, Yl, d_lm, s);
+    float* Yl = (float*)(ws + L.Yl);
+    // last residual update, final norm of the head rows only
+    launch_resid_norm(bf, X, part, D.g_down.ks, M, D.d, m->final_norm, eps, Yl, d_rows, s);
     GemmArgs h{};
     h.X = Yl;
     h.ldx = D.d;
@@ -401,18 +417,17 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     h.M = nlm;
     h.K = D.d;
     h.N = D.V;
-    h.ntiles = D.g_lm.ntiles;
     h.ksplit = 1;
-    h.part = g.part;
-    h.counters = g.counters;
     h.lm = d_lm;
     h.lm_part = (float*)(ws + L.lm_part);
     h.inv_T = inv_T;
     h.logits = out->logits;
     h.draft_logit = out->draft_logit;
-    launch_gemm(EPI_STATS, bf, h, s);
-    launch_lm_finalize(d_lm, h.lm_part, nlm, h.ntiles, inv_T, out->row_argmax, out->row_max, out->row_sumexp,
-                       out->row_gap, s);
+    timed_launch(kv, VIA_KERNEL_HEAD, s, [&] {
+      launch_gemm(bf, 2, true, h, s);
+      launch_lm_finalize(d_lm, h.lm_part, nlm, gemm_tiles(D.V), inv_T, out->row_argmax, out->row_max,
+                         out->row_sumexp, out->row_gap, s);
+    });
   }
   return hip_check(kv, hipGetLastError(), "kernel launch");
 }
@@ -775,19 +790,53 @@ via_status via_kv_create(via_model* m, const via_kv_desc* d, via_kv** out) {
       return fail(VIA_EDEVICE, "hipEventCreate failed");
     }
   }
-  // split-K counters start at zero and reset themselves after each use
-  if (hipMemset(kv->ws + L.counters, 0, (size_t)kCounters * 4) != hipSuccess) {
-    for (int r = 0; r < kRing; ++r) (void)hipEventDestroy(kv->ev[r]);
-    delete kv;
-    return fail(VIA_EDEVICE, "hipMemset of the workspace failed");
-  }
   m->n_kv++;
   *out = kv;
   return VIA_OK;
 }
 
+via_status via_kv_timer_enable(via_kv* kv, uint32_t kind_mask) {
+  if (!kv) return fail(VIA_EINVAL, "null KV handle");
+  if (kind_mask >> VIA_KERNEL_COUNT) return fail(VIA_EINVAL, "unknown kernel kind in mask");
+  kv->timer_mask = kind_mask;
+  return VIA_OK;
+}
+
+via_status via_kv_timer_read(via_kv* kv, int32_t kind, int32_t* launches, double* total_ms) {
+  if (!kv || !launches || !total_ms) return fail(VIA_EINVAL, "null argument");
+  if (kind < 0 || kind >= VIA_KERNEL_COUNT) return fail(VIA_EINVAL, "unknown kernel kind");
+  int n = 0;
+  double ms = 0;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> keep;
+  for (auto& t : kv->timed) {
+    if (t.first != kind) {
+      keep.push_back(t);
+      continue;
+    }
+    via_status st = hip_check(kv, hipEventSynchronize(t.second.second), "hipEventSynchronize");
+    if (st) return st;
+    float e = 0.f;
+    if ((st = hip_check(kv, hipEventElapsedTime(&e, t.second.first, t.second.second), "hipEventElapsedTime")))
+      return st;
+    ms += e;
+    ++n;
+    kv->ev_pool.push_back(t.second.first);
+    kv->ev_pool.push_back(t.second.second);
+  }
+  kv->timed.swap(keep);
+  *launches = n;
+  *total_ms = ms;
+  return VIA_OK;
+}
+
 via_status via_kv_destroy(via_kv* kv) {
   if (!kv) return fail(VIA_EINVAL, "null KV handle");
+  for (auto& t : kv->timed) {
+    (void)hipEventSynchronize(t.second.second);
+    kv->ev_pool.push_back(t.second.first);
+    kv->ev_pool.push_back(t.second.second);
+  }
+  for (hipEvent_t e : kv->ev_pool) (void)hipEventDestroy(e);
   for (int r = 0; r < kRing; ++r) {
     if (kv->ev_used[r]) (void)hipEventSynchronize(kv->ev[r]);
     (void)hipEventDestroy(kv->ev[r]);

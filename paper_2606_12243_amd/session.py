@@ -199,6 +199,55 @@ class GreedyDrafter:
         kv = sess.kv
         self.out = via.Out(kv.max_batch, kv.max_rows, kv.max_drafts, sess.m.desc["vocab"], logits=False)
 
+    def tree(self, seqs, budget, branch, step):
+        """Token tree per sequence: per depth, earlier nodes expand first with
+        up to ``branch`` children, the parent's top tokens under q (probe
+        forward of the tree so far), each replaced at random."""
+        s = self.s
+        out = {}
+        for q in seqs:
+            toks, parents, frontier = [], [], [-1]
+            for depth, nb in enumerate(budget, start=1):
+                plan, left = [], nb
+                for u in frontier:
+                    if left <= 0:
+                        break
+                    plan.append((u, min(branch, left)))
+                    left -= plan[-1][1]
+                # probe rows: root + every node so far (all fed), ancestors mask
+                rn = [-1] + list(range(len(toks)))
+                row_of = {u: r for r, u in enumerate(rn)}
+                dep = {}
+                for j in range(len(toks)):
+                    dep[j] = 1 if parents[j] < 0 else dep[parents[j]] + 1
+                masks = []
+                for r, u in enumerate(rn):
+                    mk = 1 | (1 << r)
+                    while u >= 0:
+                        mk |= 1 << row_of[u]
+                        u = parents[u]
+                    masks.append(mk)
+                rows = [s.tokens[q][-1]] + list(toks)
+                w = via.WindowBuf([q], [rows], [[0]], [[0]], parents=[[-1]],
+                                  depths=[[0] + [dep[j] for j in range(len(toks))]], masks=[masks],
+                                  lags=[s.lag(q)], max_drafts=1)
+                outt = via.Out(1, len(rows), 1, s.m.desc["vocab"], logits=True)
+                via.check(via.via_verify_probe(s.m.h, s.kv.h, via.CACHE_FULL, C.byref(w.c), C.byref(s.p),
+                                               C.byref(outt.c), s.sp()))
+                lg = outt.logits.view(len(rows), -1)
+                new_frontier = []
+                for u, take in plan:
+                    top = torch.topk(lg[row_of[u]], take).indices.cpu().tolist()
+                    for t in top:
+                        j = len(toks)
+                        rep, tok = self.corrupt(q, step, j)
+                        toks.append(tok if rep else int(t))
+                        parents.append(u)
+                        new_frontier.append(j)
+                frontier = new_frontier
+            out[q] = (toks, parents)
+        return out
+
     def chain(self, seqs, k, step):
         s = self.s
         drafts = {q: [] for q in seqs}

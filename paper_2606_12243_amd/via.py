@@ -112,6 +112,8 @@ via_verify_probe = _sig("via_verify_probe", I32, P, P, I32, C.POINTER(Window), C
 via_tier_decide = _sig("via_tier_decide", I32, P, C.POINTER(TierParams), C.POINTER(VerifyOut),
                        C.POINTER(VerifyOut), C.POINTER(Decision), P)
 via_kv_commit_rollback = _sig("via_kv_commit_rollback", I32, P, C.POINTER(Decision), P)
+via_kv_timer_enable = _sig("via_kv_timer_enable", I32, P, C.c_uint32)
+via_kv_timer_read = _sig("via_kv_timer_read", I32, P, I32, PI32, C.POINTER(C.c_double))
 via_last_error = _sig("via_last_error", C.c_char_p)
 via_version = _sig("via_version", C.c_char_p)
 
@@ -119,7 +121,10 @@ EXPORTS = ["via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_mo
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide",
-           "via_kv_commit_rollback", "via_last_error", "via_version"]
+           "via_kv_commit_rollback", "via_kv_timer_enable", "via_kv_timer_read", "via_last_error",
+           "via_version"]
+KERNEL_QKV, KERNEL_ATTN, KERNEL_O, KERNEL_GATEUP, KERNEL_DOWN, KERNEL_HEAD = range(6)
+KERNEL_NAMES = ["qkv", "attn", "o", "gateup", "down", "head"]
 
 
 def check(status):
@@ -190,7 +195,7 @@ class KV:
     """Paged full/slim KV pools, workspace and pinned staging of one handle."""
 
     def __init__(self, model: Model, max_seqs, max_blocks_per_seq, blocks_full, blocks_slim, max_rows,
-                 max_batch, max_drafts, device="cuda", zero_pools=True):
+                 max_batch, max_drafts, device="cuda", zero_pools=True, pools=None):
         self.model = model
         d = model.cdesc
         esz = 2 if model.desc["dtype"] == "bf16" else 4
@@ -198,8 +203,12 @@ class KV:
         nb_slim = via_pool_bytes(C.byref(d), len(model.route), blocks_slim, BLOCK)
         mk = torch.zeros if zero_pools else torch.empty
         dt = torch.bfloat16 if esz == 2 else torch.float32
-        self.pool_full = mk(nb_full // esz, dtype=dt, device=device)
-        self.pool_slim = mk(nb_slim // esz, dtype=dt, device=device)
+        if pools is not None:          # reuse pools (and their contents) of an earlier handle
+            self.pool_full, self.pool_slim = pools
+            assert self.pool_full.numel() * esz >= nb_full and self.pool_slim.numel() * esz >= nb_slim
+        else:
+            self.pool_full = mk(nb_full // esz, dtype=dt, device=device)
+            self.pool_slim = mk(nb_slim // esz, dtype=dt, device=device)
         wsb = via_workspace_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts)
         stb = via_staging_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts)
         self.workspace = torch.empty(wsb, dtype=torch.uint8, device=device)
@@ -224,6 +233,14 @@ class KV:
         check(via_kv_seq_info(self.h, seq, cache, C.byref(valid), tab.ctypes.data_as(PI32), len(tab),
                               C.byref(nb)))
         return valid.value, tab[:nb.value].tolist()
+
+    def timer_enable(self, mask):
+        check(via_kv_timer_enable(self.h, mask))
+
+    def timer_read(self, kind):
+        n, ms = C.c_int32(), C.c_double()
+        check(via_kv_timer_read(self.h, kind, C.byref(n), C.byref(ms)))
+        return n.value, ms.value
 
     def pool_view(self, cache):
         """Pool as [slots, blocks, 2, KVH, 16*hd] (K page token-major, V page transposed)."""
