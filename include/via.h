@@ -81,12 +81,18 @@ typedef struct {
 
 /* Weight pointers (device, caller-owned, model dtype).  Per-layer entries
  * are HOST arrays of n_layers device pointers, copied at via_model_create.
+ * Logical shapes, [out_features, in_features]:
  *   embed     [vocab, d]          lm_head [vocab, d]      final_norm [d]
  *   attn_norm [d]                 ffn_norm [d]
  *   w_qkv     [(H + 2 KVH) hd, d]  rows: Q heads, then K heads, then V heads
  *   w_o       [d, H hd]
  *   w_gate_up [2 F, d]            rows: gate (F), then up (F)
  *   w_down    [d, F]
+ * embed and the norm gains are plain row-major.  The five projection
+ * matrices (lm_head, w_qkv, w_o, w_gate_up, w_down) are in the PACKED layout
+ * written by via_pack_weight, which stores each 64-row x 32-column tile as
+ * the matrix cores consume it, so that the verify GEMMs stream weights as
+ * contiguous memory.
  * The slim-verifier reads the same pointers for its retained layers: no
  * weight is copied (Sec. 3.3). */
 typedef struct {
@@ -189,6 +195,16 @@ typedef struct {
   int32_t *packed;
   int32_t *h_packed;
 } via_decision;
+
+/* ---- weight packing ----------------------------------------------------- */
+/* Bytes of a packed [rows, cols] matrix: rows rounded up to a multiple of 64
+ * (padding rows are zero), cols must be a multiple of 32. 0 if invalid. */
+size_t via_packed_bytes(int32_t rows, int32_t cols, int32_t dtype);
+/* Pack a row-major [rows, cols] device matrix `src` into `dst` (device,
+ * via_packed_bytes) on `stream`.  Element (r, c) goes to the 8-element group
+ *   ((((r/64) * (cols/32) + c/32) * 4 + (r%64)/16) * 64 + ((c%32)/8) * 16 + r%16)
+ * at offset c%8.  src and dst must not overlap. */
+via_status via_pack_weight(const void *src, void *dst, int32_t rows, int32_t cols, int32_t dtype, void *stream);
 
 /* ---- sizes -------------------------------------------------------------- */
 size_t via_pool_bytes(const via_model_desc *desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size);

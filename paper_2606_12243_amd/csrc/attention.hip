@@ -198,6 +198,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 }
 
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
+  __shared__ float o_s[128];
   const int row = blockIdx.x, head = blockIdx.y, d = threadIdx.x;
   const RowInfo ri = a.rows[row];
   const SeqInfo si = a.seqs[ri.seq];
@@ -211,7 +212,14 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
     L += pm[1] * w;
     if (d < a.hd) O += a.part_o[(((size_t)c * a.M + row) * a.H + head) * a.hd + d] * w;
   }
-  if (d < a.hd) a.out[((size_t)row * a.H + head) * a.hd + d] = O / L;
+  if (d < a.hd) o_s[d] = O / L;
+  __syncthreads();
+  if (d < a.hd / 8) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = o_s[d * 8 + e];
+    put_afrag<true, 2>(a.out, row, head * a.hd + d * 8, v, (a.H * a.hd) >> 5, a.MBn);
+  }
 }
 
 // fp32: one wave per (row, head); lane holds head_dim/64 dims.
@@ -246,9 +254,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
       acc[e] = acc[e] * alpha + p * pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, HD, g, t, lane * PER + e)];
     m_run = m_new;
   }
-  float* out = a.out;
+  __shared__ float o_s[HD];
 #pragma unroll
-  for (int e = 0; e < PER; ++e) out[((size_t)row * a.H + head) * HD + lane * PER + e] = acc[e] / l_run;
+  for (int e = 0; e < PER; ++e) o_s[lane * PER + e] = acc[e] / l_run;
+  __syncthreads();
+  if (lane < HD / 8) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = o_s[lane * 8 + e];
+    put_afrag<false, 1>(a.out, row, head * HD + lane * 8, v, (a.H * HD) >> 5, a.MBn);
+  }
 }
 
 }  // namespace

@@ -1,7 +1,7 @@
 // Tall-skinny GEMMs of the verification forward.
 //
 // P[split][M][N] = X[M, K-slice] * W[N, K-slice]^T with M = fed rows (tens),
-// W (bf16) streamed once from HBM, X (fp32 activations) read from L2.
+// W (bf16, packed) streamed once from HBM, X (activation fragments) from L2.
 // A work-group (8 waves) owns a 64-column tile and one K slice; its waves
 // split the slice further, keep two batches of loads in flight and sum their
 // partial tiles in LDS in wave order.  The K slices of a tile ("splits") are
@@ -12,11 +12,12 @@
 // results are bitwise reproducible and independent of M.
 //
 // bf16 path: v_mfma_f32_16x16x32_bf16.  Lane l holds row/column l%16 and
-// K sub-block (l/16)*8 .. +7 of each 32-wide step (a load instruction reads
-// 64 contiguous bytes of each of 16 weight rows).  The fp32 activations enter
-// the matrix cores as NT bf16 terms: x = hi + (mid) + lo, hi and mid
-// truncated, the last rounded to nearest, so NT = 3 keeps ~24 significant
-// bits and NT = 2 ~16.  Output register r of lane l is row (l/16)*4 + r,
+// K sub-block (l/16)*8 .. +7 of each 32-wide step.  Weights are pre-packed
+// (via_pack_weight) and activations are written by their producer kernels
+// as fragments (afrag_group), so every load instruction of a wave reads one
+// contiguous 1 KB block and the inner loop is loads + MFMA only.  fp32
+// activations enter the matrix cores as NT bf16 terms (x = hi + [mid +] lo),
+// NT = 3 keeping ~24 significant bits and NT = 2 ~16.  Output register r of lane l is row (l/16)*4 + r,
 // column l%16.  The head GEMM (split 1) reduces its tile to per-row
 // (max, second, sum-exp, argmax) partials and draft-token logits in place.
 // fp32 path: plain FMA on the vector ALUs (small models only).
@@ -42,99 +43,52 @@ __device__ __forceinline__ uint4 zero_if(uint4 v, bool ok) {
   return v;
 }
 
-__device__ __forceinline__ uint32_t pack2(uint32_t lo16, uint32_t hi16) { return (lo16 & 0xFFFFu) | (hi16 << 16); }
-
-// Split 8 fp32 values into NT bf16x8 terms (hi, [mid,] lo).
-template <int NT>
-__device__ __forceinline__ void split_terms(const float* x, uint4* out) {
-  uint32_t t[NT][8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float r = x[e];
-#pragma unroll
-    for (int q = 0; q < NT; ++q) {
-      uint32_t u = __float_as_uint(r);
-      uint32_t b = (q == NT - 1) ? (uint32_t)f2bf(r) : (u >> 16);  // last term rounded, others truncated
-      t[q][e] = b;
-      r = r - __uint_as_float(b << 16);
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < NT; ++q)
-    out[q] = make_uint4(pack2(t[q][0], t[q][1]), pack2(t[q][2], t[q][3]), pack2(t[q][4], t[q][5]),
-                        pack2(t[q][6], t[q][7]));
-}
-
-// lds[16*MB][64] = X[m0 .., K slice] * W[c0 .. c0+64, K slice]^T
+// lds[16*MB][64] = X[m0 .., K slice] * W[c0 .. c0+64, K slice]^T, X given as
+// NT bf16-term fragments and W packed: each load is one contiguous 1 KB block.
 template <int MB, int NT>
 __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int k_beg, int k_end, float* lds) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, g = lane >> 4;
-  const uint16_t* W = (const uint16_t*)a.W;
-  const float* X = (const float*)a.X;
+  const int S = a.K >> 5;
   const int st_beg = k_beg >> 5, st_all = (k_end - k_beg) >> 5;
   const int per = (st_all + kWaves - 1) / kWaves;
   const int s0 = st_beg + wave * per, s1 = min(st_beg + st_all, s0 + per);
+  const uint4* wt = (const uint4*)a.W + (size_t)(c0 >> 6) * S * (4 * 64) + lane;
+  const uint4* xt = (const uint4*)a.X + (size_t)(m0 >> 4) * 64 + lane;
+  const size_t x_step = (size_t)a.MBn * 64, x_term = (size_t)S * x_step;
 
-  const uint4* wp[kNB];
-  bool wv[kNB];
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    const int col = c0 + nb * 16 + n;
-    wv[nb] = col < a.N;
-    wp[nb] = (const uint4*)(W + (size_t)(wv[nb] ? col : 0) * a.K + g * 8);
-  }
-  const uint4* xp[MB];
-  bool xv[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int m = m0 + mb * 16 + n;
-    xv[mb] = m < a.M;
-    xp[mb] = (const uint4*)(X + (size_t)(xv[mb] ? m : 0) * a.ldx + g * 8);
-  }
   f32x4 acc[MB][kNB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // two batches in flight; loads are unconditional (rows past the end read
-  // row 0, steps past the slice re-read its last step) and masked afterwards
-  uint4 wb[2][kBatch][kNB], xb[2][kBatch][MB][2];
+  uint4 wb[2][kBatch][kNB], xb[2][kBatch][NT][MB];
+  // steps past the slice re-read its last step and are skipped by compute
   auto issue = [&](int buf, int s) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int st = min(s + u, s1 - 1);
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) wb[buf][u][nb] = wp[nb][st * 4];
+      for (int nb = 0; nb < kNB; ++nb) wb[buf][u][nb] = wt[(st * 4 + nb) * 64];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        xb[buf][u][mb][0] = xp[mb][st * 8];
-        xb[buf][u][mb][1] = xp[mb][st * 8 + 1];
-      }
+      for (int q = 0; q < NT; ++q)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) xb[buf][u][q][mb] = xt[q * x_term + st * x_step + mb * 64];
     }
   };
   auto compute = [&](int buf, int s) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      const bool live = (s + u) < s1;
-      bf16x8 bw[kNB];
+      if (s + u >= s1) break;  // wave-uniform
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) bw[nb] = as_bf16x8(zero_if(wb[buf][u][nb], wv[nb] && live));
+      for (int q = 0; q < NT; ++q)
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        float xf[8];
-        __builtin_memcpy(xf, &xb[buf][u][mb][0], 32);
-        uint4 terms[NT];
-        split_terms<NT>(xf, terms);
-#pragma unroll
-        for (int q = 0; q < NT; ++q) {
-          const bf16x8 av = as_bf16x8(zero_if(terms[q], xv[mb]));
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int nb = 0; nb < kNB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw[nb], acc[mb][nb], 0, 0, 0);
-        }
-      }
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xb[buf][u][q][mb]),
+                                                                as_bf16x8(wb[buf][u][nb]), acc[mb][nb], 0, 0, 0);
     }
   };
   // buffer indices are compile-time constants (a runtime index would put
@@ -165,19 +119,23 @@ __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int k_beg, int k_en
   }
 }
 
-// fp32 tile on the vector ALUs.
+// fp32 tile on the vector ALUs (X fragments with one fp32 term).
 template <int MB>
 __device__ void tile_f32(const GemmArgs& a, int c0, int m0, int k_beg, int k_end, float* lds) {
   const float* W = (const float*)a.W;
   const float* X = (const float*)a.X;
+  const size_t steps = a.K >> 5;
   for (int e = threadIdx.x; e < 16 * MB * kTileN; e += kThreads) {
     const int r = e / kTileN, c = e - r * kTileN;
     const int m = m0 + r, col = c0 + c;
     float acc = 0.f;
     if (m < a.M && col < a.N) {
-      const float* x = X + (size_t)m * a.ldx;
-      const float* w = W + (size_t)col * a.K;
-      for (int k = k_beg; k < k_end; ++k) acc = fmaf(x[k], w[k], acc);
+      // packed weight element (col, k): group ((tile*steps + k/32)*4 + nb)*64 + ((k%32)/8)*16 + col%16
+      const size_t base = (size_t)(col >> 6) * steps * 4 * 64 + ((col & 63) >> 4) * 64 + (col & 15);
+      for (int k = k_beg; k < k_end; ++k) {
+        const float xv = X[afrag_group(0, m, k & ~7, (int)steps, a.MBn) * 8 + (k & 7)];
+        acc = fmaf(xv, W[(base + (size_t)(k >> 5) * 256 + ((k & 31) >> 3) * 16) * 8 + (k & 7)], acc);
+      }
     }
     lds[e] = acc;
   }
@@ -269,7 +227,7 @@ template <typename T, int NT, bool STATS>
 void launch_e(const GemmArgs& a, hipStream_t s) {
   // up to 32 rows per work-group (register budget); more rows take more
   // m-groups, whose neighbouring work-groups re-read the same W rows
-  const int mb = a.M > 16 ? 2 : 1;
+  const int mb = gemm_rows_per_group(a.M) / 16;
   const int mgroups = (a.M + 16 * mb - 1) / (16 * mb);
   dim3 grid(gemm_tiles(a.N) * a.ksplit * mgroups);
   if (mb == 1)
@@ -327,9 +285,39 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(const LmRow* lm, const
   }
 }
 
+// Row-major [rows, cols] -> packed tiles; one thread per 8-element group.
+template <typename T>
+__global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int rows, int cols, size_t groups) {
+  const size_t gidx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (gidx >= groups) return;
+  const int steps = cols >> 5;
+  const int lane = (int)(gidx & 63);
+  size_t q = gidx >> 6;
+  const int nb = (int)(q & 3);
+  q >>= 2;
+  const int st = (int)(q % steps);
+  const size_t tile = q / steps;
+  const size_t r = tile * 64 + nb * 16 + (lane & 15);
+  const size_t c = (size_t)st * 32 + (lane >> 4) * 8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) dst[gidx * 8 + e] = r < (size_t)rows ? src[r * cols + c + e] : T(0);
+}
+
 }  // namespace
 
+void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, hipStream_t s) {
+  const size_t groups = (size_t)((rows + 63) / 64) * 64 * (cols / 8);
+  const dim3 grid((unsigned)((groups + 255) / 256));
+  if (bf16)
+    hipLaunchKernelGGL(pack_kernel<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)src, (uint16_t*)dst, rows, cols,
+                       groups);
+  else
+    hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(256), 0, s, (const float*)src, (float*)dst, rows, cols, groups);
+}
+
 int gemm_tiles(int N) { return (N + kTileN - 1) / kTileN; }
+
+int gemm_rows_per_group(int M) { return M > 16 ? 32 : 16; }
 
 void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s) {
   if (!bf16) {

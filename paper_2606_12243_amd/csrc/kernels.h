@@ -9,8 +9,8 @@ namespace via {
 
 // P[split] = X W^T (or, with `lm`, the head's per-tile row statistics).
 struct GemmArgs {
-  const void* X;       // [M, ldx] fp32 activations
-  int ldx;
+  const void* X;       // activation fragments (afrag_group), MBn row blocks
+  int MBn;
   const void* W;       // [N, K] weights (model dtype)
   int M, K, N;
   int ksplit;          // K slices, each written as its own partial tile
@@ -27,13 +27,18 @@ struct GemmArgs {
 void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s);
 // 64-column tiles of an N-column GEMM.
 int gemm_tiles(int N);
+// Rows per GEMM work-group for M rows (16 or 32); fragments pad M to a multiple.
+int gemm_rows_per_group(int M);
+// Row-major [rows, cols] -> packed weight tiles (see include/via.h).
+void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, hipStream_t s);
 
-// X[m] += sum_s P[s][m] (split order; P may be null); Y[.] = RMSNorm(X[m]) * g.
-// With `rows`, row m is written to Y[rows[m].lm] and skipped when lm < 0.
-void launch_resid_norm(bool bf16_gain, float* X, const float* P, int ksplit, int M, int d, const void* g, float eps,
-                       float* Y, const RowInfo* rows, hipStream_t s);
-// h[m, f] = silu(sum_s P[s][m][f]) * sum_s P[s][m][F + f]
-void launch_swiglu(const float* P, int ksplit, int M, int F, float* H, hipStream_t s);
+// X[m] += sum_s P[s][m] (split order; P may be null); the RMSNorm of the row
+// times g is written as activation fragments (`terms` bf16 terms, or fp32),
+// to fragment row rows[m].lm when `rows` is given (rows with lm < 0 skipped).
+void launch_resid_norm(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
+                       float eps, void* Y, int MBn, const RowInfo* rows, hipStream_t s);
+// h[m, f] = silu(sum_s P[s][m][f]) * sum_s P[s][m][F + f], as fragments.
+void launch_swiglu(bool bf16, const float* P, int ksplit, int M, int F, void* H, int MBn, hipStream_t s);
 // Sum QKV partials, rotate-half RoPE at each row's position, Q -> fp32
 // buffer, K/V -> the paged cache (model dtype).
 struct QkvArgs {
@@ -70,7 +75,8 @@ struct AttnArgs {
   float scale;             // 1/sqrt(hd)
   float* part_o;           // [max_chunks][M][H][hd]
   float* part_ml;          // [max_chunks][M][H][2]
-  float* out;              // [M, H * hd] fp32
+  void* out;               // activation fragments of [M, H * hd] (2 bf16 terms, or fp32)
+  int MBn;
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 

@@ -15,23 +15,55 @@ __global__ __launch_bounds__(256) void embed_kernel(const T* E, const RowInfo* r
   for (int i = threadIdx.x; i < d; i += 256) X[(size_t)m * d + i] = to_f<T>(e[i]);
 }
 
-// x = X[m] + sum_s P[s][m] (split order); X[m] = x; y = x / sqrt(mean(x^2) + eps) * g.
-template <typename G>
+// Sum of the split partials of one float4, in split order (4 loads in flight).
+__device__ __forceinline__ float4 split_sum4(const float* P, size_t stride, int ksplit, size_t off) {
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  int sp = 0;
+  for (; sp + 4 <= ksplit; sp += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = *(const float4*)(P + (size_t)(sp + q) * stride + off);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc.x += v[q].x;
+      acc.y += v[q].y;
+      acc.z += v[q].z;
+      acc.w += v[q].w;
+    }
+  }
+  for (; sp < ksplit; ++sp) {
+    const float4 v = *(const float4*)(P + (size_t)sp * stride + off);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  return acc;
+}
+
+// x = X[m] + sum_s P[s][m] (split order); X[m] = x; y = x / sqrt(mean(x^2) + eps) * g,
+// written as activation fragments (row rows[m].lm when `rows` is given).
+// One work-group per row; d is a multiple of 64, each thread owns float4s.
+template <typename G, bool BF16, int NT>
 __global__ __launch_bounds__(256) void resid_norm_kernel(float* X, const float* P, int ksplit, int M, int d,
-                                                         const G* g, float eps, float* Y, const RowInfo* rows) {
+                                                         const G* g, float eps, void* Y, int MBn,
+                                                         const RowInfo* rows) {
   __shared__ float red[256];
   const int m = blockIdx.x;
   float* x = X + (size_t)m * d;
+  const size_t stride = (size_t)M * d;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = x[i];
+  for (int i = threadIdx.x * 4; i < d; i += 1024) {
+    float4 v = *(float4*)(x + i);
     if (P) {
-      float acc = 0.f;
-      for (int sp = 0; sp < ksplit; ++sp) acc += P[((size_t)sp * M + m) * d + i];
-      v = v + acc;
-      x[i] = v;
+      const float4 acc = split_sum4(P, stride, ksplit, (size_t)m * d + i);
+      v.x = v.x + acc.x;
+      v.y = v.y + acc.y;
+      v.z = v.z + acc.z;
+      v.w = v.w + acc.w;
+      *(float4*)(x + i) = v;
     }
-    ss += v * v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   red[threadIdx.x] = ss;
   __syncthreads();
@@ -42,71 +74,75 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(float* X, const float* 
   const int out = rows ? rows[m].lm : m;
   if (out < 0) return;
   const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256) Y[(size_t)out * d + i] = x[i] * inv * to_f<G>(g[i]);
-}
-
-// h = silu(gate) * up from the gate/up partial sums
-__global__ __launch_bounds__(256) void swiglu_kernel(const float* P, int ksplit, int M, int F, float* H) {
-  const int m = blockIdx.x;
-  const size_t N = 2 * (size_t)F;
-  for (int f = threadIdx.x; f < F; f += 256) {
-    float gt = 0.f, up = 0.f;
-    for (int sp = 0; sp < ksplit; ++sp) {
-      const float* p = P + ((size_t)sp * M + m) * N;
-      gt += p[f];
-      up += p[F + f];
-    }
-    H[(size_t)m * F + f] = gt / (1.0f + expf(-gt)) * up;
+  for (int k0 = threadIdx.x * 8; k0 < d; k0 += 2048) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = x[k0 + e] * inv * to_f<G>(g[k0 + e]);
+    put_afrag<BF16, NT>(Y, out, k0, v, d >> 5, MBn);
   }
 }
 
-// QKV partial sums -> rotate-half RoPE -> Q (fp32) and paged K/V (model dtype)
+// h = silu(gate) * up from the gate/up partial sums, as fragments; grid (M, F / 2048).
+template <bool BF16, int NT>
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* P, int ksplit, int M, int F, void* H, int MBn) {
+  const int m = blockIdx.x;
+  const int f = blockIdx.y * 2048 + threadIdx.x * 8;
+  if (f >= F) return;
+  const size_t N = 2 * (size_t)F, stride = (size_t)M * N;
+  float v[8];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const float4 gt = split_sum4(P, stride, ksplit, (size_t)m * N + f + 4 * h);
+    const float4 up = split_sum4(P, stride, ksplit, (size_t)m * N + F + f + 4 * h);
+    v[4 * h + 0] = gt.x / (1.0f + expf(-gt.x)) * up.x;
+    v[4 * h + 1] = gt.y / (1.0f + expf(-gt.y)) * up.y;
+    v[4 * h + 2] = gt.z / (1.0f + expf(-gt.z)) * up.z;
+    v[4 * h + 3] = gt.w / (1.0f + expf(-gt.w)) * up.w;
+  }
+  put_afrag<BF16, NT>(H, m, f, v, F >> 5, MBn);
+}
+
+// QKV partial sums -> rotate-half RoPE -> Q (fp32) and paged K/V (model
+// dtype); grid (M, H + 2 KVH), thread i owns the pair (i, i + hd/2).
 template <typename T>
-__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
-  __shared__ double s_cos[64], s_sin[64];
-  const int m = blockIdx.x;
+__global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
+  const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
   const int half = a.hd >> 1;
+  if (i >= half) return;
   const RowInfo ri = a.rows[m];
-  if (threadIdx.x < half) {
-    // angle pos * theta^(-2i/hd) in fp64
-    const double inv = pow((double)a.theta, -2.0 * (double)threadIdx.x / (double)a.hd);
-    const double ang = (double)ri.pos * inv;
-    s_cos[threadIdx.x] = cos(ang);
-    s_sin[threadIdx.x] = sin(ang);
+  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
+  const size_t c = (size_t)m * N + (size_t)hh * a.hd + i;
+  float x1 = 0.f, x2 = 0.f;
+  for (int sp = 0; sp < a.ksplit; ++sp) {
+    x1 += a.P[sp * stride + c];
+    x2 += a.P[sp * stride + c + half];
   }
-  __syncthreads();
+  float y1 = x1, y2 = x2;
+  if (hh < a.H + a.KVH) {
+    // angle pos * theta^(-2i/hd) and the rotation in fp64
+    const double inv = pow((double)a.theta, -2.0 * (double)i / (double)a.hd);
+    const double ang = (double)ri.pos * inv;
+    const double cs = cos(ang), sn = sin(ang);
+    y1 = (float)((double)x1 * cs - (double)x2 * sn);
+    y2 = (float)((double)x2 * cs + (double)x1 * sn);
+  }
+  if (hh < a.H) {
+    float* q = a.q + ((size_t)m * a.H + hh) * a.hd;
+    q[i] = y1;
+    q[i + half] = y2;
+    return;
+  }
   const SeqInfo si = a.seqs[ri.seq];
   const int blk = a.btab[si.bt + ri.slot / kBlock], t = ri.slot % kBlock;
   T* pool = (T*)a.pool;
-  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd;
-  const int pairs = (a.H + 2 * a.KVH) * half;
-  for (int e = threadIdx.x; e < pairs; e += 256) {
-    const int hh = e / half, i = e - hh * half;
-    const size_t c = (size_t)hh * a.hd + i;
-    float x1 = 0.f, x2 = 0.f;
-    for (int sp = 0; sp < a.ksplit; ++sp) {
-      const float* p = a.P + ((size_t)sp * a.M + m) * N;
-      x1 += p[c];
-      x2 += p[c + half];
-    }
-    float y1 = x1, y2 = x2;
-    if (hh < a.H + a.KVH) {
-      y1 = (float)((double)x1 * s_cos[i] - (double)x2 * s_sin[i]);
-      y2 = (float)((double)x2 * s_cos[i] + (double)x1 * s_sin[i]);
-    }
-    if (hh < a.H) {
-      float* q = a.q + ((size_t)m * a.H + hh) * a.hd;
-      q[i] = y1;
-      q[i + half] = y2;
-    } else if (hh < a.H + a.KVH) {
-      const int gk = hh - a.H;
-      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i)] = from_f<T>(y1);
-      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + half)] = from_f<T>(y2);
-    } else {
-      const int gv = hh - a.H - a.KVH;
-      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i)] = from_f<T>(y1);
-      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + half)] = from_f<T>(y2);
-    }
+  if (hh < a.H + a.KVH) {
+    const int gk = hh - a.H;
+    pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i)] = from_f<T>(y1);
+    pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + half)] = from_f<T>(y2);
+  } else {
+    const int gv = hh - a.H - a.KVH;
+    pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i)] = from_f<T>(y1);
+    pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + half)] = from_f<T>(y2);
   }
 }
 
@@ -226,25 +262,33 @@ void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, f
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)E, rows, d, X);
 }
 
-void launch_resid_norm(bool bf16_gain, float* X, const float* P, int ksplit, int M, int d, const void* g, float eps,
-                       float* Y, const RowInfo* rows, hipStream_t s) {
-  if (bf16_gain)
-    hipLaunchKernelGGL(resid_norm_kernel<uint16_t>, dim3(M), dim3(256), 0, s, X, P, ksplit, M, d, (const uint16_t*)g,
-                       eps, Y, rows);
+void launch_resid_norm(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
+                       float eps, void* Y, int MBn, const RowInfo* rows, hipStream_t s) {
+  if (!bf16)
+    hipLaunchKernelGGL((resid_norm_kernel<float, false, 1>), dim3(M), dim3(256), 0, s, X, P, ksplit, M, d,
+                       (const float*)g, eps, Y, MBn, rows);
+  else if (terms >= 3)
+    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 3>), dim3(M), dim3(256), 0, s, X, P, ksplit, M, d,
+                       (const uint16_t*)g, eps, Y, MBn, rows);
   else
-    hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(M), dim3(256), 0, s, X, P, ksplit, M, d, (const float*)g, eps,
-                       Y, rows);
+    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 2>), dim3(M), dim3(256), 0, s, X, P, ksplit, M, d,
+                       (const uint16_t*)g, eps, Y, MBn, rows);
 }
 
-void launch_swiglu(const float* P, int ksplit, int M, int F, float* H, hipStream_t s) {
-  hipLaunchKernelGGL(swiglu_kernel, dim3(M), dim3(256), 0, s, P, ksplit, M, F, H);
+void launch_swiglu(bool bf16, const float* P, int ksplit, int M, int F, void* H, int MBn, hipStream_t s) {
+  const dim3 grid(M, (F + 2047) / 2048);
+  if (bf16)
+    hipLaunchKernelGGL((swiglu_kernel<true, 2>), grid, dim3(256), 0, s, P, ksplit, M, F, H, MBn);
+  else
+    hipLaunchKernelGGL((swiglu_kernel<false, 1>), grid, dim3(256), 0, s, P, ksplit, M, F, H, MBn);
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
+  const dim3 grid(a.M, a.H + 2 * a.KVH);
   if (bf16)
-    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, dim3(a.M), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, grid, dim3(64), 0, s, a);
   else
-    hipLaunchKernelGGL(qkv_finish_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(64), 0, s, a);
 }
 
 void launch_decide(const DecideArgs& a, hipStream_t s) {

@@ -77,7 +77,7 @@ Dims dims_of(const via_model_desc* d) {
 }
 
 struct Layout {
-  size_t X, Y, Q, A, Hb, Yl, part, att_o, att_ml, lm_part;
+  size_t X, Yf, Q, Af, Hf, Ylf, part, att_o, att_ml, lm_part;
   size_t rows, seqs, btab, items, lm;  // plan region
   size_t step_seqs, dtok, drow, dpar;  // step region
   size_t c_btab, c_moves;              // commit region
@@ -97,13 +97,16 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
     return r;
   };
   const size_t R = max_rows;
-  (void)es;
+  // activation fragments: rows padded to the GEMM row group; bf16 models
+  // keep 3 bf16 terms for the QKV input, 2 elsewhere; fp32 models 1 fp32
+  const size_t Rp = (size_t)ceil_div(max_rows, 32) * 32;
+  const size_t f3 = es == 2 ? 6 : 4, f2 = 4;
   L.X = take(R * D.d * 4);
-  L.Y = take(R * D.d * 4);
+  L.Yf = take(Rp * D.d * f3);
   L.Q = take(R * D.H * D.hd * 4);
-  L.A = take(R * D.H * D.hd * 4);
-  L.Hb = take(R * D.F * 4);
-  L.Yl = take(R * D.d * 4);
+  L.Af = take(Rp * D.H * D.hd * f2);
+  L.Hf = take(Rp * D.F * f2);
+  L.Ylf = take(Rp * D.d * f2);
   size_t part = 0;
   for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down}) part = std::max(part, (size_t)g.ks * R * g.N * 4);
   L.part = take(part);
@@ -326,11 +329,12 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   const SeqInfo* d_seqs = (const SeqInfo*)(ws + L.seqs);
   const int32_t* d_btab = (const int32_t*)(ws + L.btab);
   float* X = (float*)(ws + L.X);
-  float* Y = (float*)(ws + L.Y);
+  void* Yf = ws + L.Yf;
   float* Q = (float*)(ws + L.Q);
-  float* A = (float*)(ws + L.A);
-  float* Hb = (float*)(ws + L.Hb);
+  void* Af = ws + L.Af;
+  void* Hf = ws + L.Hf;
   float* part = (float*)(ws + L.part);
+  const int MBn = ceil_div(M, gemm_rows_per_group(M)) * gemm_rows_per_group(M) / 16;
   void* pool = cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim;
   const int pool_blocks = cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim;
   std::vector<int> route;
@@ -340,10 +344,10 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     route = m->route;
   const float eps = m->d.rms_eps;
 
-  auto gemm = [&](const float* Xin, int ldx, const void* W, const GemmShape& sh, int terms, int kind) {
+  auto gemm = [&](const void* Xf, const void* W, const GemmShape& sh, int terms, int kind) {
     GemmArgs g{};
-    g.X = Xin;
-    g.ldx = ldx;
+    g.X = Xf;
+    g.MBn = MBn;
     g.W = W;
     g.M = M;
     g.K = sh.K;
@@ -354,7 +358,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   };
 
   launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
-  launch_resid_norm(bf, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], eps, Y, nullptr, s);
+  launch_resid_norm(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], eps, Yf, MBn, nullptr, s);
   AttnArgs at{};
   at.q = Q;
   at.pool = pool;
@@ -373,7 +377,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   at.scale = (float)(1.0 / std::sqrt((double)D.hd));
   at.part_o = (float*)(ws + L.att_o);
   at.part_ml = (float*)(ws + L.att_ml);
-  at.out = A;
+  at.out = Af;
+  at.MBn = MBn;
   QkvArgs qa{};
   qa.P = part;
   qa.ksplit = D.g_qkv.ks;
@@ -391,28 +396,29 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   for (size_t si = 0; si < route.size(); ++si) {
     const int l = route[si];
     // Q/K/V: three bf16 terms per activation (the K/V are rounded to the cache's bf16)
-    gemm(Y, D.d, m->w_qkv[l], D.g_qkv, 3, VIA_KERNEL_QKV);
+    gemm(Yf, m->w_qkv[l], D.g_qkv, 3, VIA_KERNEL_QKV);
     qa.layer_slot = (int)si;
     launch_qkv_finish(bf, qa, s);
     at.layer_slot = (int)si;
     timed_launch(kv, VIA_KERNEL_ATTN, s, [&] { launch_attention(bf, at, s); });
-    gemm(A, D.H * D.hd, m->w_o[l], D.g_o, 2, VIA_KERNEL_O);
-    launch_resid_norm(bf, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], eps, Y, nullptr, s);
-    gemm(Y, D.d, m->w_gate_up[l], D.g_gu, 2, VIA_KERNEL_GATEUP);
-    launch_swiglu(part, D.g_gu.ks, M, D.F, Hb, s);
-    gemm(Hb, D.F, m->w_down[l], D.g_down, 2, VIA_KERNEL_DOWN);
+    gemm(Af, m->w_o[l], D.g_o, 2, VIA_KERNEL_O);
+    launch_resid_norm(bf, 2, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], eps, Yf, MBn, nullptr, s);
+    gemm(Yf, m->w_gate_up[l], D.g_gu, 2, VIA_KERNEL_GATEUP);
+    launch_swiglu(bf, part, D.g_gu.ks, M, D.F, Hf, MBn, s);
+    gemm(Hf, m->w_down[l], D.g_down, 2, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
-      launch_resid_norm(bf, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], eps, Y, nullptr, s);
+      launch_resid_norm(bf, 3, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], eps, Yf, MBn, nullptr, s);
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
     const LmRow* d_lm = (const LmRow*)(ws + L.lm);
-    float* Yl = (float*)(ws + L.Yl);
+    void* Ylf = ws + L.Ylf;
+    const int MBl = ceil_div(nlm, gemm_rows_per_group(nlm)) * gemm_rows_per_group(nlm) / 16;
     // last residual update, final norm of the head rows only
-    launch_resid_norm(bf, X, part, D.g_down.ks, M, D.d, m->final_norm, eps, Yl, d_rows, s);
+    launch_resid_norm(bf, 2, X, part, D.g_down.ks, M, D.d, m->final_norm, eps, Ylf, MBl, d_rows, s);
     GemmArgs h{};
-    h.X = Yl;
-    h.ldx = D.d;
+    h.X = Ylf;
+    h.MBn = MBl;
     h.W = m->lm_head;
     h.M = nlm;
     h.K = D.d;
@@ -679,6 +685,20 @@ const char* via_version(void) { return "via-gfx950 0.1"; }
 size_t via_pool_bytes(const via_model_desc* desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size) {
   if (!desc) return 0;
   return (size_t)n_layer_slots * n_blocks * 2 * desc->n_kv_heads * block_size * desc->head_dim * esize_of(desc);
+}
+
+size_t via_packed_bytes(int32_t rows, int32_t cols, int32_t dtype) {
+  if (rows < 1 || cols < 32 || cols % 32 || (dtype != VIA_DTYPE_F32 && dtype != VIA_DTYPE_BF16)) return 0;
+  return (size_t)((rows + 63) / 64) * 64 * cols * (dtype == VIA_DTYPE_BF16 ? 2 : 4);
+}
+
+via_status via_pack_weight(const void* src, void* dst, int32_t rows, int32_t cols, int32_t dtype, void* stream) {
+  if (!src || !dst) return fail(VIA_EINVAL, "null pointer");
+  if (!via_packed_bytes(rows, cols, dtype)) return fail(VIA_EINVAL, "rows >= 1, cols a positive multiple of 32, dtype f32/bf16");
+  launch_pack(dtype == VIA_DTYPE_BF16, src, dst, rows, cols, (hipStream_t)stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(VIA_EDEVICE, "pack launch: %s", hipGetErrorString(e));
+  return VIA_OK;
 }
 
 size_t via_workspace_bytes(const via_model_desc* desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
