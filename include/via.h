@@ -115,7 +115,7 @@ typedef struct {
  * layer slots) and the slim-verifier's (one slot per retained layer, in
  * route order).  Pool layout, element type = model dtype, block_size = 16:
  *   pool[slot][block][K|V][kv_head][...]
- *   K page: [16 tokens][head_dim]         (token-major)
+ *   K page: [head_dim/8][16 tokens][8]    (dim groups of 8, token-major within)
  *   V page: [head_dim][16 tokens]         (transposed)
  * Cache slot p of a sequence lives in block table[p / 16], row p % 16.
  * Sizes: via_pool_bytes() and via_workspace_bytes(). */

@@ -11,7 +11,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;        // tokens per KV page
 constexpr int kMaxChildren = 8;   // drafts verified by one row
-constexpr int kAttnChunk = 128;   // keys per attention work-group (split-KV chunk)
+constexpr int kAttnChunk = 256;   // keys per attention work-group (split-KV chunk)
+constexpr int kAttnQueries = 64;  // (row, head-in-group) queries per attention work-group
 
 // One fed row of a forward (lag row or window row).
 struct RowInfo {
@@ -34,12 +35,12 @@ struct SeqInfo {
   int32_t pad0, pad1;
 };
 
-// One attention work item: a tile of 32 (row, head-in-group) queries of a sequence.
+// One attention work item: up to kAttnQueries (row, head-in-group) queries of a
+// sequence, with the sequence's cache geometry inlined.
 struct AttnItem {
-  int32_t seq;
   int32_t q0;       // first query (row * G + g) of the tile, within the sequence
   int32_t n_chunks; // key chunks of this sequence
-  int32_t pad;
+  int32_t kv_len, row_start, n_rows, win_base, bt, n_blocks;
 };
 
 // Head row: which forward row and where its statistics go.
@@ -86,9 +87,13 @@ struct PoolRef {
 
 __device__ __forceinline__ size_t page_elems(int kvh, int hd) { return (size_t)kvh * kBlock * hd; }
 
-// Element offset of K[layer_slot][block][g][t][i]
+// Element offset of K[layer_slot][block][g] token t, dim i.  K pages are
+// dim-group-major, [hd/8][16 tokens][8]: the 16-byte pieces of one dim
+// group of a page's 16 tokens are contiguous, so an MFMA operand load of 16
+// tokens x 8 dims reads 256 contiguous bytes.
 __device__ __forceinline__ size_t k_off(int slot, int block, int nblk, int kvh, int hd, int g, int t, int i) {
-  return ((((size_t)slot * nblk + block) * 2 + 0) * kvh + g) * (size_t)(kBlock * hd) + (size_t)t * hd + i;
+  return ((((size_t)slot * nblk + block) * 2 + 0) * kvh + g) * (size_t)(kBlock * hd) +
+         ((size_t)(i >> 3) * kBlock + t) * 8 + (i & 7);
 }
 // Element offset of V[layer_slot][block][g][i][t] (transposed page)
 __device__ __forceinline__ size_t v_off(int slot, int block, int nblk, int kvh, int hd, int g, int t, int i) {

@@ -48,7 +48,8 @@ struct QkvArgs {
   const RowInfo* rows;
   const SeqInfo* seqs;
   const int32_t* btab;
-  float* q;            // [M, H, hd]
+  uint16_t* q_hi;      // [M, H, hd] bf16 hi terms of Q (fp32 models: Q itself, as float)
+  uint16_t* q_lo;      // [M, H, hd] bf16 lo terms (unused for fp32 models)
   void* pool;
   int pool_blocks, layer_slot;
 };
@@ -63,7 +64,8 @@ void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int nti
 void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, float* X, hipStream_t s);
 
 struct AttnArgs {
-  const float* q;          // [M, H, hd] fp32
+  const void* q_hi;        // [M, H, hd] bf16 hi terms of Q (fp32 models: fp32 Q)
+  const uint16_t* q_lo;    // [M, H, hd] bf16 lo terms
   const void* pool;
   int pool_blocks, layer_slot;
   const RowInfo* rows;

@@ -45,15 +45,15 @@ __device__ __forceinline__ float4 split_sum4(const float* P, size_t stride, int 
 // written as activation fragments (row rows[m].lm when `rows` is given).
 // One work-group per row; d is a multiple of 64, each thread owns float4s.
 template <typename G, bool BF16, int NT>
-__global__ __launch_bounds__(256) void resid_norm_kernel(float* X, const float* P, int ksplit, int M, int d,
-                                                         const G* g, float eps, void* Y, int MBn,
-                                                         const RowInfo* rows) {
-  __shared__ float red[256];
+__global__ __launch_bounds__(1024) void resid_norm_kernel(float* X, const float* P, int ksplit, int M, int d,
+                                                          const G* g, float eps, void* Y, int MBn,
+                                                          const RowInfo* rows) {
+  __shared__ float red[1024];
   const int m = blockIdx.x;
   float* x = X + (size_t)m * d;
   const size_t stride = (size_t)M * d;
   float ss = 0.f;
-  for (int i = threadIdx.x * 4; i < d; i += 1024) {
+  for (int i = threadIdx.x * 4; i < d; i += 4096) {
     float4 v = *(float4*)(x + i);
     if (P) {
       const float4 acc = split_sum4(P, stride, ksplit, (size_t)m * d + i);
@@ -67,14 +67,14 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(float* X, const float* 
   }
   red[threadIdx.x] = ss;
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
+  for (int o = 512; o > 0; o >>= 1) {
     if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
   const int out = rows ? rows[m].lm : m;
   if (out < 0) return;
   const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
-  for (int k0 = threadIdx.x * 8; k0 < d; k0 += 2048) {
+  for (int k0 = threadIdx.x * 8; k0 < d; k0 += 8192) {
     float v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = x[k0 + e] * inv * to_f<G>(g[k0 + e]);
@@ -127,9 +127,19 @@ __global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
     y2 = (float)((double)x2 * cs + (double)x1 * sn);
   }
   if (hh < a.H) {
-    float* q = a.q + ((size_t)m * a.H + hh) * a.hd;
-    q[i] = y1;
-    q[i + half] = y2;
+    const size_t o = ((size_t)m * a.H + hh) * a.hd + i;
+    if constexpr (sizeof(T) == 2) {
+      // Q as bf16 hi (truncated) + lo (rounded) terms for the attention MFMAs
+      const uint32_t h1 = __float_as_uint(y1) >> 16, h2 = __float_as_uint(y2) >> 16;
+      a.q_hi[o] = (uint16_t)h1;
+      a.q_hi[o + half] = (uint16_t)h2;
+      a.q_lo[o] = f2bf(y1 - __uint_as_float(h1 << 16));
+      a.q_lo[o + half] = f2bf(y2 - __uint_as_float(h2 << 16));
+    } else {
+      float* q = (float*)a.q_hi;
+      q[o] = y1;
+      q[o + half] = y2;
+    }
     return;
   }
   const SeqInfo si = a.seqs[ri.seq];
@@ -265,13 +275,13 @@ void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, f
 void launch_resid_norm(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
                        float eps, void* Y, int MBn, const RowInfo* rows, hipStream_t s) {
   if (!bf16)
-    hipLaunchKernelGGL((resid_norm_kernel<float, false, 1>), dim3(M), dim3(256), 0, s, X, P, ksplit, M, d,
+    hipLaunchKernelGGL((resid_norm_kernel<float, false, 1>), dim3(M), dim3(1024), 0, s, X, P, ksplit, M, d,
                        (const float*)g, eps, Y, MBn, rows);
   else if (terms >= 3)
-    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 3>), dim3(M), dim3(256), 0, s, X, P, ksplit, M, d,
+    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 3>), dim3(M), dim3(1024), 0, s, X, P, ksplit, M, d,
                        (const uint16_t*)g, eps, Y, MBn, rows);
   else
-    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 2>), dim3(M), dim3(256), 0, s, X, P, ksplit, M, d,
+    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 2>), dim3(M), dim3(1024), 0, s, X, P, ksplit, M, d,
                        (const uint16_t*)g, eps, Y, MBn, rows);
 }
 

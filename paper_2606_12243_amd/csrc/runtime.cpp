@@ -114,7 +114,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.att_o = take((size_t)L.max_chunks * R * D.H * D.hd * 4);
   L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
   L.lm_part = take((size_t)gemm_tiles(D.V) * R * 4 * 4);
-  L.max_items = ceil_div(max_rows * D.G, 32) + max_batch;
+  L.max_items = ceil_div(max_rows * D.G, kAttnQueries) + max_batch;
   // plan region (one upload per forward)
   size_t p0 = o;
   L.rows = take(R * sizeof(RowInfo));
@@ -330,7 +330,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   const int32_t* d_btab = (const int32_t*)(ws + L.btab);
   float* X = (float*)(ws + L.X);
   void* Yf = ws + L.Yf;
-  float* Q = (float*)(ws + L.Q);
+  void* Q = ws + L.Q;  // bf16 models: hi terms then lo terms; fp32 models: fp32 Q
+  uint16_t* Qlo = (uint16_t*)(ws + L.Q) + (size_t)M * D.H * D.hd;
   void* Af = ws + L.Af;
   void* Hf = ws + L.Hf;
   float* part = (float*)(ws + L.part);
@@ -360,7 +361,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
   launch_resid_norm(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], eps, Yf, MBn, nullptr, s);
   AttnArgs at{};
-  at.q = Q;
+  at.q_hi = Q;
+  at.q_lo = Qlo;
   at.pool = pool;
   at.pool_blocks = pool_blocks;
   at.rows = d_rows;
@@ -390,7 +392,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   qa.rows = d_rows;
   qa.seqs = d_seqs;
   qa.btab = d_btab;
-  qa.q = Q;
+  qa.q_hi = (uint16_t*)Q;
+  qa.q_lo = Qlo;
   qa.pool = pool;
   qa.pool_blocks = pool_blocks;
   for (size_t si = 0; si < route.size(); ++si) {
@@ -608,7 +611,9 @@ via_status build_verify_plan(via_kv* kv, int cache, const WinCopy& w, const std:
     }
     P.seqs.push_back(si);
     const int nq = si.n_rows * D.G;
-    for (int q0 = 0; q0 < nq; q0 += 32) P.items.push_back(AttnItem{sidx, q0, ceil_div(si.kv_len, kAttnChunk), 0});
+    for (int q0 = 0; q0 < nq; q0 += kAttnQueries)
+      P.items.push_back(AttnItem{q0, ceil_div(si.kv_len, kAttnChunk), si.kv_len, si.row_start, si.n_rows, si.win_base,
+                                 si.bt, si.n_blocks});
   }
   return VIA_OK;
 }
@@ -929,7 +934,9 @@ via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* 
         P.rows.push_back(r);
       }
       P.seqs.push_back(si);
-      for (int q0 = 0; q0 < si.n_rows * G; q0 += 32) P.items.push_back(AttnItem{0, q0, ceil_div(c1, kAttnChunk), 0});
+      for (int q0 = 0; q0 < si.n_rows * G; q0 += kAttnQueries)
+        P.items.push_back(AttnItem{q0, ceil_div(c1, kAttnChunk), si.kv_len, si.row_start, si.n_rows, si.win_base,
+                                   si.bt, si.n_blocks});
       if ((st = exec_forward(m, kv, cache, P, false, nullptr, 1.f, s))) {
         trim_blocks(kv, 0, seq_id, 0);
         trim_blocks(kv, 1, seq_id, 0);

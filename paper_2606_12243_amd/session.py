@@ -89,7 +89,8 @@ class Session:
                 if pad:
                     K = torch.cat([K, torch.zeros((pad, KVH, hd), dtype=K.dtype, device=K.device)])
                     V = torch.cat([V, torch.zeros((pad, KVH, hd), dtype=V.dtype, device=V.device)])
-                Kp = K.view(nb, via.BLOCK, KVH, hd).permute(0, 2, 1, 3).reshape(nb, KVH, via.BLOCK * hd)
+                # K page [hd/8][16 tokens][8], V page [hd][16 tokens]
+                Kp = K.view(nb, via.BLOCK, KVH, hd // 8, 8).permute(0, 2, 3, 1, 4).reshape(nb, KVH, via.BLOCK * hd)
                 Vp = V.view(nb, via.BLOCK, KVH, hd).permute(0, 2, 3, 1).reshape(nb, KVH, via.BLOCK * hd)
                 pv[s, :, 0].index_copy_(0, idx, Kp.contiguous())
                 pv[s, :, 1].index_copy_(0, idx, Vp.contiguous())

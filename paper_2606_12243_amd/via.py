@@ -262,7 +262,7 @@ class KV:
         return n.value, ms.value
 
     def pool_view(self, cache):
-        """Pool as [slots, blocks, 2, KVH, 16*hd] (K page token-major, V page transposed)."""
+        """Pool as [slots, blocks, 2, KVH, 16*hd]: K page [hd/8][16][8], V page [hd][16]."""
         m = self.model.desc
         slots = m["n_layers"] if cache == CACHE_FULL else len(self.model.route)
         nb = self.cd.blocks_full if cache == CACHE_FULL else self.cd.blocks_slim

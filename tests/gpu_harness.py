@@ -67,6 +67,31 @@ class Lockstep:
         self.drafter.attach(b)
         self.sess.prefill(b, tokens)
 
+    def add_synthetic(self, b, tokens):
+        """Sequence whose n-1 context slots hold seeded synthetic K/V (both sides)."""
+        cfg, md = self.cfg, self.md
+        n1 = len(tokens) - 1
+        bf16 = md["dtype"] == "bf16"
+        kv = {(c, s): gen.synthetic_kv(cfg, c, s, b, n1)
+              for c, slots in ((gen.CACHE_FULL, md["n_layers"]), (gen.CACHE_SLIM, len(cfg["route"])))
+              for s in range(slots)}
+
+        def t64(a):
+            if bf16:
+                return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(torch.float64)
+            return torch.from_numpy(a).to(torch.float64)
+
+        kvf = [(t64(kv[(gen.CACHE_FULL, s)][0]), t64(kv[(gen.CACHE_FULL, s)][1])) for s in range(md["n_layers"])]
+        kvs = [(t64(kv[(gen.CACHE_SLIM, s)][0]), t64(kv[(gen.CACHE_SLIM, s)][1])) for s in range(len(cfg["route"]))]
+        self.ver.attach_context(tokens, kvf, kvs)
+        self.drafter.attach(b, kvf)
+
+        def dev(a):
+            t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if bf16 else torch.from_numpy(a)
+            return t
+
+        self.sess.reserve(b, tokens, lambda c, s: (dev(kv[(c, s)][0]), dev(kv[(c, s)][1])))
+
     # ------------------------------------------------------------ checks
     def _cmp_logits(self, w, out, o_logits, b, what):
         R = w.max_rows

@@ -58,3 +58,21 @@ def test_forced_full_matches_greedy_on_gpu():
         ls.run_chain([0], G=16, k=4)
     finally:
         ls.close()
+
+
+@pytest.mark.parametrize("name", ["micro_f32", "small_bf16_hd128"])
+def test_synthetic_context_lockstep(name):
+    """Context K/V written straight into the paged pools (the layout of
+    include/via.h) instead of a prefill; ragged lengths across pages."""
+    cfg = configs.get(name)
+    cfg.update(seed_c=23, seed_d=33, seed_kv=43, corrupt=0.3, temperature=1.0)
+    print(f"[case] synthetic {name}", flush=True)
+    ls = Lockstep(cfg, max_rows=96, max_batch=2, max_drafts=8, max_blocks=32, blocks=96)
+    try:
+        ls.add_synthetic(0, gen.context_tokens(cfg, 0, 301))
+        ls.add_synthetic(1, gen.context_tokens(cfg, 1, 47))
+        steps = ls.run_chain([0, 1], G=16, k=6)
+        print(f"[done] synthetic {name} steps={steps} max_logit_err={ls.max_logit_err:.3g} "
+              f"tiers={sorted(ls.seen_tiers)} resyncs={len(ls.log)}", flush=True)
+    finally:
+        ls.close()
