@@ -1,25 +1,29 @@
 // Tall-skinny GEMMs of the verification forward.
 //
 // P[split][M][N] = X[M, K-slice] * W[N, K-slice]^T with M = fed rows (tens),
-// W (bf16, packed) streamed once from HBM, X (activation fragments) from L2.
-// A work-group (8 waves) owns a 64-column tile and one K slice; its waves
-// split the slice further, keep two batches of loads in flight and sum their
-// partial tiles in LDS in wave order.  The K slices of a tile ("splits") are
+// W (bf16, packed) streamed once from HBM.  A work-group of 8 waves owns a
+// 256-column tile, up to 64 rows and one K slice; each wave owns two
+// 16-column blocks and streams their weights over the whole slice, two
+// chunks of steps ahead of its multiply.  The activation fragments (X) of a
+// chunk are loaded once per work-group into LDS (double-buffered) and read
+// there by all eight waves, so X leaves L2 once per work-group and no
+// cross-wave reduction is needed.  The K slices of a tile ("splits") are
 // written as separate fp32 partial tiles and summed, in split order, by the
 // consumer kernel after the kernel boundary: handing partial sums between
 // work-groups inside one kernel would need a device-scope release, which
 // costs an L2 writeback on this GPU.  Every reduction has a fixed order, so
-// results are bitwise reproducible and independent of M.
+// results are bitwise reproducible.
 //
 // bf16 path: v_mfma_f32_16x16x32_bf16.  Lane l holds row/column l%16 and
 // K sub-block (l/16)*8 .. +7 of each 32-wide step.  Weights are pre-packed
 // (via_pack_weight) and activations are written by their producer kernels
-// as fragments (afrag_group), so every load instruction of a wave reads one
-// contiguous 1 KB block and the inner loop is loads + MFMA only.  fp32
+// as fragments (afrag_group), so every global load of a wave reads one
+// contiguous 1 KB block and every LDS read is conflict-free.  fp32
 // activations enter the matrix cores as NT bf16 terms (x = hi + [mid +] lo),
-// NT = 3 keeping ~24 significant bits and NT = 2 ~16.  Output register r of lane l is row (l/16)*4 + r,
-// column l%16.  The head GEMM (split 1) reduces its tile to per-row
-// (max, second, sum-exp, argmax) partials and draft-token logits in place.
+// NT = 3 keeping ~24 significant bits and NT = 2 ~16.  Output register r of
+// lane l is row (l/16)*4 + r, column l%16.  The head GEMM (split 1) reduces
+// its tile to per-row (max, second, sum-exp, argmax) partials and
+// draft-token logits in place.
 // fp32 path: plain FMA on the vector ALUs (small models only).
 #include "kernels.h"
 
@@ -29,94 +33,119 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kTileN = 64;   // columns per work-group: 4 blocks of 16
-constexpr int kNB = 4;
-constexpr int kBatch = 2;    // 32-wide K steps per load batch
+constexpr int kNBW = 2;                // 16-column blocks per wave
+constexpr int kTileN = 8 * 16 * kNBW;   // columns per work-group tile (8 waves)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ uint4 zero_if(uint4 v, bool ok) {
-  v.x = ok ? v.x : 0u;
-  v.y = ok ? v.y : 0u;
-  v.z = ok ? v.z : 0u;
-  v.w = ok ? v.w : 0u;
-  return v;
-}
+// Work-group tile: 16*MB rows x (8 * 16 * NBW) columns, one K slice.  Wave
+// w owns NBW 16-column blocks and streams their packed W over the whole
+// slice in chunks of C steps, two chunks ahead of the one it multiplies;
+// the X fragments of a chunk are loaded one chunk ahead and staged once in
+// LDS (double-buffered), where all eight waves read them: X leaves L2 once
+// per work-group and no cross-wave reduction is needed.  Columns past N are
+// computed from a clamped tile and never stored.
+template <int MB, int NT, int NBW, int C>
+struct TileShape {
+  static constexpr int kCols = 8 * 16 * NBW;
+  static constexpr int kXChunk = C * NT * MB * 64;   // uint4 per staged chunk
+  static constexpr int kXPT = kXChunk / kThreads;     // uint4 staged per thread
+};
 
-// lds[16*MB][64] = X[m0 .., K slice] * W[c0 .. c0+64, K slice]^T, X given as
-// NT bf16-term fragments and W packed: each load is one contiguous 1 KB block.
-template <int MB, int NT>
-__device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int k_beg, int k_end, float* lds) {
+template <int MB, int NT, int NBW, int C>
+__device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_end, uint4* sx,
+                          f32x4 (&acc)[NBW][MB]) {
+  using TS = TileShape<MB, NT, NBW, C>;
+  static_assert(TS::kXChunk % kThreads == 0, "chunk must split evenly over the threads");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = lane & 15, g = lane >> 4;
   const int S = a.K >> 5;
-  const int st_beg = k_beg >> 5, st_all = (k_end - k_beg) >> 5;
-  const int per = (st_all + kWaves - 1) / kWaves;
-  const int s0 = st_beg + wave * per, s1 = min(st_beg + st_all, s0 + per);
-  const uint4* wt = (const uint4*)a.W + (size_t)(c0 >> 6) * S * (4 * 64) + lane;
-  const uint4* xt = (const uint4*)a.X + (size_t)(m0 >> 4) * 64 + lane;
+  const int t64 = (a.N + 63) >> 6;
+  const uint4* wt[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    const int blk = (c0 >> 4) + wave * NBW + j;  // global 16-column block
+    const int pt = min(blk >> 2, t64 - 1);
+    wt[j] = (const uint4*)a.W + (size_t)pt * S * 256 + (blk & 3) * 64 + lane;
+  }
+  const uint4* xg = (const uint4*)a.X + (size_t)(m0 >> 4) * 64;
   const size_t x_step = (size_t)a.MBn * 64, x_term = (size_t)S * x_step;
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nst = st_end - st_beg;
+  if (nst <= 0) return;
+  const int nch = (nst + C - 1) / C;
 
-  f32x4 acc[MB][kNB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  uint4 wb[2][kBatch][kNB], xb[2][kBatch][NT][MB];
-  // steps past the slice re-read its last step and are skipped by compute
-  auto issue = [&](int buf, int s) {
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int st = min(s + u, s1 - 1);
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) wb[buf][u][nb] = wt[(st * 4 + nb) * 64];
-#pragma unroll
-      for (int q = 0; q < NT; ++q)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) xb[buf][u][q][mb] = xt[q * x_term + st * x_step + mb * 64];
-    }
-  };
-  auto compute = [&](int buf, int s) {
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      if (s + u >= s1) break;  // wave-uniform
-#pragma unroll
-      for (int q = 0; q < NT; ++q)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xb[buf][u][q][mb]),
-                                                                as_bf16x8(wb[buf][u][nb]), acc[mb][nb], 0, 0, 0);
-    }
-  };
+#define TILE_LOAD_W(w, ch)                                                  \
+  {                                                                         \
+    _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                      \
+      const size_t st = (size_t)min(st_beg + (ch) * C + sc, st_end - 1);    \
+      _Pragma("unroll") for (int j = 0; j < NBW; ++j) w[sc][j] = wt[j][st * 256]; \
+    }                                                                       \
+  }
+#define TILE_LOAD_X(ch)                                                     \
+  {                                                                         \
+    _Pragma("unroll") for (int u = 0; u < TS::kXPT; ++u) {                  \
+      const int e = threadIdx.x + u * kThreads; /* [step][term][mb][lane] */ \
+      const int l = e & 63, mb = (e >> 6) % MB, q = (e / (64 * MB)) % NT, sc = e / (64 * MB * NT); \
+      const size_t st = (size_t)min(st_beg + (ch) * C + sc, st_end - 1);   \
+      xs[u] = xg[q * x_term + st * x_step + mb * 64 + l];                   \
+    }                                                                       \
+  }
+#define TILE_STORE_X(ch)                                                    \
+  {                                                                         \
+    uint4* d = sx + ((ch) & 1) * TS::kXChunk + threadIdx.x;                 \
+    _Pragma("unroll") for (int u = 0; u < TS::kXPT; ++u) d[u * kThreads] = xs[u]; \
+  }
+#define TILE_COMPUTE(w, ch)                                                 \
+  {                                                                         \
+    const uint4* xb = sx + ((ch) & 1) * TS::kXChunk + lane;                 \
+    const int valid = nst - (ch) * C;                                       \
+    _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                      \
+      if (sc < valid) {                                                     \
+        _Pragma("unroll") for (int q = 0; q < NT; ++q)                      \
+        _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) {                 \
+          const uint4 xv = xb[((sc * NT + q) * MB + mb) * 64];              \
+          _Pragma("unroll") for (int j = 0; j < NBW; ++j)                   \
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xv), as_bf16x8(w[sc][j]), acc[j][mb], 0, 0, 0); \
+        }                                                                   \
+      }                                                                     \
+    }                                                                       \
+  }
+  // one chunk: prefetch X(ch+1) and W(ch+2), multiply chunk ch, publish
+  // X(ch+1).  Past the last chunk the prefetches repeat it (unconditional
+  // code keeps the staging registers out of scratch memory); the buffer
+  // they fill is never read.
+#define TILE_CHUNK(wcur, wnext2, ch)                                        \
+  {                                                                         \
+    TILE_LOAD_X(min((ch) + 1, nch - 1));                                    \
+    TILE_LOAD_W(wnext2, min((ch) + 2, nch - 1));                            \
+    TILE_COMPUTE(wcur, ch);                                                 \
+    TILE_STORE_X((ch) + 1);                                                 \
+    __syncthreads();                                                        \
+  }
   // buffer indices are compile-time constants (a runtime index would put
-  // the buffers in scratch memory)
-  if (s0 < s1) {
-    issue(0, s0);
-    for (int s = s0; s < s1; s += 2 * kBatch) {
-      if (s + kBatch < s1) issue(1, s + kBatch);
-      compute(0, s);
-      if (s + kBatch >= s1) break;
-      if (s + 2 * kBatch < s1) issue(0, s + 2 * kBatch);
-      compute(1, s + kBatch);
-    }
+  // the buffers in scratch memory): the chunk loop is unrolled by three
+  uint4 w0[C][NBW], w1[C][NBW], w2[C][NBW];
+  uint4 xs[TS::kXPT];
+  TILE_LOAD_X(0);
+  TILE_LOAD_W(w0, 0);
+  TILE_LOAD_W(w1, min(1, nch - 1));
+  TILE_STORE_X(0);
+  __syncthreads();
+  for (int ch = 0; ch < nch; ch += 3) {
+    TILE_CHUNK(w0, w2, ch);
+    if (ch + 1 >= nch) break;
+    TILE_CHUNK(w1, w0, ch + 1);
+    if (ch + 2 >= nch) break;
+    TILE_CHUNK(w2, w1, ch + 2);
   }
-  for (int w = 0; w < kWaves; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float* p = lds + (mb * 16 + g * 4 + r) * kTileN + nb * 16 + n;
-            *p = (w == 0) ? acc[mb][nb][r] : *p + acc[mb][nb][r];
-          }
-    }
-    __syncthreads();
-  }
+#undef TILE_CHUNK
+#undef TILE_COMPUTE
+#undef TILE_STORE_X
+#undef TILE_LOAD_X
+#undef TILE_LOAD_W
 }
 
 // fp32 tile on the vector ALUs (X fragments with one fp32 term).
@@ -155,27 +184,28 @@ __device__ __forceinline__ void merge3(float& mx, int& am, float& sc, float mx2,
 
 // Head tile epilogue, per head row: partial (max, second, sum-exp at the tile
 // max, argmax), the logit of each draft token inside the tile, and the
-// optional fp32 logits dump.  8 threads per row, 8 columns each.
+// optional fp32 logits dump.  16 threads per row, 8 columns each.
 template <int MB>
 __device__ void epi_stats(const GemmArgs& a, int tile, int m0, const float* lds) {
-  const int grp = threadIdx.x >> 3, gl = threadIdx.x & 7;  // 64 groups of 8 threads
+  const int grp = threadIdx.x >> 4, gl = threadIdx.x & 15;  // 32 groups of 16 threads
   const int c0 = tile * kTileN;
-  for (int r = grp; r < 16 * MB; r += kThreads / 8) {
+  for (int r = grp; r < 16 * MB; r += kThreads / 16) {
     const int m = m0 + r;
     if (m >= a.M) continue;  // uniform within the group
     float mx = -INFINITY, sc = -INFINITY;
     int am = 0x7fffffff;
-    for (int c = gl * 8; c < gl * 8 + 8; ++c)
+    constexpr int CPT = kTileN / 16;
+    for (int c = gl * CPT; c < gl * CPT + CPT; ++c)
       if (c0 + c < a.N) merge3(mx, am, sc, lds[r * kTileN + c], c0 + c, -INFINITY);
-    for (int o = 1; o < 8; o <<= 1) {
+    for (int o = 1; o < 16; o <<= 1) {
       const float mx2 = __shfl_xor(mx, o, 64), sc2 = __shfl_xor(sc, o, 64);
       const int am2 = __shfl_xor(am, o, 64);
       merge3(mx, am, sc, mx2, am2, sc2);
     }
     float se = 0.f;
-    for (int c = gl * 8; c < gl * 8 + 8; ++c)
+    for (int c = gl * CPT; c < gl * CPT + CPT; ++c)
       if (c0 + c < a.N) se += expf((lds[r * kTileN + c] - mx) * a.inv_T);
-    for (int o = 1; o < 8; o <<= 1) se += __shfl_xor(se, o, 64);
+    for (int o = 1; o < 16; o <<= 1) se += __shfl_xor(se, o, 64);
     const int out = a.lm[m].out;
     if (gl == 0) {
       float* p = a.lm_part + ((size_t)tile * a.M + m) * 4;
@@ -184,21 +214,27 @@ __device__ void epi_stats(const GemmArgs& a, int tile, int m0, const float* lds)
       p[2] = se;
       p[3] = __int_as_float(am);
     }
-    if (gl < a.lm[m].n_drafts) {
+    if (gl < min(a.lm[m].n_drafts, kMaxChildren)) {
       const int tk = a.lm[m].draft_tok[gl];
       if (tk >= c0 && tk < c0 + kTileN) a.draft_logit[a.lm[m].draft_idx[gl]] = lds[r * kTileN + tk - c0];
     }
     if (a.logits) {
-      for (int c = gl * 8; c < gl * 8 + 8; ++c)
+      for (int c = gl * CPT; c < gl * CPT + CPT; ++c)
         if (c0 + c < a.N) a.logits[(size_t)out * a.N + c0 + c] = lds[r * kTileN + c];
     }
   }
 }
 
-template <typename T, int MB, int NT, bool STATS>
+template <typename T, int MB, int NT, int NBW, int C, bool STATS>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
-  __shared__ float lds[16 * MB * kTileN];
-  // block -> (tile, split, m-group), m-group fastest: neighbours share W rows
+  using TS = TileShape<MB, NT, NBW, C>;
+  static_assert(TS::kCols == kTileN, "tile width");
+  constexpr int kLdsX = 2 * TS::kXChunk * 16;               // bytes of the X double buffer
+  constexpr int kLdsT = 16 * MB * kTileN * 4;                // bytes of an fp32 output tile
+  constexpr int kLds = (sizeof(T) == 2 ? kLdsX : 0) > kLdsT ? (sizeof(T) == 2 ? kLdsX : 0) : kLdsT;
+  __shared__ __align__(16) unsigned char smem[kLds];
+  float* lds = (float*)smem;
+  // block -> (tile, split, m-group), m-group fastest
   const int mgroups = (a.M + 16 * MB - 1) / (16 * MB);
   int b = blockIdx.x;
   const int mg = b % mgroups;
@@ -207,33 +243,65 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
   const int tile = b / a.ksplit;
   const int m0 = mg * 16 * MB, c0 = tile * kTileN;
   const int steps = a.K >> 5, per = (steps + a.ksplit - 1) / a.ksplit;
-  const int k_beg = min(steps, split * per) * 32, k_end = min(steps, (split + 1) * per) * 32;
-  if constexpr (sizeof(T) == 2)
-    tile_bf16<MB, NT>(a, c0, m0, k_beg, k_end, lds);
-  else
-    tile_f32<MB>(a, c0, m0, k_beg, k_end, lds);
-  if constexpr (STATS) {
-    epi_stats<MB>(a, tile, m0, lds);
+  const int st_beg = min(steps, split * per), st_end = min(steps, (split + 1) * per);
+  if constexpr (sizeof(T) == 2) {
+    f32x4 acc[NBW][MB];
+    tile_bf16<MB, NT, NBW, C>(a, c0, m0, st_beg, st_end, (uint4*)smem, acc);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, n = lane & 15, g = lane >> 4;
+    if constexpr (STATS) {
+      __syncthreads();  // the X buffers become the output tile
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) lds[(mb * 16 + g * 4 + r) * kTileN + (wave * NBW + j) * 16 + n] = acc[j][mb][r];
+      __syncthreads();
+      epi_stats<MB>(a, tile, m0, lds);
+    } else {
+      float* P = a.part + (size_t)split * a.M * a.N;
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+        const int col = c0 + (wave * NBW + j) * 16 + n;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + mb * 16 + g * 4 + r;
+            if (m < a.M && col < a.N) P[(size_t)m * a.N + col] = acc[j][mb][r];
+          }
+      }
+    }
   } else {
-    float* P = a.part + (size_t)split * a.M * a.N;
-    for (int e = threadIdx.x; e < 16 * MB * kTileN; e += kThreads) {
-      const int r = e / kTileN, c = e - r * kTileN, m = m0 + r, col = c0 + c;
-      if (m < a.M && col < a.N) P[(size_t)m * a.N + col] = lds[e];
+    tile_f32<MB>(a, c0, m0, st_beg * 32, st_end * 32, lds);
+    if constexpr (STATS) {
+      epi_stats<MB>(a, tile, m0, lds);
+    } else {
+      float* P = a.part + (size_t)split * a.M * a.N;
+      for (int e = threadIdx.x; e < 16 * MB * kTileN; e += kThreads) {
+        const int r = e / kTileN, c = e - r * kTileN, m = m0 + r, col = c0 + c;
+        if (m < a.M && col < a.N) P[(size_t)m * a.N + col] = lds[e];
+      }
     }
   }
 }
 
 template <typename T, int NT, bool STATS>
 void launch_e(const GemmArgs& a, hipStream_t s) {
-  // up to 32 rows per work-group (register budget); more rows take more
-  // m-groups, whose neighbouring work-groups re-read the same W rows
   const int mb = gemm_rows_per_group(a.M) / 16;
   const int mgroups = (a.M + 16 * mb - 1) / (16 * mb);
   dim3 grid(gemm_tiles(a.N) * a.ksplit * mgroups);
-  if (mb == 1)
-    hipLaunchKernelGGL((gemm_kernel<T, 1, NT, STATS>), grid, dim3(kThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL((gemm_kernel<T, 2, NT, STATS>), grid, dim3(kThreads), 0, s, a);
+  constexpr int NBW = kNBW;
+  // X chunk steps: the double-buffered chunk stays within 144 KB of LDS and
+  // splits evenly over the threads
+#define GEMM_CASE(MBV) hipLaunchKernelGGL((gemm_kernel<T, MBV, NT, NBW, ((NBW == 1 && NT * MBV <= 9) || (NT * MBV) % 2 ? 8 : 4), STATS>), grid, dim3(kThreads), 0, s, a)
+  switch (mb) {
+    case 1: GEMM_CASE(1); break;
+    case 2: GEMM_CASE(2); break;
+    case 3: GEMM_CASE(3); break;
+    default: GEMM_CASE(4); break;
+  }
+#undef GEMM_CASE
 }
 
 // ---------------------------------------------------------------- head stats
@@ -317,7 +385,12 @@ void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, hipS
 
 int gemm_tiles(int N) { return (N + kTileN - 1) / kTileN; }
 
-int gemm_rows_per_group(int M) { return M > 16 ? 32 : 16; }
+int gemm_rows_per_group(int M) { return M > 48 ? 64 : M > 32 ? 48 : M > 16 ? 32 : 16; }
+
+int gemm_padded_rows(int M) {
+  const int g = gemm_rows_per_group(M);
+  return (M + g - 1) / g * g;
+}
 
 void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s) {
   if (!bf16) {

@@ -25,10 +25,13 @@ struct GemmArgs {
 
 // terms: bf16 terms per fp32 activation (2 or 3); stats: head epilogue.
 void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s);
-// 64-column tiles of an N-column GEMM.
+// Column tiles (256 wide) of an N-column GEMM.
 int gemm_tiles(int N);
-// Rows per GEMM work-group for M rows (16 or 32); fragments pad M to a multiple.
+// Rows per GEMM work-group for M rows (16, 32, 48 or 64).
 int gemm_rows_per_group(int M);
+// Rows of the activation fragments for M rows: M padded to a multiple of
+// gemm_rows_per_group(M); non-decreasing in M.
+int gemm_padded_rows(int M);
 // Row-major [rows, cols] -> packed weight tiles (see include/via.h).
 void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, hipStream_t s);
 

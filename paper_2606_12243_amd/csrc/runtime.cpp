@@ -41,10 +41,12 @@ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // Split-K policy: about two work-groups per CU, at least two 32-wide K steps
 // per wave (8 waves) in each slice.  Depends only on the GEMM shape.
+// K splits of a GEMM: about one work-group per compute unit (256), with at
+// least 8 steps of 32 per split.
 int choose_ksplit(int N, int K) {
   const int tiles = gemm_tiles(N);
-  const int ks = ceil_div(512, tiles);
-  return std::max(1, std::min(ks, K / 512));
+  const int ks = (256 + tiles / 2) / tiles;
+  return std::max(1, std::min(ks, K / 256));
 }
 
 struct GemmShape {
@@ -99,7 +101,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   const size_t R = max_rows;
   // activation fragments: rows padded to the GEMM row group; bf16 models
   // keep 3 bf16 terms for the QKV input, 2 elsewhere; fp32 models 1 fp32
-  const size_t Rp = (size_t)ceil_div(max_rows, 32) * 32;
+  const size_t Rp = (size_t)gemm_padded_rows(max_rows);
   const size_t f3 = es == 2 ? 6 : 4, f2 = 4;
   L.X = take(R * D.d * 4);
   L.Yf = take(Rp * D.d * f3);
@@ -335,7 +337,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   void* Af = ws + L.Af;
   void* Hf = ws + L.Hf;
   float* part = (float*)(ws + L.part);
-  const int MBn = ceil_div(M, gemm_rows_per_group(M)) * gemm_rows_per_group(M) / 16;
+  const int MBn = gemm_padded_rows(M) / 16;
   void* pool = cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim;
   const int pool_blocks = cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim;
   std::vector<int> route;
@@ -416,7 +418,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     const int nlm = (int)P.lm.size();
     const LmRow* d_lm = (const LmRow*)(ws + L.lm);
     void* Ylf = ws + L.Ylf;
-    const int MBl = ceil_div(nlm, gemm_rows_per_group(nlm)) * gemm_rows_per_group(nlm) / 16;
+    const int MBl = gemm_padded_rows(nlm) / 16;
     // last residual update, final norm of the head rows only
     launch_resid_norm(bf, 2, X, part, D.g_down.ks, M, D.d, m->final_norm, eps, Ylf, MBl, d_rows, s);
     GemmArgs h{};
