@@ -98,6 +98,8 @@ def main():
     ap.add_argument("--config", default="8b_bf16_chain")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy 5 times (the reference kernel for HBM counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only: the verification step of a batch "
@@ -105,6 +107,14 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe:
+        src = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": src.numel() * 2, "copy_probe_bytes_written": dst.numel() * 2}))
+        return
     from paper_2606_12243_amd import via
     from paper_2606_12243_amd.session import GreedyDrafter
     from workload import configs, gen
@@ -200,9 +210,10 @@ def main():
     dom_bytes = 2 * F * d * esz
     avg_ms = ms_dom / max(1, n_launch)
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9 if n_launch else None
-    roof = {"kernel": "gemm gate/up + SwiGLU (one layer)", "bound": "hbm",
+    roof = {"kernel": "gemm_kernel: gate/up projection of one layer", "bound": "hbm",
             "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None, "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
+            "traffic": measured_traffic(args.config),
             "bytes_per_launch": dom_bytes, "avg_launch_us": round(avg_ms * 1e3, 2), "launches": n_launch}
 
     breakdown = None
@@ -242,6 +253,24 @@ def main():
     if breakdown:
         out["kernels"] = breakdown
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic(config):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by the copy-probe factor), or
+    None when the GEMM source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"gemm_gate_up_{config}_traffic.json")
+    src = os.path.join(ROOT, "paper_2606_12243_amd", "csrc", "gemm.hip")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    with open(src, "rb") as f:
+        digest = hashlib.sha256(f.read()).hexdigest()
+    if rec.get("gemm_source_sha256") != digest:
+        return None
+    return rec.get("traffic_bytes_per_launch")
 
 
 def cpu_baseline(cfg, W, recorded, init_tokens):

@@ -25,6 +25,8 @@
 // its tile to per-row (max, second, sum-exp, argmax) partials and
 // draft-token logits in place.
 // fp32 path: plain FMA on the vector ALUs (small models only).
+#include <hip/hip_ext.h>
+
 #include "kernels.h"
 
 namespace via {
@@ -226,7 +228,7 @@ __device__ void epi_stats(const GemmArgs& a, int tile, int m0, const float* lds)
 }
 
 template <typename T, int MB, int NT, int NBW, int C, bool STATS>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
+__device__ __forceinline__ void gemm_body(const GemmArgs& a) {
   using TS = TileShape<MB, NT, NBW, C>;
   static_assert(TS::kCols == kTileN, "tile width");
   constexpr int kLdsX = 2 * TS::kXChunk * 16;               // bytes of the X double buffer
@@ -286,22 +288,64 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs a) {
   }
 }
 
-template <typename T, int NT, bool STATS>
-void launch_e(const GemmArgs& a, hipStream_t s) {
-  const int mb = gemm_rows_per_group(a.M) / 16;
-  const int mgroups = (a.M + 16 * mb - 1) / (16 * mb);
-  dim3 grid(gemm_tiles(a.N) * a.ksplit * mgroups);
-  constexpr int NBW = kNBW;
-  // X chunk steps: the double-buffered chunk stays within 144 KB of LDS and
-  // splits evenly over the threads
-#define GEMM_CASE(MBV) hipLaunchKernelGGL((gemm_kernel<T, MBV, NT, NBW, ((NBW == 1 && NT * MBV <= 9) || (NT * MBV) % 2 ? 8 : 4), STATS>), grid, dim3(kThreads), 0, s, a)
-  switch (mb) {
-    case 1: GEMM_CASE(1); break;
-    case 2: GEMM_CASE(2); break;
-    case 3: GEMM_CASE(3); break;
-    default: GEMM_CASE(4); break;
+// One entry point per projection, so kernel traces name the projection.
+#define VIA_GEMM_ENTRY(NAME, NT_BF16, STATS)                                              \
+  template <typename T, int MB, int C>                                                   \
+  __global__ __launch_bounds__(kThreads) void NAME(GemmArgs a) {                         \
+    gemm_body<T, MB, (sizeof(T) == 2 ? NT_BF16 : 1), kNBW, C, STATS>(a);                 \
   }
-#undef GEMM_CASE
+VIA_GEMM_ENTRY(gemm_qkv, 3, false)
+VIA_GEMM_ENTRY(gemm_o, 2, false)
+VIA_GEMM_ENTRY(gemm_gate_up, 2, false)
+VIA_GEMM_ENTRY(gemm_down, 2, false)
+VIA_GEMM_ENTRY(gemm_head, 2, true)
+#undef VIA_GEMM_ENTRY
+
+// X chunk steps: the double-buffered chunk stays within 144 KB of LDS and
+// splits evenly over the threads.
+template <typename T, int MB, int NT>
+constexpr int chunk_steps() {
+  return sizeof(T) != 2 ? 8 : ((kNBW == 1 && NT * MB <= 9) || (NT * MB) % 2 ? 8 : 4);
+}
+
+// With timing events the launch carries them in its dispatch, so they
+// bracket the kernel itself rather than the stream around it.
+#define VIA_GEMM_LAUNCH(NAME, NT_BF16)                                                       \
+  template <typename T>                                                                      \
+  void launch_##NAME(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {       \
+    constexpr int NT = sizeof(T) == 2 ? NT_BF16 : 1;                                         \
+    const int mb = gemm_rows_per_group(a.M) / 16;                                            \
+    const int mgroups = (a.M + 16 * mb - 1) / (16 * mb);                                     \
+    const dim3 grid(gemm_tiles(a.N) * a.ksplit * mgroups);                                   \
+    auto go = [&](auto kernel) {                                                             \
+      if (e0)                                                                                \
+        hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, a);             \
+      else                                                                                   \
+        hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a);                           \
+    };                                                                                       \
+    switch (mb) {                                                                            \
+      case 1: go(NAME<T, 1, chunk_steps<T, 1, NT>()>); break;                                \
+      case 2: go(NAME<T, 2, chunk_steps<T, 2, NT>()>); break;                                \
+      case 3: go(NAME<T, 3, chunk_steps<T, 3, NT>()>); break;                                \
+      default: go(NAME<T, 4, chunk_steps<T, 4, NT>()>); break;                               \
+    }                                                                                        \
+  }
+VIA_GEMM_LAUNCH(gemm_qkv, 3)
+VIA_GEMM_LAUNCH(gemm_o, 2)
+VIA_GEMM_LAUNCH(gemm_gate_up, 2)
+VIA_GEMM_LAUNCH(gemm_down, 2)
+VIA_GEMM_LAUNCH(gemm_head, 2)
+#undef VIA_GEMM_LAUNCH
+
+template <typename T>
+void launch_role(GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  switch (role) {
+    case GemmRole::kQkv: launch_gemm_qkv<T>(a, s, e0, e1); break;
+    case GemmRole::kO: launch_gemm_o<T>(a, s, e0, e1); break;
+    case GemmRole::kGateUp: launch_gemm_gate_up<T>(a, s, e0, e1); break;
+    case GemmRole::kDown: launch_gemm_down<T>(a, s, e0, e1); break;
+    case GemmRole::kHead: launch_gemm_head<T>(a, s, e0, e1); break;
+  }
 }
 
 // ---------------------------------------------------------------- head stats
@@ -392,19 +436,11 @@ int gemm_padded_rows(int M) {
   return (M + g - 1) / g * g;
 }
 
-void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s) {
-  if (!bf16) {
-    if (stats)
-      launch_e<float, 1, true>(a, s);
-    else
-      launch_e<float, 1, false>(a, s);
-  } else if (stats) {
-    launch_e<uint16_t, 2, true>(a, s);
-  } else if (terms >= 3) {
-    launch_e<uint16_t, 3, false>(a, s);
-  } else {
-    launch_e<uint16_t, 2, false>(a, s);
-  }
+void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (bf16)
+    launch_role<uint16_t>(role, a, s, e0, e1);
+  else
+    launch_role<float>(role, a, s, e0, e1);
 }
 
 void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int ntiles, float inv_T, int32_t* row_argmax,

@@ -23,8 +23,14 @@ struct GemmArgs {
   float* draft_logit;
 };
 
-// terms: bf16 terms per fp32 activation (2 or 3); stats: head epilogue.
-void launch_gemm(bool bf16, int terms, bool stats, const GemmArgs& a, hipStream_t s);
+// Projection a GEMM computes.  Each has its own kernel entry point; the QKV
+// input carries 3 bf16 terms per fp32 activation, the others 2; the head
+// reduces its tiles to row statistics instead of writing partials.
+enum class GemmRole { kQkv, kO, kGateUp, kDown, kHead };
+// e0/e1 (both or neither): timing events recorded at the kernel's own start
+// and end.
+void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+                 hipEvent_t e1 = nullptr);
 // Column tiles (256 wide) of an N-column GEMM.
 int gemm_tiles(int N);
 // Rows per GEMM work-group for M rows (16, 32, 48 or 64).

@@ -249,6 +249,21 @@ void timed_launch(via_kv* kv, int kind, hipStream_t s, F&& launch) {
   kv->timed.push_back({kind, {a, b}});
 }
 
+// A GEMM of a timed kind carries its events in its own dispatch.
+void timed_gemm(via_kv* kv, int kind, bool bf, GemmRole role, const GemmArgs& g, hipStream_t s) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (kv->timer_mask & (1u << kind)) {
+    a = pool_event(kv);
+    b = a ? pool_event(kv) : nullptr;
+    if (a && !b) {
+      kv->ev_pool.push_back(a);
+      a = nullptr;
+    }
+  }
+  launch_gemm(bf, role, g, s, a, b);
+  if (a) kv->timed.push_back({kind, {a, b}});
+}
+
 struct Plan {
   std::vector<RowInfo> rows;
   std::vector<SeqInfo> seqs;
@@ -347,7 +362,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     route = m->route;
   const float eps = m->d.rms_eps;
 
-  auto gemm = [&](const void* Xf, const void* W, const GemmShape& sh, int terms, int kind) {
+  auto gemm = [&](const void* Xf, const void* W, const GemmShape& sh, GemmRole role, int kind) {
     GemmArgs g{};
     g.X = Xf;
     g.MBn = MBn;
@@ -357,7 +372,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     g.N = sh.N;
     g.ksplit = sh.ks;
     g.part = part;
-    timed_launch(kv, kind, s, [&] { launch_gemm(bf, terms, false, g, s); });
+    timed_gemm(kv, kind, bf, role, g, s);
   };
 
   launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
@@ -401,16 +416,16 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   for (size_t si = 0; si < route.size(); ++si) {
     const int l = route[si];
     // Q/K/V: three bf16 terms per activation (the K/V are rounded to the cache's bf16)
-    gemm(Yf, m->w_qkv[l], D.g_qkv, 3, VIA_KERNEL_QKV);
+    gemm(Yf, m->w_qkv[l], D.g_qkv, GemmRole::kQkv, VIA_KERNEL_QKV);
     qa.layer_slot = (int)si;
     launch_qkv_finish(bf, qa, s);
     at.layer_slot = (int)si;
     timed_launch(kv, VIA_KERNEL_ATTN, s, [&] { launch_attention(bf, at, s); });
-    gemm(Af, m->w_o[l], D.g_o, 2, VIA_KERNEL_O);
+    gemm(Af, m->w_o[l], D.g_o, GemmRole::kO, VIA_KERNEL_O);
     launch_resid_norm(bf, 2, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], eps, Yf, MBn, nullptr, s);
-    gemm(Yf, m->w_gate_up[l], D.g_gu, 2, VIA_KERNEL_GATEUP);
+    gemm(Yf, m->w_gate_up[l], D.g_gu, GemmRole::kGateUp, VIA_KERNEL_GATEUP);
     launch_swiglu(bf, part, D.g_gu.ks, M, D.F, Hf, MBn, s);
-    gemm(Hf, m->w_down[l], D.g_down, 2, VIA_KERNEL_DOWN);
+    gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
       launch_resid_norm(bf, 3, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], eps, Yf, MBn, nullptr, s);
   }
@@ -435,7 +450,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     h.logits = out->logits;
     h.draft_logit = out->draft_logit;
     timed_launch(kv, VIA_KERNEL_HEAD, s, [&] {
-      launch_gemm(bf, 2, true, h, s);
+      launch_gemm(bf, GemmRole::kHead, h, s);
       launch_lm_finalize(d_lm, h.lm_part, nlm, gemm_tiles(D.V), inv_T, out->row_argmax, out->row_max,
                          out->row_sumexp, out->row_gap, s);
     });
