@@ -15,28 +15,23 @@ __global__ __launch_bounds__(256) void embed_kernel(const T* E, const RowInfo* r
   for (int i = threadIdx.x; i < d; i += 256) X[(size_t)m * d + i] = to_f<T>(e[i]);
 }
 
-// Sum of the split partials of one float4, in split order (4 loads in flight).
-__device__ __forceinline__ float4 split_sum4(const float* P, size_t stride, int ksplit, size_t off) {
+// Sum of the split partials of one float4, in split order, with 8 loads in
+// flight.  Loads past the last split re-read it (unconditional loads keep the
+// code branch-free) and are dropped by a select.
+__device__ __forceinline__ float4 split_sum(const float* P, size_t stride, int ksplit, size_t off) {
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  int sp = 0;
-  for (; sp + 4 <= ksplit; sp += 4) {
-    float4 v[4];
+  for (int sp = 0; sp < ksplit; sp += 8) {
+    float4 v[8];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = *(const float4*)(P + (size_t)(sp + q) * stride + off);
+    for (int q = 0; q < 8; ++q) v[q] = *(const float4*)(P + (size_t)min(sp + q, ksplit - 1) * stride + off);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      acc.x += v[q].x;
-      acc.y += v[q].y;
-      acc.z += v[q].z;
-      acc.w += v[q].w;
+    for (int q = 0; q < 8; ++q) {
+      const bool ok = sp + q < ksplit;
+      acc.x += ok ? v[q].x : 0.f;
+      acc.y += ok ? v[q].y : 0.f;
+      acc.z += ok ? v[q].z : 0.f;
+      acc.w += ok ? v[q].w : 0.f;
     }
-  }
-  for (; sp < ksplit; ++sp) {
-    const float4 v = *(const float4*)(P + (size_t)sp * stride + off);
-    acc.x += v.x;
-    acc.y += v.y;
-    acc.z += v.z;
-    acc.w += v.w;
   }
   return acc;
 }
@@ -56,7 +51,7 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(float* X, const float*
   for (int i = threadIdx.x * 4; i < d; i += 4096) {
     float4 v = *(float4*)(x + i);
     if (P) {
-      const float4 acc = split_sum4(P, stride, ksplit, (size_t)m * d + i);
+      const float4 acc = split_sum(P, stride, ksplit, (size_t)m * d + i);
       v.x = v.x + acc.x;
       v.y = v.y + acc.y;
       v.z = v.z + acc.z;
@@ -92,8 +87,8 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* P, int ksplit,
   float v[8];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const float4 gt = split_sum4(P, stride, ksplit, (size_t)m * N + f + 4 * h);
-    const float4 up = split_sum4(P, stride, ksplit, (size_t)m * N + F + f + 4 * h);
+    const float4 gt = split_sum(P, stride, ksplit, (size_t)m * N + f + 4 * h);
+    const float4 up = split_sum(P, stride, ksplit, (size_t)m * N + F + f + 4 * h);
     v[4 * h + 0] = gt.x / (1.0f + expf(-gt.x)) * up.x;
     v[4 * h + 1] = gt.y / (1.0f + expf(-gt.y)) * up.y;
     v[4 * h + 2] = gt.z / (1.0f + expf(-gt.z)) * up.z;
@@ -102,43 +97,66 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* P, int ksplit,
   put_afrag<BF16, NT>(H, m, f, v, F >> 5, MBn);
 }
 
-// QKV partial sums -> rotate-half RoPE -> Q (fp32) and paged K/V (model
-// dtype); grid (M, H + 2 KVH), thread i owns the pair (i, i + hd/2).
+// QKV partial sums -> rotate-half RoPE -> Q (bf16 hi/lo terms, or fp32) and
+// paged K/V (model dtype).  A thread owns dims i..i+3 of one head of one row
+// and their rotation partners i+hd/2..; hd/8 threads per head, 256 per
+// work-group; grid (M, ceil((H + 2 KVH) * hd / 8 / 256)); hd <= 256.
 template <typename T>
-__global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
-  const int m = blockIdx.x, hh = blockIdx.y, i = threadIdx.x;
+__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
+  const int m = blockIdx.x;
   const int half = a.hd >> 1;
-  if (i >= half) return;
   const RowInfo ri = a.rows[m];
+  // the row's rotation angles pos * theta^(-2j/hd), j < hd/2, in fp64: computed
+  // once per work-group and shared by all its heads
+  __shared__ double s_cs[128], s_sn[128];
+  for (int j = threadIdx.x; j < half; j += 256) {
+    const double ang = (double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd);
+    sincos(ang, &s_sn[j], &s_cs[j]);
+  }
+  __syncthreads();
+  const int tph = a.hd >> 3;  // threads per head
+  const int hh = (blockIdx.y * 256 + threadIdx.x) / tph;
+  if (hh >= a.H + 2 * a.KVH) return;
+  const int i = ((blockIdx.y * 256 + threadIdx.x) % tph) * 4;
   const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
   const size_t c = (size_t)m * N + (size_t)hh * a.hd + i;
-  float x1 = 0.f, x2 = 0.f;
-  for (int sp = 0; sp < a.ksplit; ++sp) {
-    x1 += a.P[sp * stride + c];
-    x2 += a.P[sp * stride + c + half];
+  const float4 a1 = split_sum(a.P, stride, a.ksplit, c), a2 = split_sum(a.P, stride, a.ksplit, c + half);
+  float x1[4] = {a1.x, a1.y, a1.z, a1.w}, x2[4] = {a2.x, a2.y, a2.z, a2.w};
+  float y1[4], y2[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    y1[e] = x1[e];
+    y2[e] = x2[e];
   }
-  float y1 = x1, y2 = x2;
   if (hh < a.H + a.KVH) {
-    // angle pos * theta^(-2i/hd) and the rotation in fp64
-    const double inv = pow((double)a.theta, -2.0 * (double)i / (double)a.hd);
-    const double ang = (double)ri.pos * inv;
-    const double cs = cos(ang), sn = sin(ang);
-    y1 = (float)((double)x1 * cs - (double)x2 * sn);
-    y2 = (float)((double)x2 * cs + (double)x1 * sn);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double cs = s_cs[i + e], sn = s_sn[i + e];
+      y1[e] = (float)((double)x1[e] * cs - (double)x2[e] * sn);
+      y2[e] = (float)((double)x2[e] * cs + (double)x1[e] * sn);
+    }
   }
   if (hh < a.H) {
     const size_t o = ((size_t)m * a.H + hh) * a.hd + i;
     if constexpr (sizeof(T) == 2) {
       // Q as bf16 hi (truncated) + lo (rounded) terms for the attention MFMAs
-      const uint32_t h1 = __float_as_uint(y1) >> 16, h2 = __float_as_uint(y2) >> 16;
-      a.q_hi[o] = (uint16_t)h1;
-      a.q_hi[o + half] = (uint16_t)h2;
-      a.q_lo[o] = f2bf(y1 - __uint_as_float(h1 << 16));
-      a.q_lo[o + half] = f2bf(y2 - __uint_as_float(h2 << 16));
+      uint16_t h1[4], h2[4], l1[4], l2[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t u1 = __float_as_uint(y1[e]) >> 16, u2 = __float_as_uint(y2[e]) >> 16;
+        h1[e] = (uint16_t)u1;
+        h2[e] = (uint16_t)u2;
+        l1[e] = f2bf(y1[e] - __uint_as_float(u1 << 16));
+        l2[e] = f2bf(y2[e] - __uint_as_float(u2 << 16));
+      }
+      *(uint2*)(a.q_hi + o) = make_uint2(h1[0] | ((uint32_t)h1[1] << 16), h1[2] | ((uint32_t)h1[3] << 16));
+      *(uint2*)(a.q_hi + o + half) = make_uint2(h2[0] | ((uint32_t)h2[1] << 16), h2[2] | ((uint32_t)h2[3] << 16));
+      *(uint2*)(a.q_lo + o) = make_uint2(l1[0] | ((uint32_t)l1[1] << 16), l1[2] | ((uint32_t)l1[3] << 16));
+      *(uint2*)(a.q_lo + o + half) = make_uint2(l2[0] | ((uint32_t)l2[1] << 16), l2[2] | ((uint32_t)l2[3] << 16));
     } else {
       float* q = (float*)a.q_hi;
-      q[o] = y1;
-      q[o + half] = y2;
+      *(float4*)(q + o) = make_float4(y1[0], y1[1], y1[2], y1[3]);
+      *(float4*)(q + o + half) = make_float4(y2[0], y2[1], y2[2], y2[3]);
     }
     return;
   }
@@ -147,12 +165,18 @@ __global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
   T* pool = (T*)a.pool;
   if (hh < a.H + a.KVH) {
     const int gk = hh - a.H;
-    pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i)] = from_f<T>(y1);
-    pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + half)] = from_f<T>(y2);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + e)] = from_f<T>(y1[e]);
+      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + e + half)] = from_f<T>(y2[e]);
+    }
   } else {
     const int gv = hh - a.H - a.KVH;
-    pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i)] = from_f<T>(y1);
-    pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + half)] = from_f<T>(y2);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + e)] = from_f<T>(y1[e]);
+      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + e + half)] = from_f<T>(y2[e]);
+    }
   }
 }
 
@@ -294,11 +318,12 @@ void launch_swiglu(bool bf16, const float* P, int ksplit, int M, int F, void* H,
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
-  const dim3 grid(a.M, a.H + 2 * a.KVH);
+  const int threads = (a.H + 2 * a.KVH) * (a.hd / 8);
+  const dim3 grid(a.M, (threads + 255) / 256);
   if (bf16)
-    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, grid, dim3(64), 0, s, a);
+    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(64), 0, s, a);
+    hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(256), 0, s, a);
 }
 
 void launch_decide(const DecideArgs& a, hipStream_t s) {

@@ -41,12 +41,12 @@ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // Split-K policy: about two work-groups per CU, at least two 32-wide K steps
 // per wave (8 waves) in each slice.  Depends only on the GEMM shape.
-// K splits of a GEMM: about one work-group per compute unit (256), with at
-// least 8 steps of 32 per split.
+// K splits of a GEMM: as many work-groups as fit the 256 compute units in one
+// round (a GEMM work-group occupies a whole CU, so a 257th would run alone
+// in a second round), with at least 8 steps of 32 per split.
 int choose_ksplit(int N, int K) {
   const int tiles = gemm_tiles(N);
-  const int ks = (256 + tiles / 2) / tiles;
-  return std::max(1, std::min(ks, K / 256));
+  return std::max(1, std::min(256 / std::max(1, tiles), K / 256));
 }
 
 struct GemmShape {

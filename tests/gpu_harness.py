@@ -11,6 +11,10 @@ itself is within 1e-3 of a decision boundary: a top-2 logit gap below 1e-3
 (l'(d) - max l' vs T ln tau).  After such an exempt difference the GPU is
 re-synchronised to the oracle's decision (its commit takes the oracle's
 kappa/emit) and the step is logged.
+
+At full sizes the oracle can follow a sample of the batch (``sample``): the
+GPU still runs every sequence in the same launch, the sampled ones are
+compared element by element, and the rest commit the GPU's own decisions.
 """
 from __future__ import annotations
 
@@ -35,7 +39,7 @@ def logit_tol(desc):
 
 class Lockstep:
     def __init__(self, cfg, weights=None, max_rows=None, max_batch=None, max_drafts=None, max_blocks=None,
-                 blocks=None, params=None, oracle_model=None):
+                 blocks=None, params=None, oracle_model=None, gpu_model=None, sample=None):
         self.cfg = cfg
         md = cfg["model"]
         self.md = md
@@ -47,24 +51,32 @@ class Lockstep:
         self.drafter = GreedyDrafter(self.om, lambda b, step, j: gen.corruption(
             cfg["seed_d"], b, step, j, cfg.get("corrupt", 0.3), V))
         B = max_batch or cfg.get("batch", 1)
-        self.gm = via.Model(md, W, cfg["route"])
+        self.sample = None if sample is None else set(sample)
+        self.own_gm = gpu_model is None
+        self.gm = gpu_model or via.Model(md, W, cfg["route"])
         self.kv = via.KV(self.gm, max_seqs=B, max_blocks_per_seq=max_blocks or 64, blocks_full=blocks or 256,
                          blocks_slim=blocks or 256, max_rows=max_rows or 128, max_batch=B,
                          max_drafts=max_drafts or 16)
         self.sess = Session(self.gm, self.kv, via.tier_params(self.p.tau_acc, self.p.tau_full, self.p.temperature,
                                                              self.p.forced), logits=True)
+        self.o_id = {}    # GPU sequence id -> oracle sequence index
         self.log = []
         self.seen_tiers = set()
         self.max_logit_err = 0.0
 
     def close(self):
         self.kv.close()
-        self.gm.close()
+        if self.own_gm:
+            self.gm.close()
+
+    def sampled(self, b):
+        return self.sample is None or b in self.sample
 
     # ------------------------------------------------------------ setup
     def add_prompt(self, b, tokens):
-        self.ver.prefill(tokens)
-        self.drafter.attach(b)
+        if self.sampled(b):
+            self.o_id[b] = self.ver.prefill(tokens)
+            self.drafter.attach(b)
         self.sess.prefill(b, tokens)
 
     def add_synthetic(self, b, tokens):
@@ -81,10 +93,14 @@ class Lockstep:
                 return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(torch.float64)
             return torch.from_numpy(a).to(torch.float64)
 
-        kvf = [(t64(kv[(gen.CACHE_FULL, s)][0]), t64(kv[(gen.CACHE_FULL, s)][1])) for s in range(md["n_layers"])]
-        kvs = [(t64(kv[(gen.CACHE_SLIM, s)][0]), t64(kv[(gen.CACHE_SLIM, s)][1])) for s in range(len(cfg["route"]))]
-        self.ver.attach_context(tokens, kvf, kvs)
-        self.drafter.attach(b, kvf)
+        if self.sampled(b):
+            kvf = [(t64(kv[(gen.CACHE_FULL, s)][0]), t64(kv[(gen.CACHE_FULL, s)][1]))
+                   for s in range(md["n_layers"])]
+            kvs = [(t64(kv[(gen.CACHE_SLIM, s)][0]), t64(kv[(gen.CACHE_SLIM, s)][1]))
+                   for s in range(len(cfg["route"]))]
+            self.o_id[b] = self.ver.attach_context(tokens, kvf, kvs)
+            if self.sample is None:
+                self.drafter.attach(b, kvf)
 
         def dev(a):
             t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if bf16 else torch.from_numpy(a)
@@ -108,7 +124,8 @@ class Lockstep:
         """drafts: {b: Draft}; runs both sides, compares, commits."""
         p = self.p
         order = sorted(drafts)
-        dec_o = self.ver.step(drafts, p)          # oracle decides and commits
+        raw = self.ver.step({self.o_id[b]: drafts[b] for b in order if self.sampled(b)}, p)  # oracle decides, commits
+        dec_o = {b: raw[self.o_id[b]] for b in order if self.sampled(b)}
         gd = {b: (drafts[b].tok, None if self._is_chain(drafts[b]) else drafts[b].parent) for b in order}
         s = self.sess
         w = s.window(gd, with_lag=True)
@@ -119,6 +136,8 @@ class Lockstep:
         exempt = False
         T = p.temperature
         for i, b in enumerate(order):
+            if b not in dec_o:
+                continue
             do = dec_o[b]
             am = self._cmp_logits(w, s.out_slim, do["slim_logits"], i, "slim")
             st = do["slim_stats"]
@@ -139,14 +158,15 @@ class Lockstep:
             if (h1["status"][i] == 1) != (do["first_status"] == 1):
                 assert exempt, f"escalation differs for seq {b}"
         # full forward for the sequences the oracle escalated (keeps cache state in step)
-        run = np.array([1 if dec_o[b]["full_ran"] else 0 for b in order], np.int32)
+        run = np.array([(1 if dec_o[b]["full_ran"] else 0) if b in dec_o else int(h1["status"][i] == 1)
+                        for i, b in enumerate(order)], np.int32)
         if run.any():
             r, rp = via._i32(run)
             via.check(via.via_verify_full(s.m.h, s.kv.h, w.c, rp, s.p, s.out_full.c, s.sp()))
             via.check(via.via_tier_decide(s.kv.h, s.p, s.out_slim.c, s.out_full.c, s.dec.c, s.sp()))
             s.stream.synchronize()
             for i, b in enumerate(order):
-                if not run[i]:
+                if not run[i] or b not in dec_o:
                     continue
                 do = dec_o[b]
                 am = self._cmp_logits(w, s.out_full, do["full_logits"], i, "full")
@@ -158,6 +178,8 @@ class Lockstep:
         h = s._host(w)
         same = True
         for i, b in enumerate(order):
+            if b not in dec_o:
+                continue
             do = dec_o[b]
             got = (int(h["status"][i]), int(h["kappa"][i]), int(h["emit"][i]), int(h["new_len"][i]))
             want = (do["status"], do["kappa"], do["emit"], do["new_len"])
@@ -167,25 +189,36 @@ class Lockstep:
         if not same:
             self.log.append(dict(step=step_idx, kind="resync"))
             D = w.max_drafts
-            path = np.full((w.B, D), -1, np.int32)
+            path = np.array(h["path"], np.int32).reshape(w.B, -1).copy()
+            hh = {k: np.array(h[k], np.int32).copy() for k in ("status", "kappa", "emit", "new_len")}
             for i, b in enumerate(order):
+                if b not in dec_o:
+                    continue
                 pp = dec_o[b]["path"]
+                path[i, :] = -1
                 path[i, :len(pp)] = pp
-            h = dict(status=np.array([dec_o[b]["status"] for b in order], np.int32),
-                     kappa=np.array([dec_o[b]["kappa"] for b in order], np.int32),
-                     emit=np.array([dec_o[b]["emit"] for b in order], np.int32),
-                     new_len=np.array([dec_o[b]["new_len"] for b in order], np.int32), path=path)
-            s.commit(w, gd, h)
+                for k in hh:
+                    hh[k][i] = dec_o[b][k]
+            hh["path"] = path
+            s.commit(w, gd, hh)
         else:
             s.commit(w, gd)
         # committed tokens, valid lengths and block tables
         for b in order:
-            st = self.ver.seqs[b]
+            if b not in dec_o:
+                continue
+            st = self.ver.seqs[self.o_id[b]]
             assert s.tokens[b] == st.tokens, f"seq {b} token streams differ"
             for cache, oc, which in ((via.CACHE_FULL, st.full, "full"), (via.CACHE_SLIM, st.slim, "slim")):
                 valid, table = self.kv.seq_info(b, cache)
                 assert valid == oc.valid, f"seq {b} {which} valid {valid} vs {oc.valid}"
-                assert table == self.ver.block_table(which, b), f"seq {b} {which} block table differs"
+                if self.sample is None:
+                    assert table == self.ver.block_table(which, self.o_id[b]), f"seq {b} {which} block table differs"
+                else:
+                    # the GPU pool also serves the unsampled sequences: the table must cover the
+                    # valid slots with distinct blocks (the exact ids are checked at small sizes)
+                    assert len(table) == -(-valid // 16) and len(set(table)) == len(table), \
+                        f"seq {b} {which} block table {len(table)} blocks for {valid} slots"
         return dec_o, h
 
     @staticmethod
