@@ -10,10 +10,14 @@ replacements) run beforehand: an untimed reference decode records every
 step's drafts, then the KV state is reset and the recorded steps are
 replayed; W replayed steps warm up, the next K are timed.
 
-value = accepted (committed) tokens summed over the batch / timed seconds.
-The JSON line adds the verify-step latency percentiles, the roofline of the
-dominant kernel (HIP events on the library's stream during the timed
-region) and the oracle's rate on a bounded sample of the same workload.
+value = accepted (committed) tokens summed over the batch / timed seconds, at
+the workload's logit temperature (calibrated for the bf16 workloads so that
+about half of the greedy drafts clear the accept threshold).  The JSON line
+adds the verify-step latency percentiles, the roofline of the dominant
+kernel (HIP events carried by its dispatches during the timed region), the
+whole step's algorithmic bytes against HBM peak, the same workload at T = 1
+(every drafted position escalated to the full verifier) and the oracle's
+rate on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--config 8b_bf16_chain]
 """
@@ -47,9 +51,12 @@ def build_session(cfg, W, pools=None, n_steps=64):
     B = cfg["batch"]
     ctx = cfg["ctx_lens"]
     k = cfg.get("k", 8)
-    rows_per_seq = 64 if cfg["draft"] == "tree" else k * 8
-    max_rows = B * rows_per_seq
+    # rows per sequence: the window plus every committed token the full cache may
+    # still lag by (the full verifier can stay idle for the whole run; the
+    # drafter's probes and the next escalation feed those lag rows)
     grow = n_steps * ((k + 1) if cfg["draft"] != "tree" else len(cfg["tree_budget"]) + 1)
+    rows_per_seq = (64 if cfg["draft"] == "tree" else k) + grow
+    max_rows = B * rows_per_seq
     max_blocks = (max(ctx) + grow + rows_per_seq + 16) // 16 + 1
     blocks = B * max_blocks
     model = cfg.get("_model")
@@ -75,19 +82,109 @@ def attach_context(cfg, sess, synthetic):
             sess.prefill(b, toks)
 
 
-def step_bytes(cfg, h, rows_slim, rows_full):
-    """Algorithmic HBM bytes of one step: weights of the routed layers +
-    head for the slim forward, the same for all layers when q ran, plus the
-    cached K/V each forward reads."""
+def step_bytes(cfg, kv_slim_tokens, kv_full_tokens, full_ran):
+    """Algorithmic HBM bytes of one step: the routed layers' weights and the
+    head for the slim forward, every layer's weights and the head again when
+    the full verifier ran, plus the cached K/V each forward read (tokens
+    summed over the sequences it covered)."""
     from workload.configs import model_bytes
     md = cfg["model"]
     slim = model_bytes(md, cfg["route"])
     full = model_bytes(md)
     kvb = slim["kv_per_token_layer"]
-    tot = slim["layers"] + slim["head"] + kvb * len(cfg["route"]) * rows_slim["ctx"]
-    if rows_full["n"] > 0:
-        tot += full["layers"] + full["head"] + kvb * md["n_layers"] * rows_full["ctx"]
+    tot = slim["layers"] + slim["head"] + kvb * len(cfg["route"]) * kv_slim_tokens
+    if full_ran:
+        tot += full["layers"] + full["head"] + kvb * md["n_layers"] * kv_full_tokens
     return tot
+
+
+def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
+    """Reference decode with the synthetic drafter (records drafts and
+    decisions), then a fresh handle on the same pools replays the recorded
+    steps: `warmup` untimed, `steps` timed.  Returns the measurements."""
+    import torch
+    from paper_2606_12243_amd import via
+    from paper_2606_12243_amd.session import GreedyDrafter
+    from workload import gen
+    md = cfg["model"]
+    V = md["vocab"]
+    B = cfg["batch"]
+    cfg = dict(cfg, temperature=temperature)
+    synthetic = cfg.get("seed_kv") is not None
+    n_steps = warmup + steps
+    sess = build_session(cfg, W, n_steps=n_steps)
+    t0 = time.time()
+    attach_context(cfg, sess, synthetic)
+    torch.cuda.synchronize()
+    log(f"T={temperature:.4g}: context attached ({'synthetic K/V' if synthetic else 'prefill'}) "
+        f"in {time.time() - t0:.1f}s")
+    drafter = GreedyDrafter(sess, lambda b, step, j: gen.corruption(cfg["seed_d"], b, step, j, cfg["corrupt"], V))
+
+    # ---- reference decode: record drafts and decisions
+    recorded, t_draft = [], 0.0
+    init_tokens = {b: list(sess.tokens[b]) for b in range(B)}
+    for i in range(n_steps):
+        ts = time.time()
+        if cfg["draft"] == "tree":
+            drafts = drafter.tree(list(range(B)), cfg["tree_budget"], cfg["tree_branch"], i)
+        else:
+            d = drafter.chain(list(range(B)), cfg["k"], i)
+            drafts = {b: (d[b], None) for b in range(B)}
+        torch.cuda.synchronize()
+        t_draft += time.time() - ts
+        h, run = sess.step(drafts)
+        recorded.append((drafts, h["new_len"].copy(), run.copy()))
+    log(f"T={temperature:.4g}: reference decode of {n_steps} steps, drafting {t_draft:.2f}s")
+
+    # ---- reset: fresh handle on the same pools (context slots untouched)
+    pools = (sess.kv.pool_full, sess.kv.pool_slim)
+    sess.kv.close()
+
+    def fresh():
+        s2 = build_session(cfg, W, pools=pools, n_steps=n_steps)
+        if synthetic:
+            for b in range(B):
+                s2.reserve(b, init_tokens[b], None)
+        else:
+            for b in range(B):
+                s2.prefill(b, init_tokens[b])
+        torch.cuda.synchronize()
+        return s2
+
+    sess = fresh()
+    mism = 0
+    for i in range(warmup):
+        h, run = sess.step(recorded[i][0])
+        mism += int((h["new_len"] != recorded[i][1]).any())
+    torch.cuda.synchronize()
+    if timer_kind is not None:
+        sess.kv.timer_enable(1 << timer_kind)
+        sess.kv.timer_read(timer_kind)
+    lat, accepted, n_full_steps, bytes_tot = [], 0, 0, 0.0
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(warmup, n_steps):
+        drafts = recorded[i][0]
+        n_before = np.array([len(sess.tokens[b]) for b in range(B)])
+        kv_slim = sum(sess.kv.seq_info(b, via.CACHE_SLIM)[0] for b in range(B))
+        kv_full = sum(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)) for b in range(B))
+        ts = time.perf_counter()
+        w, h, run = sess.begin(drafts)
+        sess.commit(w, drafts)
+        torch.cuda.synchronize()
+        lat.append(time.perf_counter() - ts)
+        accepted += int((h["new_len"] - n_before).sum())
+        mism += int((h["new_len"] != recorded[i][1]).any())
+        n_full_steps += int(run.any())
+        bytes_tot += step_bytes(cfg, kv_slim, kv_full, bool(run.any()))
+    t_total = time.perf_counter() - t_start
+    timer = sess.kv.timer_read(timer_kind) if timer_kind is not None else (0, 0.0)
+    sess.kv.timer_enable(0)
+    sess.kv.close()
+    lat_ms = np.array(lat) * 1e3
+    return dict(value=accepted / t_total, t_total=t_total, lat_ms=lat_ms, escalation=n_full_steps / max(1, steps),
+                mismatch=mism, t_draft=t_draft, bytes=bytes_tot, timer=timer, recorded=recorded,
+                init_tokens=init_tokens, accepted=accepted)
 
 
 def main():
@@ -97,6 +194,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="8b_bf16_chain")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-full-tier", action="store_true",
+                    help="skip the T = 1 variant (every position escalated to the full verifier)")
     ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (the reference kernel for HBM counter scaling)")
@@ -116,7 +215,6 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": src.numel() * 2, "copy_probe_bytes_written": dst.numel() * 2}))
         return
     from paper_2606_12243_amd import via
-    from paper_2606_12243_amd.session import GreedyDrafter
     from workload import configs, gen
 
     cfg = configs.get(args.config)
@@ -130,124 +228,66 @@ def main():
     cfg["_model"] = via.Model(md, W, cfg["route"])
     torch.cuda.synchronize()
     log(f"weights on device in {time.time() - t0:.1f}s")
-    n_steps = args.warmup + args.steps
-    sess = build_session(cfg, W, n_steps=n_steps)
-    t0 = time.time()
-    attach_context(cfg, sess, synthetic)
-    torch.cuda.synchronize()
-    log(f"context attached ({'synthetic K/V' if synthetic else 'prefill'}) in {time.time() - t0:.1f}s")
-    V = md["vocab"]
-    drafter = GreedyDrafter(sess, lambda b, step, j: gen.corruption(cfg["seed_d"], b, step, j, cfg["corrupt"], V))
-    B = cfg["batch"]
-
-    # ---- reference decode: record drafts and decisions
-    recorded, t_draft = [], 0.0
-    init_tokens = {b: list(sess.tokens[b]) for b in range(B)}
-    for i in range(n_steps):
-        ts = time.time()
-        if cfg["draft"] == "tree":
-            drafts = drafter.tree(list(range(B)), cfg["tree_budget"], cfg["tree_branch"], i)
-        else:
-            d = drafter.chain(list(range(B)), cfg["k"], i)
-            drafts = {b: (d[b], None) for b in range(B)}
-        torch.cuda.synchronize()
-        t_draft += time.time() - ts
-        h, run = sess.step(drafts)
-        recorded.append((drafts, h["new_len"].copy(), run.copy()))
-    log(f"reference decode: {n_steps} steps, drafting {t_draft:.2f}s")
-
-    # ---- reset: fresh handle on the same pools (context slots untouched)
-    pools = (sess.kv.pool_full, sess.kv.pool_slim)
-    sess.kv.close()
-
-    def fresh():
-        s2 = build_session(cfg, W, pools=pools, n_steps=n_steps)
-        if synthetic:
-            for b in range(B):
-                s2.reserve(b, init_tokens[b], None)
-        else:
-            for b in range(B):
-                s2.prefill(b, init_tokens[b])
-        torch.cuda.synchronize()
-        return s2
-
     kinds = {"qkv": via.KERNEL_QKV, "attn": via.KERNEL_ATTN, "o": via.KERNEL_O, "gateup": via.KERNEL_GATEUP,
              "down": via.KERNEL_DOWN, "head": via.KERNEL_HEAD}
     DOM = "gateup"
-    sess = fresh()
-    mism = 0
-    for i in range(args.warmup):
-        h, run = sess.step(recorded[i][0])
-        mism += int((h["new_len"] != recorded[i][1]).any())
-    torch.cuda.synchronize()
-    sess.kv.timer_enable(1 << kinds[DOM])
-    sess.kv.timer_read(kinds[DOM])
-    lat, accepted, n_full_steps, bytes_tot = [], 0, 0, 0
-    rows_gateup = []
-    tier_counts = np.zeros(3, np.int64)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(args.warmup, n_steps):
-        drafts = recorded[i][0]
-        n_before = np.array([len(sess.tokens[b]) for b in range(B)])
-        ts = time.perf_counter()
-        w, h, run = sess.begin(drafts)
-        sess.commit(w, drafts)
-        torch.cuda.synchronize()
-        lat.append(time.perf_counter() - ts)
-        accepted += int((h["new_len"] - n_before).sum())
-        mism += int((h["new_len"] != recorded[i][1]).any())
-        n_full_steps += int(run.any())
-    t_total = time.perf_counter() - t_start
-    n_launch, ms_dom = sess.kv.timer_read(kinds[DOM])
-    sess.kv.timer_enable(0)
-
-    value = accepted / t_total
-    lat_ms = np.array(lat) * 1e3
+    T = float(cfg["temperature"])
+    res = run_workload(cfg, W, args.steps, args.warmup, T, timer_kind=kinds[DOM])
+    lat_ms = res["lat_ms"]
+    n_launch, ms_dom = res["timer"]
     # algorithmic bytes of the dominant kernel per launch: gate/up weights of one layer
     F, d = md["d_ffn"], md["d_model"]
     esz = 2 if md["dtype"] == "bf16" else 4
     dom_bytes = 2 * F * d * esz
     avg_ms = ms_dom / max(1, n_launch)
     achieved = dom_bytes / (avg_ms * 1e-3) / 1e9 if n_launch else None
-    roof = {"kernel": "gemm_kernel: gate/up projection of one layer", "bound": "hbm",
+    roof = {"kernel": "gemm_gate_up: gate/up projection of one layer", "bound": "hbm",
             "achieved": round(achieved, 1) if achieved else None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
             "traffic": measured_traffic(args.config),
             "bytes_per_launch": dom_bytes, "avg_launch_us": round(avg_ms * 1e3, 2), "launches": n_launch}
+    step_roof = {"bytes": round(res["bytes"] / args.steps), "achieved_GBs": round(res["bytes"] / res["t_total"] / 1e9, 1),
+                 "frac": round(res["bytes"] / res["t_total"] / 1e9 / HBM_PEAK_GBS, 4)}
+
+    # the same workload at T = 1, where every drafted position goes to the full verifier
+    full_tier = None
+    if not args.no_full_tier and T != 1.0:
+        r1 = run_workload(cfg, W, max(5, args.steps // 3), 2, 1.0)
+        full_tier = {"temperature": 1.0, "value": round(r1["value"], 2), "unit": "tokens/s",
+                     "ms_per_step": round(float(r1["lat_ms"].mean()), 3), "steps": len(r1["lat_ms"]),
+                     "escalation_rate": round(r1["escalation"], 3), "replay_mismatch_steps": r1["mismatch"],
+                     "step_roofline_frac": round(r1["bytes"] / r1["t_total"] / 1e9 / HBM_PEAK_GBS, 4)}
 
     breakdown = None
     if args.breakdown:
-        sess.kv.close()
-        sess = fresh()
-        sess.kv.timer_enable((1 << 6) - 1)
-        for i in range(n_steps):
-            sess.step(recorded[i][0])
-        torch.cuda.synchronize()
         breakdown = {}
         for nme, kd in kinds.items():
-            n, ms = sess.kv.timer_read(kd)
+            rb = run_workload(cfg, W, min(args.steps, 10), 2, T, timer_kind=kd)
+            n, ms = rb["timer"]
             breakdown[nme] = {"launches": n, "total_ms": round(ms, 3), "avg_us": round(ms * 1e3 / max(1, n), 2)}
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, W, recorded, init_tokens)
+        cpu = cpu_baseline(cfg, W, res["recorded"], res["init_tokens"])
 
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "metric": METRIC, "value": round(res["value"], 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(float(lat_ms.mean()), 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": md["dtype"], "data": "synthetic",
-        "config": {"workload": args.config, "batch": B, "ctx": cfg["ctx"], "draft": cfg["draft"],
+        "config": {"workload": args.config, "batch": cfg["batch"], "ctx": cfg["ctx"], "draft": cfg["draft"],
                    "k": cfg.get("k"), "route_layers": len(cfg["route"]), "n_layers": md["n_layers"],
                    "d_model": md["d_model"], "vocab": md["vocab"],
                    "context_kv": "synthetic N(0, (0.02 sqrt d)^2)" if synthetic else "prefill"},
         "latency_ms": {"p10": round(float(np.percentile(lat_ms, 10)), 3),
                        "p50": round(float(np.percentile(lat_ms, 50)), 3),
                        "p90": round(float(np.percentile(lat_ms, 90)), 3)},
-        "escalation_rate": round(n_full_steps / max(1, args.steps), 3),
-        "replay_mismatch_steps": mism,
-        "drafting_s_untimed": round(t_draft, 3),
+        "temperature": T,
+        "escalation_rate": round(res["escalation"], 3),
+        "replay_mismatch_steps": res["mismatch"],
+        "drafting_s_untimed": round(res["t_draft"], 3),
         "roofline": roof,
+        "step_roofline": step_roof,
+        "full_tier_variant": full_tier,
         "cpu_baseline": cpu,
     }
     if breakdown:

@@ -44,8 +44,9 @@ class Session:
         self.m, self.kv, self.p = model, kv, params
         self.tokens = {}
         self.want_logits = logits
-        B, R, D, V = kv.max_batch, kv.max_rows, kv.max_drafts, model.desc["vocab"]
-        # window rows per sequence are bounded by max_rows / batch at call time
+        # outputs are indexed by window row (lag rows produce none); a window has
+        # at most 64 rows per sequence (chain: one per draft; tree: VIA_MAX_TREE_ROWS)
+        B, R, D, V = kv.max_batch, min(kv.max_rows, 64), kv.max_drafts, model.desc["vocab"]
         self.out_slim = via.Out(B, R, D, V, logits)
         self.out_full = via.Out(B, R, D, V, logits)
         self.dec = via.Dec(B, D)

@@ -48,17 +48,21 @@ def models():
         gm.close()
 
 
-# (workload, verify steps, sampled sequences)
+# (workload, verify steps, sampled sequences, temperature).  At the workloads'
+# calibrated temperatures drafts split between the accept and slim tiers;
+# T = 1 sends every position to the full verifier.
 CASES = [
-    ("1b_bf16", 3, [0]),
-    ("8b_bf16_chain", 2, [3]),
-    ("8b_bf16_tree", 2, [0]),
-    ("8b_bf16_long", 1, None),  # the sequence with the longest context
+    ("1b_bf16", 3, [0], None),
+    ("8b_bf16_chain", 2, [3], None),
+    ("8b_bf16_chain", 2, [1], 1.0),
+    ("8b_bf16_tree", 2, [0], None),
+    ("8b_bf16_tree", 2, [0], 1.0),
+    ("8b_bf16_long", 1, None, None),  # None: the sequence with the longest context
 ]
 
 
-@pytest.mark.parametrize("name,steps,sample", CASES)
-def test_full_size_sampled_parity(name, steps, sample, models):
+@pytest.mark.parametrize("name,steps,sample,temperature", CASES)
+def test_full_size_sampled_parity(name, steps, sample, temperature, models):
     cfg = configs.get(name)
     md = cfg["model"]
     V = md["vocab"]
@@ -70,12 +74,12 @@ def test_full_size_sampled_parity(name, steps, sample, models):
         sample = [max(range(B), key=lambda b: ctx[b])]
     tree = cfg["draft"] == "tree"
     k = cfg.get("k", 8)
-    # the benchmark's row and block budgets
-    rows_per_seq = 64 if tree else k * 8
-    grow = (steps + 2) * ((len(cfg["tree_budget"]) + 1) if tree else (k + 1))
+    # the benchmark's row and block budgets (its default 35 replayed steps)
+    grow = 35 * ((len(cfg["tree_budget"]) + 1) if tree else (k + 1))
+    rows_per_seq = (64 if tree else k) + grow
     max_blocks = (max(ctx) + grow + rows_per_seq + 16) // 16 + 1
-    T = float(cfg["temperature"])
-    print(f"[case] {name} B={B} ctx={min(ctx)}..{max(ctx)} sample={sample} steps={steps}", flush=True)
+    T = float(cfg["temperature"] if temperature is None else temperature)
+    print(f"[case] {name} T={T:.4g} B={B} ctx={min(ctx)}..{max(ctx)} sample={sample} steps={steps}", flush=True)
     W, om, gm = models(cfg)
     ls = Lockstep(cfg, weights=W, oracle_model=om, gpu_model=gm, sample=sample, max_rows=B * rows_per_seq,
                   max_batch=B, max_drafts=64, max_blocks=max_blocks, blocks=B * max_blocks,

@@ -42,20 +42,22 @@ CONFIGS = {
         # accept threshold (tests/golden/calibrate_temperature.py).
         temperature=None, gen=64, block_size=16,
         seed_w=1002, seed_c=2002, seed_d=3002, seed_kv=None),
-    # 8B-shape bf16 verifier, batch 4, context 2048 in a paged cache.
+    # 8B-shape bf16 verifier, batch 4, context 2048 in a paged cache.  The
+    # 8B-shape workloads take the same temperature rule as the 1B shape (at
+    # T = 1 no drafted position clears the accept threshold).
     "8b_bf16_chain": dict(
         model=dict(_MODEL_8B), route=list(_ROUTE_8B), batch=4, ctx=(2048, 2048), draft="chain",
-        k=8, corrupt=0.30, temperature=1.0, gen=64, block_size=16,
+        k=8, corrupt=0.30, temperature=None, gen=64, block_size=16,
         seed_w=1003, seed_c=2003, seed_d=3003, seed_kv=4003),
     # 8B-shape with a 60-node token tree (depth 6, branching <= 4).
     "8b_bf16_tree": dict(
         model=dict(_MODEL_8B), route=list(_ROUTE_8B), batch=1, ctx=(4096, 4096), draft="tree",
-        tree_budget=[4, 12, 16, 14, 9, 5], tree_branch=4, corrupt=0.20, temperature=1.0, gen=64,
+        tree_budget=[4, 12, 16, 14, 9, 5], tree_branch=4, corrupt=0.20, temperature=None, gen=64,
         block_size=16, seed_w=1003, seed_c=2004, seed_d=3004, seed_kv=4004),
     # 8B-shape long-context batched serving: 16 sequences, ragged contexts.
     "8b_bf16_long": dict(
         model=dict(_MODEL_8B), route=list(_ROUTE_8B), batch=16, ctx=(4096, 8192), draft="chain",
-        k=6, corrupt=0.35, temperature=1.0, gen=64, block_size=16,
+        k=6, corrupt=0.35, temperature=None, gen=64, block_size=16,
         seed_w=1003, seed_c=2005, seed_d=3005, seed_kv=4005),
 }
 
