@@ -132,8 +132,11 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
             drafts = {b: (d[b], None) for b in range(B)}
         torch.cuda.synchronize()
         t_draft += time.time() - ts
+        # cached tokens each forward of this step reads (for the step's algorithmic bytes)
+        kv_slim = sum(sess.kv.seq_info(b, via.CACHE_SLIM)[0] for b in range(B))
+        kv_full = sum(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)) for b in range(B))
         h, run = sess.step(drafts)
-        recorded.append((drafts, h["new_len"].copy(), run.copy()))
+        recorded.append((drafts, h["new_len"].copy(), run.copy(), kv_slim, kv_full))
     log(f"T={temperature:.4g}: reference decode of {n_steps} steps, drafting {t_draft:.2f}s")
 
     # ---- reset: fresh handle on the same pools (context slots untouched)
@@ -151,36 +154,42 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
         torch.cuda.synchronize()
         return s2
 
-    sess = fresh()
-    mism = 0
-    for i in range(warmup):
-        h, run = sess.step(recorded[i][0])
-        mism += int((h["new_len"] != recorded[i][1]).any())
-    torch.cuda.synchronize()
-    if timer_kind is not None:
-        sess.kv.timer_enable(1 << timer_kind)
-        sess.kv.timer_read(timer_kind)
-    lat, accepted, n_full_steps, bytes_tot = [], 0, 0, 0.0
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(warmup, n_steps):
-        drafts = recorded[i][0]
-        n_before = np.array([len(sess.tokens[b]) for b in range(B)])
-        kv_slim = sum(sess.kv.seq_info(b, via.CACHE_SLIM)[0] for b in range(B))
-        kv_full = sum(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)) for b in range(B))
-        ts = time.perf_counter()
-        w, h, run = sess.begin(drafts)
-        sess.commit(w, drafts)
+    def replay(timed_kind):
+        """Warm-up steps, then the timed steps; with `timed_kind` the kernels of
+        that kind carry timing events (a separate pass, so the timed pass runs
+        without them)."""
+        s2 = fresh()
+        mism = 0
+        for i in range(warmup):
+            h, run = s2.step(recorded[i][0])
+            mism += int((h["new_len"] != recorded[i][1]).any())
         torch.cuda.synchronize()
-        lat.append(time.perf_counter() - ts)
-        accepted += int((h["new_len"] - n_before).sum())
-        mism += int((h["new_len"] != recorded[i][1]).any())
-        n_full_steps += int(run.any())
-        bytes_tot += step_bytes(cfg, kv_slim, kv_full, bool(run.any()))
-    t_total = time.perf_counter() - t_start
-    timer = sess.kv.timer_read(timer_kind) if timer_kind is not None else (0, 0.0)
-    sess.kv.timer_enable(0)
-    sess.kv.close()
+        if timed_kind is not None:
+            s2.kv.timer_enable(1 << timed_kind)
+            s2.kv.timer_read(timed_kind)
+        lat, accepted, n_full_steps = [], 0, 0
+        n_prev = [np.array([len(s2.tokens[b]) for b in range(B)])]
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        for i in range(warmup, n_steps):
+            drafts = recorded[i][0]
+            ts = time.perf_counter()
+            w, h, run = s2.begin(drafts)
+            s2.commit(w, drafts)
+            torch.cuda.synchronize()
+            lat.append(time.perf_counter() - ts)
+            mism += int((h["new_len"] != recorded[i][1]).any())
+            n_full_steps += int(run.any())
+        t_total = time.perf_counter() - t_start
+        accepted = int((np.array([len(s2.tokens[b]) for b in range(B)]) - n_prev[0]).sum())
+        timer = s2.kv.timer_read(timed_kind) if timed_kind is not None else (0, 0.0)
+        s2.kv.timer_enable(0)
+        s2.kv.close()
+        return lat, accepted, n_full_steps, t_total, mism, timer
+
+    lat, accepted, n_full_steps, t_total, mism, _ = replay(None)
+    timer = replay(timer_kind)[5] if timer_kind is not None else (0, 0.0)
+    bytes_tot = sum(step_bytes(cfg, r[3], r[4], bool(r[2].any())) for r in recorded[warmup:])
     lat_ms = np.array(lat) * 1e3
     return dict(value=accepted / t_total, t_total=t_total, lat_ms=lat_ms, escalation=n_full_steps / max(1, steps),
                 mismatch=mism, t_draft=t_draft, bytes=bytes_tot, timer=timer, recorded=recorded,

@@ -315,7 +315,7 @@ void trim_blocks(via_kv* kv, int cache, int seq, int valid) {
 }
 
 template <typename T>
-void put(std::vector<char>& blob, size_t& off, const std::vector<T>& v) {
+void put(std::vector<char>& blob, size_t off, const std::vector<T>& v) {
   if (!v.empty()) memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
 }
 
@@ -328,23 +328,30 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   if (M == 0) return VIA_OK;
   if (M > kv->d.max_rows) return fail(VIA_EINVAL, "forward of %d rows exceeds max_rows %d", M, kv->d.max_rows);
   if ((int)P.items.size() > L.max_items) return fail(VIA_EINVAL, "too many attention tiles");
-  // one upload of the whole plan region
-  std::vector<char> blob(L.plan_bytes);
-  size_t o0 = 0;
-  memcpy(blob.data() + (L.rows - L.rows), P.rows.data(), P.rows.size() * sizeof(RowInfo));
-  memcpy(blob.data() + (L.seqs - L.rows), P.seqs.data(), P.seqs.size() * sizeof(SeqInfo));
-  if (!P.btab.empty()) memcpy(blob.data() + (L.btab - L.rows), P.btab.data(), P.btab.size() * 4);
-  if (!P.items.empty()) memcpy(blob.data() + (L.items - L.rows), P.items.data(), P.items.size() * sizeof(AttnItem));
-  if (!P.lm.empty()) memcpy(blob.data() + (L.lm - L.rows), P.lm.data(), P.lm.size() * sizeof(LmRow));
-  (void)o0;
+  // one upload of the plan: its parts packed back to back (256-byte aligned)
+  // at the start of the plan region, which has room for the largest plan
+  const size_t o_rows = 0;
+  const size_t o_seqs = al(o_rows + P.rows.size() * sizeof(RowInfo));
+  const size_t o_btab = al(o_seqs + P.seqs.size() * sizeof(SeqInfo));
+  const size_t o_items = al(o_btab + P.btab.size() * 4);
+  const size_t o_lm = al(o_items + P.items.size() * sizeof(AttnItem));
+  const size_t plan_used = al(o_lm + P.lm.size() * sizeof(LmRow));
+  if (plan_used > L.plan_bytes) return fail(VIA_EINVAL, "plan of %zu bytes exceeds its region", plan_used);
+  std::vector<char> blob(plan_used);
+  put(blob, o_rows, P.rows);
+  put(blob, o_seqs, P.seqs);
+  put(blob, o_btab, P.btab);
+  put(blob, o_items, P.items);
+  put(blob, o_lm, P.lm);
   char* ws = kv->ws;
-  via_status st = upload(kv, ws + L.rows, blob.data(), L.plan_bytes, s);
+  char* plan = ws + L.rows;
+  via_status st = upload(kv, plan, blob.data(), plan_used, s);
   if (st) return st;
 
   const bool bf = m->bf16;
-  const RowInfo* d_rows = (const RowInfo*)(ws + L.rows);
-  const SeqInfo* d_seqs = (const SeqInfo*)(ws + L.seqs);
-  const int32_t* d_btab = (const int32_t*)(ws + L.btab);
+  const RowInfo* d_rows = (const RowInfo*)(plan + o_rows);
+  const SeqInfo* d_seqs = (const SeqInfo*)(plan + o_seqs);
+  const int32_t* d_btab = (const int32_t*)(plan + o_btab);
   float* X = (float*)(ws + L.X);
   void* Yf = ws + L.Yf;
   void* Q = ws + L.Q;  // bf16 models: hi terms then lo terms; fp32 models: fp32 Q
@@ -385,7 +392,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   at.rows = d_rows;
   at.seqs = d_seqs;
   at.btab = d_btab;
-  at.items = (const AttnItem*)(ws + L.items);
+  at.items = (const AttnItem*)(plan + o_items);
   at.n_items = (int)P.items.size();
   at.max_chunks = 0;
   for (const AttnItem& it : P.items) at.max_chunks = std::max(at.max_chunks, it.n_chunks);
@@ -431,7 +438,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
-    const LmRow* d_lm = (const LmRow*)(ws + L.lm);
+    const LmRow* d_lm = (const LmRow*)(plan + o_lm);
     void* Ylf = ws + L.Ylf;
     const int MBl = gemm_padded_rows(nlm) / 16;
     // last residual update, final norm of the head rows only
