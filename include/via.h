@@ -89,10 +89,12 @@ typedef struct {
  *   w_gate_up [2 F, d]            rows: gate (F), then up (F)
  *   w_down    [d, F]
  * embed and the norm gains are plain row-major.  The five projection
- * matrices (lm_head, w_qkv, w_o, w_gate_up, w_down) are in the PACKED layout
- * written by via_pack_weight, which stores each 64-row x 32-column tile as
- * the matrix cores consume it, so that the verify GEMMs stream weights as
- * contiguous memory.
+ * matrices are in the PACKED layout, which stores each 64-row x 32-column
+ * tile as the matrix cores consume it, so that the verify GEMMs stream
+ * weights as contiguous memory: lm_head, w_qkv, w_o and w_down as written
+ * by via_pack_weight, w_gate_up as written by via_pack_gate_up (gate and up
+ * rows interleaved by 8, so that one 16-row block yields both factors of
+ * eight SwiGLU outputs).
  * The slim-verifier reads the same pointers for its retained layers: no
  * weight is copied (Sec. 3.3). */
 typedef struct {
@@ -205,6 +207,16 @@ size_t via_packed_bytes(int32_t rows, int32_t cols, int32_t dtype);
  *   ((((r/64) * (cols/32) + c/32) * 4 + (r%64)/16) * 64 + ((c%32)/8) * 16 + r%16)
  * at offset c%8.  src and dst must not overlap. */
 via_status via_pack_weight(const void *src, void *dst, int32_t rows, int32_t cols, int32_t dtype, void *stream);
+/* Pack the FFN input projection: `src` is the row-major [2 d_ffn, d_model]
+ * device matrix (gate rows, then up rows) and `dst` (device,
+ * via_packed_bytes(2 d_ffn, d_model, dtype)) receives the via_pack_weight
+ * layout of the row-interleaved matrix whose row 16 b + i is gate row
+ * 8 b + i for i < 8 and up row 8 b + i - 8 for i >= 8.  The FFN is
+ * h = silu(x W_gate^T) * (x W_up^T) (SwiGLU; the paper does not fix the
+ * verifier's layer, this is the architecture reading of this library).
+ * d_ffn must be a multiple of 8.  src and dst must not overlap. */
+via_status via_pack_gate_up(const void *src, void *dst, int32_t d_ffn, int32_t d_model, int32_t dtype,
+                            void *stream);
 
 /* ---- sizes -------------------------------------------------------------- */
 size_t via_pool_bytes(const via_model_desc *desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size);

@@ -13,6 +13,7 @@ constexpr int kBlock = 16;        // tokens per KV page
 constexpr int kMaxChildren = 8;   // drafts verified by one row
 constexpr int kAttnChunk = 256;   // keys per attention work-group (split-KV chunk)
 constexpr int kAttnQueries = 64;  // (row, head-in-group) queries per attention work-group
+constexpr int kNormChunk = 512;   // columns per partial sum of squares (RMSNorm)
 
 // One fed row of a forward (lag row or window row).
 struct RowInfo {
@@ -150,6 +151,16 @@ __device__ __forceinline__ void put_afrag(void* base, int m, int k0, const float
     store_afrag<NT>((uint16_t*)base, m, k0, v, S, MBn);
   else
     store_afrag_f32((float*)base, m, k0, v, S, MBn);
+}
+
+// RMSNorm scale of row m, 1/sqrt(mean(x^2) + eps), from the per-chunk sums
+// of squares ss[c * stride + m], c < ceil(d / kNormChunk), added in chunk
+// order.
+__device__ __forceinline__ float row_scale(const float* ss, int stride, int m, int d, float eps) {
+  float t = 0.f;
+  const int nch = (d + kNormChunk - 1) / kNormChunk;
+  for (int c = 0; c < nch; ++c) t += ss[(size_t)c * stride + m];
+  return 1.0f / sqrtf(t / (float)d + eps);
 }
 
 __device__ __forceinline__ float wave_max(float v) {

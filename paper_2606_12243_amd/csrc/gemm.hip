@@ -54,9 +54,11 @@ struct TileShape {
   static constexpr int kXPT = kXChunk / kThreads;     // uint4 staged per thread
 };
 
+// `active` (wave-uniform) false: the wave helps stage X but loads no
+// weights and multiplies nothing (its accumulators stay zero).
 template <int MB, int NT, int NBW, int C>
 __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_end, uint4* sx,
-                          f32x4 (&acc)[NBW][MB]) {
+                          f32x4 (&acc)[NBW][MB], bool active = true) {
   using TS = TileShape<MB, NT, NBW, C>;
   static_assert(TS::kXChunk % kThreads == 0, "chunk must split evenly over the threads");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -80,7 +82,7 @@ __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_
   const int nch = (nst + C - 1) / C;
 
 #define TILE_LOAD_W(w, ch)                                                  \
-  {                                                                         \
+  if (active) {                                                             \
     _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                      \
       const size_t st = (size_t)min(st_beg + (ch) * C + sc, st_end - 1);    \
       _Pragma("unroll") for (int j = 0; j < NBW; ++j) w[sc][j] = wt[j][st * 256]; \
@@ -101,7 +103,7 @@ __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_
     _Pragma("unroll") for (int u = 0; u < TS::kXPT; ++u) d[u * kThreads] = xs[u]; \
   }
 #define TILE_COMPUTE(w, ch)                                                 \
-  {                                                                         \
+  if (active) {                                                             \
     const uint4* xb = sx + ((ch) & 1) * TS::kXChunk + lane;                 \
     const int valid = nst - (ch) * C;                                       \
     _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                      \
@@ -194,11 +196,13 @@ __device__ void epi_stats(const GemmArgs& a, int tile, int m0, const float* lds)
   for (int r = grp; r < 16 * MB; r += kThreads / 16) {
     const int m = m0 + r;
     if (m >= a.M) continue;  // uniform within the group
+    // the row's final RMSNorm scale (the head is linear in it)
+    const float rs = row_scale(a.ss, a.ss_stride, m, a.K, a.eps);
     float mx = -INFINITY, sc = -INFINITY;
     int am = 0x7fffffff;
     constexpr int CPT = kTileN / 16;
     for (int c = gl * CPT; c < gl * CPT + CPT; ++c)
-      if (c0 + c < a.N) merge3(mx, am, sc, lds[r * kTileN + c], c0 + c, -INFINITY);
+      if (c0 + c < a.N) merge3(mx, am, sc, lds[r * kTileN + c] * rs, c0 + c, -INFINITY);
     for (int o = 1; o < 16; o <<= 1) {
       const float mx2 = __shfl_xor(mx, o, 64), sc2 = __shfl_xor(sc, o, 64);
       const int am2 = __shfl_xor(am, o, 64);
@@ -206,7 +210,7 @@ __device__ void epi_stats(const GemmArgs& a, int tile, int m0, const float* lds)
     }
     float se = 0.f;
     for (int c = gl * CPT; c < gl * CPT + CPT; ++c)
-      if (c0 + c < a.N) se += expf((lds[r * kTileN + c] - mx) * a.inv_T);
+      if (c0 + c < a.N) se += expf((lds[r * kTileN + c] * rs - mx) * a.inv_T);
     for (int o = 1; o < 16; o <<= 1) se += __shfl_xor(se, o, 64);
     const int out = a.lm[m].out;
     if (gl == 0) {
@@ -218,11 +222,11 @@ __device__ void epi_stats(const GemmArgs& a, int tile, int m0, const float* lds)
     }
     if (gl < min(a.lm[m].n_drafts, kMaxChildren)) {
       const int tk = a.lm[m].draft_tok[gl];
-      if (tk >= c0 && tk < c0 + kTileN) a.draft_logit[a.lm[m].draft_idx[gl]] = lds[r * kTileN + tk - c0];
+      if (tk >= c0 && tk < c0 + kTileN) a.draft_logit[a.lm[m].draft_idx[gl]] = lds[r * kTileN + tk - c0] * rs;
     }
     if (a.logits) {
       for (int c = gl * CPT; c < gl * CPT + CPT; ++c)
-        if (c0 + c < a.N) a.logits[(size_t)out * a.N + c0 + c] = lds[r * kTileN + c];
+        if (c0 + c < a.N) a.logits[(size_t)out * a.N + c0 + c] = lds[r * kTileN + c] * rs;
     }
   }
 }
@@ -288,6 +292,175 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
   }
 }
 
+// Gate/up projection with SwiGLU, h = silu(x W_g) * (x W_u) (the verifier's FFN).
+// The packed weight interleaves gate and up rows by 8 (launch_pack with ffn),
+// so 16-column block b holds gate and up columns of f = 8b .. 8b+7.  A
+// work-group owns a.nb consecutive blocks (one wave each; waves past nb only
+// stage X) over all of K, so no partial sums leave it: the tile goes to LDS
+// and the epilogue writes h for its (row, 8-f group)s as 2-term fragments,
+// the down projection's input.
+template <typename T, int MB, int C>
+__global__ __launch_bounds__(kThreads) void gemm_gate_up(GemmArgs a) {
+  constexpr int NT = sizeof(T) == 2 ? 2 : 1;
+  constexpr int kCols = kWaves * 16;                        // widest tile (nb = 8)
+  constexpr int kLdsX = sizeof(T) == 2 ? 2 * TileShape<MB, NT, 1, C>::kXChunk * 16 : 0;
+  constexpr int kLdsT = 16 * MB * kCols * 4;
+  constexpr int kLds = kLdsX > kLdsT ? kLdsX : kLdsT;
+  __shared__ __align__(16) unsigned char smem[kLds];
+  float* lds = (float*)smem;
+  const int nblocks = a.N >> 4;             // 16-column blocks (= F / 8 groups of h)
+  const int blk0 = blockIdx.x * a.nb;
+  const int m0 = blockIdx.y * 16 * MB;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int ncol = min(a.nb, nblocks - blk0) * 16;  // columns of this work-group
+  if constexpr (sizeof(T) == 2) {
+    f32x4 acc[1][MB];
+    const bool active = wave < a.nb && blk0 + wave < nblocks;
+    tile_bf16<MB, NT, 1, C>(a, blk0 * 16, m0, 0, a.K >> 5, (uint4*)smem, acc, active);
+    __syncthreads();  // the X buffers become the output tile
+    if (active) {
+      const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) lds[(mb * 16 + g * 4 + r) * kCols + wave * 16 + n] = acc[0][mb][r];
+    }
+  } else {
+    const float* W = (const float*)a.W;
+    const float* X = (const float*)a.X;
+    const int steps = a.K >> 5;
+    for (int e = threadIdx.x; e < 16 * MB * ncol; e += kThreads) {
+      const int r = e / ncol, c = e - r * ncol, m = m0 + r, col = blk0 * 16 + c;
+      float s = 0.f;
+      if (m < a.M) {
+        const size_t base = (size_t)(col >> 6) * steps * 256 + ((col & 63) >> 4) * 64 + (col & 15);
+        for (int k = 0; k < a.K; ++k) {
+          const float xv = X[afrag_group(0, m, k & ~7, steps, a.MBn) * 8 + (k & 7)];
+          s = fmaf(xv, W[(base + (size_t)(k >> 5) * 256 + ((k & 31) >> 3) * 16) * 8 + (k & 7)], s);
+        }
+      }
+      lds[r * kCols + c] = s;
+    }
+  }
+  __syncthreads();
+  const int ngroups = ncol >> 4;
+  for (int e = threadIdx.x; e < 16 * MB * ngroups; e += kThreads) {
+    const int r = e / ngroups, j = e - r * ngroups, m = m0 + r;
+    if (m >= a.M) continue;
+    const float* t = lds + r * kCols + j * 16;
+    const float sc = row_scale(a.ss, a.ss_stride, m, a.K, a.eps);  // RMSNorm of the input row
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float gt = t[i] * sc, up = t[8 + i] * sc;
+      v[i] = gt / (1.0f + expf(-gt)) * up;
+    }
+    put_afrag<sizeof(T) == 2, NT>(a.H, m, (blk0 + j) * 8, v, a.F >> 5, a.MBn);
+  }
+}
+
+// Gate/up with SwiGLU for up to 32 rows, K-interleaved: wave w multiplies
+// K steps w, w + 8, w + 16, ... of all a.nb (<= 8) column blocks of the
+// work-group, loading its X fragments straight from global memory (each is
+// used by one wave only, so neither LDS staging nor a barrier sits in the
+// main loop), one step of loads ahead of its MFMAs.  Weights are read with
+// non-temporal loads: streamed once, they should not displace X from the
+// caches.  The eight waves' partial tiles are summed in LDS in wave order
+// (fixed, so the result is reproducible) and the epilogue writes h as in
+// gemm_gate_up.
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+template <int MB>
+__global__ __launch_bounds__(kThreads) void gemm_gate_up_ki(GemmArgs a) {
+  constexpr int NT = 2, NBM = kWaves;
+  __shared__ __align__(16) float red[kWaves][16 * MB][NBM * 16 + 4];
+  const int nblocks = a.N >> 4;
+  const int blk0 = blockIdx.x * a.nb;
+  const int m0 = blockIdx.y * 16 * MB;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nb = min(a.nb, nblocks - blk0);
+  const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
+  const uint4* wt[NBM];
+#pragma unroll
+  for (int j = 0; j < NBM; ++j) {
+    const int blk = blk0 + min(j, nb - 1);
+    wt[j] = (const uint4*)a.W + (size_t)min(blk >> 2, t64 - 1) * S * 256 + (blk & 3) * 64 + lane;
+  }
+  const uint4* xg = (const uint4*)a.X + (size_t)(m0 >> 4) * 64 + lane;
+  const size_t x_step = (size_t)a.MBn * 64, x_term = (size_t)S * x_step;
+  f32x4 acc[NBM][MB];
+#pragma unroll
+  for (int j = 0; j < NBM; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nst = max(0, (S - wave + kWaves - 1) / kWaves);  // steps of this wave
+  uint4 w[2][NBM], x[2][NT][MB];
+  // loads of the wave's i-th step into buffer `buf` (past the last step the
+  // last one is loaded again and never used)
+  auto load = [&](int buf, int i) {
+    const size_t st = (size_t)(wave + min(i, nst - 1) * kWaves);
+#pragma unroll
+    for (int j = 0; j < NBM; ++j)
+      if (j < nb) w[buf][j] = load_stream(wt[j] + st * 256);
+#pragma unroll
+    for (int q = 0; q < NT; ++q)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) x[buf][q][mb] = xg[q * x_term + st * x_step + mb * 64];
+  };
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < NT; ++q)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < NBM; ++j)
+          if (j < nb)
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x[buf][q][mb]), as_bf16x8(w[buf][j]),
+                                                                 acc[j][mb], 0, 0, 0);
+  };
+  if (nst > 0) {
+    load(0, 0);
+    for (int i = 0; i < nst; i += 2) {
+      load(1, i + 1);
+      compute(0);
+      if (i + 1 >= nst) break;
+      load(0, i + 2);
+      compute(1);
+    }
+  }
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < NBM; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][mb * 16 + g * 4 + r][j * 16 + n] = acc[j][mb][r];
+  __syncthreads();
+  for (int e = threadIdx.x; e < 16 * MB * nb; e += kThreads) {
+    const int r = e / nb, j = e - r * nb, m = m0 + r;
+    if (m >= a.M) continue;
+    const float sc = row_scale(a.ss, a.ss_stride, m, a.K, a.eps);  // RMSNorm of the input row
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float gt = 0.f, up = 0.f;
+#pragma unroll
+      for (int wv = 0; wv < kWaves; ++wv) {
+        gt += red[wv][r][j * 16 + i];
+        up += red[wv][r][j * 16 + 8 + i];
+      }
+      gt *= sc;
+      up *= sc;
+      v[i] = gt / (1.0f + expf(-gt)) * up;
+    }
+    put_afrag<true, NT>(a.H, m, (blk0 + j) * 8, v, a.F >> 5, a.MBn);
+  }
+}
+
 // One entry point per projection, so kernel traces name the projection.
 #define VIA_GEMM_ENTRY(NAME, NT_BF16, STATS)                                              \
   template <typename T, int MB, int C>                                                   \
@@ -296,18 +469,18 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
   }
 VIA_GEMM_ENTRY(gemm_qkv, 3, false)
 VIA_GEMM_ENTRY(gemm_o, 2, false)
-VIA_GEMM_ENTRY(gemm_gate_up, 2, false)
 VIA_GEMM_ENTRY(gemm_down, 2, false)
 VIA_GEMM_ENTRY(gemm_head, 2, true)
 #undef VIA_GEMM_ENTRY
 
 // X chunk steps: the double-buffered chunk stays within 144 KB of LDS and
-// splits evenly over the threads.
-template <typename T, int MB, int NT>
+// splits evenly over the threads (C * NT * MB a multiple of 8).
+template <typename T, int MB, int NT, int NBW = kNBW>
 constexpr int chunk_steps() {
-  return sizeof(T) != 2 ? 8 : ((kNBW == 1 && NT * MB <= 9) || (NT * MB) % 2 ? 8 : 4);
+  if (sizeof(T) != 2) return 8;
+  if (MB > 4) return NT * MB == 24 ? 2 : 4;  // 96 or 128 rows: 72-128 KB of buffers
+  return (NBW == 1 && NT * MB <= 9) || (NT * MB) % 2 ? 8 : 4;
 }
-
 // With timing events the launch carries them in its dispatch, so they
 // bracket the kernel itself rather than the stream around it.
 #define VIA_GEMM_LAUNCH(NAME, NT_BF16)                                                       \
@@ -327,12 +500,45 @@ constexpr int chunk_steps() {
       case 1: go(NAME<T, 1, chunk_steps<T, 1, NT>()>); break;                                \
       case 2: go(NAME<T, 2, chunk_steps<T, 2, NT>()>); break;                                \
       case 3: go(NAME<T, 3, chunk_steps<T, 3, NT>()>); break;                                \
-      default: go(NAME<T, 4, chunk_steps<T, 4, NT>()>); break;                               \
+      case 4: go(NAME<T, 4, chunk_steps<T, 4, NT>()>); break;                                \
+      case 6: go(NAME<T, 6, chunk_steps<T, 6, NT>()>); break;                                \
+      default: go(NAME<T, 8, chunk_steps<T, 8, NT>()>); break;                               \
     }                                                                                        \
   }
 VIA_GEMM_LAUNCH(gemm_qkv, 3)
 VIA_GEMM_LAUNCH(gemm_o, 2)
-VIA_GEMM_LAUNCH(gemm_gate_up, 2)
+
+// Gate/up with SwiGLU: grid (work-groups of a.nb blocks, row groups).
+template <typename T>
+void launch_gemm_gate_up(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  constexpr int NT = sizeof(T) == 2 ? 2 : 1;
+  const int mb = gemm_rows_per_group(a.M) / 16;
+  const int mgroups = (a.M + 16 * mb - 1) / (16 * mb);
+  const dim3 grid(((a.N >> 4) + a.nb - 1) / a.nb, mgroups);
+  auto go = [&](auto kernel) {
+    if (e0)
+      hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, a);
+    else
+      hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a);
+  };
+  if constexpr (sizeof(T) == 2) {
+    if (mb <= 2) {  // up to 32 rows: K-interleaved waves
+      if (mb == 1)
+        go(gemm_gate_up_ki<1>);
+      else
+        go(gemm_gate_up_ki<2>);
+      return;
+    }
+  }
+  switch (mb) {
+    case 1: go(gemm_gate_up<T, 1, chunk_steps<T, 1, NT, 1>()>); break;
+    case 2: go(gemm_gate_up<T, 2, chunk_steps<T, 2, NT, 1>()>); break;
+    case 3: go(gemm_gate_up<T, 3, chunk_steps<T, 3, NT, 1>()>); break;
+    case 4: go(gemm_gate_up<T, 4, chunk_steps<T, 4, NT, 1>()>); break;
+    case 6: go(gemm_gate_up<T, 6, chunk_steps<T, 6, NT, 1>()>); break;
+    default: go(gemm_gate_up<T, 8, chunk_steps<T, 8, NT, 1>()>); break;
+  }
+}
 VIA_GEMM_LAUNCH(gemm_down, 2)
 VIA_GEMM_LAUNCH(gemm_head, 2)
 #undef VIA_GEMM_LAUNCH
@@ -399,7 +605,7 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(const LmRow* lm, const
 
 // Row-major [rows, cols] -> packed tiles; one thread per 8-element group.
 template <typename T>
-__global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int rows, int cols, size_t groups) {
+__global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int rows, int cols, int ffn, size_t groups) {
   const size_t gidx = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (gidx >= groups) return;
   const int steps = cols >> 5;
@@ -411,25 +617,35 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int row
   const size_t tile = q / steps;
   const size_t r = tile * 64 + nb * 16 + (lane & 15);
   const size_t c = (size_t)st * 32 + (lane >> 4) * 8;
+  // gate/up interleave: packed row 16 b + i <- gate row 8 b + i, or up row 8 b + i - 8
+  const size_t sr = ffn > 0 ? ((r & 8) ? (size_t)ffn : 0) + (r >> 4) * 8 + (r & 7) : r;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) dst[gidx * 8 + e] = r < (size_t)rows ? src[r * cols + c + e] : T(0);
+  for (int e = 0; e < 8; ++e) dst[gidx * 8 + e] = r < (size_t)rows ? src[sr * cols + c + e] : T(0);
 }
 
 }  // namespace
 
-void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, hipStream_t s) {
+void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, int ffn, hipStream_t s) {
   const size_t groups = (size_t)((rows + 63) / 64) * 64 * (cols / 8);
   const dim3 grid((unsigned)((groups + 255) / 256));
   if (bf16)
     hipLaunchKernelGGL(pack_kernel<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)src, (uint16_t*)dst, rows, cols,
-                       groups);
+                       ffn, groups);
   else
-    hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(256), 0, s, (const float*)src, (float*)dst, rows, cols, groups);
+    hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(256), 0, s, (const float*)src, (float*)dst, rows, cols, ffn,
+                       groups);
+}
+
+int gate_up_blocks_per_group(int F) {
+  const int nblocks = F / 8;  // 2 F columns in blocks of 16
+  return std::max(1, std::min(kWaves, (nblocks + 255) / 256));
 }
 
 int gemm_tiles(int N) { return (N + kTileN - 1) / kTileN; }
 
-int gemm_rows_per_group(int M) { return M > 48 ? 64 : M > 32 ? 48 : M > 16 ? 32 : 16; }
+int gemm_rows_per_group(int M) {
+  return M > 96 ? 128 : M > 64 ? 96 : M > 48 ? 64 : M > 32 ? 48 : M > 16 ? 32 : 16;
+}
 
 int gemm_padded_rows(int M) {
   const int g = gemm_rows_per_group(M);

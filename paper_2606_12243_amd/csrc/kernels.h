@@ -21,11 +21,23 @@ struct GemmArgs {
   float inv_T;
   float* logits;       // nullable [*, V] fp32, row = LmRow::out
   float* draft_logit;
+  // gate/up projection (kGateUp): W packed with gate and up rows interleaved
+  // by 8 (N = 2 F); the SwiGLU product is written as 2-term fragments of
+  // [M, F] to H.  Each work-group owns `nb` 16-column blocks over all of K.
+  void* H;
+  int F;
+  int nb;
+  // RMSNorm of the input rows (gate/up and head): output row m is multiplied
+  // by row_scale(ss, ss_stride, m, K, eps)
+  const float* ss;
+  int ss_stride;
+  float eps;
 };
 
 // Projection a GEMM computes.  Each has its own kernel entry point; the QKV
 // input carries 3 bf16 terms per fp32 activation, the others 2; the head
-// reduces its tiles to row statistics instead of writing partials.
+// reduces its tiles to row statistics instead of writing partials; the
+// gate/up projection runs over all of K and applies SwiGLU itself.
 enum class GemmRole { kQkv, kO, kGateUp, kDown, kHead };
 // e0/e1 (both or neither): timing events recorded at the kernel's own start
 // and end.
@@ -33,21 +45,26 @@ void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hip
                  hipEvent_t e1 = nullptr);
 // Column tiles (256 wide) of an N-column GEMM.
 int gemm_tiles(int N);
-// Rows per GEMM work-group for M rows (16, 32, 48 or 64).
+// Rows per GEMM work-group for M rows (16, 32, 48, 64, 96 or 128).
 int gemm_rows_per_group(int M);
 // Rows of the activation fragments for M rows: M padded to a multiple of
 // gemm_rows_per_group(M); non-decreasing in M.
 int gemm_padded_rows(int M);
-// Row-major [rows, cols] -> packed weight tiles (see include/via.h).
-void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, hipStream_t s);
+// Row-major [rows, cols] -> packed weight tiles (see include/via.h).  With
+// ffn > 0 the source is [2 ffn, cols] (gate rows, then up rows) and packed
+// row 16 b + i takes gate row 8 b + i (i < 8) or up row 8 b + i - 8.
+void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, int ffn, hipStream_t s);
+// 16-column blocks per gate/up work-group for d_ffn = F (1..8, about one
+// work-group per compute unit).
+int gate_up_blocks_per_group(int F);
 
-// X[m] += sum_s P[s][m] (split order; P may be null); the RMSNorm of the row
-// times g is written as activation fragments (`terms` bf16 terms, or fp32),
-// to fragment row rows[m].lm when `rows` is given (rows with lm < 0 skipped).
-void launch_resid_norm(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
-                       float eps, void* Y, int MBn, const RowInfo* rows, hipStream_t s);
-// h[m, f] = silu(sum_s P[s][m][f]) * sum_s P[s][m][F + f], as fragments.
-void launch_swiglu(bool bf16, const float* P, int ksplit, int M, int F, void* H, int MBn, hipStream_t s);
+// X[m] += sum_s P[s][m] (split order; P may be null); x * g is written as
+// activation fragments (`terms` bf16 terms, or fp32), to fragment row
+// rows[m].lm when `rows` is given (rows with lm < 0 skipped), and the sums of
+// x^2 over column chunks to ss[chunk * ss_stride + row]: the consumer of the
+// next projection multiplies its output row by row_scale() (RMSNorm).
+void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
+                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s);
 // Sum QKV partials, rotate-half RoPE at each row's position, Q -> fp32
 // buffer, K/V -> the paged cache (model dtype).
 struct QkvArgs {
@@ -61,6 +78,9 @@ struct QkvArgs {
   uint16_t* q_lo;      // [M, H, hd] bf16 lo terms (unused for fp32 models)
   void* pool;
   int pool_blocks, layer_slot;
+  const float* ss;     // RMSNorm sums of squares of the input rows (row_scale)
+  int ss_stride, d;
+  float eps;
 };
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s);
 

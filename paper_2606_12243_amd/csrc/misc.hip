@@ -36,65 +36,52 @@ __device__ __forceinline__ float4 split_sum(const float* P, size_t stride, int k
   return acc;
 }
 
-// x = X[m] + sum_s P[s][m] (split order); X[m] = x; y = x / sqrt(mean(x^2) + eps) * g,
-// written as activation fragments (row rows[m].lm when `rows` is given).
-// One work-group per row; d is a multiple of 64, each thread owns float4s.
+// Residual update and RMSNorm gain, elementwise: x = X[m] + sum_s P[s][m]
+// (split order; P may be null), X[m] = x, and x * g is written as
+// activation fragments (to fragment row rows[m].lm when `rows` is given;
+// rows with lm < 0 only update X).  The RMSNorm scale 1/sqrt(mean(x^2)+eps)
+// is a per-row factor that commutes with the next projection, so its
+// consumer applies it (row_scale) after the GEMM; here each work-group adds
+// the sum of x^2 over its kNormChunk columns to ss[chunk][out].
+// Grid (ceil(d / kNormChunk), M), 64 threads of 8 columns each.
 template <typename G, bool BF16, int NT>
-__global__ __launch_bounds__(1024) void resid_norm_kernel(float* X, const float* P, int ksplit, int M, int d,
-                                                          const G* g, float eps, void* Y, int MBn,
-                                                          const RowInfo* rows) {
-  __shared__ float red[1024];
-  const int m = blockIdx.x;
+__global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P, int ksplit, int M, int d,
+                                                       const G* g, void* Y, int MBn, const RowInfo* rows,
+                                                       float* ss, int ss_stride) {
+  const int m = blockIdx.y, chunk = blockIdx.x;
+  const int k0 = chunk * kNormChunk + threadIdx.x * 8;
+  const int out = rows ? rows[m].lm : m;
   float* x = X + (size_t)m * d;
   const size_t stride = (size_t)M * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x * 4; i < d; i += 4096) {
-    float4 v = *(float4*)(x + i);
-    if (P) {
-      const float4 acc = split_sum(P, stride, ksplit, (size_t)m * d + i);
-      v.x = v.x + acc.x;
-      v.y = v.y + acc.y;
-      v.z = v.z + acc.z;
-      v.w = v.w + acc.w;
-      *(float4*)(x + i) = v;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float sq = 0.f;
+  if (k0 < d) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float4 u = *(float4*)(x + k0 + 4 * h);
+      if (P) {
+        const float4 acc = split_sum(P, stride, ksplit, (size_t)m * d + k0 + 4 * h);
+        u.x = u.x + acc.x;
+        u.y = u.y + acc.y;
+        u.z = u.z + acc.z;
+        u.w = u.w + acc.w;
+        *(float4*)(x + k0 + 4 * h) = u;
+      }
+      v[4 * h + 0] = u.x;
+      v[4 * h + 1] = u.y;
+      v[4 * h + 2] = u.z;
+      v[4 * h + 3] = u.w;
     }
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-  }
-  red[threadIdx.x] = ss;
-  __syncthreads();
-  for (int o = 512; o > 0; o >>= 1) {
-    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-    __syncthreads();
-  }
-  const int out = rows ? rows[m].lm : m;
-  if (out < 0) return;
-  const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
-  for (int k0 = threadIdx.x * 8; k0 < d; k0 += 8192) {
-    float v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = x[k0 + e] * inv * to_f<G>(g[k0 + e]);
-    put_afrag<BF16, NT>(Y, out, k0, v, d >> 5, MBn);
+    for (int e = 0; e < 8; ++e) sq += v[e] * v[e];
   }
-}
-
-// h = silu(gate) * up from the gate/up partial sums, as fragments; grid (M, F / 2048).
-template <bool BF16, int NT>
-__global__ __launch_bounds__(256) void swiglu_kernel(const float* P, int ksplit, int M, int F, void* H, int MBn) {
-  const int m = blockIdx.x;
-  const int f = blockIdx.y * 2048 + threadIdx.x * 8;
-  if (f >= F) return;
-  const size_t N = 2 * (size_t)F, stride = (size_t)M * N;
-  float v[8];
+  if (out < 0) return;  // uniform per work-group
+  sq = wave_sum(sq);
+  if (threadIdx.x == 0) ss[(size_t)chunk * ss_stride + out] = sq;
+  if (k0 >= d) return;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const float4 gt = split_sum(P, stride, ksplit, (size_t)m * N + f + 4 * h);
-    const float4 up = split_sum(P, stride, ksplit, (size_t)m * N + F + f + 4 * h);
-    v[4 * h + 0] = gt.x / (1.0f + expf(-gt.x)) * up.x;
-    v[4 * h + 1] = gt.y / (1.0f + expf(-gt.y)) * up.y;
-    v[4 * h + 2] = gt.z / (1.0f + expf(-gt.z)) * up.z;
-    v[4 * h + 3] = gt.w / (1.0f + expf(-gt.w)) * up.w;
-  }
-  put_afrag<BF16, NT>(H, m, f, v, F >> 5, MBn);
+  for (int e = 0; e < 8; ++e) v[e] = v[e] * to_f<G>(g[k0 + e]);
+  put_afrag<BF16, NT>(Y, out, k0, v, d >> 5, MBn);
 }
 
 // QKV partial sums -> rotate-half RoPE -> Q (bf16 hi/lo terms, or fp32) and
@@ -121,7 +108,9 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
   const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
   const size_t c = (size_t)m * N + (size_t)hh * a.hd + i;
   const float4 a1 = split_sum(a.P, stride, a.ksplit, c), a2 = split_sum(a.P, stride, a.ksplit, c + half);
-  float x1[4] = {a1.x, a1.y, a1.z, a1.w}, x2[4] = {a2.x, a2.y, a2.z, a2.w};
+  // the input row's RMSNorm scale (the projection is linear in it)
+  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);
+  float x1[4] = {a1.x * sc, a1.y * sc, a1.z * sc, a1.w * sc}, x2[4] = {a2.x * sc, a2.y * sc, a2.z * sc, a2.w * sc};
   float y1[4], y2[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -296,25 +285,18 @@ void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, f
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)E, rows, d, X);
 }
 
-void launch_resid_norm(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
-                       float eps, void* Y, int MBn, const RowInfo* rows, hipStream_t s) {
+void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
+                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s) {
+  const dim3 grid((d + kNormChunk - 1) / kNormChunk, M);
   if (!bf16)
-    hipLaunchKernelGGL((resid_norm_kernel<float, false, 1>), dim3(M), dim3(1024), 0, s, X, P, ksplit, M, d,
-                       (const float*)g, eps, Y, MBn, rows);
+    hipLaunchKernelGGL((resid_add_kernel<float, false, 1>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
+                       (const float*)g, Y, MBn, rows, ss, ss_stride);
   else if (terms >= 3)
-    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 3>), dim3(M), dim3(1024), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, eps, Y, MBn, rows);
+    hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 3>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
+                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride);
   else
-    hipLaunchKernelGGL((resid_norm_kernel<uint16_t, true, 2>), dim3(M), dim3(1024), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, eps, Y, MBn, rows);
-}
-
-void launch_swiglu(bool bf16, const float* P, int ksplit, int M, int F, void* H, int MBn, hipStream_t s) {
-  const dim3 grid(M, (F + 2047) / 2048);
-  if (bf16)
-    hipLaunchKernelGGL((swiglu_kernel<true, 2>), grid, dim3(256), 0, s, P, ksplit, M, F, H, MBn);
-  else
-    hipLaunchKernelGGL((swiglu_kernel<false, 1>), grid, dim3(256), 0, s, P, ksplit, M, F, H, MBn);
+    hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 2>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
+                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride);
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {

@@ -73,13 +73,13 @@ Dims dims_of(const via_model_desc* d) {
   auto shape = [&](int N, int K) { return GemmShape{N, K, f32 ? 1 : choose_ksplit(N, K)}; };
   r.g_qkv = shape(r.qkv, r.d);
   r.g_o = shape(r.d, r.H * r.hd);
-  r.g_gu = shape(2 * r.F, r.d);
+  r.g_gu = GemmShape{2 * r.F, r.d, 1};  // full K per work-group (SwiGLU epilogue)
   r.g_down = shape(r.d, r.F);
   return r;
 }
 
 struct Layout {
-  size_t X, Yf, Q, Af, Hf, Ylf, part, att_o, att_ml, lm_part;
+  size_t X, Yf, Q, Af, Hf, Ylf, part, att_o, att_ml, lm_part, ss;
   size_t rows, seqs, btab, items, lm;  // plan region
   size_t step_seqs, dtok, drow, dpar;  // step region
   size_t c_btab, c_moves;              // commit region
@@ -116,6 +116,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.att_o = take((size_t)L.max_chunks * R * D.H * D.hd * 4);
   L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
   L.lm_part = take((size_t)gemm_tiles(D.V) * R * 4 * 4);
+  L.ss = take((size_t)ceil_div(D.d, kNormChunk) * R * 4);  // RMSNorm sums of squares [chunk][row]
   L.max_items = ceil_div(max_rows * D.G, kAttnQueries) + max_batch;
   // plan region (one upload per forward)
   size_t p0 = o;
@@ -382,8 +383,10 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     timed_gemm(kv, kind, bf, role, g, s);
   };
 
+  float* ss = (float*)(ws + L.ss);
+  const int ss_stride = kv->d.max_rows;
   launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
-  launch_resid_norm(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], eps, Yf, MBn, nullptr, s);
+  launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], Yf, MBn, nullptr, ss, ss_stride, s);
   AttnArgs at{};
   at.q_hi = Q;
   at.q_lo = Qlo;
@@ -420,6 +423,10 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   qa.q_lo = Qlo;
   qa.pool = pool;
   qa.pool_blocks = pool_blocks;
+  qa.ss = ss;
+  qa.ss_stride = ss_stride;
+  qa.d = D.d;
+  qa.eps = eps;
   for (size_t si = 0; si < route.size(); ++si) {
     const int l = route[si];
     // Q/K/V: three bf16 terms per activation (the K/V are rounded to the cache's bf16)
@@ -429,12 +436,28 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     at.layer_slot = (int)si;
     timed_launch(kv, VIA_KERNEL_ATTN, s, [&] { launch_attention(bf, at, s); });
     gemm(Af, m->w_o[l], D.g_o, GemmRole::kO, VIA_KERNEL_O);
-    launch_resid_norm(bf, 2, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], eps, Yf, MBn, nullptr, s);
-    gemm(Yf, m->w_gate_up[l], D.g_gu, GemmRole::kGateUp, VIA_KERNEL_GATEUP);
-    launch_swiglu(bf, part, D.g_gu.ks, M, D.F, Hf, MBn, s);
+    launch_resid_add(bf, 2, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], Yf, MBn, nullptr, ss, ss_stride, s);
+    {
+      GemmArgs g{};
+      g.X = Yf;
+      g.MBn = MBn;
+      g.W = m->w_gate_up[l];
+      g.M = M;
+      g.K = D.d;
+      g.N = 2 * D.F;
+      g.ksplit = 1;
+      g.H = Hf;
+      g.F = D.F;
+      g.nb = gate_up_blocks_per_group(D.F);
+      g.ss = ss;
+      g.ss_stride = ss_stride;
+      g.eps = eps;
+      timed_gemm(kv, VIA_KERNEL_GATEUP, bf, GemmRole::kGateUp, g, s);
+    }
     gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
-      launch_resid_norm(bf, 3, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], eps, Yf, MBn, nullptr, s);
+      launch_resid_add(bf, 3, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
+                       ss_stride, s);
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
@@ -442,7 +465,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     void* Ylf = ws + L.Ylf;
     const int MBl = gemm_padded_rows(nlm) / 16;
     // last residual update, final norm of the head rows only
-    launch_resid_norm(bf, 2, X, part, D.g_down.ks, M, D.d, m->final_norm, eps, Ylf, MBl, d_rows, s);
+    launch_resid_add(bf, 2, X, part, D.g_down.ks, M, D.d, m->final_norm, Ylf, MBl, d_rows, ss, ss_stride, s);
     GemmArgs h{};
     h.X = Ylf;
     h.MBn = MBl;
@@ -456,6 +479,9 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     h.inv_T = inv_T;
     h.logits = out->logits;
     h.draft_logit = out->draft_logit;
+    h.ss = ss;
+    h.ss_stride = ss_stride;
+    h.eps = eps;
     timed_launch(kv, VIA_KERNEL_HEAD, s, [&] {
       launch_gemm(bf, GemmRole::kHead, h, s);
       launch_lm_finalize(d_lm, h.lm_part, nlm, gemm_tiles(D.V), inv_T, out->row_argmax, out->row_max,
@@ -724,7 +750,18 @@ size_t via_packed_bytes(int32_t rows, int32_t cols, int32_t dtype) {
 via_status via_pack_weight(const void* src, void* dst, int32_t rows, int32_t cols, int32_t dtype, void* stream) {
   if (!src || !dst) return fail(VIA_EINVAL, "null pointer");
   if (!via_packed_bytes(rows, cols, dtype)) return fail(VIA_EINVAL, "rows >= 1, cols a positive multiple of 32, dtype f32/bf16");
-  launch_pack(dtype == VIA_DTYPE_BF16, src, dst, rows, cols, (hipStream_t)stream);
+  launch_pack(dtype == VIA_DTYPE_BF16, src, dst, rows, cols, 0, (hipStream_t)stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(VIA_EDEVICE, "pack launch: %s", hipGetErrorString(e));
+  return VIA_OK;
+}
+
+via_status via_pack_gate_up(const void* src, void* dst, int32_t d_ffn, int32_t d_model, int32_t dtype, void* stream) {
+  if (!src || !dst) return fail(VIA_EINVAL, "null pointer");
+  if (d_ffn < 8 || d_ffn % 8) return fail(VIA_EINVAL, "d_ffn must be a positive multiple of 8");
+  if (!via_packed_bytes(2 * d_ffn, d_model, dtype))
+    return fail(VIA_EINVAL, "d_model a positive multiple of 32, dtype f32/bf16");
+  launch_pack(dtype == VIA_DTYPE_BF16, src, dst, 2 * d_ffn, d_model, d_ffn, (hipStream_t)stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(VIA_EDEVICE, "pack launch: %s", hipGetErrorString(e));
   return VIA_OK;

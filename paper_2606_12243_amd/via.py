@@ -93,6 +93,7 @@ def _sig(name, res, *args):
 
 via_packed_bytes = _sig("via_packed_bytes", C.c_size_t, I32, I32, I32)
 via_pack_weight = _sig("via_pack_weight", I32, P, P, I32, I32, I32, P)
+via_pack_gate_up = _sig("via_pack_gate_up", I32, P, P, I32, I32, I32, P)
 via_pool_bytes = _sig("via_pool_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32)
 via_workspace_bytes = _sig("via_workspace_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
 via_staging_bytes = _sig("via_staging_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
@@ -119,7 +120,7 @@ via_kv_timer_read = _sig("via_kv_timer_read", I32, P, I32, PI32, C.POINTER(C.c_d
 via_last_error = _sig("via_last_error", C.c_char_p)
 via_version = _sig("via_version", C.c_char_p)
 
-EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
+EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide",
@@ -174,22 +175,29 @@ class Model:
         dt = DTYPE_BF16 if bf16 else DTYPE_F32
         stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
 
-        def packed(a):
-            # row-major [rows, cols] -> device -> packed tiles (the layout the GEMMs stream)
+        def packed(a, gate_up=False):
+            # row-major [rows, cols] -> device -> packed tiles (the layout the GEMMs stream);
+            # the gate/up matrix has its gate and up rows interleaved by 8
             src = dev(a)
             rows, cols = src.shape
             nb = via_packed_bytes(rows, cols, dt)
             if nb == 0:
                 raise ViaError(EUNSUPPORTED, f"cannot pack a [{rows}, {cols}] matrix")
             dst = torch.empty(nb // src.element_size(), dtype=src.dtype, device=device)
-            check(via_pack_weight(src.data_ptr(), dst.data_ptr(), rows, cols, dt, stream))
+            if gate_up:
+                check(via_pack_gate_up(src.data_ptr(), dst.data_ptr(), rows // 2, cols, dt, stream))
+            else:
+                check(via_pack_weight(src.data_ptr(), dst.data_ptr(), rows, cols, dt, stream))
             torch.cuda.current_stream().synchronize()
             return dst
 
-        PACKED = ("lm_head", "w_qkv", "w_o", "w_gate_up", "w_down")
+        PACKED = ("lm_head", "w_qkv", "w_o", "w_down")
         self.t = {}
         for k, v in weights.items():
-            f = packed if k in PACKED else dev
+            if k == "w_gate_up":
+                f = lambda x: packed(x, gate_up=True)
+            else:
+                f = packed if k in PACKED else dev
             self.t[k] = [f(x) for x in v] if isinstance(v, list) else f(v)
         L = desc["n_layers"]
         arr = lambda k: (P * L)(*[x.data_ptr() for x in self.t[k]])
