@@ -36,6 +36,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "accepted tokens/s + verify-step latency, 8B-shape bf16 k=8; % HBM/MFMA roofline"
 
 
@@ -206,6 +207,7 @@ def main():
     ap.add_argument("--no-full-tier", action="store_true",
                     help="skip the T = 1 variant (every position escalated to the full verifier)")
     ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
+    ap.add_argument("--no-prefill-gemm", action="store_true", help="skip the prefill GEMM roofline")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (the reference kernel for HBM counter scaling)")
     args = ap.parse_args()
@@ -275,6 +277,11 @@ def main():
             n, ms = rb["timer"]
             breakdown[nme] = {"launches": n, "total_ms": round(ms, 3), "avg_us": round(ms * 1e3 / max(1, n), 2)}
 
+    prefill = None
+    if not args.no_prefill_gemm and md["dtype"] == "bf16":
+        # prefill rows of the workload: every sequence's context, capped at 8192
+        prefill = prefill_gemm_roofline(md, min(8192, int(sum(cfg["ctx_lens"]))))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, W, res["recorded"], res["init_tokens"])
@@ -297,11 +304,56 @@ def main():
         "roofline": roof,
         "step_roofline": step_roof,
         "full_tier_variant": full_tier,
+        "prefill_gemm_roofline": prefill,
         "cpu_baseline": cpu,
     }
     if breakdown:
         out["kernels"] = breakdown
     print(json.dumps(out), flush=True)
+
+
+def prefill_gemm_roofline(md, M, reps=10):
+    """The prefill GEMM (the tile kernel of forwards of more than 128 rows) on
+    plain bf16 operands at the model's four projection shapes with M prefill
+    rows: algorithmic 2 M N K flops per launch / the average launch time (HIP
+    events on the stream of the call) against the bf16 MFMA peak."""
+    import ctypes as C
+    import torch
+    from paper_2606_12243_amd import via
+    d, F, V = md["d_model"], md["d_ffn"], md["vocab"]
+    H, KVH, hd = md["n_heads"], md["n_kv_heads"], md["head_dim"]
+    shapes = {"qkv": ((H + 2 * KVH) * hd, d), "o": (d, H * hd), "gate_up": (2 * F, d), "down": (d, F)}
+    stream = torch.cuda.current_stream()
+    sp = C.c_void_p(stream.cuda_stream)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    out, tot_flop, tot_ms = {}, 0.0, 0.0
+    for name, (N, K) in shapes.items():
+        Mp = (M + 15) // 16 * 16
+        x = (torch.randn(Mp * K, generator=g, device="cuda") * 0.5).to(torch.bfloat16)  # fragment layout
+        w = torch.empty(via.via_packed_bytes(N, K, via.DTYPE_BF16) // 2, dtype=torch.bfloat16, device="cuda")
+        w.copy_((torch.randn(w.numel(), generator=g, device="cuda") * 0.02).to(torch.bfloat16))
+        c = torch.empty(M, N, dtype=torch.float32, device="cuda")
+        run = lambda: via.check(via.via_gemm_bf16(x.data_ptr(), w.data_ptr(), c.data_ptr(), M, N, K, sp))
+        run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        flop = 2.0 * M * N * K
+        tf = flop / (ms * 1e-3) / 1e12
+        out[name] = {"N": N, "K": K, "us": round(ms * 1e3, 1), "TFLOPs": round(tf, 1),
+                     "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+        tot_flop += flop
+        tot_ms += ms
+        del x, w, c
+    ach = tot_flop / (tot_ms * 1e-3) / 1e12
+    return {"kernel": "gemm_prefill: the four projections of one layer, plain bf16", "bound": "mfma",
+            "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None, "M": M, "shapes": out}
 
 
 def measured_traffic(config):

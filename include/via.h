@@ -218,6 +218,21 @@ via_status via_pack_weight(const void *src, void *dst, int32_t rows, int32_t col
 via_status via_pack_gate_up(const void *src, void *dst, int32_t d_ffn, int32_t d_model, int32_t dtype,
                             void *stream);
 
+/* ---- prefill GEMM --------------------------------------------------------
+ * C = X W^T for bf16 X [M, K] and W [N, K], fp32 accumulation and output:
+ * the compute-bound tile kernel that runs every projection of a forward of
+ * more than 128 rows (a prefill), exposed for measurement and tests.  (A
+ * forward feeds it its fp32 activations as 2 or 3 bf16 terms, one pass each;
+ * this call runs one.)
+ *   X  device bf16, ceil(M/16)*16 rows, in the activation-fragment layout:
+ *      element (m, k) is at 8-element group
+ *      ((k/32) * ceil(M/16) + m/16) * 64 + ((k%32)/8) * 16 + m%16, offset k%8
+ *      (rows past M may hold anything; they are never stored)
+ *   W  device bf16 in the via_pack_weight layout of [N, K]
+ *   C  device fp32 [M, N] row-major, written
+ * K must be a multiple of 32.  Asynchronous on `stream`. */
+via_status via_gemm_bf16(const void *X, const void *W, float *C, int32_t M, int32_t N, int32_t K, void *stream);
+
 /* ---- sizes -------------------------------------------------------------- */
 size_t via_pool_bytes(const via_model_desc *desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size);
 size_t via_workspace_bytes(const via_model_desc *desc, int32_t max_rows, int32_t max_batch,

@@ -623,6 +623,134 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int row
   for (int e = 0; e < 8; ++e) dst[gidx * 8 + e] = r < (size_t)rows ? src[sr * cols + c + e] : T(0);
 }
 
+// ------------------------------------------------------------- prefill GEMM
+// Many-row GEMM (prefill-sized M): C[M, N] = sum over the NT activation terms
+// of X_q[M, K] W[N, K]^T, fp32, written as one partial tile (split 1) so the
+// consumers of the verify GEMMs read it unchanged.  Compute-bound: a
+// work-group of 8 waves owns a 256 x 256 tile; wave (wm, wn) computes rows
+// wm*128 .. +128 and columns wn*64 .. +64 with v_mfma_f32_16x16x32_bf16.  A
+// stage is one 32-wide K step of the tile: 16 row blocks of X and 16 column
+// blocks of W, each a contiguous 1 KB fragment in both layouts, copied
+// verbatim into LDS by global_load_lds_dwordx4 (16 bytes per lane written at
+// m0 + 16 * lane).  Four stages rotate in LDS, loaded three steps ahead.  The
+// copies are issued by inline asm so that the compiler, which would otherwise
+// make every LDS read wait for all outstanding copies, leaves their
+// completion to the explicit vmcnt waits below.  Work-groups are dispatched
+// round-robin over the 8 XCDs; XCD x takes a contiguous range of tiles, taken
+// in groups of 8 row tiles so that co-resident work-groups share operand
+// blocks in its L2.
+constexpr int kPfBM = 256, kPfBN = 256, kPfStages = 4, kPfStage = 32 * 1024;
+constexpr int kPfGroupM = 8;
+
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+__global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) {
+  __shared__ __align__(1024) unsigned char smem[kPfStages * kPfStage];
+  const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
+  const int tiles_n = (a.N + kPfBN - 1) / kPfBN, tiles_m = (a.M + kPfBM - 1) / kPfBM;
+  const int ntiles = tiles_m * tiles_n;
+  const int per = (ntiles + 7) / 8;
+  const int tile = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (tile >= ntiles) return;  // uniform
+  const int grp = tile / (kPfGroupM * tiles_n), in = tile % (kPfGroupM * tiles_n);
+  const int gm = min(kPfGroupM, tiles_m - grp * kPfGroupM);
+  const int m0 = (grp * kPfGroupM + in % gm) * kPfBM, n0 = (in / gm) * kPfBN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave >> 2, wn = wave & 3;
+  const int iters = nt * S;  // K32 steps over all terms
+  // wave w copies row blocks w, w + 8 and column blocks w, w + 8 of each stage;
+  // blocks past the matrix are clamped (their products are never stored)
+  const uint4* xa[2];
+  const uint4* wb[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    xa[h] = (const uint4*)a.X + (size_t)min((m0 >> 4) + h * 8 + wave, a.MBn - 1) * 64 + lane;
+    const int cb = (n0 >> 4) + h * 8 + wave;
+    wb[h] = (const uint4*)a.W + (size_t)min(cb >> 2, t64 - 1) * S * 256 + (cb & 3) * 64 + lane;
+  }
+  const size_t xstep = (size_t)a.MBn * 64;
+  const uint32_t lds_base =
+      __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(__attribute__((address_space(3))) void*)(smem + wave * 1024));
+  auto issue = [&](int it) {
+    const int q = it / S, ks = it - q * S;
+    const uint32_t d = lds_base + (it % kPfStages) * kPfStage;
+    lds_dma16(xa[0] + ((size_t)q * S + ks) * xstep, d);
+    lds_dma16(xa[1] + ((size_t)q * S + ks) * xstep, d + 8 * 1024);
+    lds_dma16(wb[0] + (size_t)ks * 256, d + 16 * 1024);
+    lds_dma16(wb[1] + (size_t)ks * 256, d + 24 * 1024);
+  };
+  f32x4 acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < kPfStages - 1; ++p) issue(min(p, iters - 1));
+  for (int it = 0; it < iters; ++it) {
+    // this wave's copies of stage `it` are the oldest 4 of its 4 * (stages - 1)
+    // outstanding ones; its LDS reads of stage it - 1 are complete.  After the
+    // barrier every wave's part of stage `it` is in LDS and stage it - 1's
+    // buffer is free for stage it + 3 (past the end the last stage is copied
+    // again into a buffer nothing reads).
+    __builtin_amdgcn_s_waitcnt((4 * (kPfStages - 2)) | (0x7 << 4) | (0x0 << 8));
+    __builtin_amdgcn_s_barrier();
+    issue(min(it + kPfStages - 1, iters - 1));
+    const uint4* st = (const uint4*)(smem + (it % kPfStages) * kPfStage);
+    uint4 af[8], bfr[4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) af[i] = st[(wm * 8 + i) * 64 + lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bfr[j] = st[(16 + wn * 4 + j) * 64 + lane];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(af[i]), as_bf16x8(bfr[j]), acc[i][j], 0, 0, 0);
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the trailing copies land before the work-group ends
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + wn * 64 + j * 16 + n;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = m0 + wm * 128 + i * 16 + g * 4 + r;
+        if (row < a.M && col < a.N) a.part[(size_t)row * a.N + col] = acc[i][j][r];
+      }
+    }
+}
+
+// SwiGLU over a prefill gate/up product P[M, 2F] whose columns interleave
+// gate and up by 8 (the packed gate/up order): h = silu(g s) * (u s) with the
+// input row's RMSNorm scale s, written as 2-term fragments.  One thread per
+// (row, 8-f group).
+__global__ __launch_bounds__(256) void swiglu_rows_kernel(GemmArgs a) {
+  const int groups = a.F >> 3;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= a.M * groups) return;
+  const int m = e / groups, j = e - m * groups;
+  const float* t = a.part + (size_t)m * a.N + j * 16;
+  const float sc = row_scale(a.ss, a.ss_stride, m, a.K, a.eps);
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float gt = t[i] * sc, up = t[8 + i] * sc;
+    v[i] = gt / (1.0f + expf(-gt)) * up;
+  }
+  put_afrag<true, 2>(a.H, m, j * 8, v, a.F >> 5, a.MBn);
+}
+
+void launch_prefill(const GemmArgs& a, int nt, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const int ntiles = ((a.M + kPfBM - 1) / kPfBM) * ((a.N + kPfBN - 1) / kPfBN);
+  const dim3 grid((ntiles + 7) / 8 * 8);
+  if (e0)
+    hipExtLaunchKernelGGL(gemm_prefill, grid, dim3(kThreads), 0, s, e0, e1, 0, a, nt);
+  else
+    hipLaunchKernelGGL(gemm_prefill, grid, dim3(kThreads), 0, s, a, nt);
+}
+
 }  // namespace
 
 void launch_pack(bool bf16, const void* src, void* dst, int rows, int cols, int ffn, hipStream_t s) {
@@ -652,12 +780,26 @@ int gemm_padded_rows(int M) {
   return (M + g - 1) / g * g;
 }
 
+bool gemm_is_prefill(bool bf16, int M) { return bf16 && M > kPrefillMinRows; }
+
 void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (role != GemmRole::kHead && gemm_is_prefill(bf16, a.M)) {
+    // many rows: the compute-bound tile kernel (one partial, ksplit 1)
+    const int nt = role == GemmRole::kQkv ? 3 : 2;
+    launch_prefill(a, nt, s, e0, e1);
+    if (role == GemmRole::kGateUp) {
+      const int n = a.M * (a.F >> 3);
+      hipLaunchKernelGGL(swiglu_rows_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
+    }
+    return;
+  }
   if (bf16)
     launch_role<uint16_t>(role, a, s, e0, e1);
   else
     launch_role<float>(role, a, s, e0, e1);
 }
+
+void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) { launch_prefill(a, 1, s, nullptr, nullptr); }
 
 void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int ntiles, float inv_T, int32_t* row_argmax,
                         float* row_max, float* row_sumexp, float* row_gap, hipStream_t s) {

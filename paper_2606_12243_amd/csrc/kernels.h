@@ -43,6 +43,13 @@ enum class GemmRole { kQkv, kO, kGateUp, kDown, kHead };
 // and end.
 void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
                  hipEvent_t e1 = nullptr);
+// Forwards of more rows than this run their projections (bf16 models) on the
+// compute-bound prefill GEMM, which writes one partial (ksplit must be 1).
+constexpr int kPrefillMinRows = 128;
+bool gemm_is_prefill(bool bf16, int M);
+// Plain bf16 product a.part[M, N] = X[M, K] W[N, K]^T (one activation term)
+// on the prefill GEMM.
+void launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
 // Column tiles (256 wide) of an N-column GEMM.
 int gemm_tiles(int N);
 // Rows per GEMM work-group for M rows (16, 32, 48, 64, 96 or 128).

@@ -15,25 +15,44 @@ __global__ __launch_bounds__(256) void embed_kernel(const T* E, const RowInfo* r
   for (int i = threadIdx.x; i < d; i += 256) X[(size_t)m * d + i] = to_f<T>(e[i]);
 }
 
-// Sum of the split partials of one float4, in split order, with 8 loads in
-// flight.  Loads past the last split re-read it (unconditional loads keep the
-// code branch-free) and are dropped by a select.
-__device__ __forceinline__ float4 split_sum(const float* P, size_t stride, int ksplit, size_t off) {
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int sp = 0; sp < ksplit; sp += 8) {
-    float4 v[8];
+// Split partials of two float4s (offsets o0 and o1): split_load16 issues
+// the loads of splits 0..15 (past the last split it re-reads the last one:
+// unconditional loads keep the code branch-free), split_reduce16 sums them
+// in split order (the re-reads dropped by a select), and split_sum2 does
+// both for splits sp0.. with 16 splits of loads in flight per round.
+__device__ __forceinline__ void split_load16(const float* P, size_t stride, int ksplit, int sp0, size_t o0, size_t o1,
+                                             float4 (&v0)[16], float4 (&v1)[16]) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v[q] = *(const float4*)(P + (size_t)min(sp + q, ksplit - 1) * stride + off);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const bool ok = sp + q < ksplit;
-      acc.x += ok ? v[q].x : 0.f;
-      acc.y += ok ? v[q].y : 0.f;
-      acc.z += ok ? v[q].z : 0.f;
-      acc.w += ok ? v[q].w : 0.f;
-    }
+  for (int q = 0; q < 16; ++q) {
+    const size_t base = (size_t)min(sp0 + q, ksplit - 1) * stride;
+    v0[q] = *(const float4*)(P + base + o0);
+    v1[q] = *(const float4*)(P + base + o1);
   }
-  return acc;
+}
+
+__device__ __forceinline__ void split_reduce16(int ksplit, int sp0, const float4 (&v0)[16], const float4 (&v1)[16],
+                                               float4& s0, float4& s1) {
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const bool ok = sp0 + q < ksplit;
+    s0.x += ok ? v0[q].x : 0.f;
+    s0.y += ok ? v0[q].y : 0.f;
+    s0.z += ok ? v0[q].z : 0.f;
+    s0.w += ok ? v0[q].w : 0.f;
+    s1.x += ok ? v1[q].x : 0.f;
+    s1.y += ok ? v1[q].y : 0.f;
+    s1.z += ok ? v1[q].z : 0.f;
+    s1.w += ok ? v1[q].w : 0.f;
+  }
+}
+
+__device__ __forceinline__ void split_sum2(const float* P, size_t stride, int ksplit, int sp0, size_t o0, size_t o1,
+                                           float4& s0, float4& s1) {
+  for (int sp = sp0; sp < ksplit; sp += 16) {
+    float4 v0[16], v1[16];
+    split_load16(P, stride, ksplit, sp, o0, o1, v0, v1);
+    split_reduce16(ksplit, sp, v0, v1, s0, s1);
+  }
 }
 
 // Residual update and RMSNorm gain, elementwise: x = X[m] + sum_s P[s][m]
@@ -56,15 +75,16 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
   float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float sq = 0.f;
   if (k0 < d) {
+    float4 acc[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+    if (P) split_sum2(P, stride, ksplit, 0, (size_t)m * d + k0, (size_t)m * d + k0 + 4, acc[0], acc[1]);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       float4 u = *(float4*)(x + k0 + 4 * h);
       if (P) {
-        const float4 acc = split_sum(P, stride, ksplit, (size_t)m * d + k0 + 4 * h);
-        u.x = u.x + acc.x;
-        u.y = u.y + acc.y;
-        u.z = u.z + acc.z;
-        u.w = u.w + acc.w;
+        u.x = u.x + acc[h].x;
+        u.y = u.y + acc[h].y;
+        u.z = u.z + acc[h].z;
+        u.w = u.w + acc[h].w;
         *(float4*)(x + k0 + 4 * h) = u;
       }
       v[4 * h + 0] = u.x;
@@ -93,6 +113,15 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
   const int m = blockIdx.x;
   const int half = a.hd >> 1;
   const RowInfo ri = a.rows[m];
+  const int tph = a.hd >> 3;  // threads per head
+  const int hh = (blockIdx.y * 256 + threadIdx.x) / tph;
+  const bool live = hh < a.H + 2 * a.KVH;
+  const int i = ((blockIdx.y * 256 + threadIdx.x) % tph) * 4;
+  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
+  const size_t c = (size_t)m * N + (size_t)hh * a.hd + i;
+  // the first 16 splits' loads go out before the angle computation below
+  float4 v1[16], v2[16];
+  if (live) split_load16(a.P, stride, a.ksplit, 0, c, c + half, v1, v2);
   // the row's rotation angles pos * theta^(-2j/hd), j < hd/2, in fp64: computed
   // once per work-group and shared by all its heads
   __shared__ double s_cs[128], s_sn[128];
@@ -101,13 +130,10 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
     sincos(ang, &s_sn[j], &s_cs[j]);
   }
   __syncthreads();
-  const int tph = a.hd >> 3;  // threads per head
-  const int hh = (blockIdx.y * 256 + threadIdx.x) / tph;
-  if (hh >= a.H + 2 * a.KVH) return;
-  const int i = ((blockIdx.y * 256 + threadIdx.x) % tph) * 4;
-  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
-  const size_t c = (size_t)m * N + (size_t)hh * a.hd + i;
-  const float4 a1 = split_sum(a.P, stride, a.ksplit, c), a2 = split_sum(a.P, stride, a.ksplit, c + half);
+  if (!live) return;
+  float4 a1 = make_float4(0.f, 0.f, 0.f, 0.f), a2 = a1;
+  split_reduce16(a.ksplit, 0, v1, v2, a1, a2);
+  if (a.ksplit > 16) split_sum2(a.P, stride, a.ksplit, 16, c, c + half, a1, a2);
   // the input row's RMSNorm scale (the projection is linear in it)
   const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);
   float x1[4] = {a1.x * sc, a1.y * sc, a1.z * sc, a1.w * sc}, x2[4] = {a2.x * sc, a2.y * sc, a2.z * sc, a2.w * sc};

@@ -109,8 +109,13 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.Af = take(Rp * D.H * D.hd * f2);
   L.Hf = take(Rp * D.F * f2);
   L.Ylf = take(Rp * D.d * f2);
+  // split-K partials of forwards of up to kPrefillMinRows rows; longer
+  // (prefill-sized) forwards write one partial of all their rows
   size_t part = 0;
-  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down}) part = std::max(part, (size_t)g.ks * R * g.N * 4);
+  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down}) {
+    part = std::max(part, (size_t)g.ks * std::min<size_t>(R, kPrefillMinRows) * g.N * 4);
+    if (gemm_is_prefill(es == 2, (int)R)) part = std::max(part, R * g.N * 4);
+  }
   L.part = take(part);
   L.max_chunks = ceil_div(max_blocks * kBlock, kAttnChunk);
   L.att_o = take((size_t)L.max_chunks * R * D.H * D.hd * 4);
@@ -370,6 +375,9 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     route = m->route;
   const float eps = m->d.rms_eps;
 
+  // K splits of each projection's partials (one on the prefill GEMM)
+  const bool prefill_gemm = gemm_is_prefill(bf, M);
+  auto ks = [&](const GemmShape& sh) { return prefill_gemm ? 1 : sh.ks; };
   auto gemm = [&](const void* Xf, const void* W, const GemmShape& sh, GemmRole role, int kind) {
     GemmArgs g{};
     g.X = Xf;
@@ -378,7 +386,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     g.M = M;
     g.K = sh.K;
     g.N = sh.N;
-    g.ksplit = sh.ks;
+    g.ksplit = ks(sh);
     g.part = part;
     timed_gemm(kv, kind, bf, role, g, s);
   };
@@ -410,7 +418,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   at.MBn = MBn;
   QkvArgs qa{};
   qa.P = part;
-  qa.ksplit = D.g_qkv.ks;
+  qa.ksplit = ks(D.g_qkv);
   qa.M = M;
   qa.H = D.H;
   qa.KVH = D.KVH;
@@ -436,7 +444,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     at.layer_slot = (int)si;
     timed_launch(kv, VIA_KERNEL_ATTN, s, [&] { launch_attention(bf, at, s); });
     gemm(Af, m->w_o[l], D.g_o, GemmRole::kO, VIA_KERNEL_O);
-    launch_resid_add(bf, 2, X, part, D.g_o.ks, M, D.d, m->ffn_norm[l], Yf, MBn, nullptr, ss, ss_stride, s);
+    launch_resid_add(bf, 2, X, part, ks(D.g_o), M, D.d, m->ffn_norm[l], Yf, MBn, nullptr, ss, ss_stride, s);
     {
       GemmArgs g{};
       g.X = Yf;
@@ -446,6 +454,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
       g.K = D.d;
       g.N = 2 * D.F;
       g.ksplit = 1;
+      g.part = part;  // the prefill GEMM's gate/up product (consumed by its SwiGLU pass)
       g.H = Hf;
       g.F = D.F;
       g.nb = gate_up_blocks_per_group(D.F);
@@ -456,7 +465,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     }
     gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
-      launch_resid_add(bf, 3, X, part, D.g_down.ks, M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
+      launch_resid_add(bf, 3, X, part, ks(D.g_down), M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
                        ss_stride, s);
   }
   if (head && !P.lm.empty()) {
@@ -465,7 +474,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     void* Ylf = ws + L.Ylf;
     const int MBl = gemm_padded_rows(nlm) / 16;
     // last residual update, final norm of the head rows only
-    launch_resid_add(bf, 2, X, part, D.g_down.ks, M, D.d, m->final_norm, Ylf, MBl, d_rows, ss, ss_stride, s);
+    launch_resid_add(bf, 2, X, part, ks(D.g_down), M, D.d, m->final_norm, Ylf, MBl, d_rows, ss, ss_stride, s);
     GemmArgs h{};
     h.X = Ylf;
     h.MBn = MBl;
@@ -753,6 +762,24 @@ via_status via_pack_weight(const void* src, void* dst, int32_t rows, int32_t col
   launch_pack(dtype == VIA_DTYPE_BF16, src, dst, rows, cols, 0, (hipStream_t)stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(VIA_EDEVICE, "pack launch: %s", hipGetErrorString(e));
+  return VIA_OK;
+}
+
+via_status via_gemm_bf16(const void* X, const void* W, float* C, int32_t M, int32_t N, int32_t K, void* stream) {
+  if (!X || !W || !C) return fail(VIA_EINVAL, "null pointer");
+  if (M < 1 || N < 1 || K < 32 || K % 32) return fail(VIA_EINVAL, "M, N >= 1 and K a positive multiple of 32");
+  GemmArgs g{};
+  g.X = X;
+  g.MBn = ceil_div(M, 16);
+  g.W = W;
+  g.M = M;
+  g.K = K;
+  g.N = N;
+  g.ksplit = 1;
+  g.part = C;
+  launch_gemm_bf16(g, (hipStream_t)stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(VIA_EDEVICE, "gemm launch: %s", hipGetErrorString(e));
   return VIA_OK;
 }
 

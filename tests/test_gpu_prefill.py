@@ -1,0 +1,91 @@
+"""The prefill GEMM: the compute-bound tile kernel that runs every projection
+of a forward of more than 128 rows.
+
+* via_gemm_bf16 (one activation term) against a float64 product of the same
+  bf16 operands, within the rigorous bound of fp32 accumulation of exact bf16
+  products, |err| <= K * 2^-24 * (|X| |W|^T); shapes cover one row, ragged
+  M/N tails of the 256 x 256 tiles, K of one stage, and full prefill sizes.
+* A prefill-sized forward (prompts of 300 and 129 tokens, so the prefill GEMM
+  with its 2- and 3-term activations and the separate SwiGLU pass builds the
+  caches), followed by lock-step decoding against the oracle.
+"""
+import ctypes as C
+
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2606_12243_amd import via  # noqa: E402
+from workload import configs, gen  # noqa: E402
+
+from gpu_harness import Lockstep  # noqa: E402
+
+
+def to_fragments(x):
+    """Row-major [M, K] -> the activation-fragment layout of include/via.h
+    (rows padded to a multiple of 16 with zeros)."""
+    M, K = x.shape
+    Mp = (M + 15) // 16 * 16
+    xp = torch.zeros(Mp, K, dtype=x.dtype)
+    xp[:M] = x
+    # element (m, k) -> group ((k/32) * Mp/16 + m/16) * 64 + ((k%32)/8) * 16 + m%16, offset k%8
+    return xp.view(Mp // 16, 16, K // 32, 4, 8).permute(2, 0, 3, 1, 4).contiguous()
+
+
+def gemm_bf16(x, w):
+    M, K = x.shape
+    N = w.shape[0]
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    xd = to_fragments(x).cuda()
+    wd = w.cuda()
+    wp = torch.empty(via.via_packed_bytes(N, K, via.DTYPE_BF16) // 2, dtype=torch.bfloat16, device="cuda")
+    via.check(via.via_pack_weight(wd.data_ptr(), wp.data_ptr(), N, K, via.DTYPE_BF16, stream))
+    c = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    via.check(via.via_gemm_bf16(xd.data_ptr(), wp.data_ptr(), c.data_ptr(), M, N, K, stream))
+    torch.cuda.synchronize()
+    return c.cpu()
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 32), (300, 200, 96), (257, 513, 64), (2048, 1024, 4096),
+                                   (8192, 512, 1024)])
+def test_gemm_bf16_matches_fp64_reference(M, N, K):
+    print(f"[case] gemm_bf16 M={M} N={N} K={K}", flush=True)
+    g = torch.Generator().manual_seed(M * 7 + N * 3 + K)
+    x = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    w = torch.randn(N, K, generator=g).to(torch.bfloat16)
+    c = gemm_bf16(x, w).double()
+    ref = x.double() @ w.double().T
+    bound = K * 2.0 ** -24 * (x.double().abs() @ w.double().abs().T) + 1e-30
+    assert torch.isfinite(c).all(), "every output element is written"
+    ratio = ((c - ref).abs() / bound).max().item()
+    print(f"[done] max |err| / bound = {ratio:.3g}", flush=True)
+    assert ratio <= 1.0
+
+
+def test_gemm_bf16_rejects_bad_shapes():
+    stream = C.c_void_p(0)
+    assert via.via_gemm_bf16(None, None, None, 1, 1, 32, stream) == via.EINVAL
+    buf = torch.empty(64, dtype=torch.float32, device="cuda")
+    p = buf.data_ptr()
+    assert via.via_gemm_bf16(p, p, p, 1, 1, 48, stream) == via.EINVAL   # K not a multiple of 32
+    assert via.via_gemm_bf16(p, p, p, 0, 1, 32, stream) == via.EINVAL
+
+
+@pytest.mark.parametrize("name", ["micro_bf16", "small_bf16_hd128"])
+def test_prefill_sized_forward_lockstep(name):
+    cfg = configs.get(name)
+    cfg.update(seed_c=24, seed_d=34, corrupt=0.3, temperature=1.0)
+    print(f"[case] prefill-sized forward {name}", flush=True)
+    ls = Lockstep(cfg, max_rows=320, max_batch=2, max_drafts=8, max_blocks=32, blocks=128)
+    try:
+        ls.add_prompt(0, gen.context_tokens(cfg, 0, 300))  # 299 rows per forward: ragged 256-row tiles
+        ls.add_prompt(1, gen.context_tokens(cfg, 1, 130))  # 129 rows: just past the threshold
+        steps = ls.run_chain([0, 1], G=16, k=6)
+        print(f"[done] {name} steps={steps} max_logit_err={ls.max_logit_err:.3g} tiers={sorted(ls.seen_tiers)} "
+              f"resyncs={len(ls.log)}", flush=True)
+    finally:
+        ls.close()
