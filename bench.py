@@ -313,7 +313,7 @@ def main():
 
 
 def prefill_gemm_roofline(md, M, reps=10):
-    """The prefill GEMM (the tile kernel of forwards of more than 128 rows) on
+    """The prefill GEMM (the tile kernel of forwards of more than 512 rows) on
     plain bf16 operands at the model's four projection shapes with M prefill
     rows: algorithmic 2 M N K flops per launch / the average launch time (HIP
     events on the stream of the call) against the bf16 MFMA peak."""

@@ -45,7 +45,9 @@ void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hip
                  hipEvent_t e1 = nullptr);
 // Forwards of more rows than this run their projections (bf16 models) on the
 // compute-bound prefill GEMM, which writes one partial (ksplit must be 1).
-constexpr int kPrefillMinRows = 128;
+// Below it the weight-streaming GEMMs, at most 4 passes of 128-row groups
+// over the weights, cost less than 256 x 256 tiles too few to fill the GPU.
+constexpr int kPrefillMinRows = 512;
 bool gemm_is_prefill(bool bf16, int M);
 // Plain bf16 product a.part[M, N] = X[M, K] W[N, K]^T (one activation term)
 // on the prefill GEMM.

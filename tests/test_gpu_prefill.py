@@ -1,11 +1,11 @@
 """The prefill GEMM: the compute-bound tile kernel that runs every projection
-of a forward of more than 128 rows.
+of a forward of more than 512 rows.
 
 * via_gemm_bf16 (one activation term) against a float64 product of the same
   bf16 operands, within the rigorous bound of fp32 accumulation of exact bf16
   products, |err| <= K * 2^-24 * (|X| |W|^T); shapes cover one row, ragged
   M/N tails of the 256 x 256 tiles, K of one stage, and full prefill sizes.
-* A prefill-sized forward (prompts of 300 and 129 tokens, so the prefill GEMM
+* A prefill-sized forward (prompts of 600 and 514 tokens, so the prefill GEMM
   with its 2- and 3-term activations and the separate SwiGLU pass builds the
   caches), followed by lock-step decoding against the oracle.
 """
@@ -80,10 +80,10 @@ def test_prefill_sized_forward_lockstep(name):
     cfg = configs.get(name)
     cfg.update(seed_c=24, seed_d=34, corrupt=0.3, temperature=1.0)
     print(f"[case] prefill-sized forward {name}", flush=True)
-    ls = Lockstep(cfg, max_rows=320, max_batch=2, max_drafts=8, max_blocks=32, blocks=128)
+    ls = Lockstep(cfg, max_rows=640, max_batch=2, max_drafts=8, max_blocks=48, blocks=192)
     try:
-        ls.add_prompt(0, gen.context_tokens(cfg, 0, 300))  # 299 rows per forward: ragged 256-row tiles
-        ls.add_prompt(1, gen.context_tokens(cfg, 1, 130))  # 129 rows: just past the threshold
+        ls.add_prompt(0, gen.context_tokens(cfg, 0, 600))  # 599 rows per forward: ragged 256-row tiles
+        ls.add_prompt(1, gen.context_tokens(cfg, 1, 514))  # 513 rows: just past the threshold
         steps = ls.run_chain([0, 1], G=16, k=6)
         print(f"[done] {name} steps={steps} max_logit_err={ls.max_logit_err:.3g} tiers={sorted(ls.seen_tiers)} "
               f"resyncs={len(ls.log)}", flush=True)
