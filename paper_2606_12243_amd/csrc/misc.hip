@@ -104,74 +104,60 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
   put_afrag<BF16, NT>(Y, out, k0, v, d >> 5, MBn);
 }
 
-// QKV partial sums -> rotate-half RoPE -> Q (bf16 hi/lo terms, or fp32) and
-// paged K/V (model dtype).  A thread owns dims i..i+3 of one head of one row
-// and their rotation partners i+hd/2..; hd/8 threads per head, 256 per
-// work-group; grid (M, ceil((H + 2 KVH) * hd / 8 / 256)); hd <= 256.
+// QKV partial sums -> RMSNorm scale of the input row -> rotate-half RoPE at
+// the row's position -> Q (bf16 hi/lo terms, or fp32) and paged K/V (model
+// dtype).  One work-group of 64 threads per (row, head of Q, K or V); thread
+// j owns the rotation pair (j, j + hd/2) and its angle pos * theta^(-2j/hd),
+// computed in fp64 while the loads of the pair's split partials (all in
+// flight at once, summed in split order) are outstanding.
 template <typename T>
-__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
-  const int m = blockIdx.x;
+__global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
+  const int m = blockIdx.x, hh = blockIdx.y, j = threadIdx.x;
   const int half = a.hd >> 1;
-  const RowInfo ri = a.rows[m];
-  const int tph = a.hd >> 3;  // threads per head
-  const int hh = (blockIdx.y * 256 + threadIdx.x) / tph;
-  const bool live = hh < a.H + 2 * a.KVH;
-  const int i = ((blockIdx.y * 256 + threadIdx.x) % tph) * 4;
+  if (j >= half) return;
   const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
-  const size_t c = (size_t)m * N + (size_t)hh * a.hd + i;
-  // the first 16 splits' loads go out before the angle computation below
-  float4 v1[16], v2[16];
-  if (live) split_load16(a.P, stride, a.ksplit, 0, c, c + half, v1, v2);
-  // the row's rotation angles pos * theta^(-2j/hd), j < hd/2, in fp64: computed
-  // once per work-group and shared by all its heads
-  __shared__ double s_cs[128], s_sn[128];
-  for (int j = threadIdx.x; j < half; j += 256) {
-    const double ang = (double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd);
-    sincos(ang, &s_sn[j], &s_cs[j]);
-  }
-  __syncthreads();
-  if (!live) return;
-  float4 a1 = make_float4(0.f, 0.f, 0.f, 0.f), a2 = a1;
-  split_reduce16(a.ksplit, 0, v1, v2, a1, a2);
-  if (a.ksplit > 16) split_sum2(a.P, stride, a.ksplit, 16, c, c + half, a1, a2);
-  // the input row's RMSNorm scale (the projection is linear in it)
-  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);
-  float x1[4] = {a1.x * sc, a1.y * sc, a1.z * sc, a1.w * sc}, x2[4] = {a2.x * sc, a2.y * sc, a2.z * sc, a2.w * sc};
-  float y1[4], y2[4];
+  const size_t c = (size_t)m * N + (size_t)hh * a.hd + j;
+  float v1[16], v2[16];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    y1[e] = x1[e];
-    y2[e] = x2[e];
+  for (int q = 0; q < 16; ++q) {
+    const size_t base = (size_t)min(q, a.ksplit - 1) * stride;
+    v1[q] = a.P[base + c];
+    v2[q] = a.P[base + c + half];
   }
+  const RowInfo ri = a.rows[m];
+  double cs = 1.0, sn = 0.0;
+  if (hh < a.H + a.KVH) sincos((double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), &sn, &cs);
+  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);  // RMSNorm of the input row
+  float x1 = 0.f, x2 = 0.f;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    x1 += q < a.ksplit ? v1[q] : 0.f;
+    x2 += q < a.ksplit ? v2[q] : 0.f;
+  }
+  for (int sp = 16; sp < a.ksplit; ++sp) {
+    x1 += a.P[(size_t)sp * stride + c];
+    x2 += a.P[(size_t)sp * stride + c + half];
+  }
+  x1 *= sc;
+  x2 *= sc;
+  float y1 = x1, y2 = x2;
   if (hh < a.H + a.KVH) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const double cs = s_cs[i + e], sn = s_sn[i + e];
-      y1[e] = (float)((double)x1[e] * cs - (double)x2[e] * sn);
-      y2[e] = (float)((double)x2[e] * cs + (double)x1[e] * sn);
-    }
+    y1 = (float)((double)x1 * cs - (double)x2 * sn);
+    y2 = (float)((double)x2 * cs + (double)x1 * sn);
   }
   if (hh < a.H) {
-    const size_t o = ((size_t)m * a.H + hh) * a.hd + i;
+    const size_t o = ((size_t)m * a.H + hh) * a.hd + j;
     if constexpr (sizeof(T) == 2) {
       // Q as bf16 hi (truncated) + lo (rounded) terms for the attention MFMAs
-      uint16_t h1[4], h2[4], l1[4], l2[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t u1 = __float_as_uint(y1[e]) >> 16, u2 = __float_as_uint(y2[e]) >> 16;
-        h1[e] = (uint16_t)u1;
-        h2[e] = (uint16_t)u2;
-        l1[e] = f2bf(y1[e] - __uint_as_float(u1 << 16));
-        l2[e] = f2bf(y2[e] - __uint_as_float(u2 << 16));
-      }
-      *(uint2*)(a.q_hi + o) = make_uint2(h1[0] | ((uint32_t)h1[1] << 16), h1[2] | ((uint32_t)h1[3] << 16));
-      *(uint2*)(a.q_hi + o + half) = make_uint2(h2[0] | ((uint32_t)h2[1] << 16), h2[2] | ((uint32_t)h2[3] << 16));
-      *(uint2*)(a.q_lo + o) = make_uint2(l1[0] | ((uint32_t)l1[1] << 16), l1[2] | ((uint32_t)l1[3] << 16));
-      *(uint2*)(a.q_lo + o + half) = make_uint2(l2[0] | ((uint32_t)l2[1] << 16), l2[2] | ((uint32_t)l2[3] << 16));
+      const uint32_t u1 = __float_as_uint(y1) >> 16, u2 = __float_as_uint(y2) >> 16;
+      a.q_hi[o] = (uint16_t)u1;
+      a.q_hi[o + half] = (uint16_t)u2;
+      a.q_lo[o] = f2bf(y1 - __uint_as_float(u1 << 16));
+      a.q_lo[o + half] = f2bf(y2 - __uint_as_float(u2 << 16));
     } else {
       float* q = (float*)a.q_hi;
-      *(float4*)(q + o) = make_float4(y1[0], y1[1], y1[2], y1[3]);
-      *(float4*)(q + o + half) = make_float4(y2[0], y2[1], y2[2], y2[3]);
+      q[o] = y1;
+      q[o + half] = y2;
     }
     return;
   }
@@ -180,18 +166,12 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
   T* pool = (T*)a.pool;
   if (hh < a.H + a.KVH) {
     const int gk = hh - a.H;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + e)] = from_f<T>(y1[e]);
-      pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, i + e + half)] = from_f<T>(y2[e]);
-    }
+    pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, j)] = from_f<T>(y1);
+    pool[k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gk, t, j + half)] = from_f<T>(y2);
   } else {
     const int gv = hh - a.H - a.KVH;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + e)] = from_f<T>(y1[e]);
-      pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, i + e + half)] = from_f<T>(y2[e]);
-    }
+    pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, j)] = from_f<T>(y1);
+    pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, j + half)] = from_f<T>(y2);
   }
 }
 
@@ -326,12 +306,11 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
-  const int threads = (a.H + 2 * a.KVH) * (a.hd / 8);
-  const dim3 grid(a.M, (threads + 255) / 256);
+  const dim3 grid(a.M, a.H + 2 * a.KVH);
   if (bf16)
-    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, grid, dim3(64), 0, s, a);
   else
-    hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(64), 0, s, a);
 }
 
 void launch_decide(const DecideArgs& a, hipStream_t s) {
