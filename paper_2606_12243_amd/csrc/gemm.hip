@@ -152,27 +152,66 @@ __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_
 #undef TILE_LOAD_W
 }
 
-// fp32 tile on the vector ALUs (X fragments with one fp32 term).
+// fp32 tile on the vector ALUs (X fragments with one fp32 term): rows
+// m0 .. m0+16*MB, columns c0 .. c0+ncols (ncols <= kTileN), K range
+// [k_beg, k_end), written to lds[r * ldc + c].  Thread t owns column
+// t % kTileN and every other 8-wide K group (t / kTileN selects which); the
+// 8 consecutive weights of a column and K group are 32 contiguous bytes of
+// the packed layout (two float4 loads), used for the 16 rows of a row block
+// (row blocks run one after another, so 16 accumulators suffice).  The two
+// halves are added in LDS, half 0 + half 1, so the order is fixed.
 template <int MB>
-__device__ void tile_f32(const GemmArgs& a, int c0, int m0, int k_beg, int k_end, float* lds) {
-  const float* W = (const float*)a.W;
-  const float* X = (const float*)a.X;
-  const size_t steps = a.K >> 5;
-  for (int e = threadIdx.x; e < 16 * MB * kTileN; e += kThreads) {
-    const int r = e / kTileN, c = e - r * kTileN;
-    const int m = m0 + r, col = c0 + c;
-    float acc = 0.f;
-    if (m < a.M && col < a.N) {
-      // packed weight element (col, k): group ((tile*steps + k/32)*4 + nb)*64 + ((k%32)/8)*16 + col%16
-      const size_t base = (size_t)(col >> 6) * steps * 4 * 64 + ((col & 63) >> 4) * 64 + (col & 15);
-      for (int k = k_beg; k < k_end; ++k) {
-        const float xv = X[afrag_group(0, m, k & ~7, (int)steps, a.MBn) * 8 + (k & 7)];
-        acc = fmaf(xv, W[(base + (size_t)(k >> 5) * 256 + ((k & 31) >> 3) * 16) * 8 + (k & 7)], acc);
+__device__ void tile_f32(const GemmArgs& a, int c0, int m0, int k_beg, int k_end, float* lds, int ncols = kTileN,
+                         int ldc = kTileN) {
+  static_assert(kThreads == 2 * kTileN, "two threads per column");
+  const float4* W = (const float4*)a.W;
+  const float4* X = (const float4*)a.X;
+  const int steps = a.K >> 5;
+  const int c = threadIdx.x % kTileN, part = threadIdx.x / kTileN;
+  const int col = c0 + c;
+  const bool live = c < ncols && col < a.N;
+  // group of (col, k) in the packed layout: wbase + (k/32) * 256 + ((k%32)/8) * 16
+  const size_t wbase = (size_t)(col >> 6) * steps * 256 + ((col & 63) >> 4) * 64 + (col & 15);
+#pragma unroll 1
+  for (int mb = 0; mb < MB; ++mb) {
+    const int r0 = m0 + mb * 16;
+    if (r0 >= a.M) break;  // uniform
+    const int nr = min(16, a.M - r0);
+    float acc[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    if (live) {
+      for (int kg = (k_beg >> 3) + part; kg < (k_end >> 3); kg += 2) {
+        const size_t wg = wbase + (size_t)(kg >> 2) * 256 + (kg & 3) * 16;
+        const float4 w0 = W[wg * 2], w1 = W[wg * 2 + 1];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          if (r >= nr) break;  // uniform
+          const size_t xg = afrag_group(0, r0 + r, kg * 8, steps, a.MBn);
+          const float4 x0 = X[xg * 2], x1 = X[xg * 2 + 1];
+          float t = acc[r];
+          t = fmaf(x0.x, w0.x, t);
+          t = fmaf(x0.y, w0.y, t);
+          t = fmaf(x0.z, w0.z, t);
+          t = fmaf(x0.w, w0.w, t);
+          t = fmaf(x1.x, w1.x, t);
+          t = fmaf(x1.y, w1.y, t);
+          t = fmaf(x1.z, w1.z, t);
+          t = fmaf(x1.w, w1.w, t);
+          acc[r] = t;
+        }
       }
     }
-    lds[e] = acc;
+    float* o = lds + (size_t)mb * 16 * ldc + c;
+    if (part == 1 && c < ncols)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[r * ldc] = acc[r];
+    __syncthreads();
+    if (part == 0 && c < ncols)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[r * ldc] = acc[r] + o[r * ldc];
+    __syncthreads();
   }
-  __syncthreads();
 }
 
 // (max, argmax, second) merge with lowest-index tie break
@@ -326,21 +365,7 @@ __global__ __launch_bounds__(kThreads) void gemm_gate_up(GemmArgs a) {
         for (int r = 0; r < 4; ++r) lds[(mb * 16 + g * 4 + r) * kCols + wave * 16 + n] = acc[0][mb][r];
     }
   } else {
-    const float* W = (const float*)a.W;
-    const float* X = (const float*)a.X;
-    const int steps = a.K >> 5;
-    for (int e = threadIdx.x; e < 16 * MB * ncol; e += kThreads) {
-      const int r = e / ncol, c = e - r * ncol, m = m0 + r, col = blk0 * 16 + c;
-      float s = 0.f;
-      if (m < a.M) {
-        const size_t base = (size_t)(col >> 6) * steps * 256 + ((col & 63) >> 4) * 64 + (col & 15);
-        for (int k = 0; k < a.K; ++k) {
-          const float xv = X[afrag_group(0, m, k & ~7, steps, a.MBn) * 8 + (k & 7)];
-          s = fmaf(xv, W[(base + (size_t)(k >> 5) * 256 + ((k & 31) >> 3) * 16) * 8 + (k & 7)], s);
-        }
-      }
-      lds[r * kCols + c] = s;
-    }
+    tile_f32<MB>(a, blk0 * 16, m0, 0, a.K, lds, ncol, kCols);
   }
   __syncthreads();
   const int ngroups = ncol >> 4;

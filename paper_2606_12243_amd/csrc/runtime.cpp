@@ -70,7 +70,7 @@ Dims dims_of(const via_model_desc* d) {
   r.qkv = (r.H + 2 * r.KVH) * r.hd;
   r.G = r.H / std::max(1, r.KVH);
   const bool f32 = d->dtype != VIA_DTYPE_BF16;
-  auto shape = [&](int N, int K) { return GemmShape{N, K, f32 ? 1 : choose_ksplit(N, K)}; };
+  auto shape = [&](int N, int K) { return GemmShape{N, K, choose_ksplit(N, K)}; };
   r.g_qkv = shape(r.qkv, r.d);
   r.g_o = shape(r.d, r.H * r.hd);
   r.g_gu = GemmShape{2 * r.F, r.d, 1};  // full K per work-group (SwiGLU epilogue)

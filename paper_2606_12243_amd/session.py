@@ -101,7 +101,7 @@ class Session:
         self.tokens.pop(seq, None)
 
     def lag(self, seq):
-        vf, _ = self.kv.seq_info(seq, via.CACHE_FULL)
+        vf = self.kv.valid_len(seq, via.CACHE_FULL)
         n = len(self.tokens[seq])
         return self.tokens[seq][vf:n - 1]
 
@@ -136,8 +136,10 @@ class Session:
     # ------------------------------------------------------------------ step
     def begin(self, drafts: dict):
         """Slim forward, decision, and the full forward where needed.
-        Returns (window, host decision, full ran per batch entry)."""
-        w = self.window(drafts, with_lag=True)
+        Returns (window, host decision, full ran per batch entry).  The slim
+        forward ignores lag rows; the window of the full forward (same rows)
+        carries them and is built only when some sequence escalates."""
+        w = self.window(drafts)
         self._w = w
         via.check(via.via_verify_slim(self.m.h, self.kv.h, C.byref(w.c), C.byref(self.p),
                                       C.byref(self.out_slim.c), self.sp()))
@@ -148,7 +150,8 @@ class Session:
         run = (h["status"] == 1).astype(np.int32)
         if run.any():
             r, rp = via._i32(run)
-            via.check(via.via_verify_full(self.m.h, self.kv.h, C.byref(w.c), rp, C.byref(self.p),
+            wl = self.window(drafts, with_lag=True)
+            via.check(via.via_verify_full(self.m.h, self.kv.h, C.byref(wl.c), rp, C.byref(self.p),
                                           C.byref(self.out_full.c), self.sp()))
             via.check(via.via_tier_decide(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c),
                                           C.byref(self.out_full.c), C.byref(self.dec.c), self.sp()))

@@ -254,6 +254,11 @@ class KV:
             check(via_kv_destroy(self.h))
             self.h = None
 
+    def valid_len(self, seq, cache):
+        valid, nb = C.c_int32(), C.c_int32()
+        check(via_kv_seq_info(self.h, seq, cache, C.byref(valid), None, 0, C.byref(nb)))
+        return valid.value
+
     def seq_info(self, seq, cache):
         valid, nb = C.c_int32(), C.c_int32()
         check(via_kv_seq_info(self.h, seq, cache, C.byref(valid), None, 0, C.byref(nb)))
