@@ -56,27 +56,47 @@ struct TileShape {
 
 // `active` (wave-uniform) false: the wave helps stage X but loads no
 // weights and multiplies nothing (its accumulators stay zero).
-template <int MB, int NT, int NBW, int C>
-__device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_end, uint4* sx,
-                          f32x4 (&acc)[NBW][MB], bool active = true) {
+//
+// M32 (two 16-column blocks per wave, an even number of row blocks): the
+// products run on v_mfma_f32_32x32x16_bf16, twice the rate of the 16x16x32
+// form on this GPU.  Its operands are gathered from the same 1 KB
+// fragments: lane l of a 32-row (or 32-column) x 16-K operand takes
+// row (column) l%32 -- block (l/16)%2 of the pair, row l%16 -- and K group
+// 2h + l/32 of the 32-wide step (half h), i.e. fragment lane
+// (2h + l/32)*16 + l%16.  acc is then f32x16[MB/2]: 32-row tile i holds
+// rows 32i + (r/4)*8 + (l/32)*4 + r%4, column l%32 of the wave's 32.
+template <int MB, int NT, int NBW, int C, bool M32 = false, typename Acc>
+__device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_end, uint4* sx, Acc& acc,
+                          bool active = true) {
   using TS = TileShape<MB, NT, NBW, C>;
   static_assert(TS::kXChunk % kThreads == 0, "chunk must split evenly over the threads");
+  static_assert(!M32 || (NBW == 2 && MB % 2 == 0), "32x32 tiles need two column blocks and row-block pairs");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int S = a.K >> 5;
   const int t64 = (a.N + 63) >> 6;
+  const int sel = (lane >> 4) & 1;                        // M32: block of the pair
+  const int fl = M32 ? ((lane >> 5) * 16 + (lane & 15)) : lane;  // M32: fragment lane of half 0
   const uint4* wt[NBW];
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
-    const int blk = (c0 >> 4) + wave * NBW + j;  // global 16-column block
+    // M32: wt[j] is K half j of the lane's block; otherwise block j, own lane
+    const int blk = (c0 >> 4) + wave * NBW + (M32 ? sel : j);  // global 16-column block
     const int pt = min(blk >> 2, t64 - 1);
-    wt[j] = (const uint4*)a.W + (size_t)pt * S * 256 + (blk & 3) * 64 + lane;
+    wt[j] = (const uint4*)a.W + (size_t)pt * S * 256 + (blk & 3) * 64 + (M32 ? fl + j * 32 : lane);
   }
   const uint4* xg = (const uint4*)a.X + (size_t)(m0 >> 4) * 64;
   const size_t x_step = (size_t)a.MBn * 64, x_term = (size_t)S * x_step;
+  if constexpr (M32) {
 #pragma unroll
-  for (int j = 0; j < NBW; ++j)
+    for (int i = 0; i < MB / 2; ++i)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  } else {
+#pragma unroll
+    for (int j = 0; j < NBW; ++j)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) acc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   const int nst = st_end - st_beg;
   if (nst <= 0) return;
   const int nch = (nst + C - 1) / C;
@@ -104,15 +124,29 @@ __device__ void tile_bf16(const GemmArgs& a, int c0, int m0, int st_beg, int st_
   }
 #define TILE_COMPUTE(w, ch)                                                 \
   if (active) {                                                             \
-    const uint4* xb = sx + ((ch) & 1) * TS::kXChunk + lane;                 \
     const int valid = nst - (ch) * C;                                       \
-    _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                      \
-      if (sc < valid) {                                                     \
-        _Pragma("unroll") for (int q = 0; q < NT; ++q)                      \
-        _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) {                 \
-          const uint4 xv = xb[((sc * NT + q) * MB + mb) * 64];              \
-          _Pragma("unroll") for (int j = 0; j < NBW; ++j)                   \
-            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xv), as_bf16x8(w[sc][j]), acc[j][mb], 0, 0, 0); \
+    if constexpr (M32) {                                                    \
+      const uint4* xb = sx + ((ch) & 1) * TS::kXChunk + sel * 64 + fl;      \
+      _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                    \
+        if (sc < valid) {                                                   \
+          _Pragma("unroll") for (int q = 0; q < NT; ++q)                    \
+          _Pragma("unroll") for (int i = 0; i < MB / 2; ++i)                \
+          _Pragma("unroll") for (int h = 0; h < 2; ++h) {                   \
+            const uint4 xv = xb[((sc * NT + q) * MB + 2 * i) * 64 + h * 32]; \
+            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(xv), as_bf16x8(w[sc][h]), acc[i], 0, 0, 0); \
+          }                                                                 \
+        }                                                                   \
+      }                                                                     \
+    } else {                                                                \
+      const uint4* xb = sx + ((ch) & 1) * TS::kXChunk + lane;               \
+      _Pragma("unroll") for (int sc = 0; sc < C; ++sc) {                    \
+        if (sc < valid) {                                                   \
+          _Pragma("unroll") for (int q = 0; q < NT; ++q)                    \
+          _Pragma("unroll") for (int mb = 0; mb < MB; ++mb) {               \
+            const uint4 xv = xb[((sc * NT + q) * MB + mb) * 64];            \
+            _Pragma("unroll") for (int j = 0; j < NBW; ++j)                 \
+              acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xv), as_bf16x8(w[sc][j]), acc[j][mb], 0, 0, 0); \
+          }                                                                 \
         }                                                                   \
       }                                                                     \
     }                                                                       \
@@ -289,7 +323,33 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& a) {
   const int m0 = mg * 16 * MB, c0 = tile * kTileN;
   const int steps = a.K >> 5, per = (steps + a.ksplit - 1) / a.ksplit;
   const int st_beg = min(steps, split * per), st_end = min(steps, (split + 1) * per);
-  if constexpr (sizeof(T) == 2) {
+  if constexpr (sizeof(T) == 2 && MB % 2 == 0 && NBW == 2) {
+    // 32x32x16 MFMAs: tile i, register r of lane l is row 32i + (r/4)*8 + (l/32)*4 + r%4,
+    // column wave*32 + l%32 of the work-group's tile
+    f32x16 acc[MB / 2];
+    tile_bf16<MB, NT, NBW, C, true>(a, c0, m0, st_beg, st_end, (uint4*)smem, acc);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int cl = wave * 32 + (lane & 31), rl = (lane >> 5) * 4;
+    if constexpr (STATS) {
+      __syncthreads();  // the X buffers become the output tile
+#pragma unroll
+      for (int i = 0; i < MB / 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) lds[(i * 32 + (r >> 2) * 8 + rl + (r & 3)) * kTileN + cl] = acc[i][r];
+      __syncthreads();
+      epi_stats<MB>(a, tile, m0, lds);
+    } else {
+      float* P = a.part + (size_t)split * a.M * a.N;
+      const int col = c0 + cl;
+#pragma unroll
+      for (int i = 0; i < MB / 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + i * 32 + (r >> 2) * 8 + rl + (r & 3);
+          if (m < a.M && col < a.N) P[(size_t)m * a.N + col] = acc[i][r];
+        }
+    }
+  } else if constexpr (sizeof(T) == 2) {
     f32x4 acc[NBW][MB];
     tile_bf16<MB, NT, NBW, C>(a, c0, m0, st_beg, st_end, (uint4*)smem, acc);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, n = lane & 15, g = lane >> 4;
