@@ -116,7 +116,7 @@ typedef struct {
 /* KV handle description.  Two paged caches: the full verifier's (n_layers
  * layer slots) and the slim-verifier's (one slot per retained layer, in
  * route order).  Pool layout, element type = model dtype, block_size = 16:
- *   pool[slot][block][K|V][kv_head][...]
+ *   pool[slot][kv_head][block][K|V][...]   (a head's pages of consecutive blocks adjacent)
  *   K page: [head_dim/8][16 tokens][8]    (dim groups of 8, token-major within)
  *   V page: [head_dim][16 tokens]         (transposed)
  * Cache slot p of a sequence lives in block table[p / 16], row p % 16.

@@ -1,31 +1,38 @@
-// Draft-window attention over the paged KV cache.
+// Draft-window attention over the paged KV cache (scaled dot-product
+// attention of every fed row against the visible cache slots).
 //
 // Queries of one KV head are packed across the GQA group: a work item holds
-// up to 64 (row, head-in-group) queries of one sequence, processed as two
-// sets of 32, so every K/V byte a work-group streams serves all query heads
-// that share it.  Keys are split into chunks of kAttnChunk slots (one
-// work-group each, split-KV); a combine kernel merges the per-chunk (max,
-// sum, output) partials in chunk order.  Visibility of slot p for row r:
+// up to 32 (row, head-in-group) queries of one sequence (one MFMA column
+// block), so every K/V byte a work-group streams serves all query heads that
+// share it.  Work-groups are dispatched round-robin over the 8 XCDs in
+// linear order and the item index is the grid's slowest, so when splits x
+// KV heads is a multiple of 8 the items of a sequence that share a (KV head,
+// split) run on one XCD and their repeated K/V reads can hit its L2.  The keys of a sequence are split into spans of `span` keys (a
+// multiple of 32 the host picks so that the whole launch has about one
+// work-group per compute unit); a work-group streams its span and writes
+// one (max, sum, output) partial per query, and a combine kernel merges the
+// partials of a query in split order.  Visibility of slot p for row r:
 // p < vis_len[r], or p is a window slot whose bit is set in the row's tree
 // mask.
 //
-// bf16 path (four waves per work-group, v_mfma_f32_32x32x16_bf16; each wave
-// issues all loads of its two 32-key blocks at once and keeps them in
-// registers for both query sets; per set, a wave computes the scores of
-// both blocks, so its softmax max is final before any P.V product, and the
-// four waves' (max, sum, output) are merged in LDS in wave order):
-//   S^T = K Q^T: A = 32 keys x hd (keys as rows, so each lane owns one
-//     query column and 16 keys: the softmax row statistics need only the
-//     lane itself and its partner lane l^32); B = Q^T staged in LDS;
+// bf16 path: four waves per work-group; wave w takes the 32-key blocks
+// w, w+4, ... of the span and streams them with the loads of its next block
+// in flight while the current one is multiplied (online softmax per wave,
+// the four waves merged in a fixed order at the end).  Both products run on
+// v_mfma_f32_32x32x16_bf16:
+//   S^T = K Q^T: A = 32 keys x 16 dims (keys as rows, so each lane owns one
+//     query column and 16 keys; the row statistics of a query need only the
+//     lane and its partner l^32); B = Q^T staged in LDS;
 //   O^T += V^T P^T: B = P^T straight from the S^T registers, A = V^T read
-//     from the transposed V pages (16 contiguous bytes per lane);
+//     from the transposed V pages (16 contiguous bytes per lane).
 //   A-row m of the K tile holds key pi(m) = (m/16)*16 + ((m/4)%2)*8 +
-//     ((m/8)%2)*4 + m%4, which makes register r of S^T hold key
-//     (r/8)*16 + (l/32)*8 + r%8: the 8-key groups the PV step consumes.
-//   Q (fp32) and P are fed to the MFMA as bf16 hi + lo terms (two
-//   products each), so both keep ~16 significant bits; K and V are the
-//   cache's bf16 values, exact operands.  Partial maxima are in log2 units.
-// fp32 path: one wave per (row, head), keys streamed with an online softmax.
+//     ((m/8)%2)*4 + m%4 of the block, which makes register r of lane l hold
+//     key (r/8)*16 + (l/32)*8 + r%8: the B-operand slice of the PV step r/8.
+//   Q (fp32) and P are fed as bf16 hi + lo terms (two products each), so
+//     both keep ~16 significant bits; K and V are the cache's bf16 values,
+//     exact operands.  Maxima are kept in log2 units.
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace via {
@@ -42,257 +49,314 @@ __device__ __forceinline__ bool key_visible(int key, int kv_len, const RowInfo& 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
+__device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+// K and V operands of one 32-key block (block b of the work-group's span).
 template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a) {
-  constexpr int KS = HD / 32;                // 32-dim contraction steps of S^T
-  constexpr int NDB = HD / 16;               // 16-row d blocks of O^T
-  constexpr int BPW = kAttnChunk / 4 / 32;   // 32-key blocks per wave
-  constexpr int QSETS = kAttnQueries / 16;   // 16-query sets per item
-  const AttnItem si = a.items[blockIdx.z];
-  const int chunk = blockIdx.x;
-  if (chunk >= si.n_chunks) return;
-  const int g = blockIdx.y;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, grp = lane >> 4;
-  const int G = a.H / a.KVH;
-  const int nq = min(kAttnQueries, si.n_rows * G - si.q0);
-  const int nsets = (nq + 15) >> 4;  // work-group uniform
-  const uint16_t* pool = (const uint16_t*)a.pool;
-  const int last_blk = si.n_blocks - 1;
+struct KvRegs {
+  uint4 k[HD / 16];     // S-step ks: key pi(l%32), dims ks*16 + (l/32)*8 .. +7
+  uint4 v[HD / 32][2];  // d tile dt, PV step t: dim dt*32 + l%32, keys t*16 + (l/32)*8 .. +7
+};
 
-  // Q hi/lo terms in the B-operand layout of S^T = K Q^T, [set][term][step][lane]:
-  // lane (c, grp) holds query c of the set, dims step*32 + grp*8 .. +7, so
-  // each ds_read of a wave is one contiguous 1 KB block.
-  __shared__ uint4 sq[QSETS][2][KS][64];
-  __shared__ float4 sh_o[4][NDB][64];  // the four waves' unscaled outputs
-  __shared__ float sh_m[4][64], sh_l[4][64];
-  constexpr int QPT = QSETS * 2 * KS * 64 / 256;  // staged uint4 per thread
-  static_assert(QPT % QSETS == 0, "a thread's staged entries of one set must share a wave-uniform set index");
-  uint4 qst[QPT];
-#pragma unroll
-  for (int u = 0; u < QPT; ++u) {
-    const int e = threadIdx.x + u * 256;
-    const int l = e & 63, ks = (e >> 6) % KS, term = (e / (64 * KS)) & 1, set = e / (128 * KS);
-    qst[u] = make_uint4(0, 0, 0, 0);
-    if (set < nsets) {  // uniform across the work-group for a given u
-      const int qi = si.q0 + set * 16 + (l & 15);
-      const int rl = qi / G;
-      const bool ok = rl < si.n_rows;
-      const int rw = si.row_start + (ok ? rl : 0), hh = g * G + (qi - rl * G);
-      const uint16_t* src = term ? a.q_lo : (const uint16_t*)a.q_hi;
-      const uint4 v = *(const uint4*)(src + ((size_t)rw * a.H + hh) * HD + ks * 32 + (l >> 4) * 8);
-      qst[u] = ok ? v : make_uint4(0, 0, 0, 0);
-    }
-  }
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// K/V are read once per forward: streamed past the caches (nontemporal)
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
 
-  // This wave's keys: two 32-key blocks.  K tile h (16 keys) of block j has
-  // A-row m = key pi_h(m) = (m/4)*8 + h*4 + m%4 of the block, which makes the
-  // S^T registers of lane (c, grp) hold keys grp*8 .. grp*8+7 of the block:
-  // exactly the contraction slice of the P^T operand of the PV product.
-  const int kw = chunk * kAttnChunk + wave * (BPW * 32);
-  const int k_end = min(si.kv_len, chunk * kAttnChunk + kAttnChunk);
-  const int nb = kw >= k_end ? 0 : min(BPW, (k_end - kw + 31) / 32);  // wave-uniform
-  uint4 kr[BPW][2][KS], vr[BPW][NDB];
+template <int HD>
+__device__ __forceinline__ void load_block(KvRegs<HD>& r, const uint16_t* pool, const AttnArgs& a, int g,
+                                           const int* spage, int b, int ql, int half) {
+  const int m = ql;
+  const int key = ((m >> 4) << 4) + (((m >> 2) & 1) << 3) + (((m >> 3) & 1) << 2) + (m & 3);
+  const uint4* kp =
+      (const uint4*)(pool + k_off(a.layer_slot, spage[2 * b + (key >> 4)], a.pool_blocks, a.KVH, HD, g, key & 15, half * 8));
 #pragma unroll
-  for (int j = 0; j < BPW; ++j) {
-    if (j >= nb) break;
-    const int kb = kw + j * 32;
+  for (int ks = 0; ks < HD / 16; ++ks) r.k[ks] = load_stream(kp + ks * 2 * kBlock);  // dim group 2*ks + half
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int key = kb + (c >> 2) * 8 + h * 4 + (c & 3);
-      const int blk = a.btab[si.bt + min(key / kBlock, last_blk)];
-      const uint4* kp = (const uint4*)(pool + k_off(a.layer_slot, blk, a.pool_blocks, a.KVH, HD, g, key % kBlock, grp * 8));
+  for (int t = 0; t < 2; ++t) {
+    const uint4* vp =
+        (const uint4*)(pool + v_off(a.layer_slot, spage[2 * b + t], a.pool_blocks, a.KVH, HD, g, half * 8, ql));
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kr[j][h][ks] = kp[ks * 4 * kBlock];  // dim group ks*4 + grp
-    }
-    const int vkey = kb + grp * 8;
-    const int vblk = a.btab[si.bt + min(vkey / kBlock, last_blk)];
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      vr[j][db] = *(const uint4*)(pool + v_off(a.layer_slot, vblk, a.pool_blocks, a.KVH, HD, g, vkey % kBlock, db * 16 + c));
+    for (int dt = 0; dt < HD / 32; ++dt) r.v[dt][t] = load_stream(vp + dt * 32 * kBlock / 8);
   }
+}
+
+// The lane's query (lane % 32 of the work item's 32).
+struct QueryState {
+  bool valid;
+  int row, head, vis;
+  uint64_t mask;
+};
+
+template <int HD>
+__device__ __forceinline__ void compute_block(KvRegs<HD>& r, int kb, const AttnItem& it, const QueryState& qs,
+                                              const uint4 (*sq)[HD / 16][64], int lane, int half, float sl2,
+                                              f32x16 (&o)[HD / 32], float& mrun, float& lrun) {
+  constexpr int KS = HD / 16, DT = HD / 32;
+  if (kb + 32 > it.kv_len) {  // zero V of keys past the written slots (their page rows may hold anything)
 #pragma unroll
-  for (int u = 0; u < QPT; ++u) {
-    const int e = threadIdx.x + u * 256;
-    sq[e / (128 * KS)][(e / (64 * KS)) & 1][(e >> 6) % KS][e & 63] = qst[u];
-  }
-  // zero V of keys past the written slots (their page rows may hold anything)
+    for (int t = 0; t < 2; ++t) {
+      const int valid8 = it.kv_len - (kb + t * 16 + half * 8);
 #pragma unroll
-  for (int j = 0; j < BPW; ++j) {
-    if (j >= nb) break;
-    const int valid8 = si.kv_len - (kw + j * 32 + grp * 8);
+      for (int dt = 0; dt < DT; ++dt) {
+        uint32_t w[4];
+        __builtin_memcpy(w, &r.v[dt][t], 16);
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      uint32_t w[4];
-      __builtin_memcpy(w, &vr[j][db], 16);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t keep = (2 * q + 1 < valid8 ? 0xFFFF0000u : 0u) | (2 * q < valid8 ? 0xFFFFu : 0u);
-        w[q] &= keep;
+        for (int q = 0; q < 4; ++q)
+          w[q] &= (2 * q + 1 < valid8 ? 0xFFFF0000u : 0u) | (2 * q < valid8 ? 0xFFFFu : 0u);
+        __builtin_memcpy(&r.v[dt][t], w, 16);
       }
-      __builtin_memcpy(&vr[j][db], w, 16);
     }
   }
-  const float sl2 = a.scale * 1.4426950408889634f;
-
-  // fully unrolled over the compile-time set count: the rolled form of this
-  // loop was compiled to code that produced wrong outputs from the second
-  // set on (an all-sets harness against an fp64 reference showed it)
+  // Q is re-read from LDS for every block rather than held in registers
+  // (which the register budget of two work-groups per compute unit does not
+  // allow): an opaque zero keeps the compiler from hoisting the reads
+  int zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+  {
+    f32x16 s;
 #pragma unroll
-  for (int set = 0; set < QSETS; ++set) {
-    if (set >= nsets) break;
-    __syncthreads();  // Q staged; the previous set's readers of sh_* are done
-    const int qi = si.q0 + set * 16 + c;
-    const int rloc = qi / G;
-    const bool qvalid = rloc < si.n_rows;
-    const int row = si.row_start + (qvalid ? rloc : 0);
-    const int head = g * G + (qi - rloc * G);
-    const RowInfo ri = a.rows[row];
-
-    f32x4 sacc[BPW][2];
-#pragma unroll
-    for (int j = 0; j < BPW; ++j)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) sacc[j][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 16; ++i) s[i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const uint4 qh = sq[set][0][ks][lane], ql = sq[set][1][ks][lane];
-#pragma unroll
-      for (int j = 0; j < BPW; ++j) {
-        if (j >= nb) break;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          sacc[j][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[j][h][ks]), as_bf16x8(qh), sacc[j][h], 0, 0, 0);
-          sacc[j][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[j][h][ks]), as_bf16x8(ql), sacc[j][h], 0, 0, 0);
-        }
-      }
+      s = mfma32(r.k[ks], sq[0][ks][lane + zero], s);
+      s = mfma32(r.k[ks], sq[1][ks][lane + zero], s);
     }
     // masked scores become -inf; the max is taken on unscaled scores (scale > 0)
-    float m_raw = -INFINITY;
+    const bool full = __all(!qs.valid || (kb + 32 <= qs.vis && kb + 32 <= it.kv_len));
+    if (!full) {
+      RowInfo ri;
+      ri.vis_len = qs.vis;
+      ri.mask = qs.mask;
 #pragma unroll
-    for (int j = 0; j < BPW; ++j) {
-      if (j >= nb) break;
-      const int kb = kw + j * 32;
-      // a block every key of which is visible to every valid query skips the masks
-      const bool full = __all(!qvalid || (kb + 32 <= ri.vis_len && kb + 32 <= si.kv_len));
-      if (!full) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int key = kb + grp * 8 + h * 4 + r;
-            if (!(qvalid && key_visible(key, si.kv_len, ri, si.win_base))) sacc[j][h][r] = -INFINITY;
-          }
+      for (int i = 0; i < 16; ++i) {
+        const int key = kb + (i >> 3) * 16 + half * 8 + (i & 7);
+        if (!(qs.valid && key_visible(key, it.kv_len, ri, it.win_base))) s[i] = -INFINITY;
       }
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) m_raw = fmaxf(m_raw, sacc[j][h][r]);
     }
-    m_raw = fmaxf(m_raw, __shfl_xor(m_raw, 16, 64));
-    m_raw = fmaxf(m_raw, __shfl_xor(m_raw, 32, 64));
-    const float m_run = m_raw * sl2;                        // log2 units (-inf stays -inf)
-    const float neg_m = m_run == -INFINITY ? 0.f : -m_run;  // all-masked query: every p is 0
-
-    float l_run = 0.f;
-    f32x4 o[NDB];
+    float bm = s[0];
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 1; i < 16; ++i) bm = fmaxf(bm, s[i]);
+    bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+    const float mn = fmaxf(mrun, bm * sl2);  // log2 units; -inf stays -inf
+    if (__any(mn > mrun)) {
+      const float alpha = mn == mrun ? 1.f : __builtin_amdgcn_exp2f(mrun - mn);
 #pragma unroll
-    for (int j = 0; j < BPW; ++j) {
-      if (j >= nb) break;
-      // P = 2^(s * scale * log2(e) - max') as bf16 hi (truncated) + lo (rounded) terms
+      for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+      lrun *= alpha;
+      mrun = mn;
+    }
+    const float neg_m = mrun == -INFINITY ? 0.f : -mrun;  // nothing visible yet: every p is 0
+    // P = 2^(s * scale * log2(e) - max) as bf16 hi (truncated) + lo (rounded) terms
+    uint4 ph[2], pl[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
       uint32_t hw[4], lw[4];
 #pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[j][e2 >> 1][(e2 & 1) * 2], sl2, neg_m));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[j][e2 >> 1][(e2 & 1) * 2 + 1], sl2, neg_m));
-        l_run += p0;
-        l_run += p1;
-        hw[e2] = __builtin_amdgcn_perm(__float_as_uint(p1), __float_as_uint(p0), 0x07060302u);
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[t * 8 + 2 * e], sl2, neg_m));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[t * 8 + 2 * e + 1], sl2, neg_m));
+        lrun += p0;
+        lrun += p1;
+        hw[e] = __builtin_amdgcn_perm(__float_as_uint(p1), __float_as_uint(p0), 0x07060302u);
         const float r0 = p0 - __uint_as_float(__float_as_uint(p0) & 0xFFFF0000u);
         const float r1 = p1 - __uint_as_float(__float_as_uint(p1) & 0xFFFF0000u);
         const bf16x2 lo = {(__bf16)r0, (__bf16)r1};
-        lw[e2] = __builtin_bit_cast(uint32_t, lo);
+        lw[e] = __builtin_bit_cast(uint32_t, lo);
       }
-      const uint4 hv = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-      const uint4 lv = make_uint4(lw[0], lw[1], lw[2], lw[3]);
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[j][db]), as_bf16x8(hv), o[db], 0, 0, 0);
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[j][db]), as_bf16x8(lv), o[db], 0, 0, 0);
-      }
+      ph[t] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      pl[t] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
     }
-    l_run += __shfl_xor(l_run, 16, 64);
-    l_run += __shfl_xor(l_run, 32, 64);
-
-    // merge the four waves' (max, sum, output) in wave order; wave w
-    // finishes d blocks w*NDB/4 .. of the set's partials
-    sh_m[wave][lane] = m_run;
-    sh_l[wave][lane] = l_run;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) sh_o[wave][db][lane] = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
-    __syncthreads();
-    float mw[4], cw[4];
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int w = 0; w < 4; ++w) mw[w] = sh_m[w][lane];
-    const float M = fmaxf(fmaxf(mw[0], mw[1]), fmaxf(mw[2], mw[3]));
-#pragma unroll
-    for (int w = 0; w < 4; ++w) cw[w] = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[w] - M);
-    if (qvalid) {
-      // O^T lane (c, grp), register r -> query c, d = db*16 + grp*4 + r
-      float* po = a.part_o + (((size_t)chunk * a.M + row) * a.H + head) * HD;
-#pragma unroll
-      for (int dd = 0; dd < NDB / 4; ++dd) {
-        const int db = wave * (NDB / 4) + dd;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float4 v = sh_o[w][db][lane];
-          acc.x += v.x * cw[w];
-          acc.y += v.y * cw[w];
-          acc.z += v.z * cw[w];
-          acc.w += v.w * cw[w];
-        }
-        *(float4*)(po + db * 16 + grp * 4) = acc;
+      for (int dt = 0; dt < DT; ++dt) {
+        o[dt] = mfma32(r.v[dt][t], ph[t], o[dt]);
+        o[dt] = mfma32(r.v[dt][t], pl[t], o[dt]);
       }
-      if (wave == 0 && grp == 0) {
-        float L = 0.f;
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnArgs a) {
+  constexpr int KS = HD / 16, DT = HD / 32;
+  const AttnItem it = a.items[blockIdx.z];
+  const int split = blockIdx.x;
+  if (split >= it.n_chunks) return;
+  const int g = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, ql = lane & 31, half = lane >> 5;
+  const int G = a.H / a.KVH;
+  const int k0 = split * a.span;
+  const int k1 = min(it.kv_len, k0 + a.span);
+  const int nblk = (k1 - k0 + 31) >> 5;  // 32-key blocks of the span
+  const uint16_t* pool = (const uint16_t*)a.pool;
+
+  __shared__ int spage[kAttnMaxSpan / kBlock];
+  __shared__ uint4 sq[2][KS][64];  // Q hi/lo terms in the B-operand layout of S^T = K Q^T
+  __shared__ float mo[2][DT * 16][64];    // wave merge: unscaled outputs, max, sum
+  __shared__ float mm[2][64], ml[2][64];
+
+  for (int t = threadIdx.x; t < 2 * nblk; t += 256) spage[t] = a.btab[it.bt + min((k0 >> 4) + t, it.n_blocks - 1)];
+  constexpr int QPT = 2 * KS * 64 / 256;  // staged uint4 per thread
 #pragma unroll
-        for (int w = 0; w < 4; ++w) L += sh_l[w][lane] * cw[w];
-        float* pm = a.part_ml + (((size_t)chunk * a.M + row) * a.H + head) * 2;
-        pm[0] = M;
-        pm[1] = L;
+  for (int u = 0; u < QPT; ++u) {
+    const int e = threadIdx.x + u * 256;
+    const int l = e & 63, ks = (e >> 6) % KS, term = e / (64 * KS);
+    const int qi = it.q0 + (l & 31);
+    const int rl = qi / G;
+    const bool ok = rl < it.n_rows;
+    const int rw = it.row_start + (ok ? rl : 0), hh = g * G + (qi - rl * G);
+    const uint16_t* src = term ? a.q_lo : (const uint16_t*)a.q_hi;
+    const uint4 v = *(const uint4*)(src + ((size_t)rw * a.H + (ok ? hh : 0)) * HD + ks * 16 + (l >> 5) * 8);
+    sq[term][ks][l] = ok ? v : make_uint4(0, 0, 0, 0);
+  }
+  QueryState qs;
+  {
+    const int qi = it.q0 + ql;
+    const int rl = qi / G;
+    qs.valid = rl < it.n_rows;
+    qs.row = it.row_start + (qs.valid ? rl : 0);
+    qs.head = g * G + (qi - rl * G);
+    const RowInfo ri = a.rows[qs.row];
+    qs.vis = ri.vis_len;
+    qs.mask = ri.mask;
+  }
+  __syncthreads();
+
+  const float sl2 = a.scale * 1.4426950408889634f;
+  f32x16 o[DT];
+  float mrun = -INFINITY, lrun = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[dt][i] = 0.f;
+  // wave w streams blocks w, w+4, ...: two register sets, the next block's
+  // loads in flight while the current one is multiplied.  The load past the
+  // wave's last block re-reads that block (an L2 hit) so that every load is
+  // unconditional and the waits stay exact.
+  const int cnt = nblk > wave ? (nblk - wave + 3) >> 2 : 0;
+  if (cnt > 0) {
+    auto blk = [&](int i) { return wave + 4 * min(i, cnt - 1); };
+    KvRegs<HD> r0, r1;
+    load_block<HD>(r0, pool, a, g, spage, blk(0), ql, half);
+    for (int i = 0; i < cnt; i += 2) {
+      load_block<HD>(r1, pool, a, g, spage, blk(i + 1), ql, half);
+      compute_block<HD>(r0, k0 + blk(i) * 32, it, qs, sq, lane, half, sl2, o, mrun, lrun);
+      if (i + 1 >= cnt) break;
+      load_block<HD>(r0, pool, a, g, spage, blk(i + 2), ql, half);
+      compute_block<HD>(r1, k0 + blk(i + 1) * 32, it, qs, sq, lane, half, sl2, o, mrun, lrun);
+    }
+  }
+
+  // merge the four waves in a fixed order: (w0 + w2) + (w1 + w3)
+  float lt = lrun + __shfl_xor(lrun, 32, 64);
+  float mx = mrun;
+  auto merge_from = [&](int buf) {
+    const float mb = mm[buf][lane], lb = ml[buf][lane];
+    const float M = fmaxf(mx, mb);
+    const float ca = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mx - M);
+    const float cb = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mb - M);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[dt][i] = o[dt][i] * ca + mo[buf][dt * 16 + i][lane] * cb;
+    lt = lt * ca + lb * cb;
+    mx = M;
+  };
+  auto store_to = [&](int buf) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mo[buf][dt * 16 + i][lane] = o[dt][i];
+    mm[buf][lane] = mx;
+    ml[buf][lane] = lt;
+  };
+  if (wave >= 2) store_to(wave - 2);
+  __syncthreads();
+  if (wave < 2) merge_from(wave);
+  __syncthreads();
+  if (wave == 1) store_to(0);
+  __syncthreads();
+  if (wave == 0) {
+    merge_from(0);
+    if (qs.valid) {
+      // O^T lane l, register i of d tile dt -> dim dt*32 + (i/4)*8 + (l/32)*4 + i%4
+      float* po = a.part_o + (((size_t)split * a.M + qs.row) * a.H + qs.head) * HD;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4)
+          *(float4*)(po + dt * 32 + i4 * 8 + half * 4) =
+              make_float4(o[dt][4 * i4], o[dt][4 * i4 + 1], o[dt][4 * i4 + 2], o[dt][4 * i4 + 3]);
+      if (half == 0) {
+        float* pm = a.part_ml + (((size_t)split * a.M + qs.row) * a.H + qs.head) * 2;
+        pm[0] = mx;
+        pm[1] = lt;
       }
     }
   }
 }
 
+// Merge the split partials of each query in split order and write the
+// normalised output as activation fragments.  Work-group: QPW queries of
+// one item and KV head, HD/8 threads per query (8 dims each).
+template <int HD>
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
-  __shared__ float o_s[128];
-  const int row = blockIdx.x, head = blockIdx.y, d = threadIdx.x;
-  const RowInfo ri = a.rows[row];
-  const SeqInfo si = a.seqs[ri.seq];
-  const int nch = (si.kv_len + kAttnChunk - 1) / kAttnChunk;
-  float M = -INFINITY;
-#pragma unroll 4
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, a.part_ml[(((size_t)c * a.M + row) * a.H + head) * 2]);
-  float L = 0.f, O = 0.f;
-#pragma unroll 4
-  for (int c = 0; c < nch; ++c) {
-    const float* pm = a.part_ml + (((size_t)c * a.M + row) * a.H + head) * 2;
-    const float w = exp2f(pm[0] - M);  // partial maxima are in log2 units
-    const float ov = d < a.hd ? a.part_o[(((size_t)c * a.M + row) * a.H + head) * a.hd + d] : 0.f;
-    L += pm[1] * w;
-    O += ov * w;
-  }
-  if (d < a.hd) o_s[d] = O / L;
-  __syncthreads();
-  if (d < a.hd / 8) {
-    float v[8];
+  constexpr int TPQ = HD / 8, QPW = 128 / TPQ, GROUPS = kAttnQueries / QPW;
+  const AttnItem it = a.items[blockIdx.x / GROUPS];
+  const int g = blockIdx.y, G = a.H / a.KVH;
+  const int qi = it.q0 + (blockIdx.x % GROUPS) * QPW + threadIdx.x / TPQ, d0 = (threadIdx.x % TPQ) * 8;
+  const int rl = qi / G;
+  if (qi - it.q0 >= kAttnQueries || rl >= it.n_rows) return;
+  const int row = it.row_start + rl, head = g * G + (qi - rl * G);
+  const int n = it.n_chunks;
+  const size_t stride_ml = (size_t)a.M * a.H * 2, stride_o = (size_t)a.M * a.H * HD;
+  const float* pml = a.part_ml + ((size_t)row * a.H + head) * 2;
+  const float* po = a.part_o + ((size_t)row * a.H + head) * HD + d0;
+  float2 ml[kAttnMaxSplits];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = o_s[d * 8 + e];
-    put_afrag<true, 2>(a.out, row, head * a.hd + d * 8, v, (a.H * a.hd) >> 5, a.MBn);
+  for (int c = 0; c < kAttnMaxSplits; ++c)
+    if (c < n) ml[c] = *(const float2*)(pml + c * stride_ml);
+  float M = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < kAttnMaxSplits; ++c)
+    if (c < n) M = fmaxf(M, ml[c].x);
+  float L = 0.f, O[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) O[e] = 0.f;
+#pragma unroll
+  for (int c0 = 0; c0 < kAttnMaxSplits; c0 += 8) {
+    if (c0 >= n) break;
+    float4 v[8][2];
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      if (c0 + c < n) {
+        v[c][0] = *(const float4*)(po + (c0 + c) * stride_o);
+        v[c][1] = *(const float4*)(po + (c0 + c) * stride_o + 4);
+      }
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      if (c0 + c < n) {
+        const float w = __builtin_amdgcn_exp2f(ml[c0 + c].x - M);  // partial maxima are in log2 units
+        L += ml[c0 + c].y * w;
+        O[0] += v[c][0].x * w;
+        O[1] += v[c][0].y * w;
+        O[2] += v[c][0].z * w;
+        O[3] += v[c][0].w * w;
+        O[4] += v[c][1].x * w;
+        O[5] += v[c][1].y * w;
+        O[6] += v[c][1].z * w;
+        O[7] += v[c][1].w * w;
+      }
   }
+  const float inv = 1.f / L;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) O[e] *= inv;
+  put_afrag<true, 2>(a.out, row, head * HD + d0, O, (a.H * HD) >> 5, a.MBn);
 }
 
 // fp32: one wave per (row, head); lane holds head_dim/64 dims.
@@ -344,11 +408,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {
   if (bf16) {
     dim3 grid(a.max_chunks, a.KVH, a.n_items);
-    if (a.hd == 128)
-      hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(256), 0, s, a);
-    else
-      hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, a);
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.M, a.H), dim3(128), 0, s, a);
+    if (a.hd == 128) {
+      hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_items * (kAttnQueries / 8), a.KVH), dim3(128), 0, s, a);
+    } else {
+      hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(a.n_items * (kAttnQueries / 16), a.KVH), dim3(128), 0, s, a);
+    }
   } else {
     dim3 grid(a.M, a.H);
     if (a.hd == 128)
@@ -356,6 +422,27 @@ void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {
     else
       hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(64), 0, s, a);
   }
+}
+
+int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int target_groups, AttnArgs& at) {
+  long long blocks = 0;
+  int max_kv = 0;
+  for (int i = 0; i < n_items; ++i) {
+    blocks += (long long)KVH * ((items[i].kv_len + 31) / 32);
+    max_kv = std::max(max_kv, items[i].kv_len);
+  }
+  long long per = std::max<long long>(1, (blocks + target_groups - 1) / target_groups);
+  int span = (int)std::min<long long>(per * 32, kAttnMaxSpan);
+  const int need = ((max_kv + 31) / 32 + max_splits - 1) / max_splits * 32;  // at most max_splits splits
+  span = std::max(span, need);
+  if (span > kAttnMaxSpan) return -1;
+  at.span = span;
+  at.max_chunks = 0;
+  for (int i = 0; i < n_items; ++i) {
+    items[i].n_chunks = (items[i].kv_len + span - 1) / span;
+    at.max_chunks = std::max(at.max_chunks, items[i].n_chunks);
+  }
+  return 0;
 }
 
 }  // namespace via

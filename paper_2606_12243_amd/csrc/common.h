@@ -11,8 +11,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;        // tokens per KV page
 constexpr int kMaxChildren = 8;   // drafts verified by one row
-constexpr int kAttnChunk = 256;   // keys per attention work-group (split-KV chunk)
-constexpr int kAttnQueries = 64;  // (row, head-in-group) queries per attention work-group
+constexpr int kAttnMaxSplits = 32;  // key splits per sequence (partials one query's combine merges)
+constexpr int kAttnMaxSpan = 8192;  // keys of one split (pages of a split's work-group, x16)
+constexpr int kAttnTargetGroups = 256;  // attention work-groups a forward aims for (one per compute unit)
+constexpr int kAttnQueries = 32;  // (row, head-in-group) queries per attention work-group
 constexpr int kNormChunk = 512;   // columns per partial sum of squares (RMSNorm)
 
 // One fed row of a forward (lag row or window row).
@@ -40,7 +42,7 @@ struct SeqInfo {
 // sequence, with the sequence's cache geometry inlined.
 struct AttnItem {
   int32_t q0;       // first query (row * G + g) of the tile, within the sequence
-  int32_t n_chunks; // key chunks of this sequence
+  int32_t n_chunks; // key splits of this sequence: ceil(kv_len / span)
   int32_t kv_len, row_start, n_rows, win_base, bt, n_blocks;
 };
 
@@ -88,17 +90,21 @@ struct PoolRef {
 
 __device__ __forceinline__ size_t page_elems(int kvh, int hd) { return (size_t)kvh * kBlock * hd; }
 
-// Element offset of K[layer_slot][block][g] token t, dim i.  K pages are
-// dim-group-major, [hd/8][16 tokens][8]: the 16-byte pieces of one dim
-// group of a page's 16 tokens are contiguous, so an MFMA operand load of 16
-// tokens x 8 dims reads 256 contiguous bytes.
+// Pool layout: [layer_slot][kv_head g][block][K page | V page].  A KV
+// head's pages of consecutive blocks are adjacent, so attention over a
+// sequence whose blocks were allocated in order streams one contiguous
+// region per (layer, head).
+// Element offset of K token t, dim i.  K pages are dim-group-major,
+// [hd/8][16 tokens][8]: the 16-byte pieces of one dim group of a page's 16
+// tokens are contiguous, so an MFMA operand load of 16 tokens x 8 dims reads
+// 256 contiguous bytes.
 __device__ __forceinline__ size_t k_off(int slot, int block, int nblk, int kvh, int hd, int g, int t, int i) {
-  return ((((size_t)slot * nblk + block) * 2 + 0) * kvh + g) * (size_t)(kBlock * hd) +
+  return ((((size_t)slot * kvh + g) * nblk + block) * 2 + 0) * (size_t)(kBlock * hd) +
          ((size_t)(i >> 3) * kBlock + t) * 8 + (i & 7);
 }
-// Element offset of V[layer_slot][block][g][i][t] (transposed page)
+// Element offset of V token t, dim i: the V page is transposed, [hd][16 tokens]
 __device__ __forceinline__ size_t v_off(int slot, int block, int nblk, int kvh, int hd, int g, int t, int i) {
-  return ((((size_t)slot * nblk + block) * 2 + 1) * kvh + g) * (size_t)(kBlock * hd) + (size_t)i * kBlock + t;
+  return ((((size_t)slot * kvh + g) * nblk + block) * 2 + 1) * (size_t)(kBlock * hd) + (size_t)i * kBlock + t;
 }
 
 // Activation fragments: the GEMM input X [M, K] as the matrix cores read it.

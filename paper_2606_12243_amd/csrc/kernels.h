@@ -110,15 +110,21 @@ struct AttnArgs {
   const SeqInfo* seqs;
   const int32_t* btab;
   const AttnItem* items;
-  int n_items, max_chunks;
+  int n_items, max_chunks; // max_chunks: most splits of any item (grid x)
+  int span;                // keys per split (a multiple of 32)
   int M, H, KVH, hd;
   float scale;             // 1/sqrt(hd)
-  float* part_o;           // [max_chunks][M][H][hd]
-  float* part_ml;          // [max_chunks][M][H][2]
+  float* part_o;           // [split][M][H][hd]
+  float* part_ml;          // [split][M][H][2]: max (log2 units), sum
   void* out;               // activation fragments of [M, H * hd] (2 bf16 terms, or fp32)
   int MBn;
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
+// Host: pick the split span for a forward's attention items (about
+// target_groups work-groups over all items and KV heads, at most max_splits
+// splits per sequence), set every item's n_chunks and at.span,
+// at.max_chunks.  Returns -1 if a sequence needs a span above kAttnMaxSpan.
+int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int target_groups, AttnArgs& at);
 
 // Tree compaction: copy K/V of slot src -> dst for every layer slot.
 struct KvMove {

@@ -117,7 +117,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
     if (gemm_is_prefill(es == 2, (int)R)) part = std::max(part, R * g.N * 4);
   }
   L.part = take(part);
-  L.max_chunks = ceil_div(max_blocks * kBlock, kAttnChunk);
+  L.max_chunks = std::min(kAttnMaxSplits, ceil_div(max_blocks * kBlock, 32));
   L.att_o = take((size_t)L.max_chunks * R * D.H * D.hd * 4);
   L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
   L.lm_part = take((size_t)gemm_tiles(D.V) * R * 4 * 4);
@@ -334,6 +334,10 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   if (M == 0) return VIA_OK;
   if (M > kv->d.max_rows) return fail(VIA_EINVAL, "forward of %d rows exceeds max_rows %d", M, kv->d.max_rows);
   if ((int)P.items.size() > L.max_items) return fail(VIA_EINVAL, "too many attention tiles");
+  // key splits of the attention items: about one work-group per compute unit
+  AttnArgs at{};
+  if (plan_attention(P.items.data(), (int)P.items.size(), D.KVH, L.max_chunks, kAttnTargetGroups, at))
+    return fail(VIA_EINVAL, "a sequence is too long for %d attention splits", L.max_chunks);
   // one upload of the plan: its parts packed back to back (256-byte aligned)
   // at the start of the plan region, which has room for the largest plan
   const size_t o_rows = 0;
@@ -395,7 +399,6 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   const int ss_stride = kv->d.max_rows;
   launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
   launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], Yf, MBn, nullptr, ss, ss_stride, s);
-  AttnArgs at{};
   at.q_hi = Q;
   at.q_lo = Qlo;
   at.pool = pool;
@@ -405,8 +408,6 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   at.btab = d_btab;
   at.items = (const AttnItem*)(plan + o_items);
   at.n_items = (int)P.items.size();
-  at.max_chunks = 0;
-  for (const AttnItem& it : P.items) at.max_chunks = std::max(at.max_chunks, it.n_chunks);
   at.M = M;
   at.H = D.H;
   at.KVH = D.KVH;
@@ -671,7 +672,7 @@ via_status build_verify_plan(via_kv* kv, int cache, const WinCopy& w, const std:
     P.seqs.push_back(si);
     const int nq = si.n_rows * D.G;
     for (int q0 = 0; q0 < nq; q0 += kAttnQueries)
-      P.items.push_back(AttnItem{q0, ceil_div(si.kv_len, kAttnChunk), si.kv_len, si.row_start, si.n_rows, si.win_base,
+      P.items.push_back(AttnItem{q0, 0, si.kv_len, si.row_start, si.n_rows, si.win_base,
                                  si.bt, si.n_blocks});
   }
   return VIA_OK;
@@ -1023,7 +1024,7 @@ via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* 
       }
       P.seqs.push_back(si);
       for (int q0 = 0; q0 < si.n_rows * G; q0 += kAttnQueries)
-        P.items.push_back(AttnItem{q0, ceil_div(c1, kAttnChunk), si.kv_len, si.row_start, si.n_rows, si.win_base,
+        P.items.push_back(AttnItem{q0, 0, si.kv_len, si.row_start, si.n_rows, si.win_base,
                                    si.bt, si.n_blocks});
       if ((st = exec_forward(m, kv, cache, P, false, nullptr, 1.f, s))) {
         trim_blocks(kv, 0, seq_id, 0);

@@ -91,10 +91,10 @@ class Session:
                     K = torch.cat([K, torch.zeros((pad, KVH, hd), dtype=K.dtype, device=K.device)])
                     V = torch.cat([V, torch.zeros((pad, KVH, hd), dtype=V.dtype, device=V.device)])
                 # K page [hd/8][16 tokens][8], V page [hd][16 tokens]
-                Kp = K.view(nb, via.BLOCK, KVH, hd // 8, 8).permute(0, 2, 3, 1, 4).reshape(nb, KVH, via.BLOCK * hd)
-                Vp = V.view(nb, via.BLOCK, KVH, hd).permute(0, 2, 3, 1).reshape(nb, KVH, via.BLOCK * hd)
-                pv[s, :, 0].index_copy_(0, idx, Kp.contiguous())
-                pv[s, :, 1].index_copy_(0, idx, Vp.contiguous())
+                Kp = K.view(nb, via.BLOCK, KVH, hd // 8, 8).permute(2, 0, 3, 1, 4).reshape(KVH, nb, via.BLOCK * hd)
+                Vp = V.view(nb, via.BLOCK, KVH, hd).permute(2, 0, 3, 1).reshape(KVH, nb, via.BLOCK * hd)
+                pv[s, :, :, 0].index_copy_(1, idx, Kp.contiguous())
+                pv[s, :, :, 1].index_copy_(1, idx, Vp.contiguous())
 
     def release(self, seq):
         via.check(via.via_kv_seq_release(self.kv.h, seq))

@@ -276,12 +276,12 @@ class KV:
         return n.value, ms.value
 
     def pool_view(self, cache):
-        """Pool as [slots, blocks, 2, KVH, 16*hd]: K page [hd/8][16][8], V page [hd][16]."""
+        """Pool as [slots, KVH, blocks, 2, 16*hd]: K page [hd/8][16][8], V page [hd][16]."""
         m = self.model.desc
         slots = m["n_layers"] if cache == CACHE_FULL else len(self.model.route)
         nb = self.cd.blocks_full if cache == CACHE_FULL else self.cd.blocks_slim
         t = self.pool_full if cache == CACHE_FULL else self.pool_slim
-        return t.view(slots, nb, 2, m["n_kv_heads"], BLOCK * m["head_dim"])
+        return t.view(slots, m["n_kv_heads"], nb, 2, BLOCK * m["head_dim"])
 
 
 class WindowBuf:
