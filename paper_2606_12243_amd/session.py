@@ -157,6 +157,7 @@ class Session:
                                           C.byref(self.out_full.c), C.byref(self.dec.c), self.sp()))
             self.stream.synchronize()
             h = self._host(w)
+        self._h = h
         return w, h, run
 
     def _host(self, w):
@@ -173,8 +174,11 @@ class Session:
             hp = self.dec.h_packed.numpy()
             hp[:B], hp[B:2 * B], hp[2 * B:3 * B], hp[3 * B:4 * B] = h["status"], h["kappa"], h["emit"], h["new_len"]
             hp[4 * B:4 * B + B * D] = np.asarray(h["path"], np.int32).reshape(-1)
+        elif getattr(self, "_w", None) is w and getattr(self, "_h", None) is not None:
+            h = self._h  # the decision begin() read back for this window
         else:
             h = self._host(w)
+        self._h = None
         via.check(via.via_kv_commit_rollback(self.kv.h, C.byref(self.dec.c), self.sp()))
         for b, s in enumerate(w.a["seq"].tolist()):
             if h["status"][b] != 0:

@@ -69,10 +69,11 @@ class KvDesc(C.Structure):
 
 
 class Window(C.Structure):
+    # host pointers (int32 arrays; row_mask uint64), passed as addresses
     _fields_ = [("batch", I32), ("max_rows", I32), ("max_drafts", I32), ("max_lag", I32),
-                ("seq_id", PI32), ("n_rows", PI32), ("row_tok", PI32), ("row_depth", PI32),
-                ("row_mask", C.POINTER(C.c_uint64)), ("n_drafts", PI32), ("draft_tok", PI32),
-                ("draft_row", PI32), ("draft_parent", PI32), ("n_lag", PI32), ("lag_tok", PI32)]
+                ("seq_id", P), ("n_rows", P), ("row_tok", P), ("row_depth", P),
+                ("row_mask", P), ("n_drafts", P), ("draft_tok", P),
+                ("draft_row", P), ("draft_parent", P), ("n_lag", P), ("lag_tok", P)]
 
 
 class VerifyOut(C.Structure):
@@ -285,43 +286,64 @@ class KV:
 
 
 class WindowBuf:
-    """Host arrays of a via_window (kept alive with the struct)."""
+    """Host arrays of a via_window (kept alive with the struct).  Every int32
+    field lives in one buffer (the tree masks in a uint64 one), filled from
+    Python lists and converted once: per-step cost matters, the window is
+    built on the step's critical path."""
 
     def __init__(self, seq_ids, rows, drafts, draft_rows, parents=None, depths=None, masks=None,
                  lags=None, max_rows=None, max_drafts=None):
         B = len(seq_ids)
         self.B = B
-        self.max_rows = max_rows or max(len(r) for r in rows)
-        self.max_drafts = max_drafts or max(1, max(len(d) for d in drafts))
-        self.max_lag = max(1, max((len(l) for l in lags), default=1)) if lags else 1
-        R, D, Lg = self.max_rows, self.max_drafts, self.max_lag
-        self.a = {}
-
-        def grid(lists, width, fill=0, dtype=np.int32):
-            g = np.full((B, width), fill, dtype=dtype)
-            for b, l in enumerate(lists):
-                g[b, :len(l)] = l
-            return g.reshape(-1)
-
-        self.a["seq"] = np.asarray(seq_ids, np.int32)
-        self.a["n_rows"] = np.asarray([len(r) for r in rows], np.int32)
-        self.a["row_tok"] = grid(rows, R)
-        self.a["n_drafts"] = np.asarray([len(d) for d in drafts], np.int32)
-        self.a["draft_tok"] = grid(drafts, D)
-        self.a["draft_row"] = grid(draft_rows, D)
+        self.max_rows = R = max_rows or max(len(r) for r in rows)
+        self.max_drafts = D = max_drafts or max(1, max(len(d) for d in drafts))
+        self.max_lag = Lg = max(1, max((len(l) for l in lags), default=1)) if lags else 1
         tree = parents is not None
+        spec = [("seq", B), ("n_rows", B), ("row_tok", B * R), ("n_drafts", B), ("draft_tok", B * D),
+                ("draft_row", B * D)]
         if tree:
-            self.a["draft_parent"] = grid(parents, D, -1)
-            self.a["row_depth"] = grid(depths, R)
-            self.a["row_mask"] = grid(masks, R, 0, np.uint64)
+            spec += [("draft_parent", B * D), ("row_depth", B * R)]
         if lags is not None:
-            self.a["n_lag"] = np.asarray([len(l) for l in lags], np.int32)
-            self.a["lag_tok"] = grid(lags, Lg)
-        g = lambda k: self.a[k].ctypes.data_as(PI32) if k in self.a else None
-        self.c = Window(B, R, D, Lg, g("seq"), g("n_rows"), g("row_tok"), g("row_depth"),
-                        self.a["row_mask"].ctypes.data_as(C.POINTER(C.c_uint64)) if tree else None,
-                        g("n_drafts"), g("draft_tok"), g("draft_row"), g("draft_parent"), g("n_lag"),
-                        g("lag_tok"))
+            spec += [("n_lag", B), ("lag_tok", B * Lg)]
+        off, o = {}, 0
+        for name, n in spec:
+            off[name] = o
+            o += n
+        buf = [0] * o
+
+        def put(name, lists, width):
+            base = off[name]
+            for b, l in enumerate(lists):
+                buf[base + b * width: base + b * width + len(l)] = l
+
+        buf[0:B] = seq_ids
+        buf[off["n_rows"]:off["n_rows"] + B] = [len(r) for r in rows]
+        put("row_tok", rows, R)
+        buf[off["n_drafts"]:off["n_drafts"] + B] = [len(d) for d in drafts]
+        put("draft_tok", drafts, D)
+        put("draft_row", draft_rows, D)
+        if tree:
+            buf[off["draft_parent"]:off["draft_parent"] + B * D] = [-1] * (B * D)
+            put("draft_parent", parents, D)
+            put("row_depth", depths, R)
+        if lags is not None:
+            buf[off["n_lag"]:off["n_lag"] + B] = [len(l) for l in lags]
+            put("lag_tok", lags, Lg)
+        arr = np.array(buf, np.int32)
+        self._buf = arr
+        self.a = {name: arr[off[name]:off[name] + n] for name, n in spec}
+        addr = arr.ctypes.data
+        ptr = lambda k: addr + 4 * off[k] if k in off else None
+        mask_ptr = None
+        if tree:
+            mk = [0] * (B * R)
+            for b, l in enumerate(masks):
+                mk[b * R: b * R + len(l)] = l
+            self.a["row_mask"] = np.array(mk, np.uint64)
+            mask_ptr = self.a["row_mask"].ctypes.data
+        self.c = Window(B, R, D, Lg, ptr("seq"), ptr("n_rows"), ptr("row_tok"), ptr("row_depth"), mask_ptr,
+                        ptr("n_drafts"), ptr("draft_tok"), ptr("draft_row"), ptr("draft_parent"), ptr("n_lag"),
+                        ptr("lag_tok"))
 
 
 class Out:
