@@ -628,6 +628,112 @@ VIA_GEMM_LAUNCH(gemm_down, 2)
 VIA_GEMM_LAUNCH(gemm_head, 2)
 #undef VIA_GEMM_LAUNCH
 
+
+// QKV, O and down projections of forwards of up to 32 rows (bf16): the
+// weight-streaming decomposition of the gate/up kernel with split-K partials.
+// A work-group owns a.nb 16-column blocks and K split blockIdx.y (a.ksplit
+// equal ranges of 32-wide steps); its 8 waves interleave the split's steps
+// (wave w takes steps w, w+8, ...) over all its blocks, loading X fragments
+// straight from global memory (each is used by one wave; they stay in L2)
+// and weights with non-temporal loads, one step ahead.  The 8 wave partial
+// tiles are summed in LDS in wave order and written to
+// a.part[split][M][N], which the consumer sums in split order.  Fewer,
+// longer splits than the LDS-staged kernels write a quarter of the partials.
+template <int MB, int NT>
+__global__ __launch_bounds__(kThreads) void gemm_ki_part(GemmArgs a) {
+  constexpr int NBM = kWaves;
+  __shared__ __align__(16) float red[kWaves][16 * MB][NBM * 16 + 4];
+  const int nblocks = a.N >> 4;
+  const int blk0 = blockIdx.x * a.nb;
+  const int split = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nb = min(a.nb, nblocks - blk0);
+  const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
+  const int per = (S + a.ksplit - 1) / a.ksplit;
+  const int s_beg = min(S, split * per), s_end = min(S, s_beg + per);
+  const uint4* wt[NBM];
+#pragma unroll
+  for (int j = 0; j < NBM; ++j) {
+    const int blk = blk0 + min(j, nb - 1);
+    wt[j] = (const uint4*)a.W + (size_t)min(blk >> 2, t64 - 1) * S * 256 + (blk & 3) * 64 + lane;
+  }
+  const uint4* xg = (const uint4*)a.X + lane;
+  const size_t x_step = (size_t)a.MBn * 64, x_term = (size_t)S * x_step;
+  f32x4 acc[NBM][MB];
+#pragma unroll
+  for (int j = 0; j < NBM; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nst = max(0, (s_end - s_beg - wave + kWaves - 1) / kWaves);  // steps of this wave
+  uint4 w[2][NBM], x[2][NT][MB];
+  // loads of the wave's i-th step into buffer `buf` (past the last step the
+  // last one is loaded again and never used)
+  auto load = [&](int buf, int i) {
+    const size_t st = (size_t)(s_beg + wave + min(i, nst - 1) * kWaves);
+#pragma unroll
+    for (int j = 0; j < NBM; ++j)
+      if (j < nb) w[buf][j] = load_stream(wt[j] + st * 256);
+#pragma unroll
+    for (int q = 0; q < NT; ++q)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) x[buf][q][mb] = xg[q * x_term + st * x_step + mb * 64];
+  };
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < NT; ++q)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < NBM; ++j)
+          if (j < nb)
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x[buf][q][mb]), as_bf16x8(w[buf][j]),
+                                                                 acc[j][mb], 0, 0, 0);
+  };
+  if (nst > 0) {
+    load(0, 0);
+    for (int i = 0; i < nst; i += 2) {
+      load(1, i + 1);
+      compute(0);
+      if (i + 1 >= nst) break;
+      load(0, i + 2);
+      compute(1);
+    }
+  }
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < NBM; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][mb * 16 + g * 4 + r][j * 16 + n] = acc[j][mb][r];
+  __syncthreads();
+  float* P = a.part + (size_t)split * a.M * a.N;
+  const int cols = nb * 16;
+  for (int e = threadIdx.x; e < 16 * MB * cols; e += kThreads) {
+    const int r = e / cols, c = e - r * cols;
+    if (r >= a.M) continue;
+    float v = 0.f;
+#pragma unroll
+    for (int wv = 0; wv < kWaves; ++wv) v += red[wv][r][c];
+    P[(size_t)r * a.N + blk0 * 16 + c] = v;
+  }
+}
+
+template <int NT>
+void launch_ki_part(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid(((a.N >> 4) + a.nb - 1) / a.nb, a.ksplit);
+  auto go = [&](auto kernel) {
+    if (e0)
+      hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, a);
+    else
+      hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a);
+  };
+  if (a.M <= 16)
+    go(gemm_ki_part<1, NT>);
+  else
+    go(gemm_ki_part<2, NT>);
+}
+
 template <typename T>
 void launch_role(GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (role) {
@@ -856,6 +962,17 @@ int gate_up_blocks_per_group(int F) {
 
 int gemm_tiles(int N) { return (N + kTileN - 1) / kTileN; }
 
+bool gemm_uses_ki(GemmRole role, int M, int N) {
+  return (role == GemmRole::kQkv || role == GemmRole::kO || role == GemmRole::kDown) && M <= 32 && N % 16 == 0;
+}
+
+void gemm_ki_plan(int N, int K, int* nb, int* ksplit) {
+  const int S = K / 32, blocks = N / 16;
+  const int ks = std::max(1, std::min(4, S / 32));  // at least 4 steps per wave in a split
+  *ksplit = ks;
+  *nb = std::max(1, std::min(kWaves, (blocks * ks + 255) / 256));
+}
+
 int gemm_rows_per_group(int M) {
   return M > 96 ? 128 : M > 64 ? 96 : M > 48 ? 64 : M > 32 ? 48 : M > 16 ? 32 : 16;
 }
@@ -876,6 +993,13 @@ void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hip
       const int n = a.M * (a.F >> 3);
       hipLaunchKernelGGL(swiglu_rows_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
     }
+    return;
+  }
+  if (bf16 && a.nb > 0 && gemm_uses_ki(role, a.M, a.N)) {
+    if (role == GemmRole::kQkv)
+      launch_ki_part<3>(a, s, e0, e1);
+    else
+      launch_ki_part<2>(a, s, e0, e1);
     return;
   }
   if (bf16)

@@ -54,6 +54,12 @@ bool gemm_is_prefill(bool bf16, int M);
 void launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
 // Column tiles (256 wide) of an N-column GEMM.
 int gemm_tiles(int N);
+// QKV, O and down projections of forwards of up to 32 rows (bf16 models, N a
+// multiple of 16) run on the K-interleaved split-K kernel, whose work-groups
+// own a.nb 16-column blocks of one of a.ksplit K splits; gemm_ki_plan picks
+// both for an [N, K] weight (about 256 work-groups).
+bool gemm_uses_ki(GemmRole role, int M, int N);
+void gemm_ki_plan(int N, int K, int* nb, int* ksplit);
 // Rows per GEMM work-group for M rows (16, 32, 48, 64, 96 or 128).
 int gemm_rows_per_group(int M);
 // Rows of the activation fragments for M rows: M padded to a multiple of

@@ -51,6 +51,8 @@ int choose_ksplit(int N, int K) {
 
 struct GemmShape {
   int N, K, ks;
+  GemmRole role;
+  int nb_ki, ks_ki;  // the K-interleaved kernel's blocks per work-group and splits (forwards of <= 32 rows)
 };
 
 struct Dims {
@@ -70,11 +72,15 @@ Dims dims_of(const via_model_desc* d) {
   r.qkv = (r.H + 2 * r.KVH) * r.hd;
   r.G = r.H / std::max(1, r.KVH);
   const bool f32 = d->dtype != VIA_DTYPE_BF16;
-  auto shape = [&](int N, int K) { return GemmShape{N, K, choose_ksplit(N, K)}; };
-  r.g_qkv = shape(r.qkv, r.d);
-  r.g_o = shape(r.d, r.H * r.hd);
-  r.g_gu = GemmShape{2 * r.F, r.d, 1};  // full K per work-group (SwiGLU epilogue)
-  r.g_down = shape(r.d, r.F);
+  auto shape = [&](int N, int K, GemmRole role) {
+    GemmShape g{N, K, choose_ksplit(N, K), role, 1, 1};
+    gemm_ki_plan(N, K, &g.nb_ki, &g.ks_ki);
+    return g;
+  };
+  r.g_qkv = shape(r.qkv, r.d, GemmRole::kQkv);
+  r.g_o = shape(r.d, r.H * r.hd, GemmRole::kO);
+  r.g_gu = GemmShape{2 * r.F, r.d, 1, GemmRole::kGateUp, 1, 1};  // full K per work-group (SwiGLU epilogue)
+  r.g_down = shape(r.d, r.F, GemmRole::kDown);
   return r;
 }
 
@@ -113,7 +119,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   // (prefill-sized) forwards write one partial of all their rows
   size_t part = 0;
   for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down}) {
-    part = std::max(part, (size_t)g.ks * std::min<size_t>(R, kPrefillMinRows) * g.N * 4);
+    part = std::max(part, (size_t)std::max(g.ks, g.ks_ki) * std::min<size_t>(R, kPrefillMinRows) * g.N * 4);
     if (gemm_is_prefill(es == 2, (int)R)) part = std::max(part, R * g.N * 4);
   }
   L.part = take(part);
@@ -381,7 +387,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
 
   // K splits of each projection's partials (one on the prefill GEMM)
   const bool prefill_gemm = gemm_is_prefill(bf, M);
-  auto ks = [&](const GemmShape& sh) { return prefill_gemm ? 1 : sh.ks; };
+  auto ki = [&](const GemmShape& sh) { return bf && gemm_uses_ki(sh.role, M, sh.N); };
+  auto ks = [&](const GemmShape& sh) { return prefill_gemm ? 1 : ki(sh) ? sh.ks_ki : sh.ks; };
   auto gemm = [&](const void* Xf, const void* W, const GemmShape& sh, GemmRole role, int kind) {
     GemmArgs g{};
     g.X = Xf;
@@ -391,6 +398,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     g.K = sh.K;
     g.N = sh.N;
     g.ksplit = ks(sh);
+    g.nb = ki(sh) ? sh.nb_ki : 0;
     g.part = part;
     timed_gemm(kv, kind, bf, role, g, s);
   };
