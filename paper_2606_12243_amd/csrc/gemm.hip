@@ -412,7 +412,24 @@ __global__ __launch_bounds__(kThreads) void gemm_gate_up(GemmArgs a) {
   const int m0 = blockIdx.y * 16 * MB;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int ncol = min(a.nb, nblocks - blk0) * 16;  // columns of this work-group
-  if constexpr (sizeof(T) == 2) {
+  if constexpr (sizeof(T) == 2 && MB % 2 == 0 && MB >= 4) {
+    // 64 or more rows: each wave owns a pair of blocks on 32x32x16 MFMAs, so
+    // every X fragment read from LDS serves 32 columns (a.nb even; waves past
+    // nb / 2 only stage X).  One block per wave makes the LDS reads of X the
+    // limit.
+    f32x16 acc[MB / 2];
+    const bool active = 2 * wave < a.nb && blk0 + 2 * wave < nblocks;
+    tile_bf16<MB, NT, 2, C, true>(a, blk0 * 16, m0, 0, a.K >> 5, (uint4*)smem, acc, active);
+    __syncthreads();  // the X buffers become the output tile
+    if (active) {
+      // tile i, register r of lane l: row 32i + (r/4)*8 + (l/32)*4 + r%4, column wave*32 + l%32
+      const int cl = wave * 32 + (lane & 31), rl = (lane >> 5) * 4;
+#pragma unroll
+      for (int i = 0; i < MB / 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) lds[(i * 32 + (r >> 2) * 8 + rl + (r & 3)) * kCols + cl] = acc[i][r];
+    }
+  } else if constexpr (sizeof(T) == 2) {
     f32x4 acc[1][MB];
     const bool active = wave < a.nb && blk0 + wave < nblocks;
     tile_bf16<MB, NT, 1, C>(a, blk0 * 16, m0, 0, a.K >> 5, (uint4*)smem, acc, active);
@@ -599,12 +616,15 @@ void launch_gemm_gate_up(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEve
   constexpr int NT = sizeof(T) == 2 ? 2 : 1;
   const int mb = gemm_rows_per_group(a.M) / 16;
   const int mgroups = (a.M + 16 * mb - 1) / (16 * mb);
-  const dim3 grid(((a.N >> 4) + a.nb - 1) / a.nb, mgroups);
+  GemmArgs b = a;
+  if (sizeof(T) == 2 && mb >= 4 && mb % 2 == 0)  // block pairs per wave: an even count, ~256 work-groups
+    b.nb = std::min(kWaves, 2 * std::max(1, ((a.N >> 4) + 511) / 512));
+  const dim3 grid(((b.N >> 4) + b.nb - 1) / b.nb, mgroups);
   auto go = [&](auto kernel) {
     if (e0)
-      hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, a);
+      hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, b);
     else
-      hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, b);
   };
   if constexpr (sizeof(T) == 2) {
     if (mb <= 2) {  // up to 32 rows: K-interleaved waves
@@ -619,7 +639,7 @@ void launch_gemm_gate_up(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEve
     case 1: go(gemm_gate_up<T, 1, chunk_steps<T, 1, NT, 1>()>); break;
     case 2: go(gemm_gate_up<T, 2, chunk_steps<T, 2, NT, 1>()>); break;
     case 3: go(gemm_gate_up<T, 3, chunk_steps<T, 3, NT, 1>()>); break;
-    case 4: go(gemm_gate_up<T, 4, chunk_steps<T, 4, NT, 1>()>); break;
+    case 4: go(gemm_gate_up<T, 4, chunk_steps<T, 4, NT, 2>()>); break;  // block pairs (bf16)
     case 6: go(gemm_gate_up<T, 6, chunk_steps<T, 6, NT, 1>()>); break;
     default: go(gemm_gate_up<T, 8, chunk_steps<T, 8, NT, 1>()>); break;
   }
