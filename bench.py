@@ -200,7 +200,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="8b_bf16_chain")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -257,8 +257,12 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
             "traffic": measured_traffic(args.config),
             "bytes_per_launch": dom_bytes, "avg_launch_us": round(avg_ms * 1e3, 2), "launches": n_launch}
-    step_roof = {"bytes": round(res["bytes"] / args.steps), "achieved_GBs": round(res["bytes"] / res["t_total"] / 1e9, 1),
-                 "frac": round(res["bytes"] / res["t_total"] / 1e9 / HBM_PEAK_GBS, 4)}
+    copy_gbs = measured_copy_gbs()
+    step_gbs = res["bytes"] / res["t_total"] / 1e9
+    step_roof = {"bytes": round(res["bytes"] / args.steps), "achieved_GBs": round(step_gbs, 1),
+                 "frac": round(step_gbs / HBM_PEAK_GBS, 4),
+                 "copy_kernel_GBs": round(copy_gbs, 1), "frac_of_copy_kernel": round(step_gbs / copy_gbs, 4)}
+    roof["frac_of_copy_kernel"] = round(achieved / copy_gbs, 4) if achieved else None
 
     # the same workload at T = 1, where every drafted position goes to the full verifier
     full_tier = None
@@ -310,6 +314,26 @@ def main():
     if breakdown:
         out["kernels"] = breakdown
     print(json.dumps(out), flush=True)
+
+
+def measured_copy_gbs(nbytes=1 << 30, reps=5):
+    """A plain device-to-device copy of 1 GiB (bytes read + bytes written per
+    second), the measured HBM ceiling the roofline fractions are also given
+    against."""
+    import torch
+    src = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
 def prefill_gemm_roofline(md, M, reps=10):

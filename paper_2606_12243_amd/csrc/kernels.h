@@ -78,8 +78,31 @@ int gate_up_blocks_per_group(int F);
 // rows[m].lm when `rows` is given (rows with lm < 0 skipped), and the sums of
 // x^2 over column chunks to ss[chunk * ss_stride + row]: the consumer of the
 // next projection multiplies its output row by row_scale() (RMSNorm).
+// Xcopy (nullable): the updated rows are also stored there ([M, d] fp32).
 void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
-                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s);
+                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s,
+                      float* Xcopy = nullptr);
+
+// One row of a full forward that starts after the P layers the slim route
+// shares with it (route layer i == i for i < P).
+struct PrefixXfer {
+  int32_t src_row;           // row of the same step's slim forward
+  int32_t t;                 // slot within the page (position % 16)
+  int32_t src_blk, dst_blk;  // page of the position in the slim and the full cache
+};
+struct PrefixArgs {
+  const PrefixXfer* xfer;  // [M]
+  int M, P, d, KVH, hd;
+  const float* Xpref;      // slim forward's residual stream after layer P - 1, [slim rows, d]
+  float* X;                // the full forward's residual stream [M, d]
+  const void* slim_pool;
+  int slim_blocks;
+  void* full_pool;
+  int full_blocks;
+};
+// K/V of layers 0..P-1 copied slim -> full cache at every row's position and
+// X[m] = Xpref[xfer[m].src_row].
+void launch_prefix_copy(bool bf16, const PrefixArgs& a, hipStream_t s);
 // Sum QKV partials, rotate-half RoPE at each row's position, Q -> fp32
 // buffer, K/V -> the paged cache (model dtype).
 struct QkvArgs {

@@ -66,7 +66,7 @@ __device__ __forceinline__ void split_sum2(const float* P, size_t stride, int ks
 template <typename G, bool BF16, int NT>
 __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P, int ksplit, int M, int d,
                                                        const G* g, void* Y, int MBn, const RowInfo* rows,
-                                                       float* ss, int ss_stride) {
+                                                       float* ss, int ss_stride, float* Xcopy) {
   const int m = blockIdx.y, chunk = blockIdx.x;
   const int k0 = chunk * kNormChunk + threadIdx.x * 8;
   const int out = rows ? rows[m].lm : m;
@@ -87,6 +87,7 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
         u.w = u.w + acc[h].w;
         *(float4*)(x + k0 + 4 * h) = u;
       }
+      if (Xcopy) *(float4*)(Xcopy + (size_t)m * d + k0 + 4 * h) = u;
       v[4 * h + 0] = u.x;
       v[4 * h + 1] = u.y;
       v[4 * h + 2] = u.z;
@@ -292,17 +293,17 @@ void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, f
 }
 
 void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
-                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s) {
+                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s, float* Xcopy) {
   const dim3 grid((d + kNormChunk - 1) / kNormChunk, M);
   if (!bf16)
     hipLaunchKernelGGL((resid_add_kernel<float, false, 1>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const float*)g, Y, MBn, rows, ss, ss_stride);
+                       (const float*)g, Y, MBn, rows, ss, ss_stride, Xcopy);
   else if (terms >= 3)
     hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 3>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride);
+                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy);
   else
     hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 2>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride);
+                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy);
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
@@ -326,6 +327,48 @@ void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KV
   else
     hipLaunchKernelGGL(kv_move_kernel<float>, dim3(1, n_slots), dim3(128), 0, s, (float*)pool, pool_blocks, KVH,
                        hd, btab, moves, n_moves);
+}
+
+
+namespace {
+
+// Full forward that starts after the layers it shares with the slim route
+// (route layer i == i for i < a.P): grid (M, P + 1).  y < P: the row's K and
+// V of layer y, copied from the slim cache (slot y) to the full cache (slot
+// y) at the row's position; y == P: the row's residual stream after layer
+// P - 1, taken from the slim forward of the same step.
+template <typename T>
+__global__ __launch_bounds__(256) void prefix_copy_kernel(PrefixArgs a) {
+  const int m = blockIdx.x, y = blockIdx.y;
+  const PrefixXfer x = a.xfer[m];
+  if (y == a.P) {
+    const float* src = a.Xpref + (size_t)x.src_row * a.d;
+    float* dst = a.X + (size_t)m * a.d;
+    for (int i = threadIdx.x; i < a.d; i += 256) dst[i] = src[i];
+    return;
+  }
+  const T* sp = (const T*)a.slim_pool;
+  T* dp = (T*)a.full_pool;
+  const int n = a.KVH * a.hd;
+  for (int e = threadIdx.x; e < 2 * n; e += 256) {
+    const int g = (e % n) / a.hd, i = e % a.hd;
+    if (e < n)
+      dp[k_off(y, x.dst_blk, a.full_blocks, a.KVH, a.hd, g, x.t, i)] =
+          sp[k_off(y, x.src_blk, a.slim_blocks, a.KVH, a.hd, g, x.t, i)];
+    else
+      dp[v_off(y, x.dst_blk, a.full_blocks, a.KVH, a.hd, g, x.t, i)] =
+          sp[v_off(y, x.src_blk, a.slim_blocks, a.KVH, a.hd, g, x.t, i)];
+  }
+}
+
+}  // namespace
+
+void launch_prefix_copy(bool bf16, const PrefixArgs& a, hipStream_t s) {
+  const dim3 grid(a.M, a.P + 1);
+  if (bf16)
+    hipLaunchKernelGGL(prefix_copy_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(prefix_copy_kernel<float>, grid, dim3(256), 0, s, a);
 }
 
 }  // namespace via

@@ -86,7 +86,8 @@ Dims dims_of(const via_model_desc* d) {
 
 struct Layout {
   size_t X, Yf, Q, Af, Hf, Ylf, part, att_o, att_ml, lm_part, ss;
-  size_t rows, seqs, btab, items, lm;  // plan region
+  size_t Xpref;                        // slim forward's residual stream after the shared layers
+  size_t rows, seqs, btab, items, lm, xfer;  // plan region
   size_t step_seqs, dtok, drow, dpar;  // step region
   size_t c_btab, c_moves;              // commit region
   size_t plan_bytes, step_bytes, commit_bytes;
@@ -128,6 +129,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
   L.lm_part = take((size_t)gemm_tiles(D.V) * R * 4 * 4);
   L.ss = take((size_t)ceil_div(D.d, kNormChunk) * R * 4);  // RMSNorm sums of squares [chunk][row]
+  L.Xpref = take(R * D.d * 4);
   L.max_items = ceil_div(max_rows * D.G, kAttnQueries) + max_batch;
   // plan region (one upload per forward)
   size_t p0 = o;
@@ -136,6 +138,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.btab = take((size_t)max_batch * max_blocks * 4);
   L.items = take((size_t)L.max_items * sizeof(AttnItem));
   L.lm = take(R * sizeof(LmRow));
+  L.xfer = take(R * sizeof(PrefixXfer));
   L.plan_bytes = o - p0;
   size_t s0 = o;
   L.step_seqs = take((size_t)max_batch * sizeof(StepSeq));
@@ -194,6 +197,8 @@ struct via_kv {
   std::set<int> free_[2];
   bool step_open = false;
   WinCopy win;
+  bool xpref_ok = false;      // the open step's slim forward saved its state after the shared layers
+  std::vector<int> slim_row0; // first row of each batch entry in that slim forward
   std::vector<int> step_n;  // committed length n per batch entry at step start
   bool sticky = false;
   hipEvent_t ev[kRing];
@@ -282,6 +287,7 @@ struct Plan {
   std::vector<int32_t> btab;
   std::vector<AttnItem> items;
   std::vector<LmRow> lm;
+  std::vector<PrefixXfer> xfer;  // forwards that start after the shared layers
   std::vector<char> blob;
 };
 
@@ -332,8 +338,20 @@ void put(std::vector<char>& blob, size_t off, const std::vector<T>& v) {
 }
 
 // Forward of one route over the planned rows; optional fused head.
+// Leading layers the slim route shares with the full model (route[i] == i):
+// the slim forward's state after them is the full model's.
+int shared_prefix(const via_model* m) {
+  int n = 0;
+  while (n < (int)m->route.size() && m->route[n] == n) ++n;
+  return n;
+}
+
+// start_si > 0: the forward begins at route position start_si from the
+// slim forward's saved state (P.xfer gives each row's source and pages);
+// save_prefix: store the residual stream after the shared layers (slim
+// forwards of a step).
 via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head, const via_verify_out* out,
-                        float inv_T, hipStream_t s) {
+                        float inv_T, hipStream_t s, int start_si = 0, bool save_prefix = false) {
   const Layout& L = kv->L;
   const Dims& D = m->D;
   const int M = (int)P.rows.size();
@@ -351,7 +369,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   const size_t o_btab = al(o_seqs + P.seqs.size() * sizeof(SeqInfo));
   const size_t o_items = al(o_btab + P.btab.size() * 4);
   const size_t o_lm = al(o_items + P.items.size() * sizeof(AttnItem));
-  const size_t plan_used = al(o_lm + P.lm.size() * sizeof(LmRow));
+  const size_t o_xfer = al(o_lm + P.lm.size() * sizeof(LmRow));
+  const size_t plan_used = al(o_xfer + P.xfer.size() * sizeof(PrefixXfer));
   if (plan_used > L.plan_bytes) return fail(VIA_EINVAL, "plan of %zu bytes exceeds its region", plan_used);
   std::vector<char> blob(plan_used);
   put(blob, o_rows, P.rows);
@@ -359,6 +378,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   put(blob, o_btab, P.btab);
   put(blob, o_items, P.items);
   put(blob, o_lm, P.lm);
+  put(blob, o_xfer, P.xfer);
   char* ws = kv->ws;
   char* plan = ws + L.rows;
   via_status st = upload(kv, plan, blob.data(), plan_used, s);
@@ -405,8 +425,28 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
 
   float* ss = (float*)(ws + L.ss);
   const int ss_stride = kv->d.max_rows;
-  launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
-  launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[0]], Yf, MBn, nullptr, ss, ss_stride, s);
+  const int n_shared = shared_prefix(m);
+  if (start_si > 0) {
+    if (start_si != n_shared || (int)P.xfer.size() != M || cache != VIA_CACHE_FULL)
+      return fail(VIA_EINVAL, "internal: forward from the shared layers without its row map");
+    PrefixArgs pa{};
+    pa.xfer = (const PrefixXfer*)(plan + o_xfer);
+    pa.M = M;
+    pa.P = start_si;
+    pa.d = D.d;
+    pa.KVH = D.KVH;
+    pa.hd = D.hd;
+    pa.Xpref = (const float*)(ws + L.Xpref);
+    pa.X = X;
+    pa.slim_pool = kv->d.pool_slim;
+    pa.slim_blocks = kv->d.blocks_slim;
+    pa.full_pool = kv->d.pool_full;
+    pa.full_blocks = kv->d.blocks_full;
+    launch_prefix_copy(bf, pa, s);
+  } else {
+    launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
+  }
+  launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[start_si]], Yf, MBn, nullptr, ss, ss_stride, s);
   at.q_hi = Q;
   at.q_lo = Qlo;
   at.pool = pool;
@@ -444,7 +484,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   qa.ss_stride = ss_stride;
   qa.d = D.d;
   qa.eps = eps;
-  for (size_t si = 0; si < route.size(); ++si) {
+  for (size_t si = start_si; si < route.size(); ++si) {
     const int l = route[si];
     // Q/K/V: three bf16 terms per activation (the K/V are rounded to the cache's bf16)
     gemm(Yf, m->w_qkv[l], D.g_qkv, GemmRole::kQkv, VIA_KERNEL_QKV);
@@ -475,7 +515,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
       launch_resid_add(bf, 3, X, part, ks(D.g_down), M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
-                       ss_stride, s);
+                       ss_stride, s, save_prefix && (int)si + 1 == n_shared ? (float*)(ws + L.Xpref) : nullptr);
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
@@ -725,7 +765,34 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   Plan P;
   std::vector<std::pair<int, int>> taken;
   if ((st = build_verify_plan(kv, cache, *wp, run, win, true, P, &taken))) return st;
-  st = exec_forward(m, kv, cache, P, true, out, 1.0f / p->temperature, s);
+  // The full forward of a step starts after the layers the slim route shares
+  // with it when no running sequence has lag rows: the slim forward of the
+  // step saved those rows' state, and their K/V of the shared layers are
+  // copied from the slim cache.
+  const int n_shared = shared_prefix(m);
+  const bool save = !probe && cache == VIA_CACHE_SLIM && n_shared > 0 && n_shared < (int)m->route.size();
+  int start_si = 0;
+  if (!probe && cache == VIA_CACHE_FULL && kv->xpref_ok && n_shared > 0) {
+    bool lag0 = true;
+    for (int b : run) {
+      const SeqSt& S = kv->seqs[wp->seq[b]];
+      lag0 = lag0 && S.valid[VIA_CACHE_FULL] == S.valid[VIA_CACHE_SLIM];
+    }
+    if (lag0) {
+      start_si = n_shared;
+      for (size_t q = 0; q < run.size(); ++q) {
+        const int b = run[q];
+        const SeqSt& S = kv->seqs[wp->seq[b]];
+        const SeqInfo& si = P.seqs[q];
+        for (int rr = 0; rr < si.n_rows; ++rr) {
+          const int pos = si.win_base + rr;
+          P.xfer.push_back(PrefixXfer{kv->slim_row0[b] + rr, pos % kBlock, S.table[VIA_CACHE_SLIM][pos / kBlock],
+                                      S.table[VIA_CACHE_FULL][pos / kBlock]});
+        }
+      }
+    }
+  }
+  st = exec_forward(m, kv, cache, P, true, out, 1.0f / p->temperature, s, start_si, save);
   if (probe) {
     release_taken(kv, cache, taken);
     return st;
@@ -735,6 +802,9 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
     return st;
   }
   if (cache == VIA_CACHE_SLIM) {
+    kv->xpref_ok = save;
+    kv->slim_row0.assign(w.batch, 0);
+    for (size_t q = 0; q < run.size(); ++q) kv->slim_row0[run[q]] = P.seqs[q].row_start;
     kv->win = w;
     kv->step_open = true;
     kv->step_n.assign(w.batch, 0);
@@ -1236,6 +1306,7 @@ via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* str
     S.full_ran = false;
   }
   kv->step_open = false;
+  kv->xpref_ok = false;
   return VIA_OK;
 }
 

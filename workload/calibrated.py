@@ -7,7 +7,7 @@ frozen as fp32 literals.
 """
 TEMPERATURE = {
     '1b_bf16': 28.40304946899414,
-    '8b_bf16_chain': 50.530677795410156,
-    '8b_bf16_long': 50.530677795410156,
-    '8b_bf16_tree': 50.530677795410156,
+    '8b_bf16_chain': 33.97911834716797,
+    '8b_bf16_long': 33.97911834716797,
+    '8b_bf16_tree': 33.97911834716797,
 }

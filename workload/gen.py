@@ -149,6 +149,12 @@ def synthetic_kv(cfg: dict, cache: int, layer_slot: int, b: int, n: int):
     bf16 = m["dtype"] == "bf16"
     shape = (n, m["n_kv_heads"], m["head_dim"])
     std = kv_std(m)
+    # The slim route's leading layers are the full model's first layers
+    # (route[i] == i), so a prefill caches the same keys and values for them
+    # in both caches: those slim slots draw the full cache's stream.
+    route = cfg["route"]
+    if cache == CACHE_SLIM and all(route[i] == i for i in range(layer_slot + 1)):
+        cache = CACHE_FULL
     K = normal_tensor(shape, cfg["seed_kv"], (cache, layer_slot, b, 0), std=std, bf16=bf16)
     V = normal_tensor(shape, cfg["seed_kv"], (cache, layer_slot, b, 1), std=std, bf16=bf16)
     return K, V
