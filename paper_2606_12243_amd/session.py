@@ -162,9 +162,11 @@ class Session:
 
     def _host(self, w):
         B, D = w.B, w.max_drafts
-        hp = self.dec.h_packed.numpy()
-        return dict(status=hp[:B].copy(), kappa=hp[B:2 * B].copy(), emit=hp[2 * B:3 * B].copy(),
-                    new_len=hp[3 * B:4 * B].copy(), path=hp[4 * B:4 * B + B * D].reshape(B, D).copy())
+        if getattr(self, "_hp", None) is None:
+            self._hp = self.dec.h_packed.numpy()  # view of the pinned read-back block
+        a = self._hp[:4 * B + B * D].copy()
+        return dict(status=a[:B], kappa=a[B:2 * B], emit=a[2 * B:3 * B], new_len=a[3 * B:4 * B],
+                    path=a[4 * B:].reshape(B, D))
 
     def commit(self, w, drafts: dict, h=None):
         """Commit the open step; ``h`` (host decision) may replace the
@@ -180,14 +182,15 @@ class Session:
             h = self._host(w)
         self._h = None
         via.check(via.via_kv_commit_rollback(self.kv.h, C.byref(self.dec.c), self.sp()))
+        status, kappa, emit = (np.asarray(h[k]).tolist() for k in ("status", "kappa", "emit"))
+        path = np.asarray(h["path"]).reshape(B, -1).tolist()
         for b, s in enumerate(w.a["seq"].tolist()):
-            if h["status"][b] != 0:
+            if status[b] != 0:
                 continue
             tok = drafts[s][0]
-            k = int(h["kappa"][b])
-            new = [tok[j] for j in h["path"][b][:k]]
-            if h["emit"][b] >= 0:
-                new.append(int(h["emit"][b]))
+            new = [tok[j] for j in path[b][:kappa[b]]]
+            if emit[b] >= 0:
+                new.append(emit[b])
             self.tokens[s].extend(new)
         return h
 
