@@ -233,6 +233,22 @@ via_status via_pack_gate_up(const void *src, void *dst, int32_t d_ffn, int32_t d
  * K must be a multiple of 32.  Asynchronous on `stream`. */
 via_status via_gemm_bf16(const void *X, const void *W, float *C, int32_t M, int32_t N, int32_t K, void *stream);
 
+/* Routing-mask cost of DIMR (Sec. 3, Eqs. 9-12): for every row r, with
+ * l_q = log softmax(q_logits[r] / T) (the full verifier q) and
+ * l_p = log softmax(p_logits[r] / T) (the routed slim verifier q'_z),
+ *   cost[r] = sum_v p(v) max(0, log(1 - alpha) + l_p(v) - l_q(v))
+ *           + sum_v q(v) max(0, log(beta)      + l_p(v) - l_q(v)),
+ * the ReLU form of R^KL_{alpha,beta}(q || q'_z) (Eq. 11); summed over a
+ * window of positions it is the cost C(z) a routing search minimises
+ * (Eq. 12).
+ *   q_logits, p_logits  device fp32 [rows][ld], entries [0, vocab) used
+ *                       (finite), e.g. the logits dumps of two forwards
+ *   cost                device fp32 [rows], written
+ * Requires 0 <= alpha < 1, beta > 0, T > 0, ld >= vocab >= 1; rows == 0
+ * is a no-op.  Asynchronous on `stream`; EINVAL before any launch. */
+via_status via_dimr_cost(const float *q_logits, const float *p_logits, int32_t rows, int32_t vocab, int32_t ld,
+                         float temperature, float alpha, float beta, float *cost, void *stream);
+
 /* ---- sizes -------------------------------------------------------------- */
 size_t via_pool_bytes(const via_model_desc *desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size);
 size_t via_workspace_bytes(const via_model_desc *desc, int32_t max_rows, int32_t max_batch,

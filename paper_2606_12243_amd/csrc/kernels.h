@@ -103,6 +103,17 @@ struct PrefixArgs {
 // K/V of layers 0..P-1 copied slim -> full cache at every row's position and
 // X[m] = Xpref[xfer[m].src_row].
 void launch_prefix_copy(bool bf16, const PrefixArgs& a, hipStream_t s);
+
+// DIMR routing cost per row (Eq. 11): q = full verifier logits, p = routed
+// slim verifier logits, both [rows][ld] fp32 (first `vocab` entries used).
+struct DimrArgs {
+  const float* q;
+  const float* p;
+  int rows, vocab, ld;
+  float inv_T, log_1m_alpha, log_beta;
+  float* cost;  // [rows]
+};
+void launch_dimr_cost(const DimrArgs& a, hipStream_t s);
 // Sum QKV partials, rotate-half RoPE at each row's position, Q -> fp32
 // buffer, K/V -> the paged cache (model dtype).
 struct QkvArgs {

@@ -862,6 +862,30 @@ via_status via_gemm_bf16(const void* X, const void* W, float* C, int32_t M, int3
   return VIA_OK;
 }
 
+via_status via_dimr_cost(const float* q_logits, const float* p_logits, int32_t rows, int32_t vocab, int32_t ld,
+                         float temperature, float alpha, float beta, float* cost, void* stream) {
+  if (rows < 0 || vocab < 1 || ld < vocab) return fail(VIA_EINVAL, "rows >= 0, vocab >= 1 and ld >= vocab");
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(VIA_EINVAL, "temperature must be > 0");
+  if (!(alpha >= 0.f && alpha < 1.f) || !(beta > 0.f) || !std::isfinite(beta))
+    return fail(VIA_EINVAL, "need 0 <= alpha < 1 and beta > 0");
+  if (rows == 0) return VIA_OK;
+  if (!q_logits || !p_logits || !cost) return fail(VIA_EINVAL, "null pointer");
+  DimrArgs a{};
+  a.q = q_logits;
+  a.p = p_logits;
+  a.rows = rows;
+  a.vocab = vocab;
+  a.ld = ld;
+  a.inv_T = 1.0f / temperature;
+  a.log_1m_alpha = (float)std::log(1.0 - (double)alpha);
+  a.log_beta = (float)std::log((double)beta);
+  a.cost = cost;
+  launch_dimr_cost(a, (hipStream_t)stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(VIA_EDEVICE, "dimr cost launch: %s", hipGetErrorString(e));
+  return VIA_OK;
+}
+
 via_status via_pack_gate_up(const void* src, void* dst, int32_t d_ffn, int32_t d_model, int32_t dtype, void* stream) {
   if (!src || !dst) return fail(VIA_EINVAL, "null pointer");
   if (d_ffn < 8 || d_ffn % 8) return fail(VIA_EINVAL, "d_ffn must be a positive multiple of 8");

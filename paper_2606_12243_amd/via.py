@@ -97,6 +97,7 @@ via_pack_weight = _sig("via_pack_weight", I32, P, P, I32, I32, I32, P)
 via_pack_gate_up = _sig("via_pack_gate_up", I32, P, P, I32, I32, I32, P)
 via_gemm_bf16 = _sig("via_gemm_bf16", I32, P, P, P, I32, I32, I32, P)
 via_pool_bytes = _sig("via_pool_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32)
+via_dimr_cost = _sig("via_dimr_cost", I32, P, P, I32, I32, I32, C.c_float, C.c_float, C.c_float, P, P)
 via_workspace_bytes = _sig("via_workspace_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
 via_staging_bytes = _sig("via_staging_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
 via_model_create = _sig("via_model_create", I32, C.POINTER(ModelDesc), C.POINTER(Weights), C.POINTER(P))
@@ -122,7 +123,7 @@ via_kv_timer_read = _sig("via_kv_timer_read", I32, P, I32, PI32, C.POINTER(C.c_d
 via_last_error = _sig("via_last_error", C.c_char_p)
 via_version = _sig("via_version", C.c_char_p)
 
-EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_bf16", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
+EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_bf16", "via_dimr_cost", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide",
