@@ -286,6 +286,8 @@ def main():
         # prefill rows of the workload: every sequence's context, capped at 8192
         prefill = prefill_gemm_roofline(md, min(8192, int(sum(cfg["ctx_lens"]))))
 
+    dimr = dimr_cost_roofline(md)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, W, res["recorded"], res["init_tokens"])
@@ -309,11 +311,45 @@ def main():
         "step_roofline": step_roof,
         "full_tier_variant": full_tier,
         "prefill_gemm_roofline": prefill,
+        "dimr_cost_roofline": dimr,
         "cpu_baseline": cpu,
     }
     if breakdown:
         out["kernels"] = breakdown
     print(json.dumps(out), flush=True)
+
+
+def dimr_cost_roofline(md, rows=64, reps=10):
+    """via_dimr_cost (the routing-mask cost over the vocabulary, one row per
+    calibration position) on random fp32 logits of the model's vocabulary:
+    algorithmic bytes = one read of both [rows, V] logit matrices; the kernel
+    reads them twice (log-partition pass, cost pass)."""
+    import ctypes as C
+    import torch
+    from paper_2606_12243_amd import via
+    V = md["vocab"]
+    g = torch.Generator(device="cuda").manual_seed(11)
+    q = torch.randn(rows, V, device="cuda", generator=g) * 4
+    p = q + torch.randn(rows, V, device="cuda", generator=g)
+    out = torch.empty(rows, device="cuda")
+    stream = torch.cuda.current_stream()
+    sp = C.c_void_p(stream.cuda_stream)
+    call = lambda: via.check(via.via_dimr_cost(q.data_ptr(), p.data_ptr(), rows, V, V, 1.0, 0.0, 1.0,
+                                               out.data_ptr(), sp))
+    call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    alg = 2 * rows * V * 4
+    return {"kernel": "dimr_cost_kernel: routing-mask cost, one row per calibration position", "bound": "hbm",
+            "rows": rows, "vocab": V, "us": round(us, 2), "bytes_per_launch": alg,
+            "achieved": round(alg / (us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
 
 
 def measured_copy_gbs(nbytes=1 << 30, reps=5):
