@@ -49,6 +49,7 @@ import numpy as np
 import torch
 
 from .model import OracleModel, SeqCache, causal, forward_window
+from .sampling import accept_prob, inverse_cdf, residual, tempered
 
 A, S, F = "A", "S", "F"
 FORCED_NONE, FORCED_ACCEPT, FORCED_SLIM, FORCED_FULL = -1, 0, 1, 2
@@ -277,12 +278,17 @@ class Verifier:
         return logits[nl:]
 
     # ------------------------------------------------------------------ step
-    def step(self, drafts: dict, p: TierParams) -> dict:
+    def step(self, drafts: dict, p: TierParams, sampling: dict = None) -> dict:
         """One verification step for the active sequences.
 
         ``drafts``: {seq index: Draft}.  Returns {seq: decision dict} and
         commits every decision (tokens, cache lengths, tree compaction,
         block frees).
+
+        ``sampling`` (chain drafts only) switches the rewrite and escalation
+        rules to sampling (App. A, module ``sampling``): dict with ``alpha``,
+        ``beta``, ``probs`` {seq: [k, V] drafter distributions p_j} and ``u``
+        {seq: [k][3] uniforms: acceptance, slim sample, residual sample}.
         """
         order = sorted(drafts)
         T = p.temperature
@@ -299,7 +305,7 @@ class Verifier:
             tiers = [tier_of(c, p) for c in conf]
             dec[b] = dict(conf=conf, tiers=tiers, slim_stats=stt, draft_row=draft_row, slim_logits=lg,
                           slim_draft_logit=[float(lg[draft_row[j], d.tok[j]]) for j in range(len(d.tok))])
-            dec[b].update(self._walk(d, tiers, conf, stt, None))
+            dec[b].update(self._walk_any(b, d, tiers, conf, slim[b], None, p, sampling))
             dec[b]["first_status"] = dec[b]["status"]
         full = {}
         for b in order:                               # escalation to q
@@ -311,13 +317,51 @@ class Verifier:
                 d = drafts[b]
                 dec[b]["full_draft_logit"] = [float(lg[dec[b]["draft_row"][j], d.tok[j]])
                                               for j in range(len(d.tok))]
-                dec[b].update(self._walk(d, dec[b]["tiers"], dec[b]["conf"], slim[b][1], full[b][1]))
+                dec[b].update(self._walk_any(b, d, dec[b]["tiers"], dec[b]["conf"], slim[b], full[b], p, sampling))
                 dec[b]["full_ran"] = True
             else:
                 dec[b]["full_ran"] = False
         for b in order:
             self._commit(b, drafts[b], dec[b])
         return dec
+
+    def _walk_any(self, b, d: Draft, tiers, conf, slim, full, p: TierParams, sampling):
+        if sampling is None:
+            return self._walk(d, tiers, conf, slim[1], None if full is None else full[1])
+        return self._walk_sampled(d, tiers, slim, full, p.temperature, sampling["alpha"], sampling["beta"],
+                                  sampling["probs"][b], sampling["u"][b])
+
+    @staticmethod
+    def _walk_sampled(d: Draft, tiers, slim, full, T, alpha, beta, probs, u):
+        """Chain walk with sampling rules: accept-tier drafts are kept; a
+        slim-tier position emits a sample of q'_j (uniform u[j][1]); an
+        escalated position keeps d_j with probability A.2 (accepted iff
+        u[j][0] < that probability), else emits a sample of the A.3 residual
+        (uniform u[j][2])."""
+        if d.parent is not None and any(par != j - 1 for j, par in enumerate(d.parent)):
+            raise ValueError("sampling mode takes chain drafts")
+        path = []
+        for j in range(len(d.tok)):
+            if tiers[j] == A:
+                path.append(j)
+                continue
+            if tiers[j] == S:
+                qs = tempered(slim[0][j], T)
+                return dict(kappa=len(path), emit=inverse_cdf(qs, float(u[j][1])), path=path,
+                            needs_full=False, status=0)
+            if full is None:
+                return dict(kappa=len(path), emit=-1, path=path, needs_full=True, status=1)
+            if not math.isfinite(full[1]["max"][j]):
+                return dict(kappa=len(path), emit=-1, path=path, needs_full=False, status=2)
+            q = tempered(full[0][j], T)
+            pj = torch.as_tensor(probs[j], dtype=torch.float64)
+            x = d.tok[j]
+            if float(u[j][0]) < accept_prob(float(q[x]), float(pj[x]), alpha):
+                path.append(j)
+                continue
+            return dict(kappa=len(path), emit=inverse_cdf(residual(q, pj, beta), float(u[j][2])), path=path,
+                        needs_full=False, status=0)
+        return dict(kappa=len(path), emit=-1, path=path, needs_full=False, status=0)
 
     @staticmethod
     def _walk(d: Draft, tiers, conf, slim_stats, full_stats):
