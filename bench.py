@@ -44,7 +44,7 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def build_session(cfg, W, pools=None, n_steps=64):
+def build_session(cfg, W, pools=None, n_steps=64, logits=False):
     import torch
     from paper_2606_12243_amd import via
     from paper_2606_12243_amd.session import Session
@@ -64,7 +64,7 @@ def build_session(cfg, W, pools=None, n_steps=64):
     kv = via.KV(model, max_seqs=B, max_blocks_per_seq=max_blocks, blocks_full=blocks, blocks_slim=blocks,
                 max_rows=max_rows, max_batch=B, max_drafts=64, zero_pools=False, pools=pools)
     p = via.tier_params(0.9, 0.5, cfg["temperature"])
-    return Session(model, kv, p)
+    return Session(model, kv, p, logits=logits)
 
 
 def attach_context(cfg, sess, synthetic):
@@ -99,10 +99,32 @@ def step_bytes(cfg, kv_slim_tokens, kv_full_tokens, full_ran):
     return tot
 
 
-def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
+def sampling_inputs(cfg, drafts, step, alpha, beta):
+    """Synthetic sampling-rule inputs of one step: the drafter's distribution
+    p_j over the vocabulary (a softmax of N(0, 1.5^2) logits with the drafted
+    token raised by 4, so p puts visible mass on its own draft) and the
+    step's uniforms, both seeded by (seed_d, step)."""
+    import torch
+    from paper_2606_12243_amd import via
+    V = cfg["model"]["vocab"]
+    B = len(drafts)
+    D = max(1, max(len(drafts[b][0]) for b in drafts))
+    g = torch.Generator(device="cuda").manual_seed(cfg["seed_d"] * 1000 + step)
+    z = torch.randn((B, D, V), generator=g, device="cuda") * 1.5
+    for i, b in enumerate(drafts):
+        tok = drafts[b][0]
+        z[i, torch.arange(len(tok), device="cuda"), torch.tensor(tok, device="cuda")] += 4.0
+    rng = np.random.default_rng([cfg["seed_d"], step])
+    U = rng.random((B, D, 3)).astype(np.float32)
+    return via.Sampling(alpha, beta, torch.softmax(z, -1), np.minimum(U, np.float32(0.99999)))
+
+
+def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=None):
     """Reference decode with the synthetic drafter (records drafts and
     decisions), then a fresh handle on the same pools replays the recorded
-    steps: `warmup` untimed, `steps` timed.  Returns the measurements."""
+    steps: `warmup` untimed, `steps` timed.  Returns the measurements.
+    ``sampling`` = (alpha, beta) switches to the sampling rules with the
+    synthetic inputs of ``sampling_inputs`` (recorded with the drafts)."""
     import torch
     from paper_2606_12243_amd import via
     from paper_2606_12243_amd.session import GreedyDrafter
@@ -113,7 +135,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
     cfg = dict(cfg, temperature=temperature)
     synthetic = cfg.get("seed_kv") is not None
     n_steps = warmup + steps
-    sess = build_session(cfg, W, n_steps=n_steps)
+    sess = build_session(cfg, W, n_steps=n_steps, logits=sampling is not None)
     t0 = time.time()
     attach_context(cfg, sess, synthetic)
     torch.cuda.synchronize()
@@ -131,13 +153,14 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
         else:
             d = drafter.chain(list(range(B)), cfg["k"], i)
             drafts = {b: (d[b], None) for b in range(B)}
+        smp = sampling_inputs(cfg, drafts, i, *sampling) if sampling is not None else None
         torch.cuda.synchronize()
         t_draft += time.time() - ts
         # cached tokens each forward of this step reads (for the step's algorithmic bytes)
         kv_slim = sum(sess.kv.seq_info(b, via.CACHE_SLIM)[0] for b in range(B))
         kv_full = sum(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)) for b in range(B))
-        h, run = sess.step(drafts)
-        recorded.append((drafts, h["new_len"].copy(), run.copy(), kv_slim, kv_full))
+        h, run = sess.step(drafts, smp)
+        recorded.append((drafts, h["new_len"].copy(), run.copy(), kv_slim, kv_full, smp))
     log(f"T={temperature:.4g}: reference decode of {n_steps} steps, drafting {t_draft:.2f}s")
 
     # ---- reset: fresh handle on the same pools (context slots untouched)
@@ -145,7 +168,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
     sess.kv.close()
 
     def fresh():
-        s2 = build_session(cfg, W, pools=pools, n_steps=n_steps)
+        s2 = build_session(cfg, W, pools=pools, n_steps=n_steps, logits=sampling is not None)
         if synthetic:
             for b in range(B):
                 s2.reserve(b, init_tokens[b], None)
@@ -162,7 +185,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
         s2 = fresh()
         mism = 0
         for i in range(warmup):
-            h, run = s2.step(recorded[i][0])
+            h, run = s2.step(recorded[i][0], recorded[i][5])
             mism += int((h["new_len"] != recorded[i][1]).any())
         torch.cuda.synchronize()
         if timed_kind is not None:
@@ -175,7 +198,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None):
         for i in range(warmup, n_steps):
             drafts = recorded[i][0]
             ts = time.perf_counter()
-            w, h, run = s2.begin(drafts)
+            w, h, run = s2.begin(drafts, recorded[i][5])
             s2.commit(w, drafts)
             torch.cuda.synchronize()
             lat.append(time.perf_counter() - ts)
@@ -207,6 +230,7 @@ def main():
     ap.add_argument("--no-full-tier", action="store_true",
                     help="skip the T = 1 variant (every position escalated to the full verifier)")
     ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
+    ap.add_argument("--no-sampling", action="store_true", help="skip the sampling-rules variant")
     ap.add_argument("--no-prefill-gemm", action="store_true", help="skip the prefill GEMM roofline")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (the reference kernel for HBM counter scaling)")
@@ -240,7 +264,7 @@ def main():
     torch.cuda.synchronize()
     log(f"weights on device in {time.time() - t0:.1f}s")
     kinds = {"qkv": via.KERNEL_QKV, "attn": via.KERNEL_ATTN, "o": via.KERNEL_O, "gateup": via.KERNEL_GATEUP,
-             "down": via.KERNEL_DOWN, "head": via.KERNEL_HEAD}
+             "down": via.KERNEL_DOWN, "head": via.KERNEL_HEAD, "decide": via.KERNEL_DECIDE}
     DOM = "gateup"
     T = float(cfg["temperature"])
     res = run_workload(cfg, W, args.steps, args.warmup, T, timer_kind=kinds[DOM])
@@ -272,6 +296,17 @@ def main():
                      "ms_per_step": round(float(r1["lat_ms"].mean()), 3), "steps": len(r1["lat_ms"]),
                      "escalation_rate": round(r1["escalation"], 3), "replay_mismatch_steps": r1["mismatch"],
                      "step_roofline_frac": round(r1["bytes"] / r1["t_total"] / 1e9 / HBM_PEAK_GBS, 4)}
+
+    # the same workload under the sampling rules (App. A, lossless alpha = 0,
+    # beta = 1): logits kept, the decision draws the owed samples
+    sampled = None
+    if not args.no_sampling:
+        rs = run_workload(cfg, W, max(5, args.steps // 3), 2, T, timer_kind=kinds["decide"], sampling=(0.0, 1.0))
+        n, ms = rs["timer"]
+        sampled = {"alpha": 0.0, "beta": 1.0, "temperature": T, "value": round(rs["value"], 2), "unit": "tokens/s",
+                   "ms_per_step": round(float(rs["lat_ms"].mean()), 3), "steps": len(rs["lat_ms"]),
+                   "escalation_rate": round(rs["escalation"], 3), "replay_mismatch_steps": rs["mismatch"],
+                   "decide_launches": n, "decide_avg_us": round(ms * 1e3 / max(1, n), 2)}
 
     breakdown = None
     if args.breakdown:
@@ -310,6 +345,7 @@ def main():
         "roofline": roof,
         "step_roofline": step_roof,
         "full_tier_variant": full_tier,
+        "sampling_rules_variant": sampled,
         "prefill_gemm_roofline": prefill,
         "dimr_cost_roofline": dimr,
         "cpu_baseline": cpu,

@@ -311,6 +311,36 @@ via_status via_verify_probe(via_model *m, via_kv *kv, int32_t cache, const via_w
  * decision and copies `packed` to `h_packed`. */
 via_status via_tier_decide(via_kv *kv, const via_tier_params *p, const via_verify_out *slim,
                            const via_verify_out *full, via_decision *dec, void *stream);
+/* Sampling rules (App. A) for chain drafts.  An accept-tier draft is kept;
+ * at a slim-tier position the walk stops and emits a sample of the slim
+ * verifier q' = softmax(l'/T) (App. B.1, rewrite from q'); an escalated
+ * draft x with drafter probability p(x) and verifier probability
+ * q(x) = softmax(l/T)(x) is kept iff uniforms[.., 0] < min(1, q(x) /
+ * ((1 - alpha) p(x))) (Eq. A.2; p(x) = 0 keeps it), else the walk stops and
+ * emits a sample of norm(max(0, q/beta - p)) (Eq. A.3; q itself if that has
+ * no mass).  alpha = 0, beta = 1 is the lossless rule.  A sample with
+ * uniform u is the first token, in id order, whose running weight exceeds
+ * u times the total weight.  When every draft is kept nothing is emitted.
+ *   draft_probs  device fp32 [batch * window.max_drafts * vocab]: p of each
+ *                draft position (row b * max_drafts + j), caller-owned.
+ *   uniforms     host fp32 [batch * window.max_drafts * 3] in [0, 1): per
+ *                draft the acceptance, slim-sample and residual-sample
+ *                uniforms (b * max_drafts + j) * 3 + {0, 1, 2}; copied
+ *                during the call. */
+typedef struct {
+  float alpha, beta; /* 0 <= alpha < 1, beta > 0 */
+  const float *draft_probs;
+  const float *uniforms;
+} via_sampling;
+/* via_tier_decide under the sampling rules.  Both verify outputs must carry
+ * logits (slim->logits, and full->logits when full is given); both decide
+ * calls of a step take the same sampling arguments.  EUNSUPPORTED for tree
+ * windows, EINVAL for alpha/beta out of range, missing arrays or a uniform
+ * outside [0, 1).  Writes the decision as via_tier_decide does, with the
+ * sampled token in `emit`. */
+via_status via_tier_decide_sampled(via_kv *kv, const via_tier_params *p, const via_verify_out *slim,
+                                   const via_verify_out *full, const via_sampling *smp, via_decision *dec,
+                                   void *stream);
 /* Commit the open step from dec->h_packed (read on the host: synchronise
  * first).  Appends kappa drafts (+ emit) per sequence: slim valid length
  * becomes n'-1; full valid length becomes n'-1 if the full verifier ran
@@ -331,7 +361,8 @@ via_status via_kv_commit_rollback(via_kv *kv, const via_decision *dec, void *str
 #define VIA_KERNEL_GATEUP 3 /* gate/up projection + SwiGLU */
 #define VIA_KERNEL_DOWN 4   /* down projection + residual */
 #define VIA_KERNEL_HEAD 5   /* output head + row statistics */
-#define VIA_KERNEL_COUNT 6
+#define VIA_KERNEL_DECIDE 6 /* tier decision (+ the sampling rules' draw) */
+#define VIA_KERNEL_COUNT 7
 via_status via_kv_timer_enable(via_kv *kv, uint32_t kind_mask);
 via_status via_kv_timer_read(via_kv *kv, int32_t kind, int32_t *launches, double *total_ms);
 

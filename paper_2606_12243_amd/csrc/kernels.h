@@ -175,6 +175,15 @@ struct KvMove {
 void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KVH, int hd,
                      const int32_t* btab, const KvMove* moves, int n_moves, hipStream_t s);
 
+// A sampled token the decision still owes (kind 1: slim-tier rewrite from
+// q', kind 2: residual of a rejected escalated draft; 0: none).
+// The vocabulary is cut into at most this many slices for the draw.
+constexpr int kSampleSlices = 64;
+struct SampleReq {
+  int32_t kind, out, j;
+  float u;
+};
+
 struct DecideArgs {
   const StepSeq* seqs;
   int batch, max_rows, max_drafts;
@@ -192,7 +201,20 @@ struct DecideArgs {
   int8_t* tier;
   float* conf;
   int32_t* packed;
+  // sampling rules (chain drafts; draft_probs null: greedy rules)
+  const float* draft_probs;   // [batch * max_drafts * vocab] drafter distributions
+  const float* u;             // [batch * max_drafts * 3] uniforms: accept, slim sample, residual sample
+  const float* s_logits;      // [batch * max_rows * vocab]
+  const float* f_logits;      // same, full verifier (null on the first pass)
+  const float* s_row_sumexp;
+  const float* f_row_sumexp;
+  float alpha, beta;
+  int vocab;
+  SampleReq* req;             // [batch]
+  double* slice_sum;          // [batch * kSampleSlices * 2] per-slice weight sums
 };
+// Decision kernel, then (sampling rules) the sampling kernel that fills the
+// emitted tokens it left open.
 void launch_decide(const DecideArgs& a, hipStream_t s);
 
 }  // namespace via

@@ -206,6 +206,53 @@ __global__ __launch_bounds__(64) void decide_kernel(DecideArgs a) {
   int* emit = a.packed + 2 * B;
   int* new_len = a.packed + 3 * B;
   int* path = a.packed + 4 * B + base;
+  if (a.draft_probs) {
+    // sampling rules (App. A), chain drafts in order: an accept-tier draft is
+    // kept; a slim-tier position owes a sample of q'; an escalated draft x is
+    // kept with probability min(1, q(x) / ((1 - alpha) p(x))) (Eq. A.2),
+    // accepted iff its uniform is below that, else it owes a sample of the
+    // A.3 residual.  The owed sample is drawn by the sampling kernels.
+    int k = 0, st = 0;
+    SampleReq rq{0, 0, 0, 0.f};
+    for (int j = 0; j < ss.n_drafts; ++j) {
+      const int t = a.tier[base + j];
+      const int out = b * a.max_rows + a.draft_row[base + j];
+      if (t == 0) {
+        path[k++] = j;
+        continue;
+      }
+      if (t == 1) {
+        rq = SampleReq{1, out, j, a.u[(size_t)(base + j) * 3 + 1]};
+        break;
+      }
+      if (!have_full) {
+        st = 1;
+        break;
+      }
+      const float fm = a.f_row_max[out];
+      if (!isfinite(fm)) {
+        st = 2;
+        break;
+      }
+      const float qx = expf((a.f_draft_logit[base + j] - fm) * a.inv_T) / a.f_row_sumexp[out];
+      const float px = a.draft_probs[(size_t)(base + j) * a.vocab + a.draft_tok[base + j]];
+      const float keep = px <= 0.f ? 1.f : fminf(1.f, qx / ((1.f - a.alpha) * px));
+      if (a.u[(size_t)(base + j) * 3] < keep) {
+        path[k++] = j;
+        continue;
+      }
+      rq = SampleReq{2, out, j, a.u[(size_t)(base + j) * 3 + 2]};
+      break;
+    }
+    if (st != 0) rq.kind = 0;
+    a.req[b] = rq;
+    status[b] = st;
+    kappa[b] = k;
+    emit[b] = -1;  // a sample owed is written by sample_pick_kernel
+    new_len[b] = st == 2 ? ss.n : ss.n + k + (rq.kind ? 1 : 0);
+    for (int q = k; q < D; ++q) path[q] = -1;
+    return;
+  }
   int u = -1, k = 0, em = -1, st = 0;
   for (;;) {
     // children of u, in draft order
@@ -314,8 +361,222 @@ void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(64), 0, s, a);
 }
 
+namespace {
+
+// Owed samples (App. A): the token a uniform u draws from weights w(v),
+// v < V, is the first v in id order whose running sum exceeds u * sum(w)
+// (the last token with weight when rounding leaves no crossing).  Weights:
+// kind 1 the slim row's exp((l - max) / T); kind 2 the A.3 residual
+// max(0, q / beta - p), q = exp((l - max) / T) / sum, or q itself when the
+// residual has no mass.
+//
+// The vocabulary is cut into slices of kSampleThreads * E ids; thread t of a
+// slice owns the E consecutive ids starting at t * E.  Sums are fp64 in one
+// fixed grouping, shared by both kernels: a thread's ids in order; four
+// consecutive threads in order per lane of wave 0; a 64-lane inclusive scan.
+// sample_sums_kernel (one work-group per slice and sequence) writes each
+// slice's residual and q sums; sample_pick_kernel (one per sequence) finds
+// the crossing slice from them, rescans that slice with the same grouping,
+// and walks the crossing lane, thread and id.
+constexpr int kSampleThreads = 256;
+
+struct SampleGeom {
+  int E, slice, G;
+};
+__host__ __device__ inline SampleGeom sample_geom(int V) {
+  int E = (V + kSampleSlices * kSampleThreads - 1) / (kSampleSlices * kSampleThreads);
+  if (E < 1) E = 1;
+  const int slice = E * kSampleThreads;
+  return SampleGeom{E, slice, (V + slice - 1) / slice};
+}
+
+struct SampleRow {
+  const float* lg;
+  const float* p;
+  float mx, inv_z, inv_T, inv_beta;
+};
+__device__ inline SampleRow sample_row(const DecideArgs& a, const SampleReq& r, int b) {
+  const size_t V = (size_t)a.vocab;
+  SampleRow w;
+  w.lg = (r.kind == 1 ? a.s_logits : a.f_logits) + (size_t)r.out * V;
+  w.p = a.draft_probs + (size_t)(b * a.max_drafts + r.j) * V;
+  w.mx = r.kind == 1 ? a.s_row_max[r.out] : a.f_row_max[r.out];
+  w.inv_z = r.kind == 2 ? 1.f / a.f_row_sumexp[r.out] : 1.f;
+  w.inv_T = a.inv_T;
+  w.inv_beta = 1.f / a.beta;
+  return w;
+}
+// q-weight of id v (kind 1: unnormalised q', kind 2: q)
+__device__ inline float q_weight(const SampleRow& w, int v) { return expf((w.lg[v] - w.mx) * w.inv_T) * w.inv_z; }
+__device__ inline float r_weight(const SampleRow& w, int v, float q) { return fmaxf(0.f, q * w.inv_beta - w.p[v]); }
+
+// Inclusive scan of one fp64 value over the 64 lanes of a wave.
+__device__ inline double wave_scan(double x, int lane) {
+  for (int d = 1; d < 64; d <<= 1) {
+    const double y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
+// Thread sums of one slice (both weight kinds) into LDS.
+__device__ inline void slice_thread_sums(const SampleRow& w, int kind, int V, const SampleGeom& g, int slice_id,
+                                         double* tq, double* tr) {
+  const int t = threadIdx.x;
+  const int lo = slice_id * g.slice + t * g.E;
+  double sq = 0.0, sr = 0.0;
+  for (int e = 0; e < g.E; ++e) {
+    const int v = lo + e;
+    if (v >= V) break;
+    const float q = q_weight(w, v);
+    sq += (double)q;
+    if (kind == 2) sr += (double)r_weight(w, v, q);
+  }
+  tq[t] = sq;
+  tr[t] = sr;
+}
+
+// Lane sums (four threads in order) and their inclusive scan, wave 0.
+__device__ inline double lane_scan(const double* ts, int lane, double* lane_sum) {
+  const double x = ((ts[4 * lane] + ts[4 * lane + 1]) + ts[4 * lane + 2]) + ts[4 * lane + 3];
+  *lane_sum = x;
+  return wave_scan(x, lane);
+}
+
+__global__ __launch_bounds__(kSampleThreads) void sample_sums_kernel(DecideArgs a) {
+  const int b = blockIdx.y, g = blockIdx.x;
+  const SampleReq r = a.req[b];
+  if (r.kind == 0) return;  // uniform per work-group
+  const SampleGeom geo = sample_geom(a.vocab);
+  __shared__ double tq[kSampleThreads], tr[kSampleThreads];
+  const SampleRow w = sample_row(a, r, b);
+  slice_thread_sums(w, r.kind, a.vocab, geo, g, tq, tr);
+  __syncthreads();
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  double ls;
+  const double iq = lane_scan(tq, lane, &ls);
+  const double ir = lane_scan(tr, lane, &ls);
+  if (lane == 63) {
+    double* out = a.slice_sum + ((size_t)b * kSampleSlices + g) * 2;
+    out[0] = iq;
+    out[1] = ir;
+  }
+}
+
+__global__ __launch_bounds__(kSampleThreads) void sample_pick_kernel(DecideArgs a) {
+  const int b = blockIdx.x;
+  const SampleReq r = a.req[b];
+  if (r.kind == 0) return;  // uniform per work-group
+  const int V = a.vocab;
+  const SampleGeom geo = sample_geom(V);
+  const SampleRow w = sample_row(a, r, b);
+  const int t = threadIdx.x, lane = t & 63;
+  __shared__ double tq[kSampleThreads], tr[kSampleThreads];
+  __shared__ int s_slice, s_last, s_resid;
+  __shared__ double s_acc, s_target;
+  if (t < 64) {
+    // slice level: totals, the weights in use, the crossing slice
+    const double* ssum = a.slice_sum + (size_t)b * kSampleSlices * 2;
+    const double xq = lane < geo.G ? ssum[lane * 2] : 0.0, xr = lane < geo.G ? ssum[lane * 2 + 1] : 0.0;
+    const double iq = wave_scan(xq, lane), ir = wave_scan(xr, lane);
+    const double tot_r = __shfl(ir, 63, 64);
+    const bool resid = r.kind == 2 && tot_r > 0.0;
+    const double x = resid ? xr : xq, inc = resid ? ir : iq;
+    const double tot = __shfl(inc, 63, 64);
+    const double target = (double)r.u * tot;
+    // crossings only at slices with weight (sums of zeros may round apart)
+    const unsigned long long cross = __ballot(lane < geo.G && x > 0.0 && inc > target);
+    const unsigned long long pos = __ballot(x > 0.0);
+    if (lane == 0) {
+      int c, last = 0;
+      if (cross) {
+        c = __ffsll((long long)cross) - 1;
+      } else {
+        c = pos ? 63 - __clzll((long long)pos) : 0;
+        last = 1;
+      }
+      s_slice = c;
+      s_last = last;
+      s_resid = resid ? 1 : 0;
+      s_target = target;
+    }
+    // running sum before the crossing slice: the previous lane's prefix
+    const int c = cross ? __ffsll((long long)cross) - 1 : 0;
+    const double before = __shfl(inc, c > 0 ? c - 1 : 0, 64);
+    if (lane == 0) s_acc = c > 0 ? before : 0.0;
+  }
+  __syncthreads();
+  const int c = s_slice;
+  const bool resid = s_resid != 0;
+  slice_thread_sums(w, resid ? 2 : 1, V, geo, c, tq, tr);
+  __syncthreads();
+  if (t >= 64) return;
+  const double* ts = resid ? tr : tq;
+  double ls;
+  const double inc = lane_scan(ts, lane, &ls);
+  const double target = s_target;
+  const double run0 = s_acc;
+  bool last = s_last != 0;
+  unsigned long long cross = last ? 0ull : __ballot(ls > 0.0 && run0 + inc > target);
+  if (!cross) last = true;
+  const unsigned long long pos = __ballot(ls > 0.0);
+  int L;
+  if (!last)
+    L = __ffsll((long long)cross) - 1;
+  else
+    L = pos ? 63 - __clzll((long long)pos) : 0;
+  if (lane != L) return;
+  // the chosen lane: its four threads in order, then the chosen thread's ids
+  double run = run0 + (inc - ls);
+  int th = -1;
+  if (!last) {
+    for (int i = 0; i < 4; ++i) {
+      const double v = ts[4 * L + i];
+      if (v > 0.0 && run + v > target) {
+        th = 4 * L + i;
+        break;
+      }
+      run += v;
+    }
+  }
+  bool take_last = th < 0;
+  if (take_last) {
+    th = 4 * L;
+    for (int i = 3; i >= 0; --i)
+      if (ts[4 * L + i] > 0.0) {
+        th = 4 * L + i;
+        break;
+      }
+  }
+  const int lo = c * geo.slice + th * geo.E;
+  int tok = -1, lastpos = lo < V ? lo : V - 1;
+  for (int e = 0; e < geo.E; ++e) {
+    const int v = lo + e;
+    if (v >= V) break;
+    const float q = q_weight(w, v);
+    const float wt = resid ? r_weight(w, v, q) : q;
+    if (wt > 0.f) {
+      lastpos = v;
+      run += (double)wt;
+      if (!take_last && run > target) {
+        tok = v;
+        break;
+      }
+    }
+  }
+  a.packed[2 * a.batch + b] = tok >= 0 ? tok : lastpos;
+}
+
+}  // namespace
+
 void launch_decide(const DecideArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(decide_kernel, dim3(a.batch), dim3(64), 0, s, a);
+  if (a.draft_probs) {
+    const SampleGeom g = sample_geom(a.vocab);
+    hipLaunchKernelGGL(sample_sums_kernel, dim3(g.G, a.batch), dim3(kSampleThreads), 0, s, a);
+    hipLaunchKernelGGL(sample_pick_kernel, dim3(a.batch), dim3(kSampleThreads), 0, s, a);
+  }
 }
 
 void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KVH, int hd, const int32_t* btab,

@@ -88,7 +88,8 @@ struct Layout {
   size_t X, Yf, Q, Af, Hf, Ylf, part, att_o, att_ml, lm_part, ss;
   size_t Xpref;                        // slim forward's residual stream after the shared layers
   size_t rows, seqs, btab, items, lm, xfer;  // plan region
-  size_t step_seqs, dtok, drow, dpar;  // step region
+  size_t step_seqs, dtok, drow, dpar, du;  // step region
+  size_t sreq, ssum;                   // sampling requests and slice sums of a decision
   size_t c_btab, c_moves;              // commit region
   size_t plan_bytes, step_bytes, commit_bytes;
   size_t total;
@@ -145,7 +146,10 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.dtok = take((size_t)max_batch * max_drafts * 4);
   L.drow = take((size_t)max_batch * max_drafts * 4);
   L.dpar = take((size_t)max_batch * max_drafts * 4);
+  L.du = take((size_t)max_batch * max_drafts * 3 * 4);
   L.step_bytes = o - s0;
+  L.sreq = take((size_t)max_batch * sizeof(SampleReq));
+  L.ssum = take((size_t)max_batch * kSampleSlices * 2 * sizeof(double));
   size_t c0 = o;
   L.c_btab = take((size_t)2 * max_batch * max_blocks * 4);
   L.c_moves = take((size_t)2 * max_batch * max_drafts * sizeof(KvMove));
@@ -1182,8 +1186,8 @@ via_status via_verify_probe(via_model* m, via_kv* kv, int32_t cache, const via_w
   return verify_impl(m, kv, cache, win, nullptr, p, out, (hipStream_t)stream, true);
 }
 
-via_status via_tier_decide(via_kv* kv, const via_tier_params* p, const via_verify_out* slim,
-                           const via_verify_out* full, via_decision* dec, void* stream) {
+via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_out* slim,
+                       const via_verify_out* full, const via_sampling* smp, via_decision* dec, void* stream) {
   if (!kv || !dec) return fail(VIA_EINVAL, "null argument");
   if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
   via_status st = check_params(p);
@@ -1208,6 +1212,16 @@ via_status via_tier_decide(via_kv* kv, const via_tier_params* p, const via_verif
   memcpy(blob.data() + (L.dtok - L.step_seqs), w.draft_tok.data(), (size_t)B * Dd * 4);
   memcpy(blob.data() + (L.drow - L.step_seqs), w.draft_row.data(), (size_t)B * Dd * 4);
   memcpy(blob.data() + (L.dpar - L.step_seqs), w.draft_parent.data(), (size_t)B * Dd * 4);
+  if (smp) {
+    if (w.tree) return fail(VIA_EUNSUPPORTED, "sampling rules take chain drafts");
+    if (!(smp->alpha >= 0.f && smp->alpha < 1.f) || !(smp->beta > 0.f) || !std::isfinite(smp->beta))
+      return fail(VIA_EINVAL, "need 0 <= alpha < 1 and beta > 0");
+    if (!smp->draft_probs || !smp->uniforms) return fail(VIA_EINVAL, "draft_probs and uniforms are required");
+    if (!slim->logits || (full && !full->logits)) return fail(VIA_EINVAL, "sampling needs the logits outputs");
+    for (size_t i = 0; i < (size_t)B * Dd * 3; ++i)
+      if (!(smp->uniforms[i] >= 0.f && smp->uniforms[i] < 1.f)) return fail(VIA_EINVAL, "uniforms must lie in [0, 1)");
+    memcpy(blob.data() + (L.du - L.step_seqs), smp->uniforms, (size_t)B * Dd * 3 * 4);
+  }
   if ((st = upload(kv, kv->ws + L.step_seqs, blob.data(), L.step_bytes, s))) return st;
   DecideArgs a{};
   a.seqs = (const StepSeq*)(kv->ws + L.step_seqs);
@@ -1232,10 +1246,37 @@ via_status via_tier_decide(via_kv* kv, const via_tier_params* p, const via_verif
   a.tier = dec->tier;
   a.conf = dec->conf;
   a.packed = dec->packed;
-  launch_decide(a, s);
+  if (smp) {
+    a.draft_probs = smp->draft_probs;
+    a.u = (const float*)(kv->ws + L.du);
+    a.s_logits = slim->logits;
+    a.s_row_sumexp = slim->row_sumexp;
+    if (full) {
+      a.f_logits = full->logits;
+      a.f_row_sumexp = full->row_sumexp;
+    }
+    a.alpha = smp->alpha;
+    a.beta = smp->beta;
+    a.vocab = kv->m->d.vocab;
+    a.req = (SampleReq*)(kv->ws + L.sreq);
+    a.slice_sum = (double*)(kv->ws + L.ssum);
+  }
+  timed_launch(kv, VIA_KERNEL_DECIDE, s, [&] { launch_decide(a, s); });
   if ((st = hip_check(kv, hipGetLastError(), "decide launch"))) return st;
   size_t bytes = (size_t)(4 * B + B * Dd) * 4;
   return hip_check(kv, hipMemcpyAsync(dec->h_packed, dec->packed, bytes, hipMemcpyDeviceToHost, s), "decision copy");
+}
+
+via_status via_tier_decide(via_kv* kv, const via_tier_params* p, const via_verify_out* slim,
+                           const via_verify_out* full, via_decision* dec, void* stream) {
+  return decide_impl(kv, p, slim, full, nullptr, dec, stream);
+}
+
+via_status via_tier_decide_sampled(via_kv* kv, const via_tier_params* p, const via_verify_out* slim,
+                                   const via_verify_out* full, const via_sampling* smp, via_decision* dec,
+                                   void* stream) {
+  if (!smp) return fail(VIA_EINVAL, "null sampling parameters");
+  return decide_impl(kv, p, slim, full, smp, dec, stream);
 }
 
 via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* stream) {

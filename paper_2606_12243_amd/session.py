@@ -134,17 +134,29 @@ class Session:
                              max_rows=max(len(r) for r in rows), max_drafts=max(1, max(len(d) for d in dtoks)))
 
     # ------------------------------------------------------------------ step
-    def begin(self, drafts: dict):
+    def _decide(self, full, sampling):
+        fo = C.byref(self.out_full.c) if full else None
+        if sampling is None:
+            via.check(via.via_tier_decide(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c), fo,
+                                          C.byref(self.dec.c), self.sp()))
+        else:
+            via.check(via.via_tier_decide_sampled(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c), fo,
+                                                  C.byref(sampling.c), C.byref(self.dec.c), self.sp()))
+
+    def begin(self, drafts: dict, sampling: via.Sampling = None):
         """Slim forward, decision, and the full forward where needed.
         Returns (window, host decision, full ran per batch entry).  The slim
         forward ignores lag rows; the window of the full forward (same rows)
-        carries them and is built only when some sequence escalates."""
+        carries them and is built only when some sequence escalates.
+        ``sampling`` (chain drafts, a session with logits) selects the
+        sampling rules; its arrays follow the window's batch order."""
+        if sampling is not None and not self.want_logits:
+            raise ValueError("sampling rules need a session created with logits=True")
         w = self.window(drafts)
         self._w = w
         via.check(via.via_verify_slim(self.m.h, self.kv.h, C.byref(w.c), C.byref(self.p),
                                       C.byref(self.out_slim.c), self.sp()))
-        via.check(via.via_tier_decide(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c), None,
-                                      C.byref(self.dec.c), self.sp()))
+        self._decide(False, sampling)
         self.stream.synchronize()
         h = self._host(w)
         run = (h["status"] == 1).astype(np.int32)
@@ -153,8 +165,7 @@ class Session:
             wl = self.window(drafts, with_lag=True)
             via.check(via.via_verify_full(self.m.h, self.kv.h, C.byref(wl.c), rp, C.byref(self.p),
                                           C.byref(self.out_full.c), self.sp()))
-            via.check(via.via_tier_decide(self.kv.h, C.byref(self.p), C.byref(self.out_slim.c),
-                                          C.byref(self.out_full.c), C.byref(self.dec.c), self.sp()))
+            self._decide(True, sampling)
             self.stream.synchronize()
             h = self._host(w)
         self._h = h
@@ -194,8 +205,8 @@ class Session:
             self.tokens[s].extend(new)
         return h
 
-    def step(self, drafts: dict):
-        w, h, run = self.begin(drafts)
+    def step(self, drafts: dict, sampling: via.Sampling = None):
+        w, h, run = self.begin(drafts, sampling)
         self.commit(w, drafts)
         return h, run
 

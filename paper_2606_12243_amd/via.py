@@ -85,6 +85,10 @@ class Decision(C.Structure):
     _fields_ = [("tier", P), ("conf", P), ("packed", P), ("h_packed", P)]
 
 
+class SamplingC(C.Structure):
+    _fields_ = [("alpha", C.c_float), ("beta", C.c_float), ("draft_probs", P), ("uniforms", P)]
+
+
 def _sig(name, res, *args):
     f = getattr(lib, name)
     f.restype = res
@@ -117,6 +121,8 @@ via_verify_probe = _sig("via_verify_probe", I32, P, P, I32, C.POINTER(Window), C
                         C.POINTER(VerifyOut), P)
 via_tier_decide = _sig("via_tier_decide", I32, P, C.POINTER(TierParams), C.POINTER(VerifyOut),
                        C.POINTER(VerifyOut), C.POINTER(Decision), P)
+via_tier_decide_sampled = _sig("via_tier_decide_sampled", I32, P, C.POINTER(TierParams), C.POINTER(VerifyOut),
+                               C.POINTER(VerifyOut), C.POINTER(SamplingC), C.POINTER(Decision), P)
 via_kv_commit_rollback = _sig("via_kv_commit_rollback", I32, P, C.POINTER(Decision), P)
 via_kv_timer_enable = _sig("via_kv_timer_enable", I32, P, C.c_uint32)
 via_kv_timer_read = _sig("via_kv_timer_read", I32, P, I32, PI32, C.POINTER(C.c_double))
@@ -126,11 +132,11 @@ via_version = _sig("via_version", C.c_char_p)
 EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_bf16", "via_dimr_cost", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
-           "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide",
+           "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide", "via_tier_decide_sampled",
            "via_kv_commit_rollback", "via_kv_timer_enable", "via_kv_timer_read", "via_last_error",
            "via_version"]
-KERNEL_QKV, KERNEL_ATTN, KERNEL_O, KERNEL_GATEUP, KERNEL_DOWN, KERNEL_HEAD = range(6)
-KERNEL_NAMES = ["qkv", "attn", "o", "gateup", "down", "head"]
+KERNEL_QKV, KERNEL_ATTN, KERNEL_O, KERNEL_GATEUP, KERNEL_DOWN, KERNEL_HEAD, KERNEL_DECIDE = range(7)
+KERNEL_NAMES = ["qkv", "attn", "o", "gateup", "down", "head", "decide"]
 
 
 def check(status):
@@ -386,6 +392,17 @@ class Dec:
         B = self.B
         h[:B], h[B:2 * B], h[2 * B:3 * B], h[3 * B:4 * B] = status, kappa, emit, new_len
         h[4 * B:] = np.asarray(path, np.int32).reshape(-1)
+
+
+class Sampling:
+    """Sampling-rule arguments of one step: alpha, beta, the drafter's
+    distributions ``draft_probs`` (device fp32 [batch, max_drafts, vocab],
+    kept referenced here) and the uniforms [batch, max_drafts, 3] (host)."""
+
+    def __init__(self, alpha, beta, draft_probs, uniforms):
+        self.probs = draft_probs.to(torch.float32).contiguous()
+        self.u = np.ascontiguousarray(uniforms, np.float32)
+        self.c = SamplingC(alpha, beta, self.probs.data_ptr(), self.u.ctypes.data)
 
 
 def tier_params(tau_acc=0.9, tau_full=0.5, temperature=1.0, forced=FORCED_NONE):
