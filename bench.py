@@ -220,6 +220,72 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
                 init_tokens=init_tokens, accepted=accepted)
 
 
+def run_drafter_variant(cfg, W, steps, warmup, temperature, route_d):
+    """The serving loop with a drafter model: the verifier's weights under
+    the nested route ``route_d`` (inside the slim route) draft k tokens per
+    sequence from their temperature-T softmax, the verifier checks them under
+    the lossless sampling rules (alpha = 0, beta = 1) with the drafter's p,
+    and the drafter's cache takes the committed tokens.  Every phase is
+    timed (synchronised); uniforms are seeded."""
+    import torch
+    from paper_2606_12243_amd import via
+    from paper_2606_12243_amd.session import ModelDrafter
+    from workload import gen
+    md = cfg["model"]
+    B, k = cfg["batch"], cfg["k"]
+    cfg = dict(cfg, temperature=temperature)
+    n_steps = warmup + steps
+    sess = build_session(cfg, W, n_steps=n_steps, logits=True)
+    attach_context(cfg, sess, cfg.get("seed_kv") is not None)
+    dm = via.Model(md, W, list(route_d))
+    max_blocks = (max(cfg["ctx_lens"]) + n_steps * (k + 1) + 32) // 16 + 1
+    dkv = via.KV(dm, max_seqs=B, max_blocks_per_seq=max_blocks, blocks_full=B * max_blocks,
+                 blocks_slim=B * max_blocks, max_rows=max(B * k, max(cfg["ctx_lens"])), max_batch=B,
+                 max_drafts=k + 1, zero_pools=False)
+    dr = ModelDrafter(dm, dkv, temperature)
+    for b in range(B):
+        dr.attach(b, list(sess.tokens[b]))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng([cfg["seed_d"], 77])
+    seqs = list(range(B))
+    t_draft, t_verify, t_sync, accepted = [], [], [], 0
+    for i in range(n_steps):
+        Ud = rng.random((B, k)).astype(np.float32)
+        Uv = np.minimum(rng.random((B, k, 3)).astype(np.float32), np.float32(0.99999))
+        t0 = time.perf_counter()
+        d, P = dr.draft(seqs, k, Ud)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        drafts = {b: (d[b], None) for b in seqs}
+        n0 = [len(sess.tokens[b]) for b in seqs]
+        sess.step(drafts, via.Sampling(0.0, 1.0, P, Uv))
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        dr.sync({b: sess.tokens[b][n0[b]:] for b in seqs})
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        if i >= warmup:
+            t_draft.append(t1 - t0)
+            t_verify.append(t2 - t1)
+            t_sync.append(t3 - t2)
+            accepted += sum(len(sess.tokens[b]) - n0[b] for b in seqs)
+    dkv.close()
+    dm.close()
+    sess.kv.close()
+    tot = sum(t_draft) + sum(t_verify) + sum(t_sync)
+    # algorithmic bytes of drafting: k probe forwards, each the route's
+    # weights and the head (the cached K/V the probes read is small beside it)
+    from workload.configs import model_bytes
+    mb = model_bytes(md, list(route_d))
+    draft_gbs = k * (mb["layers"] + mb["head"]) / float(np.mean(t_draft)) / 1e9
+    return {"drafter_route": list(route_d), "temperature": temperature, "alpha": 0.0, "beta": 1.0,
+            "value": round(accepted / tot, 2), "unit": "tokens/s (drafting included)", "steps": steps,
+            "tokens_per_step": round(accepted / steps, 3),
+            "ms_draft": round(1e3 * float(np.mean(t_draft)), 3), "ms_verify": round(1e3 * float(np.mean(t_verify)), 3),
+            "ms_drafter_sync": round(1e3 * float(np.mean(t_sync)), 3),
+            "draft_achieved_GBs": round(draft_gbs, 1), "draft_frac_of_hbm_peak": round(draft_gbs / HBM_PEAK_GBS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -231,6 +297,7 @@ def main():
                     help="skip the T = 1 variant (every position escalated to the full verifier)")
     ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
     ap.add_argument("--no-sampling", action="store_true", help="skip the sampling-rules variant")
+    ap.add_argument("--no-drafter", action="store_true", help="skip the drafter-model variant")
     ap.add_argument("--no-prefill-gemm", action="store_true", help="skip the prefill GEMM roofline")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (the reference kernel for HBM counter scaling)")
@@ -308,6 +375,12 @@ def main():
                    "escalation_rate": round(rs["escalation"], 3), "replay_mismatch_steps": rs["mismatch"],
                    "decide_launches": n, "decide_avg_us": round(ms * 1e3 / max(1, n), 2)}
 
+    # the serving loop with a drafter model nested in the slim route (its
+    # first layer), drafting included in the time
+    drafter = None
+    if not args.no_drafter and cfg["draft"] == "chain":
+        drafter = run_drafter_variant(cfg, W, max(5, args.steps // 5), 2, T, cfg["route"][:1])
+
     breakdown = None
     if args.breakdown:
         breakdown = {}
@@ -346,6 +419,7 @@ def main():
         "step_roofline": step_roof,
         "full_tier_variant": full_tier,
         "sampling_rules_variant": sampled,
+        "drafter_model_variant": drafter,
         "prefill_gemm_roofline": prefill,
         "dimr_cost_roofline": dimr,
         "cpu_baseline": cpu,

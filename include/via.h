@@ -341,6 +341,21 @@ typedef struct {
 via_status via_tier_decide_sampled(via_kv *kv, const via_tier_params *p, const via_verify_out *slim,
                                    const via_verify_out *full, const via_sampling *smp, via_decision *dec,
                                    void *stream);
+/* Draw one token per requested row from softmax(l/T) of a forward's logits
+ * (the drafter's draw: App. A's p is this distribution).  For i < n the
+ * row is out rows row[i] (host, each in [0, out_rows), the row count of the
+ * forward that wrote `out`); the token is the first id whose running weight
+ * exp((l - max)/T) exceeds uniforms[i] (host, in [0, 1)) times the total,
+ * written to tokens[i] (device).  probs (device, nullable) receives each
+ * row's probabilities exp((l - max)/T) / row_sumexp at probs[i * probs_ld
+ * + v] (probs_ld >= vocab).
+ * temperature must be the one the forward's statistics were taken at.
+ * Uses the handle's workspace: call it on the handle's stream, between
+ * steps or inside one.  EINVAL for n outside [0, max_batch] or bad
+ * arguments. */
+via_status via_sample_rows(via_kv *kv, const via_verify_out *out, int32_t out_rows, int32_t n, const int32_t *row,
+                           float temperature, const float *uniforms, int32_t *tokens, float *probs,
+                           int32_t probs_ld, void *stream);
 /* Commit the open step from dec->h_packed (read on the host: synchronise
  * first).  Appends kappa drafts (+ emit) per sequence: slim valid length
  * becomes n'-1; full valid length becomes n'-1 if the full verifier ran

@@ -212,9 +212,14 @@ struct DecideArgs {
   int vocab;
   SampleReq* req;             // [batch]
   double* slice_sum;          // [batch * kSampleSlices * 2] per-slice weight sums
+  int32_t* tok_out;           // drawn tokens [batch]; null: the decision's emit slots
 };
 // Decision kernel, then (sampling rules) the sampling kernel that fills the
 // emitted tokens it left open.
 void launch_decide(const DecideArgs& a, hipStream_t s);
+// Draws of the requests in a.req (kind 1 over a.s_logits rows) into
+// a.tok_out; with probs, also writes each request row's softmax
+// exp((l - max) / T) / s_row_sumexp as probs[i * probs_ld + v].
+void launch_sample_rows(const DecideArgs& a, float* probs, int probs_ld, hipStream_t s);
 
 }  // namespace via

@@ -565,7 +565,24 @@ __global__ __launch_bounds__(kSampleThreads) void sample_pick_kernel(DecideArgs 
       }
     }
   }
-  a.packed[2 * a.batch + b] = tok >= 0 ? tok : lastpos;
+  const int drawn = tok >= 0 ? tok : lastpos;
+  if (a.tok_out)
+    a.tok_out[b] = drawn;
+  else
+    a.packed[2 * a.batch + b] = drawn;
+}
+
+// probs[i * ld + v] = exp((l - max) / T) / sum for request i's row.
+__global__ __launch_bounds__(kSampleThreads) void sample_probs_kernel(DecideArgs a, float* probs, int ld) {
+  const int i = blockIdx.y;
+  const SampleReq r = a.req[i];
+  const SampleGeom geo = sample_geom(a.vocab);
+  const float* lg = a.s_logits + (size_t)r.out * a.vocab;
+  const float mx = a.s_row_max[r.out], inv_z = 1.f / a.s_row_sumexp[r.out];
+  float* o = probs + (size_t)i * ld;
+  const int lo = blockIdx.x * geo.slice;
+  const int hi = min(a.vocab, lo + geo.slice);
+  for (int v = lo + threadIdx.x; v < hi; v += kSampleThreads) o[v] = expf((lg[v] - mx) * a.inv_T) * inv_z;
 }
 
 }  // namespace
@@ -577,6 +594,13 @@ void launch_decide(const DecideArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(sample_sums_kernel, dim3(g.G, a.batch), dim3(kSampleThreads), 0, s, a);
     hipLaunchKernelGGL(sample_pick_kernel, dim3(a.batch), dim3(kSampleThreads), 0, s, a);
   }
+}
+
+void launch_sample_rows(const DecideArgs& a, float* probs, int probs_ld, hipStream_t s) {
+  const SampleGeom g = sample_geom(a.vocab);
+  hipLaunchKernelGGL(sample_sums_kernel, dim3(g.G, a.batch), dim3(kSampleThreads), 0, s, a);
+  hipLaunchKernelGGL(sample_pick_kernel, dim3(a.batch), dim3(kSampleThreads), 0, s, a);
+  if (probs) hipLaunchKernelGGL(sample_probs_kernel, dim3(g.G, a.batch), dim3(kSampleThreads), 0, s, a, probs, probs_ld);
 }
 
 void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KVH, int hd, const int32_t* btab,

@@ -1279,6 +1279,43 @@ via_status via_tier_decide_sampled(via_kv* kv, const via_tier_params* p, const v
   return decide_impl(kv, p, slim, full, smp, dec, stream);
 }
 
+via_status via_sample_rows(via_kv* kv, const via_verify_out* out, int32_t out_rows, int32_t n, const int32_t* row,
+                           float temperature, const float* uniforms, int32_t* tokens, float* probs, int32_t probs_ld,
+                           void* stream) {
+  if (!kv || !out) return fail(VIA_EINVAL, "null argument");
+  if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
+  if (n < 0 || n > kv->d.max_batch) return fail(VIA_EINVAL, "need 0 <= n <= max_batch");
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(VIA_EINVAL, "temperature must be > 0");
+  if (probs && probs_ld < kv->m->d.vocab) return fail(VIA_EINVAL, "probs_ld must be >= vocab");
+  if (n == 0) return VIA_OK;
+  if (!out->logits || !out->row_max || !out->row_sumexp || !tokens || !row || !uniforms)
+    return fail(VIA_EINVAL, "logits, row statistics, rows, uniforms and tokens are required");
+  std::vector<SampleReq> req(n);
+  for (int i = 0; i < n; ++i) {
+    if (row[i] < 0 || row[i] >= out_rows) return fail(VIA_EINVAL, "row %d outside [0, %d)", row[i], out_rows);
+    if (!(uniforms[i] >= 0.f && uniforms[i] < 1.f)) return fail(VIA_EINVAL, "uniforms must lie in [0, 1)");
+    req[i] = SampleReq{1, row[i], i, uniforms[i]};
+  }
+  const Layout& L = kv->L;
+  hipStream_t s = (hipStream_t)stream;
+  via_status st = upload(kv, kv->ws + L.sreq, req.data(), (size_t)n * sizeof(SampleReq), s);
+  if (st) return st;
+  DecideArgs a{};
+  a.batch = n;
+  a.max_drafts = 1;
+  a.s_logits = out->logits;
+  a.s_row_max = out->row_max;
+  a.s_row_sumexp = out->row_sumexp;
+  a.inv_T = 1.0f / temperature;
+  a.beta = 1.f;
+  a.vocab = kv->m->d.vocab;
+  a.req = (SampleReq*)(kv->ws + L.sreq);
+  a.slice_sum = (double*)(kv->ws + L.ssum);
+  a.tok_out = tokens;
+  launch_sample_rows(a, probs, probs_ld, s);
+  return hip_check(kv, hipGetLastError(), "sample launch");
+}
+
 via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* stream) {
   if (!kv || !dec || !dec->h_packed) return fail(VIA_EINVAL, "null argument");
   if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");

@@ -287,3 +287,64 @@ class GreedyDrafter:
                 rep, tok = self.corrupt(q, step, j)
                 drafts[q].append(tok if rep else g)
         return drafts
+
+
+class ModelDrafter:
+    """Drafter model on the same kernels: its temperature-T softmax is the
+    drafting distribution p of the sampling rules (App. A).  The model may
+    share the verifier's weights under a shallower route (a nested mask
+    inside the slim route) or be a separate small model with the same
+    vocabulary.
+
+    It keeps its own cache of the committed prefix (the model's route, slim
+    cache of its own handle).  ``draft`` feeds the pending token and the
+    drafts so far as probe rows (no change to the cache) and draws each next
+    token from p with ``via_sample_rows``; ``sync`` appends the tokens a
+    verify step committed (a forced-accept step of the drafter's handle).
+    """
+
+    def __init__(self, model: via.Model, kv: via.KV, temperature=1.0):
+        self.sess = Session(model, kv, via.tier_params(0.9, 0.5, temperature, via.FORCED_ACCEPT), logits=True)
+        self.T = float(temperature)
+        self.V = model.desc["vocab"]
+        self.tok = torch.empty(kv.max_batch, dtype=torch.int32, device="cuda")
+
+    def attach(self, seq, tokens):
+        self.sess.prefill(seq, tokens)
+
+    def release(self, seq):
+        self.sess.release(seq)
+
+    def draft(self, seqs, k, uniforms=None):
+        """k drafts per sequence: ({seq: tokens}, p) with p the drafting
+        distributions as a device fp32 [len(seqs), k, V] tensor (the layout
+        ``via.Sampling`` takes).  ``uniforms`` (host [len(seqs), k] in
+        [0, 1)) selects the draws; None drafts greedily (lowest id among the
+        maxima)."""
+        s = self.sess
+        B, V = len(seqs), self.V
+        P = torch.empty((B, k, V), dtype=torch.float32, device="cuda")
+        drafts = {q: [] for q in seqs}
+        U = np.zeros((B, k), np.float32) if uniforms is None else np.ascontiguousarray(uniforms, np.float32)
+        for j in range(k):
+            rows = [[s.tokens[q][-1]] + drafts[q] for q in seqs]
+            w = via.WindowBuf(seqs, rows, [[] for _ in seqs], [[] for _ in seqs], max_drafts=1)
+            via.check(via.via_verify_probe(s.m.h, s.kv.h, via.CACHE_SLIM, C.byref(w.c), C.byref(s.p),
+                                           C.byref(s.out_slim.c), s.sp()))
+            R = w.max_rows
+            r, rp = via._i32([b * R + len(rows[b]) - 1 for b in range(B)])
+            u = np.ascontiguousarray(U[:, j])
+            via.check(via.via_sample_rows(s.kv.h, C.byref(s.out_slim.c), B * R, B, rp, self.T, u.ctypes.data,
+                                          self.tok.data_ptr(), P[:, j].data_ptr(), k * V, s.sp()))
+            got = (s.out_slim.row_argmax[r.tolist()] if uniforms is None else self.tok[:B]).cpu().tolist()
+            for b, q in enumerate(seqs):
+                drafts[q].append(int(got[b]))
+        return drafts, P
+
+    def sync(self, new_tokens: dict):
+        """Append the tokens each sequence committed ({seq: [tokens]}; empty
+        lists are skipped)."""
+        todo = {q: (list(t), None) for q, t in new_tokens.items() if len(t)}
+        if todo:
+            h, _ = self.sess.step(todo)
+            assert (np.asarray(h["status"]) == 0).all()

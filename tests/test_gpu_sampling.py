@@ -38,9 +38,9 @@ if not torch.cuda.is_available():  # pragma: no cover
 from oracle.decode import (FORCED_FULL, FORCED_NONE, FORCED_SLIM, Draft, GreedyDrafter,  # noqa: E402
                            TierParams, Verifier)
 from oracle.model import OracleModel  # noqa: E402
-from oracle.sampling import accept_prob, residual, tempered  # noqa: E402
+from oracle.sampling import accept_prob, inverse_cdf, residual, tempered  # noqa: E402
 from paper_2606_12243_amd import via  # noqa: E402
-from paper_2606_12243_amd.session import Session  # noqa: E402
+from paper_2606_12243_amd.session import ModelDrafter, Session  # noqa: E402
 from workload import configs, gen  # noqa: E402
 
 TIER_CODE = {"A": 0, "S": 1, "F": 2}
@@ -70,7 +70,8 @@ def pick_uniform(w, err, rng):
 
 
 class SampledLockstep:
-    def __init__(self, name, params, alpha, beta, greedy_drafts=False, seed=0, batch=3, k=4):
+    def __init__(self, name, params, alpha, beta, greedy_drafts=False, seed=0, batch=3, k=4, drafter_route=None,
+                 drafter_T=1.0):
         cfg = configs.get(name)
         cfg["seed_c"] = 21 + seed
         cfg["seed_d"] = 31 + seed
@@ -92,6 +93,16 @@ class SampledLockstep:
             V = self.md["vocab"]
             self.drafter = GreedyDrafter(self.om, lambda b, step, j: gen.corruption(cfg["seed_d"], b, step, j,
                                                                                       0.3, V))
+        # drafter model on the same weights under a shallower route (GPU:
+        # ModelDrafter; oracle: cache-free forwards of that route)
+        self.dr, self.rel_p = None, 0.0
+        if drafter_route is not None:
+            self.dr_route, self.dr_T = list(drafter_route), float(drafter_T)
+            self.dr_model = via.Model(self.md, W, self.dr_route)
+            self.dr_kv = via.KV(self.dr_model, max_seqs=batch, max_blocks_per_seq=16, blocks_full=64,
+                                blocks_slim=64, max_rows=64, max_batch=batch, max_drafts=8)
+            self.dr = ModelDrafter(self.dr_model, self.dr_kv, self.dr_T)
+            self.rel_p = math.exp(2 * logit_tol(self.md) / self.dr_T) - 1
         self.oid = {}
         for b in range(batch):
             toks = gen.context_tokens(cfg, b, 9 + 5 * b)
@@ -99,11 +110,44 @@ class SampledLockstep:
             self.sess.prefill(b, toks)
             if self.drafter:
                 self.drafter.attach(b)
+            if self.dr:
+                self.dr.attach(b, toks)
         self.stats = dict(exact=0, loose=0, kept=0, rejected=0, slim=0, fallback=0, steps=0)
 
     def close(self):
+        if self.dr:
+            self.dr_kv.close()
+            self.dr_model.close()
         self.kv.close()
         self.gm.close()
+
+    def model_drafts(self, order):
+        """Drafts of the drafter model: the oracle picks each uniform
+        (margin-safe midpoint of a token's interval under its own p) and its
+        token; the GPU drafter draws with the same uniforms.  Compared: the
+        tokens (exactly) and p (within the induced relative error)."""
+        U = np.zeros((len(order), self.k), np.float32)
+        drafts, probs = {}, {}
+        for i, b in enumerate(order):
+            pre = list(self.ver.seqs[self.oid[b]].tokens)
+            d, rows = [], []
+            for j in range(self.k):
+                lg = self.om.forward_sequence(pre + d, self.dr_route)[-1]
+                p = tempered(lg, self.dr_T)
+                u, exact, lo, hi = pick_uniform(p, 2 * self.rel_p, self.rng)
+                assert exact, "no token interval is wide enough for an exact draw"
+                U[i, j] = u
+                d.append(inverse_cdf(p, u))
+                rows.append(p)
+            drafts[b], probs[b] = Draft.chain(d), torch.stack(rows)
+        dg, P = self.dr.draft(order, self.k, U)
+        for i, b in enumerate(order):
+            assert dg[b] == drafts[b].tok, f"drafter tokens {dg[b]} vs oracle {drafts[b].tok}"
+            pg = P[i].double().cpu()
+            err = (pg - probs[b]).abs() - (self.rel_p * probs[b] + 1e-7)
+            assert float(err.max()) <= 0, f"drafter p off by {float((pg - probs[b]).abs().max())}"
+        self.stats["drafted"] = self.stats.get("drafted", 0) + len(order) * self.k
+        return drafts, probs, P
 
     def drafts(self, step):
         V = self.md["vocab"]
@@ -131,8 +175,12 @@ class SampledLockstep:
 
     def step(self, step):
         T = self.p.temperature
-        drafts = self.drafts(step)
-        probs = self.probs(drafts)
+        P_dev = None
+        if self.dr:
+            drafts, probs, P_dev = self.model_drafts(list(range(self.B)))
+        else:
+            drafts = self.drafts(step)
+            probs = self.probs(drafts)
         order = sorted(drafts)
         oids = {b: self.oid[b] for b in order}
         D = max(len(drafts[b].tok) for b in order)
@@ -156,7 +204,7 @@ class SampledLockstep:
                 if do["full_ran"]:
                     q = tempered(do["full_logits"][row], T)
                     a = accept_prob(float(q[x]), float(probs[b][j, x]), self.alpha)
-                    m = rel * a + 1e-6
+                    m = (rel + self.rel_p) * a + 1e-6
                     can_keep, can_reject = a - m > 0, a + m < 1
                     keep = can_keep and (not can_reject or self.rng.random() < 0.6)
                     u0 = self.rng.uniform(0.0, a - m) if keep else self.rng.uniform(a + m, 1.0) if can_reject else 0.5
@@ -166,7 +214,7 @@ class SampledLockstep:
                         err = 2 * rel
                         self.stats["fallback"] += 1
                     else:
-                        err = 2 * rel * (float(q.sum()) / self.beta) / float(r.sum())
+                        err = 2 * (rel * float(q.sum()) / self.beta + self.rel_p) / float(r.sum())
                     U[i, j, 2], ex2, lo2, hi2 = pick_uniform(r, err, self.rng)
                     checks[(b, j, 2)] = (ex2, lo2, hi2, err)
         # the oracle's real step
@@ -176,10 +224,12 @@ class SampledLockstep:
                                             u={oids[b]: U[i, :len(drafts[b].tok)].astype(np.float64).tolist()
                                                for i, b in enumerate(order)}))
         # the GPU step: same drafts, p, uniforms
-        P = torch.full((self.B, D, self.md["vocab"]), 1.0 / self.md["vocab"], dtype=torch.float32)
-        for i, b in enumerate(order):
-            P[i, :len(drafts[b].tok)] = probs[b].float()
-        smp = via.Sampling(self.alpha, self.beta, P.cuda(), U)
+        if P_dev is None:
+            P = torch.full((self.B, D, self.md["vocab"]), 1.0 / self.md["vocab"], dtype=torch.float32)
+            for i, b in enumerate(order):
+                P[i, :len(drafts[b].tok)] = probs[b].float()
+            P_dev = P.cuda()
+        smp = via.Sampling(self.alpha, self.beta, P_dev, U)
         gd = {b: (drafts[b].tok, None) for b in order}
         w, h, run = self.sess.begin(gd, smp)
         tiers_g = self.sess.dec.tier.cpu().numpy()
@@ -226,9 +276,14 @@ class SampledLockstep:
             pp = dec_o[oids[b]]["path"]
             path[i, :len(pp)] = pp
         hh["path"] = path
+        n0 = {b: len(self.sess.tokens[b]) for b in order}
         self.sess.commit(w, gd, h=hh)
         for b in order:
             assert self.sess.tokens[b] == self.ver.seqs[oids[b]].tokens
+        if self.dr:
+            self.dr.sync({b: self.sess.tokens[b][n0[b]:] for b in order})
+            for b in order:
+                assert self.dr.sess.tokens[b] == self.sess.tokens[b]
         self.stats["steps"] += 1
 
 
@@ -264,6 +319,57 @@ def test_sampled_decisions_match_oracle(name, params, alpha, beta, greedy):
             assert st["exact"] > 0
     finally:
         ls.close()
+
+
+@pytest.mark.parametrize("params,alpha,beta,drafter_T", [
+    (TierParams(0.9, 0.5, 1.0, FORCED_FULL), 0.0, 1.0, 1.0),
+    (TierParams(0.6, 0.05, 1.0, FORCED_NONE), 0.2, 1.0, 0.7),
+])
+def test_model_drafter_and_sampled_verification(params, alpha, beta, drafter_T):
+    """Drafts and p from a drafter model (the micro model's layer 0, nested in
+    the slim route [0, 2]) against the oracle's forwards of that route, then
+    the sampled verification of those drafts, for several steps (the
+    drafter's cache follows the committed tokens)."""
+    print(f"[case] model drafter forced={params.forced} alpha={alpha} drafter T={drafter_T}", flush=True)
+    ls = SampledLockstep("micro_f32", params, alpha, beta, seed=5 + params.forced, drafter_route=[0],
+                         drafter_T=drafter_T)
+    try:
+        for step in range(4):
+            ls.step(step)
+        print(f"[done] {ls.stats}", flush=True)
+        assert ls.stats["drafted"] == 4 * ls.B * ls.k and ls.stats["exact"] > 0
+    finally:
+        ls.close()
+
+
+def test_sample_rows_rejects_bad_arguments():
+    cfg = configs.get("micro_f32")
+    cfg["seed_c"] = 3
+    md = cfg["model"]
+    W = gen.model_weights(cfg)
+    gm = via.Model(md, W, cfg["route"])
+    kv = via.KV(gm, max_seqs=2, max_blocks_per_seq=8, blocks_full=16, blocks_slim=16, max_rows=16,
+                max_batch=2, max_drafts=4)
+    try:
+        out = via.Out(2, 8, 4, md["vocab"], logits=True)
+        tok = torch.zeros(2, dtype=torch.int32, device="cuda")
+        sp = C.c_void_p(0)
+        u = np.array([0.5, 0.5], np.float32)
+        ok_r, ok_rp = via._i32([0, 3])
+        call = lambda n, rows, uu, T=1.0, ld=md["vocab"]: via.via_sample_rows(  # noqa: E731
+            kv.h, C.byref(out.c), 16, n, rows, T, uu.ctypes.data, tok.data_ptr(), None, ld, sp)
+        assert call(3, ok_rp, u) == via.EINVAL                         # n > max_batch
+        r2, rp2 = via._i32([0, 16])
+        assert call(2, rp2, u) == via.EINVAL                           # row outside [0, out_rows)
+        assert call(2, ok_rp, np.array([0.5, 1.0], np.float32)) == via.EINVAL
+        assert call(2, ok_rp, u, T=0.0) == via.EINVAL
+        assert via.via_sample_rows(kv.h, C.byref(out.c), 16, 2, ok_rp, 1.0, u.ctypes.data, tok.data_ptr(),
+                                   out.logits.data_ptr(), md["vocab"] - 1, sp) == via.EINVAL  # probs_ld < vocab
+        assert call(0, ok_rp, u) == via.OK
+        torch.cuda.synchronize()
+    finally:
+        kv.close()
+        gm.close()
 
 
 def test_sampled_decide_rejects_bad_arguments():
