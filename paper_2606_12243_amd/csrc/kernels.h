@@ -79,9 +79,11 @@ int gate_up_blocks_per_group(int F);
 // x^2 over column chunks to ss[chunk * ss_stride + row]: the consumer of the
 // next projection multiplies its output row by row_scale() (RMSNorm).
 // Xcopy (nullable): the updated rows are also stored there ([M, d] fp32).
+// E (nullable, model dtype [vocab, d]): X[m] is first set to the embedding
+// row of token erows[m].tok (P is then ignored).
 void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
                       void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s,
-                      float* Xcopy = nullptr);
+                      float* Xcopy = nullptr, const void* E = nullptr, const RowInfo* erows = nullptr);
 
 // One row of a full forward that starts after the P layers the slim route
 // shares with it (route layer i == i for i < P).
@@ -137,9 +139,6 @@ void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s);
 void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int ntiles, float inv_T,
                         int32_t* row_argmax, float* row_max, float* row_sumexp, float* row_gap,
                         hipStream_t s);
-
-// Embedding gather into the fp32 residual stream.
-void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, float* X, hipStream_t s);
 
 struct AttnArgs {
   const void* q_hi;        // [M, H, hd] bf16 hi terms of Q (fp32 models: fp32 Q)

@@ -8,13 +8,6 @@ namespace via {
 
 namespace {
 
-template <typename T>
-__global__ __launch_bounds__(256) void embed_kernel(const T* E, const RowInfo* rows, int d, float* X) {
-  const int m = blockIdx.x;
-  const T* e = E + (size_t)rows[m].tok * d;
-  for (int i = threadIdx.x; i < d; i += 256) X[(size_t)m * d + i] = to_f<T>(e[i]);
-}
-
 // Split partials of two float4s (offsets o0 and o1): split_load16 issues
 // the loads of splits 0..15 (past the last split it re-reads the last one:
 // unconditional loads keep the code branch-free), split_reduce16 sums them
@@ -66,7 +59,8 @@ __device__ __forceinline__ void split_sum2(const float* P, size_t stride, int ks
 template <typename G, bool BF16, int NT>
 __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P, int ksplit, int M, int d,
                                                        const G* g, void* Y, int MBn, const RowInfo* rows,
-                                                       float* ss, int ss_stride, float* Xcopy) {
+                                                       float* ss, int ss_stride, float* Xcopy, const G* E,
+                                                       const RowInfo* erows) {
   const int m = blockIdx.y, chunk = blockIdx.x;
   const int k0 = chunk * kNormChunk + threadIdx.x * 8;
   const int out = rows ? rows[m].lm : m;
@@ -74,7 +68,20 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
   const size_t stride = (size_t)M * d;
   float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float sq = 0.f;
-  if (k0 < d) {
+  if (k0 < d && E) {
+    // embedding rows: X[m] = E[tok]
+    const G* e = E + (size_t)erows[m].tok * d + k0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = to_f<G>(e[i]);
+    *(float4*)(x + k0) = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(x + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    if (Xcopy) {
+      *(float4*)(Xcopy + (size_t)m * d + k0) = make_float4(v[0], v[1], v[2], v[3]);
+      *(float4*)(Xcopy + (size_t)m * d + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sq += v[i] * v[i];
+  } else if (k0 < d) {
     float4 acc[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
     if (P) split_sum2(P, stride, ksplit, 0, (size_t)m * d + k0, (size_t)m * d + k0 + 4, acc[0], acc[1]);
 #pragma unroll
@@ -332,25 +339,19 @@ __global__ __launch_bounds__(128) void kv_move_kernel(T* pool, int nblk, int KVH
 
 }  // namespace
 
-void launch_embed(bool bf16, const void* E, const RowInfo* rows, int M, int d, float* X, hipStream_t s) {
-  if (bf16)
-    hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, s, (const uint16_t*)E, rows, d, X);
-  else
-    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)E, rows, d, X);
-}
-
 void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
-                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s, float* Xcopy) {
+                      void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s, float* Xcopy,
+                      const void* E, const RowInfo* erows) {
   const dim3 grid((d + kNormChunk - 1) / kNormChunk, M);
   if (!bf16)
     hipLaunchKernelGGL((resid_add_kernel<float, false, 1>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const float*)g, Y, MBn, rows, ss, ss_stride, Xcopy);
+                       (const float*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const float*)E, erows);
   else if (terms >= 3)
     hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 3>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy);
+                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const uint16_t*)E, erows);
   else
     hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 2>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy);
+                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const uint16_t*)E, erows);
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {

@@ -447,10 +447,10 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     pa.full_pool = kv->d.pool_full;
     pa.full_blocks = kv->d.blocks_full;
     launch_prefix_copy(bf, pa, s);
-  } else {
-    launch_embed(bf, m->embed, d_rows, M, D.d, X, s);
   }
-  launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[start_si]], Yf, MBn, nullptr, ss, ss_stride, s);
+  // first layer's input norm; from layer 0 it also gathers the embedding rows into X
+  launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[start_si]], Yf, MBn, nullptr, ss, ss_stride, s,
+                   nullptr, start_si > 0 ? nullptr : m->embed, d_rows);
   at.q_hi = Q;
   at.q_lo = Qlo;
   at.pool = pool;
