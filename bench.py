@@ -395,6 +395,8 @@ def main():
         prefill = prefill_gemm_roofline(md, min(8192, int(sum(cfg["ctx_lens"]))))
 
     dimr = dimr_cost_roofline(md)
+    dimr["at_1024_rows"] = {k: v for k, v in dimr_cost_roofline(md, rows=1024).items()
+                            if k in ("us", "bytes_per_launch", "achieved", "frac")}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -4,9 +4,9 @@
 // l = log softmax(logits / T):
 //   R = sum_v p(v) ReLU(log(1-alpha) + l_p(v) - l_q(v))
 //     + sum_v q(v) ReLU(log(beta)    + l_p(v) - l_q(v)).
-// One work-group per row streams both rows twice: an online (max, sum of
-// exponentials) pass for the two log-partition functions, then the cost
-// pass.  Partial sums are combined in a fixed order (fp64), so the result is
+// One 1024-thread work-group per row streams both rows twice (16 loads of
+// each matrix in flight per thread): an online (max, sum of exponentials)
+// pass for the two log-partition functions, then the cost pass.  Partial sums are combined in a fixed order (fp64), so the result is
 // reproducible.
 #include "kernels.h"
 
@@ -14,7 +14,10 @@ namespace via {
 
 namespace {
 
-constexpr int kDimrThreads = 256;
+constexpr int kDimrThreads = 1024;
+// ids per thread per round: all their loads are issued before any use, so a
+// thread keeps kDimrUnroll loads of each matrix in flight
+constexpr int kDimrUnroll = 16;
 
 __device__ __forceinline__ void online_add(float& m, float& s, float z) {
   if (z > m) {
@@ -43,10 +46,22 @@ __global__ __launch_bounds__(kDimrThreads) void dimr_cost_kernel(DimrArgs a) {
   const float* p = a.p + (size_t)row * a.ld;
   __shared__ float sm[4][kDimrThreads];
   __shared__ double sd[2][kDimrThreads];
+  constexpr int kRound = kDimrThreads * kDimrUnroll;
   float mq = -INFINITY, sq = 0.f, mp = -INFINITY, sp = 0.f;
-  for (int v = t; v < a.vocab; v += kDimrThreads) {
-    online_add(mq, sq, q[v] * a.inv_T);
-    online_add(mp, sp, p[v] * a.inv_T);
+  for (int base = 0; base < a.vocab; base += kRound) {
+    float zq[kDimrUnroll], zp[kDimrUnroll];
+#pragma unroll
+    for (int u = 0; u < kDimrUnroll; ++u) {
+      const int v = min(base + u * kDimrThreads + t, a.vocab - 1);  // past the end: re-read, then dropped
+      zq[u] = q[v];
+      zp[u] = p[v];
+    }
+#pragma unroll
+    for (int u = 0; u < kDimrUnroll; ++u)
+      if (base + u * kDimrThreads + t < a.vocab) {
+        online_add(mq, sq, zq[u] * a.inv_T);
+        online_add(mp, sp, zp[u] * a.inv_T);
+      }
   }
   sm[0][t] = mq;
   sm[1][t] = sq;
@@ -71,13 +86,24 @@ __global__ __launch_bounds__(kDimrThreads) void dimr_cost_kernel(DimrArgs a) {
   const float lzq = sm[0][0] + logf(sm[1][0]);
   const float lzp = sm[2][0] + logf(sm[3][0]);
   double c1 = 0.0, c2 = 0.0;
-  for (int v = t; v < a.vocab; v += kDimrThreads) {
-    const float lq = q[v] * a.inv_T - lzq;
-    const float lp = p[v] * a.inv_T - lzp;
-    const float d = lp - lq;
-    const float z1 = a.log_1m_alpha + d, z2 = a.log_beta + d;
-    if (z1 > 0.f) c1 += (double)(expf(lp) * z1);
-    if (z2 > 0.f) c2 += (double)(expf(lq) * z2);
+  for (int base = 0; base < a.vocab; base += kRound) {
+    float zq[kDimrUnroll], zp[kDimrUnroll];
+#pragma unroll
+    for (int u = 0; u < kDimrUnroll; ++u) {
+      const int v = min(base + u * kDimrThreads + t, a.vocab - 1);
+      zq[u] = q[v];
+      zp[u] = p[v];
+    }
+#pragma unroll
+    for (int u = 0; u < kDimrUnroll; ++u) {
+      if (base + u * kDimrThreads + t >= a.vocab) continue;
+      const float lq = zq[u] * a.inv_T - lzq;
+      const float lp = zp[u] * a.inv_T - lzp;
+      const float d = lp - lq;
+      const float z1 = a.log_1m_alpha + d, z2 = a.log_beta + d;
+      if (z1 > 0.f) c1 += (double)(expf(lp) * z1);
+      if (z2 > 0.f) c2 += (double)(expf(lq) * z2);
+    }
   }
   sd[0][t] = c1;
   sd[1][t] = c2;
