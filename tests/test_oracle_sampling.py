@@ -117,3 +117,28 @@ def test_forced_escalation_with_zero_uniform_keeps_every_draft():
                    sampling=dict(alpha=0.0, beta=1.0, probs=probs, u={0: [[0.0, 0.5, 0.5]] * 4}))[0]
     assert dec["kappa"] == 4 and dec["emit"] == -1 and dec["full_ran"]
     assert ver.seqs[0].tokens[-4:] == d
+
+
+def test_sampled_walk_first_token_is_distributed_as_q():
+    """The walk itself (not only its rules): with escalated positions, the
+    lossless rule and the first draft drawn from p_0, the first committed
+    token (d_0 if kept, else the emitted sample) is distributed as q_0,
+    integrated over grids of the acceptance and residual uniforms.  A walk
+    that read the wrong uniform, the wrong p row or the wrong q row fails."""
+    V, G = 5, 48
+    g = torch.Generator().manual_seed(4)
+    fl = torch.randn(2, V, generator=g, dtype=torch.float64) * 1.5       # full logits, rows 0 and 1
+    p = torch.softmax(torch.randn(2, V, generator=g, dtype=torch.float64) * 1.5, -1)
+    q0 = tempered(fl[0], 1.0)
+    full = (fl, {"max": fl.max(dim=1).values.tolist()})
+    slim = (torch.zeros(2, V, dtype=torch.float64), None)
+    grid_g = (np.arange(G) + 0.5) / G
+    dist = np.zeros(V)
+    for d0 in range(V):
+        for u0 in grid_g:
+            for u2 in grid_g:
+                u = [[float(u0), 0.5, float(u2)], [0.99, 0.5, 0.5]]   # the second draft is never kept
+                dec = Verifier._walk_sampled(Draft.chain([d0, 0]), ["F", "F"], slim, full, 1.0, 0.0, 1.0, p, u)
+                first = d0 if dec["kappa"] >= 1 else dec["emit"]
+                dist[first] += float(p[0, d0]) / (G * G)
+    assert np.allclose(dist, q0.numpy(), atol=3.0 / G)
