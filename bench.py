@@ -367,7 +367,7 @@ def main():
     # the same workload under the sampling rules (App. A, lossless alpha = 0,
     # beta = 1): logits kept, the decision draws the owed samples
     sampled = None
-    if not args.no_sampling:
+    if not args.no_sampling and cfg["draft"] == "chain":  # the sampling rules take chain drafts
         rs = run_workload(cfg, W, max(5, args.steps // 3), 2, T, timer_kind=kinds["decide"], sampling=(0.0, 1.0))
         n, ms = rs["timer"]
         sampled = {"alpha": 0.0, "beta": 1.0, "temperature": T, "value": round(rs["value"], 2), "unit": "tokens/s",
