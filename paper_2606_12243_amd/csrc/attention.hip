@@ -317,6 +317,15 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
   const size_t stride_ml = (size_t)a.M * a.H * 2, stride_o = (size_t)a.M * a.H * HD;
   const float* pml = a.part_ml + ((size_t)row * a.H + head) * 2;
   const float* po = a.part_o + ((size_t)row * a.H + head) * HD + d0;
+  // the first 8 splits' outputs are loaded with the statistics (no
+  // dependence between them), so the common case is one round of loads
+  float4 v[8][2];
+#pragma unroll
+  for (int c = 0; c < 8; ++c)
+    if (c < n) {
+      v[c][0] = *(const float4*)(po + c * stride_o);
+      v[c][1] = *(const float4*)(po + c * stride_o + 4);
+    }
   float2 ml[kAttnMaxSplits];
 #pragma unroll
   for (int c = 0; c < kAttnMaxSplits; ++c)
@@ -331,13 +340,14 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
 #pragma unroll
   for (int c0 = 0; c0 < kAttnMaxSplits; c0 += 8) {
     if (c0 >= n) break;
-    float4 v[8][2];
+    if (c0 > 0) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
-      if (c0 + c < n) {
-        v[c][0] = *(const float4*)(po + (c0 + c) * stride_o);
-        v[c][1] = *(const float4*)(po + (c0 + c) * stride_o + 4);
-      }
+      for (int c = 0; c < 8; ++c)
+        if (c0 + c < n) {
+          v[c][0] = *(const float4*)(po + (c0 + c) * stride_o);
+          v[c][1] = *(const float4*)(po + (c0 + c) * stride_o + 4);
+        }
+    }
 #pragma unroll
     for (int c = 0; c < 8; ++c)
       if (c0 + c < n) {
