@@ -25,6 +25,8 @@ struct RowInfo {
   int32_t slot;     // cache slot the row's K/V are written to
   int32_t vis_len;  // slots [0, vis_len) are visible
   int32_t lm;       // index into the head rows, -1 if the row has no head output
+  int32_t blk;      // pool block holding `slot` (the sequence's block table entry slot / block size)
+  int32_t pad_;
   uint64_t mask;    // extra visible slots win_base + bit (tree rows)
 };
 

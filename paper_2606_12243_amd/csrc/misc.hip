@@ -169,8 +169,7 @@ __global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
     }
     return;
   }
-  const SeqInfo si = a.seqs[ri.seq];
-  const int blk = a.btab[si.bt + ri.slot / kBlock], t = ri.slot % kBlock;
+  const int blk = ri.blk, t = ri.slot % kBlock;
   T* pool = (T*)a.pool;
   if (hh < a.H + a.KVH) {
     const int gk = hh - a.H;

@@ -690,6 +690,7 @@ via_status build_verify_plan(via_kv* kv, int cache, const WinCopy& w, const std:
       r.pos = valid + i;
       r.seq = sidx;
       r.slot = valid + i;
+      r.blk = S.table[cache][r.slot / kBlock];
       r.vis_len = valid + i + 1;
       r.lm = -1;
       P.rows.push_back(r);
@@ -701,6 +702,7 @@ via_status build_verify_plan(via_kv* kv, int cache, const WinCopy& w, const std:
       r.pos = npos + w.row_depth[i];
       r.seq = sidx;
       r.slot = win_base + rr;
+      r.blk = S.table[cache][r.slot / kBlock];
       r.vis_len = w.tree ? win_base : win_base + rr + 1;
       r.mask = w.tree ? w.row_mask[i] : 0;
       r.lm = -1;
@@ -1124,6 +1126,7 @@ via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* 
         r.pos = i;
         r.seq = 0;
         r.slot = i;
+        r.blk = S.table[cache][i / kBlock];
         r.vis_len = i + 1;
         r.lm = -1;
         P.rows.push_back(r);
