@@ -37,7 +37,9 @@ Readings taken where the paper is silent or inconsistent:
 
 Parity pins: tests/test_oracle_decode.py (forced-full == greedy decoding,
 the lossless reduction of App. A; tier partition and monotonicity B.18-B.19;
-brute-force agreement; KV index invariants; chain == tree of branching 1).
+brute-force agreement; KV index invariants; chain == tree of branching 1;
+the tree walk against hand-worked walks, tests/golden/tree_walk_cases.json,
+and against the brute-force tree walk with natural tiers).
 """
 from __future__ import annotations
 

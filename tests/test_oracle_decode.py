@@ -273,3 +273,91 @@ def test_decode_is_deterministic(tiny):
     b, _, _ = run_decode(cfg, m, TierParams(0.9, 0.5, 1.0), 10)
     assert a.seqs[0].tokens == b.seqs[0].tokens
     assert a.block_table("slim", 0) == b.block_table("slim", 0)
+
+
+def _golden_tree():
+    return json.load(open(os.path.join(HERE, "golden", "tree_walk_cases.json")))
+
+
+@pytest.mark.parametrize("case", range(len(_golden_tree()["cases"])))
+def test_golden_tree_walk_cases(case):
+    """Hand-worked tree walks (tests/golden/tree_walk_cases.json) against both
+    the windowed oracle's gate walk and the brute-force tree walk."""
+    g = _golden_tree()
+    c = g["cases"][case]
+    rows = {k: torch.tensor(v, dtype=torch.float64) for k, v in g["rows"].items()}
+    T = g["temperature"]
+    p = TierParams(g["tau_acc"], g["tau_full"], T)
+    d = Draft(list(c["tok"]), list(c["parent"]))
+    row_nodes, draft_row, _, _ = d.layout()
+    zero = rows["Z"]
+    slim_rows = torch.stack([rows[c["slim"].get(str(u), "Z")] for u in row_nodes])
+    full_rows = torch.stack([rows[c["full"].get(str(u), "Z")] for u in row_nodes])
+    st = row_stats(slim_rows, T)
+    conf = [confidence(float(slim_rows[draft_row[j], d.tok[j]]), st["max"][draft_row[j]], T)
+            for j in range(len(d.tok))]
+    tiers = [tier_of(x, p) for x in conf]
+    want = c["expect"]
+    first = Verifier._walk(d, tiers, conf, st, None)
+    if want["full_used"]:
+        assert first["needs_full"] and first["status"] == 1, c["name"]
+        got = Verifier._walk(d, tiers, conf, st, row_stats(full_rows, 1.0))
+    else:
+        assert not first["needs_full"], c["name"]
+        got = first
+    assert (got["kappa"], got["path"], got["emit"], got["status"]) == \
+        (want["kappa"], want["path"], want["emit"], want["status"]), c["name"]
+    # the brute-force walk from probabilities (softmax of the same rows)
+    sm = lambda v, t: torch.softmax(v / t, dim=0)
+    bf = bruteforce.tree_walk(d.tok, d.parent, lambda u: sm(rows[c["slim"].get(str(u), "Z")], T),
+                              lambda u: sm(rows[c["full"].get(str(u), "Z")], 1.0), p.tau_acc, p.tau_full)
+    assert (bf["kappa"], bf["path"], bf["emit"], bf["status"], bf["full_used"]) == \
+        (want["kappa"], want["path"], want["emit"], want["status"], want["full_used"]), c["name"]
+    assert zero.abs().sum() == 0
+
+
+# T = 1 reaches the escalation branches (descend into argmax q, rewrite with
+# it) and slim rewrites; T = 8 accepts several siblings, so the choice by
+# confidence matters.
+@pytest.mark.parametrize("T,branches", [
+    (1.0, {"slim-rewrite", "escalate-rewrite", "escalate-descend"}),
+    (8.0, {"accept-first", "accept-by-confidence"}),
+])
+def test_tree_walk_natural_tiers_matches_bruteforce(tiny, T, branches):
+    """The windowed oracle on token trees with natural tiers (slim cache, lag
+    rows, tree mask, compaction) against the brute-force tree walk, which
+    recomputes q' and q for every node from its root path without a cache."""
+    cfg, m = tiny
+    p = TierParams(0.9, 0.5, T)
+    x = gen.context_tokens(cfg, 1, 24)
+    ver = Verifier(m, cfg["route"])
+    ver.prefill(x)
+    dr = GreedyDrafter(m, _corrupt(cfg, 0.3))
+    dr.attach(0)
+    seen = set()
+    for step in range(10):
+        tree = dr.tree(0, ver.seqs[0].tokens, [3, 4, 3], 2, step)
+        before = list(ver.seqs[0].tokens)
+        dec = ver.step({0: tree}, p)[0]
+        bf = bruteforce.verify_tree(m, cfg["route"], before, tree.tok, tree.parent, p.tau_acc, p.tau_full,
+                                    p.temperature)
+        assert (dec["kappa"], dec["path"], dec["emit"], dec["full_ran"]) == \
+            (bf["kappa"], bf["path"], bf["emit"], bf["full_used"]), f"step {step}"
+        # which branches of the rule this step took
+        u = -1
+        for j in dec["path"]:
+            kids = tree.children(u)
+            acc = [k for k in kids if dec["tiers"][k] == A]
+            if acc:
+                seen.add("accept-first" if j == kids[0] else "accept-by-confidence")
+            else:
+                seen.add("escalate-descend")
+            u = j
+        if dec["emit"] >= 0:
+            kids = tree.children(u)
+            seen.add("escalate-rewrite" if all(dec["tiers"][k] == F for k in kids) else "slim-rewrite")
+        elif tree.children(u):
+            raise AssertionError("walk stopped without a rewrite at a node with children")
+        else:
+            seen.add("leaf")
+    assert branches <= seen, seen
