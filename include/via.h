@@ -273,7 +273,14 @@ via_status via_kv_destroy(via_kv *kv);
  * contents are whatever the caller writes at those slots). */
 via_status via_kv_seq_reserve(via_kv *kv, int32_t seq_id, int32_t n_ctx);
 /* Attach `seq_id` and cache tokens[0..n) in both caches (full forward and
- * slim forward, causal; RoPE positions 0..n-1). */
+ * slim forward, causal; RoPE positions 0..n-1).  This is the committed
+ * prefix x that the verification loop of Alg. 1 starts from (App. B.1
+ * "Require"/"Ensure": the decoded sequence x grows from it); the paper does
+ * not discuss the cache itself, so both verifiers keeping their own cache of
+ * that prefix is this library's reading.  Forwards of more than 512 rows run
+ * on the compute-bound tile GEMM; longer prompts are fed in chunks of the
+ * handle's max_rows.  ENOMEM (nothing attached) when either pool lacks the
+ * blocks. */
 via_status via_prefill(via_model *m, via_kv *kv, int32_t seq_id, const int32_t *tokens, int32_t n,
                        void *stream);
 /* Detach a sequence and free its blocks.  Not during a step. */
@@ -290,12 +297,22 @@ via_status via_kv_seq_info(const via_kv *kv, int32_t seq_id, int32_t cache, int3
 
 /* Slim-verifier forward (route of via_model_set_route, slim cache) over the
  * window rows, then the fused head: per-row max/argmax/sum-exp and the
- * logit of every draft token.  Allocates cache blocks for the rows (ENOMEM
- * leaves state unchanged) and starts a step.  ESTATE if a step is open. */
+ * logit of every draft token.  This is the step of Alg. 1 (and its full form
+ * in App. B.1) that runs q' in parallel on the block's prefixes
+ * x_<t, ..., x_<t+gamma-1 to obtain q'_t..q'_{t+gamma-1}; q' = Pi_z(q) is the
+ * routed submodel of Sec. 3.3 reading q's own weights.  The per-row maximum
+ * is M' of App. B.2 (in logit form), the draft logits give q'(v) for the gate.
+ * Allocates cache blocks for the rows (ENOMEM leaves state unchanged) and
+ * starts a step.  ESTATE if a step is open. */
 via_status via_verify_slim(via_model *m, via_kv *kv, const via_window *win, const via_tier_params *p,
                            via_verify_out *out, void *stream);
 /* Full-verifier forward (all layers, full cache) for the sequences with
  * run[b] != 0 (host [batch]; NULL = all), over lag rows + window rows.
+ * This is the escalation branch of App. B.1 ("invoke q on prefix x_<t+j"
+ * when q' is not confident, region (B.3) of App. B.2): one batched forward
+ * serves every escalated position of a sequence's window.  The lag rows
+ * (committed tokens the full cache has not seen because q was not invoked
+ * on earlier steps) are this library's reading of the silent cache policy.
  * win must be the window of the open step; n_lag[b] must equal the full
  * cache's lag for each run sequence (ESTATE otherwise). */
 via_status via_verify_full(via_model *m, via_kv *kv, const via_window *win, const int32_t *run,
@@ -328,15 +345,15 @@ via_status via_tier_decide(via_kv *kv, const via_tier_params *p, const via_verif
  *                uniforms (b * max_drafts + j) * 3 + {0, 1, 2}; copied
  *                during the call. */
 typedef struct {
-  float alpha, beta; /* 0 <= alpha < 1, beta > 0 */
+  float alpha, beta; /* 0 <= alpha < 1, beta >= 1 - alpha (App. A, with Eq. A.3) */
   const float *draft_probs;
   const float *uniforms;
 } via_sampling;
 /* via_tier_decide under the sampling rules.  Both verify outputs must carry
  * logits (slim->logits, and full->logits when full is given); both decide
  * calls of a step take the same sampling arguments.  EUNSUPPORTED for tree
- * windows, EINVAL for alpha/beta out of range, missing arrays or a uniform
- * outside [0, 1).  Writes the decision as via_tier_decide does, with the
+ * windows, EINVAL for alpha outside [0, 1), beta < 1 - alpha, missing
+ * arrays or a uniform outside [0, 1).  Writes the decision as via_tier_decide does, with the
  * sampled token in `emit`. */
 via_status via_tier_decide_sampled(via_kv *kv, const via_tier_params *p, const via_verify_out *slim,
                                    const via_verify_out *full, const via_sampling *smp, via_decision *dec,
@@ -357,7 +374,11 @@ via_status via_sample_rows(via_kv *kv, const via_verify_out *out, int32_t out_ro
                            float temperature, const float *uniforms, int32_t *tokens, float *probs,
                            int32_t probs_ld, void *stream);
 /* Commit the open step from dec->h_packed (read on the host: synchronise
- * first).  Appends kappa drafts (+ emit) per sequence: slim valid length
+ * first).  This is the end of a block in Alg. 1 and App. B.1: append the
+ * accepted prefix x_t..x_{t+kappa-1} (plus the rewritten token at the
+ * earliest rewrite position j*) and discard the remaining suffix (Sec. 3.4,
+ * Step 4: the longest accepted prefix kappa is committed and decoding
+ * resumes after it).  Appends kappa drafts (+ emit) per sequence: slim valid length
  * becomes n'-1; full valid length becomes n'-1 if the full verifier ran
  * for that sequence this step, else it keeps lagging; blocks wholly past a
  * valid length are freed; tree steps move the accepted nodes' K/V to

@@ -404,7 +404,11 @@ class Verifier:
         st = self.seqs[b]
         n = st.n
         if dec["status"] == 2:
+            # not advanced: both caches keep their valid lengths, and the blocks
+            # this step's forwards took past them are freed like any others
             dec["new_len"] = n
+            self.idx_slim.trim(b, st.slim.valid)
+            self.idx_full.trim(b, st.full.valid)
             return
         new = [d.tok[j] for j in dec["path"]] + ([dec["emit"]] if dec["emit"] >= 0 else [])
         n2 = n + len(new)

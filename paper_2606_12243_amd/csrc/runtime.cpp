@@ -1217,8 +1217,10 @@ via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_ou
   memcpy(blob.data() + (L.dpar - L.step_seqs), w.draft_parent.data(), (size_t)B * Dd * 4);
   if (smp) {
     if (w.tree) return fail(VIA_EUNSUPPORTED, "sampling rules take chain drafts");
-    if (!(smp->alpha >= 0.f && smp->alpha < 1.f) || !(smp->beta > 0.f) || !std::isfinite(smp->beta))
-      return fail(VIA_EINVAL, "need 0 <= alpha < 1 and beta > 0");
+    // the residual of Eq. A.3 is defined for beta >= 1 - alpha (App. A)
+    if (!(smp->alpha >= 0.f && smp->alpha < 1.f) || !std::isfinite(smp->beta) ||
+        !((double)smp->beta >= 1.0 - (double)smp->alpha))
+      return fail(VIA_EINVAL, "need 0 <= alpha < 1 and beta >= 1 - alpha");
     if (!smp->draft_probs || !smp->uniforms) return fail(VIA_EINVAL, "draft_probs and uniforms are required");
     if (!slim->logits || (full && !full->logits)) return fail(VIA_EINVAL, "sampling needs the logits outputs");
     for (size_t i = 0; i < (size_t)B * Dd * 3; ++i)

@@ -8,9 +8,11 @@ accepted length, the emitted token, the new length, and both caches' valid
 lengths and block tables.  A difference is allowed only where the oracle
 itself is within 1e-3 of a decision boundary: a top-2 logit gap below 1e-3
 (argmax / full-tier check) or a draft logit within 1e-3 of a threshold
-(l'(d) - max l' vs T ln tau).  After such an exempt difference the GPU is
+(l'(d) - max l' vs T ln tau).  Exemptions are per sequence: a difference
+in a sequence's decision is allowed only when that sequence itself has an
+exempt position this step.  After such a difference the GPU is
 re-synchronised to the oracle's decision (its commit takes the oracle's
-kappa/emit) and the step is logged.
+kappa/emit) and the step is logged with the positions that allowed it.
 
 At full sizes the oracle can follow a sample of the batch (``sample``): the
 GPU still runs every sequence in the same launch, the sampled ones are
@@ -133,7 +135,7 @@ class Lockstep:
         via.check(via.via_tier_decide(s.kv.h, s.p, s.out_slim.c, None, s.dec.c, s.sp()))
         s.stream.synchronize()
         h1 = s._host(w)
-        exempt = False
+        exempt = {}   # batch entry -> the near-tie positions that allow it to differ
         T = p.temperature
         for i, b in enumerate(order):
             if b not in dec_o:
@@ -144,7 +146,7 @@ class Lockstep:
             for r in range(len(am)):
                 if am[r] != st["argmax"][r]:
                     assert st["gap"][r] < GAP_EXEMPT, f"slim argmax differs at gap {st['gap'][r]}"
-                    exempt = True
+                    exempt.setdefault(b, []).append(f"slim row {r} gap {st['gap'][r]:.2e}")
             D = w.max_drafts
             tier_g = s.dec.tier[i * D:i * D + len(drafts[b].tok)].cpu().numpy()
             for j, t in enumerate(do["tiers"]):
@@ -154,9 +156,9 @@ class Lockstep:
                     near = min(abs(dl - T * math.log(p.tau_acc)) if p.tau_acc > 0 else 1e9,
                                abs(dl - T * math.log(p.tau_full)) if p.tau_full > 0 else 1e9)
                     assert near < GAP_EXEMPT, f"tier of draft {j} differs ({tier_g[j]} vs {t}), margin {near}"
-                    exempt = True
+                    exempt.setdefault(b, []).append(f"draft {j} threshold margin {near:.2e}")
             if (h1["status"][i] == 1) != (do["first_status"] == 1):
-                assert exempt, f"escalation differs for seq {b}"
+                assert b in exempt, f"escalation differs for seq {b} without a near tie of its own"
         # full forward for the sequences the oracle escalated (keeps cache state in step)
         run = np.array([(1 if dec_o[b]["full_ran"] else 0) if b in dec_o else int(h1["status"][i] == 1)
                         for i, b in enumerate(order)], np.int32)
@@ -174,9 +176,9 @@ class Lockstep:
                 for rr in range(len(am)):
                     if am[rr] != st["argmax"][rr]:
                         assert st["gap"][rr] < GAP_EXEMPT, f"full argmax differs at gap {st['gap'][rr]}"
-                        exempt = True
+                        exempt.setdefault(b, []).append(f"full row {rr} gap {st['gap'][rr]:.2e}")
         h = s._host(w)
-        same = True
+        differ = []
         for i, b in enumerate(order):
             if b not in dec_o:
                 continue
@@ -184,10 +186,10 @@ class Lockstep:
             got = (int(h["status"][i]), int(h["kappa"][i]), int(h["emit"][i]), int(h["new_len"][i]))
             want = (do["status"], do["kappa"], do["emit"], do["new_len"])
             if got != want:
-                assert exempt, f"step {step_idx} seq {b}: GPU {got} oracle {want}"
-                same = False
-        if not same:
-            self.log.append(dict(step=step_idx, kind="resync"))
+                assert b in exempt, f"step {step_idx} seq {b}: GPU {got} oracle {want} without a near tie of its own"
+                differ.append(b)
+        if differ:
+            self.log.append(dict(step=step_idx, kind="resync", seqs={b: exempt[b] for b in differ}))
             D = w.max_drafts
             path = np.array(h["path"], np.int32).reshape(w.B, -1).copy()
             hh = {k: np.array(h[k], np.int32).copy() for k in ("status", "kappa", "emit", "new_len")}

@@ -397,6 +397,8 @@ def test_sampled_decide_rejects_bad_arguments():
 
         assert call(via.Sampling(1.0, 1.0, probs, good)) == via.EINVAL       # alpha = 1
         assert call(via.Sampling(0.0, 0.0, probs, good)) == via.EINVAL       # beta = 0
+        assert call(via.Sampling(0.5, 0.4, probs, good)) == via.EINVAL       # beta < 1 - alpha (Eq. A.3)
+        assert call(via.Sampling(0.5, float("inf"), probs, good)) == via.EINVAL
         bad = good.copy()
         bad[0, 1, 2] = 1.0
         assert call(via.Sampling(0.0, 1.0, probs, bad)) == via.EINVAL        # a uniform of 1

@@ -361,3 +361,28 @@ def test_tree_walk_natural_tiers_matches_bruteforce(tiny, T, branches):
         else:
             seen.add("leaf")
     assert branches <= seen, seen
+
+
+def test_nonfinite_full_logits_not_committed():
+    """A non-finite full-verifier row at an escalated position: status 2, the
+    sequence is not advanced, both caches keep their valid lengths and the
+    blocks the step took past them are free again; the slim verifier (which
+    bypasses the poisoned layer) is unaffected."""
+    cfg = configs.get("tiny_fp32")
+    W = gen.model_weights(cfg)
+    W["w_down"][1] = np.full_like(W["w_down"][1], np.inf)   # layer 1 is not in the slim route [0, 3]
+    m = OracleModel(cfg["model"], W)
+    ver = Verifier(m, cfg["route"])
+    x = gen.context_tokens(cfg, 0, 31)                      # 30 cached slots: two blocks
+    ver.prefill(x)
+    tables = (ver.block_table("full", 0), ver.block_table("slim", 0))
+    dec = ver.step({0: Draft.chain([1, 2, 3, 4])}, TierParams(0.9, 0.5, 1.0, FORCED_FULL))[0]
+    assert (dec["status"], dec["kappa"], dec["emit"], dec["new_len"]) == (2, 0, -1, len(x))
+    assert all(math.isfinite(v) for v in dec["slim_stats"]["max"])
+    assert not math.isfinite(dec["full_stats"]["max"][0])
+    st = ver.seqs[0]
+    assert st.tokens == x and st.slim.valid == st.full.valid == len(x) - 1
+    assert (ver.block_table("full", 0), ver.block_table("slim", 0)) == tables
+    # a later step without q commits normally
+    dec = ver.step({0: Draft.chain([1, 2, 3, 4])}, TierParams(0.9, 0.5, 1.0, FORCED_ACCEPT))[0]
+    assert dec["status"] == 0 and ver.seqs[0].tokens == x + [1, 2, 3, 4]
