@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libvia.so")
 OBJ = os.path.join(ROOT, "_build")
-SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "dimr.hip", "runtime.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "dimr.hip", "runtime.cpp", "host_book.cpp"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -3,68 +3,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan.h"
+
 namespace via {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kBlock = 16;        // tokens per KV page
-constexpr int kMaxChildren = 8;   // drafts verified by one row
-constexpr int kAttnMaxSplits = 32;  // key splits per sequence (partials one query's combine merges)
-constexpr int kAttnMaxSpan = 8192;  // keys of one split (pages of a split's work-group, x16)
-constexpr int kAttnTargetGroups = 256;  // attention work-groups a forward aims for (one per compute unit)
-constexpr int kAttnQueries = 32;  // (row, head-in-group) queries per attention work-group
-constexpr int kNormChunk = 512;   // columns per partial sum of squares (RMSNorm)
-
-// One fed row of a forward (lag row or window row).
-struct RowInfo {
-  int32_t tok;      // token id
-  int32_t pos;      // RoPE position
-  int32_t seq;      // index into the SeqInfo array of this forward
-  int32_t slot;     // cache slot the row's K/V are written to
-  int32_t vis_len;  // slots [0, vis_len) are visible
-  int32_t lm;       // index into the head rows, -1 if the row has no head output
-  int32_t blk;      // pool block holding `slot` (the sequence's block table entry slot / block size)
-  int32_t pad_;
-  uint64_t mask;    // extra visible slots win_base + bit (tree rows)
-};
-
-struct SeqInfo {
-  int32_t kv_len;     // slots written after the forward's K/V write
-  int32_t row_start;  // first row of this sequence in the forward
-  int32_t n_rows;     // rows of this sequence (lag + window)
-  int32_t win_base;   // slot of window row 0 (tree masks are relative to it)
-  int32_t bt;         // offset of the block table in the uploaded tables
-  int32_t n_blocks;   // block-table length
-  int32_t pad0, pad1;
-};
-
-// One attention work item: up to kAttnQueries (row, head-in-group) queries of a
-// sequence, with the sequence's cache geometry inlined.
-struct AttnItem {
-  int32_t q0;       // first query (row * G + g) of the tile, within the sequence
-  int32_t n_chunks; // key splits of this sequence: ceil(kv_len / span)
-  int32_t kv_len, row_start, n_rows, win_base, bt, n_blocks;
-};
-
-// Head row: which forward row and where its statistics go.
-struct LmRow {
-  int32_t row;      // forward row
-  int32_t out;      // b * max_rows + r in the caller's output arrays
-  int32_t n_drafts; // drafts this row verifies (<= kMaxChildren)
-  int32_t pad;
-  int32_t draft_idx[kMaxChildren];  // b * max_drafts + j
-  int32_t draft_tok[kMaxChildren];
-};
-
-// Per-sequence data of an open step, read by the tier decision.
-struct StepSeq {
-  int32_t n;          // committed length before the step
-  int32_t n_drafts;
-  int32_t full_ran;   // full forward ran this step
-  int32_t pad;
-};
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 

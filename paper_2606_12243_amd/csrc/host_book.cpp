@@ -1,0 +1,358 @@
+// Host bookkeeping of the verification step (host_book.h): plain C++, no HIP.
+#include "host_book.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+namespace via {
+
+namespace {
+thread_local std::string g_err;
+}
+
+via_status fail(via_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+const char* last_error() { return g_err.c_str(); }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+int blocks_for(int slots) { return ceil_div(slots, kBlock); }
+
+void book_init(KvBook& bk, int max_seqs, int max_blocks_per_seq, int blocks_full, int blocks_slim) {
+  bk.max_blocks_per_seq = max_blocks_per_seq;
+  bk.seqs.assign(max_seqs, SeqSt());
+  for (int c = 0; c < 2; ++c) {
+    bk.free_[c].clear();
+    const int nb = c == VIA_CACHE_FULL ? blocks_full : blocks_slim;
+    for (int i = 0; i < nb; ++i) bk.free_[c].insert(bk.free_[c].end(), i);
+  }
+}
+
+via_status book_alloc(KvBook& bk, int cache, const std::vector<std::pair<int, int>>& need,
+                      std::vector<std::pair<int, int>>* taken) {
+  size_t missing = 0;
+  for (auto& pr : need) {
+    const SeqSt& S = bk.seqs[pr.first];
+    const int want = blocks_for(pr.second);
+    if (want > bk.max_blocks_per_seq)
+      return fail(VIA_ENOMEM, "sequence %d needs %d blocks > max_blocks_per_seq %d", pr.first, want,
+                  bk.max_blocks_per_seq);
+    if (want > (int)S.table[cache].size()) missing += want - S.table[cache].size();
+  }
+  if (missing > bk.free_[cache].size())
+    return fail(VIA_ENOMEM, "%s KV pool exhausted: need %zu blocks, %zu free", cache == 0 ? "full" : "slim", missing,
+                bk.free_[cache].size());
+  for (auto& pr : need) {
+    SeqSt& S = bk.seqs[pr.first];
+    const int want = blocks_for(pr.second);
+    while ((int)S.table[cache].size() < want) {
+      const int blk = *bk.free_[cache].begin();
+      bk.free_[cache].erase(bk.free_[cache].begin());
+      S.table[cache].push_back(blk);
+      if (taken) taken->push_back({pr.first, blk});
+    }
+  }
+  return VIA_OK;
+}
+
+void book_trim(KvBook& bk, int cache, int seq, int valid) {
+  SeqSt& S = bk.seqs[seq];
+  const size_t keep = blocks_for(valid);
+  while (S.table[cache].size() > keep) {
+    bk.free_[cache].insert(S.table[cache].back());
+    S.table[cache].pop_back();
+  }
+}
+
+void book_release_taken(KvBook& bk, int cache, const std::vector<std::pair<int, int>>& taken) {
+  for (auto it = taken.rbegin(); it != taken.rend(); ++it) {
+    SeqSt& S = bk.seqs[it->first];
+    if (!S.table[cache].empty() && S.table[cache].back() == it->second) S.table[cache].pop_back();
+    bk.free_[cache].insert(it->second);
+  }
+}
+
+via_status copy_window(const KvBook& bk, const via_window* w, int vocab, int max_batch, int max_drafts,
+                       WinCopy& c) {
+  if (!w) return fail(VIA_EINVAL, "null window");
+  if (w->batch < 1 || w->batch > max_batch) return fail(VIA_EINVAL, "batch %d not in [1, %d]", w->batch, max_batch);
+  if (w->max_rows < 1 || w->max_drafts < 1 || w->max_drafts > max_drafts)
+    return fail(VIA_EINVAL, "window strides out of range (1 <= max_drafts <= %d)", max_drafts);
+  if (!w->seq_id || !w->n_rows || !w->row_tok || !w->n_drafts || !w->draft_tok || !w->draft_row)
+    return fail(VIA_EINVAL, "window arrays missing");
+  const int max_seqs = (int)bk.seqs.size();
+  c = WinCopy();
+  c.batch = w->batch;
+  c.max_rows = w->max_rows;
+  c.max_drafts = w->max_drafts;
+  c.tree = w->row_mask != nullptr || w->draft_parent != nullptr;
+  if ((w->row_mask != nullptr) != (w->draft_parent != nullptr))
+    return fail(VIA_EINVAL, "tree windows need both row_mask and draft_parent");
+  std::set<int> seen;
+  for (int b = 0; b < w->batch; ++b) {
+    const int sid = w->seq_id[b];
+    if (sid < 0 || sid >= max_seqs || !bk.seqs[sid].on) return fail(VIA_EINVAL, "sequence %d not attached", sid);
+    if (!seen.insert(sid).second) return fail(VIA_EINVAL, "sequence %d appears twice", sid);
+    const int R = w->n_rows[b], nd = w->n_drafts[b];
+    if (R < 1 || R > w->max_rows) return fail(VIA_EINVAL, "n_rows[%d]=%d out of range", b, R);
+    if (nd < 0 || nd > w->max_drafts) return fail(VIA_EINVAL, "n_drafts[%d]=%d out of range", b, nd);
+    if (c.tree && R > VIA_MAX_TREE_ROWS) return fail(VIA_EINVAL, "tree windows hold at most %d rows", VIA_MAX_TREE_ROWS);
+    c.seq.push_back(sid);
+    c.n_rows.push_back(R);
+    c.n_drafts.push_back(nd);
+  }
+  c.row_tok.assign((size_t)w->batch * w->max_rows, 0);
+  c.row_depth.assign((size_t)w->batch * w->max_rows, 0);
+  c.row_mask.assign((size_t)w->batch * w->max_rows, 0);
+  c.draft_tok.assign((size_t)w->batch * w->max_drafts, 0);
+  c.draft_row.assign((size_t)w->batch * w->max_drafts, 0);
+  c.draft_parent.assign((size_t)w->batch * w->max_drafts, -1);
+  for (int b = 0; b < w->batch; ++b) {
+    const int R = c.n_rows[b], nd = c.n_drafts[b];
+    for (int r = 0; r < R; ++r) {
+      const size_t i = (size_t)b * w->max_rows + r;
+      const int t = w->row_tok[i];
+      if (t < 0 || t >= vocab) return fail(VIA_EINVAL, "row token %d out of range", t);
+      c.row_tok[i] = t;
+      const int dep = w->row_depth ? w->row_depth[i] : r;
+      if (dep < 0 || (r == 0 && dep != 0)) return fail(VIA_EINVAL, "row depth must be >= 0 and 0 for row 0");
+      c.row_depth[i] = dep;
+      if (w->row_mask) {
+        const uint64_t mk = w->row_mask[i];
+        if (!((mk >> r) & 1) || !(mk & 1) || (r < 63 && (mk >> (r + 1))))
+          return fail(VIA_EINVAL, "row_mask[%d][%d] must contain row 0, itself and no later row", b, r);
+        c.row_mask[i] = mk;
+      }
+    }
+    std::vector<int> node_row(nd, -1);
+    for (int j = 0; j < nd; ++j) {
+      const size_t i = (size_t)b * w->max_drafts + j;
+      const int t = w->draft_tok[i], row = w->draft_row[i];
+      const int par = w->draft_parent ? w->draft_parent[i] : j - 1;
+      if (t < 0 || t >= vocab) return fail(VIA_EINVAL, "draft token %d out of range", t);
+      if (row < 0 || row >= R) return fail(VIA_EINVAL, "draft_row[%d][%d]=%d out of range", b, j, row);
+      if (par < -1 || par >= j) return fail(VIA_EINVAL, "draft_parent[%d][%d] must be -1 or < j", b, j);
+      // the row verifying draft j is its parent's row (root row 0)
+      if (par == -1 ? row != 0 : (node_row[par] >= 0 && node_row[par] != row))
+        return fail(VIA_EINVAL, "draft_row[%d][%d] inconsistent with its parent", b, j);
+      if (par >= 0) node_row[par] = row;
+      if (!w->draft_parent && row != j) return fail(VIA_EINVAL, "chain draft j must be verified by row j");
+      c.draft_tok[i] = t;
+      c.draft_row[i] = row;
+      c.draft_parent[i] = par;
+    }
+    // children per row bounded (head rows carry at most kMaxChildren drafts)
+    std::vector<int> per_row(R, 0);
+    for (int j = 0; j < nd; ++j)
+      if (++per_row[c.draft_row[(size_t)b * w->max_drafts + j]] > kMaxChildren)
+        return fail(VIA_EINVAL, "a row verifies more than %d drafts", kMaxChildren);
+  }
+  return VIA_OK;
+}
+
+static void push_items(Plan& P, const SeqInfo& si, int G) {
+  const int nq = si.n_rows * G;
+  for (int q0 = 0; q0 < nq; q0 += kAttnQueries)
+    P.items.push_back(AttnItem{q0, 0, si.kv_len, si.row_start, si.n_rows, si.win_base, si.bt, si.n_blocks});
+}
+
+via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std::vector<int>& run,
+                             const via_window* raw, bool head, int vocab, int G, Plan& P,
+                             std::vector<std::pair<int, int>>* taken) {
+  std::vector<std::pair<int, int>> need;
+  for (int b : run) {
+    const SeqSt& S = bk.seqs[w.seq[b]];
+    int n_lag = 0;
+    if (cache == VIA_CACHE_FULL) {
+      const int lag = S.valid[VIA_CACHE_SLIM] - S.valid[VIA_CACHE_FULL];
+      n_lag = (raw && raw->n_lag) ? raw->n_lag[b] : 0;
+      if (n_lag != lag)
+        return fail(VIA_ESTATE, "sequence %d: full cache lags %d tokens, window gives %d", w.seq[b], lag, n_lag);
+      if (n_lag > 0 && (!raw->lag_tok || n_lag > raw->max_lag))
+        return fail(VIA_EINVAL, "lag_tok missing or max_lag too small");
+      for (int i = 0; i < n_lag; ++i) {
+        const int t = raw->lag_tok[(size_t)b * raw->max_lag + i];
+        if (t < 0 || t >= vocab) return fail(VIA_EINVAL, "lag token out of range");
+      }
+    }
+    need.push_back({w.seq[b], S.valid[cache] + n_lag + w.n_rows[b]});
+  }
+  via_status st = book_alloc(bk, cache, need, taken);
+  if (st) return st;
+  int lm_i = 0;
+  for (size_t q = 0; q < run.size(); ++q) {
+    const int b = run[q];
+    const SeqSt& S = bk.seqs[w.seq[b]];
+    const int valid = S.valid[cache];
+    const int n_lag = need[q].second - valid - w.n_rows[b];
+    const int R = w.n_rows[b];
+    const int win_base = valid + n_lag;
+    const int npos = S.valid[VIA_CACHE_SLIM];  // position of the pending token, n - 1
+    SeqInfo si{};
+    si.row_start = (int)P.rows.size();
+    si.n_rows = n_lag + R;
+    si.kv_len = valid + n_lag + R;
+    si.win_base = win_base;
+    si.bt = (int)P.btab.size();
+    si.n_blocks = (int)S.table[cache].size();
+    for (int blk : S.table[cache]) P.btab.push_back(blk);
+    const int sidx = (int)P.seqs.size();
+    for (int i = 0; i < n_lag; ++i) {
+      RowInfo r{};
+      r.tok = raw->lag_tok[(size_t)b * raw->max_lag + i];
+      r.pos = valid + i;
+      r.seq = sidx;
+      r.slot = valid + i;
+      r.blk = S.table[cache][r.slot / kBlock];
+      r.vis_len = valid + i + 1;
+      r.lm = -1;
+      P.rows.push_back(r);
+    }
+    for (int rr = 0; rr < R; ++rr) {
+      const size_t i = (size_t)b * w.max_rows + rr;
+      RowInfo r{};
+      r.tok = w.row_tok[i];
+      r.pos = npos + w.row_depth[i];
+      r.seq = sidx;
+      r.slot = win_base + rr;
+      r.blk = S.table[cache][r.slot / kBlock];
+      r.vis_len = w.tree ? win_base : win_base + rr + 1;
+      r.mask = w.tree ? w.row_mask[i] : 0;
+      r.lm = -1;
+      if (head) {
+        LmRow lr{};
+        lr.row = (int)P.rows.size();
+        lr.out = b * w.max_rows + rr;
+        for (int j = 0; j < w.n_drafts[b]; ++j) {
+          const size_t di = (size_t)b * w.max_drafts + j;
+          if (w.draft_row[di] == rr) {
+            lr.draft_idx[lr.n_drafts] = (int)di;
+            lr.draft_tok[lr.n_drafts] = w.draft_tok[di];
+            lr.n_drafts++;
+          }
+        }
+        r.lm = lm_i++;
+        P.lm.push_back(lr);
+      }
+      P.rows.push_back(r);
+    }
+    P.seqs.push_back(si);
+    push_items(P, si, G);
+  }
+  return VIA_OK;
+}
+
+void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0, int c1, int G, Plan& P) {
+  SeqInfo si{};
+  si.row_start = 0;
+  si.n_rows = c1 - c0;
+  si.kv_len = c1;
+  si.win_base = c0;
+  si.bt = 0;
+  si.n_blocks = (int)S.table[cache].size();
+  for (int blk : S.table[cache]) P.btab.push_back(blk);
+  for (int i = c0; i < c1; ++i) {
+    RowInfo r{};
+    r.tok = tokens[i];
+    r.pos = i;
+    r.seq = 0;
+    r.slot = i;
+    r.blk = S.table[cache][i / kBlock];
+    r.vis_len = i + 1;
+    r.lm = -1;
+    P.rows.push_back(r);
+  }
+  P.seqs.push_back(si);
+  push_items(P, si, G);
+}
+
+via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int>& step_n, const int32_t* hp,
+                       int vocab, CommitMoves& cm) {
+  const int B = w.batch, Dd = std::max(1, w.max_drafts);
+  std::vector<std::vector<int>> kept_rows(B);
+  for (int b = 0; b < B; ++b) {
+    const int status = hp[b], kappa = hp[B + b], emit = hp[2 * B + b], nl = hp[3 * B + b];
+    const int* path = hp + 4 * B + b * Dd;
+    const int n = step_n[b];
+    if (status == 1) return fail(VIA_ESTATE, "sequence %d still needs the full verifier", w.seq[b]);
+    if (status != 0 && status != 2) return fail(VIA_EINVAL, "bad status %d", status);
+    if (kappa < 0 || kappa > w.n_drafts[b]) return fail(VIA_EINVAL, "kappa %d out of range", kappa);
+    if (emit < -1 || emit >= vocab) return fail(VIA_EINVAL, "emit %d out of range", emit);
+    if (status == 2) {
+      if (nl != n) return fail(VIA_EINVAL, "new_len must equal n when the sequence is not advanced");
+      continue;
+    }
+    if (nl != n + kappa + (emit >= 0 ? 1 : 0)) return fail(VIA_EINVAL, "new_len inconsistent with kappa/emit");
+    int prev = -1;
+    for (int i = 0; i < kappa; ++i) {
+      const int j = path[i];
+      if (j < 0 || j >= w.n_drafts[b] || w.draft_parent[(size_t)b * w.max_drafts + j] != prev)
+        return fail(VIA_EINVAL, "accepted path of sequence %d is not a root path", w.seq[b]);
+      prev = j;
+    }
+    // window rows that stay valid: root + the first (kept - 1) path nodes
+    const int kept = kappa + (emit >= 0 ? 1 : 0);
+    for (int i = 1; i < kept; ++i) {
+      const int node = path[i - 1];
+      int row = -1;
+      for (int j = 0; j < w.n_drafts[b]; ++j)
+        if (w.draft_parent[(size_t)b * w.max_drafts + j] == node) {
+          row = w.draft_row[(size_t)b * w.max_drafts + j];
+          break;
+        }
+      if (row < 0) return fail(VIA_EINVAL, "accepted node %d has no fed row", node);
+      kept_rows[b].push_back(row);
+    }
+  }
+  // tree compaction moves (slim cache always, full cache where it ran)
+  for (int cache = 0; cache < 2; ++cache) {
+    cm.btab[cache].clear();
+    cm.moves[cache].clear();
+    if (!w.tree) continue;
+    for (int b = 0; b < B; ++b) {
+      const SeqSt& S = bk.seqs[w.seq[b]];
+      if (hp[b] != 0) continue;
+      if (cache == VIA_CACHE_FULL && !S.full_ran) continue;
+      const int base = step_n[b] - 1;
+      const int off = (int)cm.btab[cache].size();
+      bool any = false;
+      for (size_t i = 0; i < kept_rows[b].size(); ++i) {
+        const int src = base + kept_rows[b][i], dst = base + (int)i + 1;
+        if (src != dst) {
+          cm.moves[cache].push_back(KvMove{off, src, dst, 0});
+          any = true;
+        }
+      }
+      if (any)
+        for (int blk : S.table[cache]) cm.btab[cache].push_back(blk);
+    }
+  }
+  return VIA_OK;
+}
+
+void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp) {
+  const int B = w.batch;
+  for (int b = 0; b < B; ++b) {
+    SeqSt& S = bk.seqs[w.seq[b]];
+    if (hp[b] == 0) {
+      const int nv = hp[3 * B + b] - 1;
+      S.valid[VIA_CACHE_SLIM] = nv;
+      if (S.full_ran) S.valid[VIA_CACHE_FULL] = nv;
+    }
+    book_trim(bk, VIA_CACHE_SLIM, w.seq[b], S.valid[VIA_CACHE_SLIM]);
+    book_trim(bk, VIA_CACHE_FULL, w.seq[b], S.valid[VIA_CACHE_FULL]);
+    S.full_ran = false;
+  }
+}
+
+}  // namespace via

@@ -1,0 +1,107 @@
+// Host bookkeeping of the verification step: the paged block allocator of
+// both caches, validation and copies of draft windows, the per-forward row
+// plans, and the checks and tree-compaction moves of a commit.  Plain C++
+// (no HIP), so that it builds and is tested on its own on the CPU; the
+// runtime (runtime.cpp) owns the device side.
+#pragma once
+#include <stdint.h>
+
+#include <set>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/via.h"
+#include "plan.h"
+
+namespace via {
+
+// Records a thread-local message (via_last_error) and returns `s`.
+via_status fail(via_status s, const char* fmt, ...);
+const char* last_error();
+
+int ceil_div(int a, int b);
+// Blocks a sequence needs to hold `slots` cache slots.
+int blocks_for(int slots);
+
+// Logical KV state of one sequence: valid lengths and block tables of the
+// full (index VIA_CACHE_FULL) and slim (VIA_CACHE_SLIM) caches.
+struct SeqSt {
+  bool on = false;
+  int valid[2] = {0, 0};
+  std::vector<int> table[2];
+  bool full_ran = false;  // the full verifier ran for it in the open step
+};
+
+// Both caches' sequences and free block sets.  Blocks are handed out lowest
+// id first (a min-ordered free set).
+struct KvBook {
+  int max_blocks_per_seq = 0;
+  std::vector<SeqSt> seqs;
+  std::set<int> free_[2];
+};
+void book_init(KvBook& bk, int max_seqs, int max_blocks_per_seq, int blocks_full, int blocks_slim);
+// All-or-nothing: give every (seq, slots) of `need` the blocks it lacks in
+// `cache`, lowest free id first, in the given order; taken (nullable)
+// records every (seq, block) handed out.  ENOMEM (nothing taken) if the pool
+// or a block table is too small.
+via_status book_alloc(KvBook& bk, int cache, const std::vector<std::pair<int, int>>& need,
+                      std::vector<std::pair<int, int>>* taken);
+// Free the blocks of `seq` lying wholly at or past `valid` slots.
+void book_trim(KvBook& bk, int cache, int seq, int valid);
+// Undo a book_alloc (blocks back to the pool, tables shortened).
+void book_release_taken(KvBook& bk, int cache, const std::vector<std::pair<int, int>>& taken);
+
+// Validated copy of a draft window (include/via.h, via_window).
+struct WinCopy {
+  int batch = 0, max_rows = 0, max_drafts = 0;
+  bool tree = false;
+  std::vector<int> seq, n_rows, row_tok, row_depth, n_drafts, draft_tok, draft_row, draft_parent;
+  std::vector<uint64_t> row_mask;
+};
+// EINVAL for every malformed window: batch and strides out of range, missing
+// arrays, unattached or repeated sequences, tokens outside [0, vocab), bad
+// depths or masks, drafts whose row is not their parent's row, more than
+// kMaxChildren drafts on one row.
+via_status copy_window(const KvBook& bk, const via_window* w, int vocab, int max_batch, int max_drafts,
+                       WinCopy& c);
+
+// Rows of one forward and everything the kernels index by them.
+struct Plan {
+  std::vector<RowInfo> rows;
+  std::vector<SeqInfo> seqs;
+  std::vector<int32_t> btab;
+  std::vector<AttnItem> items;
+  std::vector<LmRow> lm;
+  std::vector<PrefixXfer> xfer;  // forwards that start after the shared layers
+};
+// Plan of a verify forward of `cache` over the batch entries `run` of w: the
+// full cache's lag rows (raw->n_lag / lag_tok, which must equal the cache's
+// lag: ESTATE otherwise) and the window rows, their positions, cache slots
+// and visibility, the head rows with the drafts each verifies (`head`), the
+// attention items (kAttnQueries queries of G = H / KVH heads per item).
+// Allocates the blocks the rows need (ENOMEM: nothing allocated).
+via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std::vector<int>& run,
+                             const via_window* raw, bool head, int vocab, int G, Plan& P,
+                             std::vector<std::pair<int, int>>* taken);
+// Plan of prefill rows [c0, c1) of one sequence (causal, positions = slots).
+void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0, int c1, int G, Plan& P);
+
+// Commit of an open step from the host copy of a decision (the packed block
+// of include/via.h).  Validation (nothing changes on error): no status 1,
+// statuses 0 or 2, kappa in [0, n_drafts], emit in [-1, vocab), new_len
+// consistent (n for status 2, n + kappa + [emit >= 0] otherwise), the
+// accepted path a root path of the draft tree, every accepted node but the
+// last with a fed row.  moves[cache] receives the tree-compaction copies
+// (block-table offsets into btab[cache]); chain windows need none.
+struct CommitMoves {
+  std::vector<int32_t> btab[2];
+  std::vector<KvMove> moves[2];
+};
+via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int>& step_n, const int32_t* hp,
+                       int vocab, CommitMoves& cm);
+// Apply a validated commit: valid lengths (slim always, full where it ran),
+// blocks past them freed, full_ran cleared.
+void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp);
+
+}  // namespace via

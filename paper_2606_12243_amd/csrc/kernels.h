@@ -85,13 +85,6 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
                       void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s,
                       float* Xcopy = nullptr, const void* E = nullptr, const RowInfo* erows = nullptr);
 
-// One row of a full forward that starts after the P layers the slim route
-// shares with it (route layer i == i for i < P).
-struct PrefixXfer {
-  int32_t src_row;           // row of the same step's slim forward
-  int32_t t;                 // slot within the page (position % 16)
-  int32_t src_blk, dst_blk;  // page of the position in the slim and the full cache
-};
 struct PrefixArgs {
   const PrefixXfer* xfer;  // [M]
   int M, P, d, KVH, hd;
@@ -165,12 +158,7 @@ void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 // at.max_chunks.  Returns -1 if a sequence needs a span above kAttnMaxSpan.
 int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int target_groups, AttnArgs& at);
 
-// Tree compaction: copy K/V of slot src -> dst for every layer slot.
-struct KvMove {
-  int32_t bt;      // offset of the block table in btab
-  int32_t src, dst;
-  int32_t pad;
-};
+// Tree compaction: KvMove (plan.h) copies K/V of slot src -> dst for every layer slot.
 void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KVH, int hd,
                      const int32_t* btab, const KvMove* moves, int n_moves, hipStream_t s);
 

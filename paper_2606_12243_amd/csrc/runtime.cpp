@@ -12,23 +12,12 @@
 #include <vector>
 
 #include "../../include/via.h"
+#include "host_book.h"
 #include "kernels.h"
 
 using namespace via;
 
 namespace {
-
-thread_local std::string g_err;
-
-via_status fail(via_status s, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
-  va_end(ap);
-  g_err = buf;
-  return s;
-}
 
 constexpr size_t kAlign = 256;
 constexpr int kRing = 4;
@@ -36,8 +25,6 @@ constexpr int kRing = 4;
 size_t al(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 int esize_of(const via_model_desc* d) { return d->dtype == VIA_DTYPE_BF16 ? 2 : 4; }
-
-int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // Split-K policy: about two work-groups per CU, at least two 32-wide K steps
 // per wave (8 waves) in each slice.  Depends only on the GEMM shape.
@@ -172,24 +159,6 @@ struct via_model {
   int n_kv = 0;
 };
 
-namespace {
-
-struct SeqSt {
-  bool on = false;
-  int valid[2] = {0, 0};
-  std::vector<int> table[2];
-  bool full_ran = false;
-};
-
-struct WinCopy {
-  int batch = 0, max_rows = 0, max_drafts = 0;
-  bool tree = false;
-  std::vector<int> seq, n_rows, row_tok, row_depth, n_drafts, draft_tok, draft_row, draft_parent;
-  std::vector<uint64_t> row_mask;
-};
-
-}  // namespace
-
 struct via_kv {
   via_model* m;
   via_kv_desc d;
@@ -197,8 +166,7 @@ struct via_kv {
   char* ws;
   char* stage;
   size_t slot_bytes;
-  std::vector<SeqSt> seqs;
-  std::set<int> free_[2];
+  KvBook bk;
   bool step_open = false;
   WinCopy win;
   bool xpref_ok = false;      // the open step's slim forward saved its state after the shared layers
@@ -283,57 +251,6 @@ void timed_gemm(via_kv* kv, int kind, bool bf, GemmRole role, const GemmArgs& g,
   }
   launch_gemm(bf, role, g, s, a, b);
   if (a) kv->timed.push_back({kind, {a, b}});
-}
-
-struct Plan {
-  std::vector<RowInfo> rows;
-  std::vector<SeqInfo> seqs;
-  std::vector<int32_t> btab;
-  std::vector<AttnItem> items;
-  std::vector<LmRow> lm;
-  std::vector<PrefixXfer> xfer;  // forwards that start after the shared layers
-  std::vector<char> blob;
-};
-
-// Blocks a sequence needs to hold `slots` cache slots.
-int blocks_for(int slots) { return ceil_div(slots, kBlock); }
-
-// All-or-nothing allocation of the missing blocks of several sequences of
-// one cache, lowest free block id first, in the given order.
-via_status alloc_blocks(via_kv* kv, int cache, const std::vector<std::pair<int, int>>& need /*seq, slots*/,
-                        std::vector<std::pair<int, int>>* taken) {
-  size_t missing = 0;
-  for (auto& pr : need) {
-    const SeqSt& S = kv->seqs[pr.first];
-    int want = blocks_for(pr.second);
-    if (want > kv->d.max_blocks_per_seq)
-      return fail(VIA_ENOMEM, "sequence %d needs %d blocks > max_blocks_per_seq %d", pr.first, want,
-                  kv->d.max_blocks_per_seq);
-    if (want > (int)S.table[cache].size()) missing += want - S.table[cache].size();
-  }
-  if (missing > kv->free_[cache].size())
-    return fail(VIA_ENOMEM, "%s KV pool exhausted: need %zu blocks, %zu free", cache == 0 ? "full" : "slim", missing,
-                kv->free_[cache].size());
-  for (auto& pr : need) {
-    SeqSt& S = kv->seqs[pr.first];
-    int want = blocks_for(pr.second);
-    while ((int)S.table[cache].size() < want) {
-      int blk = *kv->free_[cache].begin();
-      kv->free_[cache].erase(kv->free_[cache].begin());
-      S.table[cache].push_back(blk);
-      if (taken) taken->push_back({pr.first, blk});
-    }
-  }
-  return VIA_OK;
-}
-
-void trim_blocks(via_kv* kv, int cache, int seq, int valid) {
-  SeqSt& S = kv->seqs[seq];
-  size_t keep = blocks_for(valid);
-  while (S.table[cache].size() > keep) {
-    kv->free_[cache].insert(S.table[cache].back());
-    S.table[cache].pop_back();
-  }
 }
 
 template <typename T>
@@ -568,183 +485,11 @@ via_status check_out(const via_verify_out* o) {
   return VIA_OK;
 }
 
-// Validate and copy a window.
-via_status copy_window(via_kv* kv, const via_window* w, WinCopy& c) {
-  const via_model* m = kv->m;
-  if (!w) return fail(VIA_EINVAL, "null window");
-  if (w->batch < 1 || w->batch > kv->d.max_batch) return fail(VIA_EINVAL, "batch %d not in [1, %d]", w->batch, kv->d.max_batch);
-  if (w->max_rows < 1 || w->max_drafts < 1 || w->max_drafts > kv->d.max_drafts)
-    return fail(VIA_EINVAL, "window strides out of range (1 <= max_drafts <= %d)", kv->d.max_drafts);
-  if (!w->seq_id || !w->n_rows || !w->row_tok || !w->n_drafts || (w->max_drafts > 0 && (!w->draft_tok || !w->draft_row)))
-    return fail(VIA_EINVAL, "window arrays missing");
-  const int V = m->d.vocab;
-  c = WinCopy();
-  c.batch = w->batch;
-  c.max_rows = w->max_rows;
-  c.max_drafts = w->max_drafts;
-  c.tree = w->row_mask != nullptr || w->draft_parent != nullptr;
-  if ((w->row_mask != nullptr) != (w->draft_parent != nullptr))
-    return fail(VIA_EINVAL, "tree windows need both row_mask and draft_parent");
-  std::set<int> seen;
-  for (int b = 0; b < w->batch; ++b) {
-    int sid = w->seq_id[b];
-    if (sid < 0 || sid >= kv->d.max_seqs || !kv->seqs[sid].on) return fail(VIA_EINVAL, "sequence %d not attached", sid);
-    if (!seen.insert(sid).second) return fail(VIA_EINVAL, "sequence %d appears twice", sid);
-    int R = w->n_rows[b], nd = w->n_drafts[b];
-    if (R < 1 || R > w->max_rows) return fail(VIA_EINVAL, "n_rows[%d]=%d out of range", b, R);
-    if (nd < 0 || nd > w->max_drafts) return fail(VIA_EINVAL, "n_drafts[%d]=%d out of range", b, nd);
-    if (c.tree && R > VIA_MAX_TREE_ROWS) return fail(VIA_EINVAL, "tree windows hold at most %d rows", VIA_MAX_TREE_ROWS);
-    c.seq.push_back(sid);
-    c.n_rows.push_back(R);
-    c.n_drafts.push_back(nd);
-  }
-  c.row_tok.assign((size_t)w->batch * w->max_rows, 0);
-  c.row_depth.assign((size_t)w->batch * w->max_rows, 0);
-  c.row_mask.assign((size_t)w->batch * w->max_rows, 0);
-  c.draft_tok.assign((size_t)w->batch * std::max(1, w->max_drafts), 0);
-  c.draft_row.assign((size_t)w->batch * std::max(1, w->max_drafts), 0);
-  c.draft_parent.assign((size_t)w->batch * std::max(1, w->max_drafts), -1);
-  for (int b = 0; b < w->batch; ++b) {
-    int R = c.n_rows[b], nd = c.n_drafts[b];
-    for (int r = 0; r < R; ++r) {
-      size_t i = (size_t)b * w->max_rows + r;
-      int t = w->row_tok[i];
-      if (t < 0 || t >= V) return fail(VIA_EINVAL, "row token %d out of range", t);
-      c.row_tok[i] = t;
-      int dep = w->row_depth ? w->row_depth[i] : r;
-      if (dep < 0 || (r == 0 && dep != 0)) return fail(VIA_EINVAL, "row depth must be >= 0 and 0 for row 0");
-      c.row_depth[i] = dep;
-      if (w->row_mask) {
-        uint64_t mk = w->row_mask[i];
-        if (!((mk >> r) & 1) || !(mk & 1) || (r < 63 && (mk >> (r + 1))))
-          return fail(VIA_EINVAL, "row_mask[%d][%d] must contain row 0, itself and no later row", b, r);
-        c.row_mask[i] = mk;
-      }
-    }
-    std::vector<int> node_row(nd, -1);
-    for (int j = 0; j < nd; ++j) {
-      size_t i = (size_t)b * w->max_drafts + j;
-      int t = w->draft_tok[i], row = w->draft_row[i];
-      int par = w->draft_parent ? w->draft_parent[i] : j - 1;
-      if (t < 0 || t >= V) return fail(VIA_EINVAL, "draft token %d out of range", t);
-      if (row < 0 || row >= R) return fail(VIA_EINVAL, "draft_row[%d][%d]=%d out of range", b, j, row);
-      if (par < -1 || par >= j) return fail(VIA_EINVAL, "draft_parent[%d][%d] must be -1 or < j", b, j);
-      // the row verifying draft j is its parent's row (root row 0)
-      if (par == -1 ? row != 0 : (node_row[par] >= 0 && node_row[par] != row))
-        return fail(VIA_EINVAL, "draft_row[%d][%d] inconsistent with its parent", b, j);
-      if (par >= 0) node_row[par] = row;
-      if (!w->draft_parent && row != j) return fail(VIA_EINVAL, "chain draft j must be verified by row j");
-      c.draft_tok[i] = t;
-      c.draft_row[i] = row;
-      c.draft_parent[i] = par;
-    }
-    // children per row bounded (head rows carry at most kMaxChildren drafts)
-    std::vector<int> per_row(R, 0);
-    for (int j = 0; j < nd; ++j)
-      if (++per_row[c.draft_row[(size_t)b * w->max_drafts + j]] > kMaxChildren)
-        return fail(VIA_EINVAL, "a row verifies more than %d drafts", kMaxChildren);
-  }
-  return VIA_OK;
-}
-
-// Rows of one verify forward; `run` selects batch entries.
-via_status build_verify_plan(via_kv* kv, int cache, const WinCopy& w, const std::vector<int>& run,
-                             const via_window* raw, bool head, Plan& P, std::vector<std::pair<int, int>>* taken) {
-  const Dims& D = kv->m->D;
-  std::vector<std::pair<int, int>> need;
-  for (int b : run) {
-    const SeqSt& S = kv->seqs[w.seq[b]];
-    int n_lag = 0;
-    if (cache == VIA_CACHE_FULL) {
-      int lag = S.valid[VIA_CACHE_SLIM] - S.valid[VIA_CACHE_FULL];
-      n_lag = (raw && raw->n_lag) ? raw->n_lag[b] : 0;
-      if (n_lag != lag) return fail(VIA_ESTATE, "sequence %d: full cache lags %d tokens, window gives %d", w.seq[b], lag, n_lag);
-      if (n_lag > 0 && (!raw->lag_tok || n_lag > raw->max_lag)) return fail(VIA_EINVAL, "lag_tok missing or max_lag too small");
-    }
-    need.push_back({w.seq[b], S.valid[cache] + n_lag + w.n_rows[b]});
-  }
-  via_status st = alloc_blocks(kv, cache, need, taken);
-  if (st) return st;
-  int lm_i = 0;
-  for (size_t q = 0; q < run.size(); ++q) {
-    const int b = run[q];
-    const SeqSt& S = kv->seqs[w.seq[b]];
-    const int valid = S.valid[cache];
-    const int n_lag = need[q].second - valid - w.n_rows[b];
-    const int R = w.n_rows[b];
-    const int win_base = valid + n_lag;
-    const int npos = S.valid[VIA_CACHE_SLIM];  // position of the pending token, n - 1
-    SeqInfo si{};
-    si.row_start = (int)P.rows.size();
-    si.n_rows = n_lag + R;
-    si.kv_len = valid + n_lag + R;
-    si.win_base = win_base;
-    si.bt = (int)P.btab.size();
-    si.n_blocks = (int)S.table[cache].size();
-    for (int blk : S.table[cache]) P.btab.push_back(blk);
-    const int sidx = (int)P.seqs.size();
-    for (int i = 0; i < n_lag; ++i) {
-      RowInfo r{};
-      r.tok = raw->lag_tok[(size_t)b * raw->max_lag + i];
-      if (r.tok < 0 || r.tok >= D.V) return fail(VIA_EINVAL, "lag token out of range");
-      r.pos = valid + i;
-      r.seq = sidx;
-      r.slot = valid + i;
-      r.blk = S.table[cache][r.slot / kBlock];
-      r.vis_len = valid + i + 1;
-      r.lm = -1;
-      P.rows.push_back(r);
-    }
-    for (int rr = 0; rr < R; ++rr) {
-      size_t i = (size_t)b * w.max_rows + rr;
-      RowInfo r{};
-      r.tok = w.row_tok[i];
-      r.pos = npos + w.row_depth[i];
-      r.seq = sidx;
-      r.slot = win_base + rr;
-      r.blk = S.table[cache][r.slot / kBlock];
-      r.vis_len = w.tree ? win_base : win_base + rr + 1;
-      r.mask = w.tree ? w.row_mask[i] : 0;
-      r.lm = -1;
-      if (head) {
-        LmRow lr{};
-        lr.row = (int)P.rows.size();
-        lr.out = b * w.max_rows + rr;
-        for (int j = 0; j < w.n_drafts[b]; ++j) {
-          size_t di = (size_t)b * w.max_drafts + j;
-          if (w.draft_row[di] == rr) {
-            lr.draft_idx[lr.n_drafts] = (int)di;
-            lr.draft_tok[lr.n_drafts] = w.draft_tok[di];
-            lr.n_drafts++;
-          }
-        }
-        r.lm = lm_i++;
-        P.lm.push_back(lr);
-      }
-      P.rows.push_back(r);
-    }
-    P.seqs.push_back(si);
-    const int nq = si.n_rows * D.G;
-    for (int q0 = 0; q0 < nq; q0 += kAttnQueries)
-      P.items.push_back(AttnItem{q0, 0, si.kv_len, si.row_start, si.n_rows, si.win_base,
-                                 si.bt, si.n_blocks});
-  }
-  return VIA_OK;
-}
-
 via_status common_checks(via_model* m, via_kv* kv) {
   if (!m || !kv) return fail(VIA_EINVAL, "null handle");
   if (kv->m != m) return fail(VIA_EINVAL, "KV handle belongs to another model");
   if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
   return VIA_OK;
-}
-
-void release_taken(via_kv* kv, int cache, const std::vector<std::pair<int, int>>& taken) {
-  for (auto it = taken.rbegin(); it != taken.rend(); ++it) {
-    SeqSt& S = kv->seqs[it->first];
-    if (!S.table[cache].empty() && S.table[cache].back() == it->second) S.table[cache].pop_back();
-    kv->free_[cache].insert(it->second);
-  }
 }
 
 via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* win, const int32_t* run_mask,
@@ -755,7 +500,7 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   WinCopy w;
   const WinCopy* wp = &w;
   if (probe || cache == VIA_CACHE_SLIM) {
-    if ((st = copy_window(kv, win, w))) return st;
+    if ((st = copy_window(kv->bk, win, m->d.vocab, kv->d.max_batch, kv->d.max_drafts, w))) return st;
   } else {
     if (!kv->step_open) return fail(VIA_ESTATE, "via_verify_full needs an open step (call via_verify_slim first)");
     if (!win || win->batch != kv->win.batch) return fail(VIA_EINVAL, "window batch differs from the open step");
@@ -770,7 +515,7 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
     if (!run_mask || run_mask[b]) run.push_back(b);
   Plan P;
   std::vector<std::pair<int, int>> taken;
-  if ((st = build_verify_plan(kv, cache, *wp, run, win, true, P, &taken))) return st;
+  if ((st = build_verify_plan(kv->bk, cache, *wp, run, win, true, m->d.vocab, m->D.G, P, &taken))) return st;
   // The full forward of a step starts after the layers the slim route shares
   // with it when no running sequence has lag rows: the slim forward of the
   // step saved those rows' state, and their K/V of the shared layers are
@@ -781,14 +526,14 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   if (!probe && cache == VIA_CACHE_FULL && kv->xpref_ok && n_shared > 0) {
     bool lag0 = true;
     for (int b : run) {
-      const SeqSt& S = kv->seqs[wp->seq[b]];
+      const SeqSt& S = kv->bk.seqs[wp->seq[b]];
       lag0 = lag0 && S.valid[VIA_CACHE_FULL] == S.valid[VIA_CACHE_SLIM];
     }
     if (lag0) {
       start_si = n_shared;
       for (size_t q = 0; q < run.size(); ++q) {
         const int b = run[q];
-        const SeqSt& S = kv->seqs[wp->seq[b]];
+        const SeqSt& S = kv->bk.seqs[wp->seq[b]];
         const SeqInfo& si = P.seqs[q];
         for (int rr = 0; rr < si.n_rows; ++rr) {
           const int pos = si.win_base + rr;
@@ -800,11 +545,11 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   }
   st = exec_forward(m, kv, cache, P, true, out, 1.0f / p->temperature, s, start_si, save);
   if (probe) {
-    release_taken(kv, cache, taken);
+    book_release_taken(kv->bk, cache, taken);
     return st;
   }
   if (st) {
-    release_taken(kv, cache, taken);
+    book_release_taken(kv->bk, cache, taken);
     return st;
   }
   if (cache == VIA_CACHE_SLIM) {
@@ -815,11 +560,11 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
     kv->step_open = true;
     kv->step_n.assign(w.batch, 0);
     for (int b = 0; b < w.batch; ++b) {
-      kv->step_n[b] = kv->seqs[w.seq[b]].valid[VIA_CACHE_SLIM] + 1;
-      kv->seqs[w.seq[b]].full_ran = false;
+      kv->step_n[b] = kv->bk.seqs[w.seq[b]].valid[VIA_CACHE_SLIM] + 1;
+      kv->bk.seqs[w.seq[b]].full_ran = false;
     }
   } else {
-    for (int b : run) kv->seqs[wp->seq[b]].full_ran = true;
+    for (int b : run) kv->bk.seqs[wp->seq[b]].full_ran = true;
   }
   return VIA_OK;
 }
@@ -828,7 +573,7 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
 
 extern "C" {
 
-const char* via_last_error(void) { return g_err.c_str(); }
+const char* via_last_error(void) { return last_error(); }
 const char* via_version(void) { return "via-gfx950 0.1"; }
 
 size_t via_pool_bytes(const via_model_desc* desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size) {
@@ -999,11 +744,7 @@ via_status via_kv_create(via_model* m, const via_kv_desc* d, via_kv** out) {
   kv->ws = (char*)d->workspace;
   kv->stage = (char*)d->pinned_staging;
   kv->slot_bytes = slot;
-  kv->seqs.resize(d->max_seqs);
-  for (int c = 0; c < 2; ++c) {
-    int nb = c == 0 ? d->blocks_full : d->blocks_slim;
-    for (int i = 0; i < nb; ++i) kv->free_[c].insert(kv->free_[c].end(), i);
-  }
+  book_init(kv->bk, d->max_seqs, d->max_blocks_per_seq, d->blocks_full, d->blocks_slim);
   for (int r = 0; r < kRing; ++r) {
     kv->ev_used[r] = false;
     if (hipEventCreateWithFlags(&kv->ev[r], hipEventDisableTiming) != hipSuccess) {
@@ -1073,7 +814,7 @@ static via_status attach_checks(via_kv* kv, int32_t seq_id, int32_t n) {
   if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
   if (kv->step_open) return fail(VIA_ESTATE, "a step is open");
   if (seq_id < 0 || seq_id >= kv->d.max_seqs) return fail(VIA_EINVAL, "seq_id %d out of range", seq_id);
-  if (kv->seqs[seq_id].on) return fail(VIA_ESTATE, "sequence %d already attached", seq_id);
+  if (kv->bk.seqs[seq_id].on) return fail(VIA_ESTATE, "sequence %d already attached", seq_id);
   if (n < 0) return fail(VIA_EINVAL, "negative length");
   return VIA_OK;
 }
@@ -1081,14 +822,14 @@ static via_status attach_checks(via_kv* kv, int32_t seq_id, int32_t n) {
 via_status via_kv_seq_reserve(via_kv* kv, int32_t seq_id, int32_t n_ctx) {
   via_status st = attach_checks(kv, seq_id, n_ctx);
   if (st) return st;
-  if (blocks_for(n_ctx) > (int)kv->free_[0].size() || blocks_for(n_ctx) > (int)kv->free_[1].size() ||
+  if (blocks_for(n_ctx) > (int)kv->bk.free_[0].size() || blocks_for(n_ctx) > (int)kv->bk.free_[1].size() ||
       blocks_for(n_ctx) > kv->d.max_blocks_per_seq)
     return fail(VIA_ENOMEM, "not enough KV blocks for %d slots", n_ctx);
-  kv->seqs[seq_id] = SeqSt();
-  kv->seqs[seq_id].on = true;
-  alloc_blocks(kv, 0, {{seq_id, n_ctx}}, nullptr);
-  alloc_blocks(kv, 1, {{seq_id, n_ctx}}, nullptr);
-  kv->seqs[seq_id].valid[0] = kv->seqs[seq_id].valid[1] = n_ctx;
+  kv->bk.seqs[seq_id] = SeqSt();
+  kv->bk.seqs[seq_id].on = true;
+  book_alloc(kv->bk, 0, {{seq_id, n_ctx}}, nullptr);
+  book_alloc(kv->bk, 1, {{seq_id, n_ctx}}, nullptr);
+  kv->bk.seqs[seq_id].valid[0] = kv->bk.seqs[seq_id].valid[1] = n_ctx;
   return VIA_OK;
 }
 
@@ -1099,45 +840,23 @@ via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* 
   if (n > 0 && !tokens) return fail(VIA_EINVAL, "null tokens");
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= m->d.vocab) return fail(VIA_EINVAL, "token %d out of range", tokens[i]);
-  if (blocks_for(n) > (int)kv->free_[0].size() || blocks_for(n) > (int)kv->free_[1].size() ||
+  if (blocks_for(n) > (int)kv->bk.free_[0].size() || blocks_for(n) > (int)kv->bk.free_[1].size() ||
       blocks_for(n) > kv->d.max_blocks_per_seq)
     return fail(VIA_ENOMEM, "not enough KV blocks for %d slots", n);
-  kv->seqs[seq_id] = SeqSt();
-  kv->seqs[seq_id].on = true;
-  SeqSt& S = kv->seqs[seq_id];
+  kv->bk.seqs[seq_id] = SeqSt();
+  kv->bk.seqs[seq_id].on = true;
+  SeqSt& S = kv->bk.seqs[seq_id];
   hipStream_t s = (hipStream_t)stream;
   const int G = m->D.G;
   for (int cache = 0; cache < 2; ++cache) {
-    alloc_blocks(kv, cache, {{seq_id, n}}, nullptr);
+    book_alloc(kv->bk, cache, {{seq_id, n}}, nullptr);
     for (int c0 = 0; c0 < n; c0 += kv->d.max_rows) {
       int c1 = std::min(n, c0 + kv->d.max_rows);
       Plan P;
-      SeqInfo si{};
-      si.row_start = 0;
-      si.n_rows = c1 - c0;
-      si.kv_len = c1;
-      si.win_base = c0;
-      si.bt = 0;
-      si.n_blocks = (int)S.table[cache].size();
-      for (int blk : S.table[cache]) P.btab.push_back(blk);
-      for (int i = c0; i < c1; ++i) {
-        RowInfo r{};
-        r.tok = tokens[i];
-        r.pos = i;
-        r.seq = 0;
-        r.slot = i;
-        r.blk = S.table[cache][i / kBlock];
-        r.vis_len = i + 1;
-        r.lm = -1;
-        P.rows.push_back(r);
-      }
-      P.seqs.push_back(si);
-      for (int q0 = 0; q0 < si.n_rows * G; q0 += kAttnQueries)
-        P.items.push_back(AttnItem{q0, 0, si.kv_len, si.row_start, si.n_rows, si.win_base,
-                                   si.bt, si.n_blocks});
+      build_prefill_plan(S, cache, tokens, c0, c1, G, P);
       if ((st = exec_forward(m, kv, cache, P, false, nullptr, 1.f, s))) {
-        trim_blocks(kv, 0, seq_id, 0);
-        trim_blocks(kv, 1, seq_id, 0);
+        book_trim(kv->bk, 0, seq_id, 0);
+        book_trim(kv->bk, 1, seq_id, 0);
         S = SeqSt();
         return st;
       }
@@ -1150,10 +869,10 @@ via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* 
 via_status via_kv_seq_release(via_kv* kv, int32_t seq_id) {
   if (!kv) return fail(VIA_EINVAL, "null KV handle");
   if (kv->step_open) return fail(VIA_ESTATE, "a step is open");
-  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
-  trim_blocks(kv, 0, seq_id, 0);
-  trim_blocks(kv, 1, seq_id, 0);
-  kv->seqs[seq_id] = SeqSt();
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->bk.seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
+  book_trim(kv->bk, 0, seq_id, 0);
+  book_trim(kv->bk, 1, seq_id, 0);
+  kv->bk.seqs[seq_id] = SeqSt();
   return VIA_OK;
 }
 
@@ -1161,8 +880,8 @@ via_status via_kv_seq_info(const via_kv* kv, int32_t seq_id, int32_t cache, int3
                            int32_t cap, int32_t* n_blocks) {
   if (!kv || !valid || !n_blocks) return fail(VIA_EINVAL, "null argument");
   if (cache != 0 && cache != 1) return fail(VIA_EINVAL, "cache must be VIA_CACHE_FULL or VIA_CACHE_SLIM");
-  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
-  const SeqSt& S = kv->seqs[seq_id];
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->bk.seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
+  const SeqSt& S = kv->bk.seqs[seq_id];
   *valid = S.valid[cache];
   *n_blocks = (int)S.table[cache].size();
   if (table) {
@@ -1209,7 +928,7 @@ via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_ou
   for (int b = 0; b < B; ++b) {
     ss[b].n = kv->step_n[b];
     ss[b].n_drafts = w.n_drafts[b];
-    ss[b].full_ran = kv->seqs[w.seq[b]].full_ran ? 1 : 0;
+    ss[b].full_ran = kv->bk.seqs[w.seq[b]].full_ran ? 1 : 0;
   }
   memcpy(blob.data(), ss.data(), B * sizeof(StepSeq));
   memcpy(blob.data() + (L.dtok - L.step_seqs), w.draft_tok.data(), (size_t)B * Dd * 4);
@@ -1326,92 +1045,28 @@ via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* str
   if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");
   if (!kv->step_open) return fail(VIA_ESTATE, "no open step to commit");
   const WinCopy& w = kv->win;
-  const int B = w.batch, Dd = std::max(1, w.max_drafts), V = kv->m->d.vocab;
   const int32_t* hp = dec->h_packed;
   // validate everything before touching state
-  std::vector<std::vector<int>> new_tokens_rows(B);
-  for (int b = 0; b < B; ++b) {
-    int status = hp[b], kappa = hp[B + b], emit = hp[2 * B + b], nl = hp[3 * B + b];
-    const int* path = hp + 4 * B + b * Dd;
-    const int n = kv->step_n[b];
-    if (status == 1) return fail(VIA_ESTATE, "sequence %d still needs the full verifier", w.seq[b]);
-    if (status != 0 && status != 2) return fail(VIA_EINVAL, "bad status %d", status);
-    if (kappa < 0 || kappa > w.n_drafts[b]) return fail(VIA_EINVAL, "kappa %d out of range", kappa);
-    if (emit < -1 || emit >= V) return fail(VIA_EINVAL, "emit %d out of range", emit);
-    if (status == 2) {
-      if (nl != n) return fail(VIA_EINVAL, "new_len must equal n when the sequence is not advanced");
-      continue;
-    }
-    if (nl != n + kappa + (emit >= 0 ? 1 : 0)) return fail(VIA_EINVAL, "new_len inconsistent with kappa/emit");
-    int prev = -1;
-    for (int i = 0; i < kappa; ++i) {
-      int j = path[i];
-      if (j < 0 || j >= w.n_drafts[b] || w.draft_parent[(size_t)b * w.max_drafts + j] != prev)
-        return fail(VIA_EINVAL, "accepted path of sequence %d is not a root path", w.seq[b]);
-      prev = j;
-    }
-    // window rows that stay valid: root + the first (kept - 1) path nodes
-    int kept = kappa + (emit >= 0 ? 1 : 0);
-    for (int i = 1; i < kept; ++i) {
-      int node = path[i - 1], row = -1;
-      for (int j = 0; j < w.n_drafts[b]; ++j)
-        if (w.draft_parent[(size_t)b * w.max_drafts + j] == node) {
-          row = w.draft_row[(size_t)b * w.max_drafts + j];
-          break;
-        }
-      if (row < 0) return fail(VIA_EINVAL, "accepted node %d has no fed row", node);
-      new_tokens_rows[b].push_back(row);
-    }
-  }
+  CommitMoves cm;
+  via_status st = plan_commit(kv->bk, w, kv->step_n, hp, kv->m->d.vocab, cm);
+  if (st) return st;
   // tree compaction moves (slim cache always, full cache where it ran)
   hipStream_t s = (hipStream_t)stream;
-  if (w.tree) {
-    for (int cache = 0; cache < 2; ++cache) {
-      std::vector<int32_t> bt;
-      std::vector<KvMove> mv;
-      for (int b = 0; b < B; ++b) {
-        const SeqSt& S = kv->seqs[w.seq[b]];
-        if (hp[b] != 0) continue;
-        if (cache == VIA_CACHE_FULL && !S.full_ran) continue;
-        int base = kv->step_n[b] - 1;
-        int off = (int)bt.size();
-        bool any = false;
-        for (size_t i = 0; i < new_tokens_rows[b].size(); ++i) {
-          int src = base + new_tokens_rows[b][i], dst = base + (int)i + 1;
-          if (src != dst) {
-            mv.push_back(KvMove{off, src, dst, 0});
-            any = true;
-          }
-        }
-        if (any)
-          for (int blk : S.table[cache]) bt.push_back(blk);
-      }
-      if (mv.empty()) continue;
-      const Layout& L = kv->L;
-      std::vector<char> blob(L.commit_bytes);
-      memcpy(blob.data(), bt.data(), bt.size() * 4);
-      memcpy(blob.data() + (L.c_moves - L.c_btab), mv.data(), mv.size() * sizeof(KvMove));
-      via_status st = upload(kv, kv->ws + L.c_btab, blob.data(), L.commit_bytes, s);
-      if (st) return st;
-      int slots = cache == VIA_CACHE_FULL ? kv->m->d.n_layers : (int)kv->m->route.size();
-      launch_kv_moves(kv->m->bf16, cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim,
-                      cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim, slots, kv->m->d.n_kv_heads,
-                      kv->m->d.head_dim, (const int32_t*)(kv->ws + L.c_btab), (const KvMove*)(kv->ws + L.c_moves),
-                      (int)mv.size(), s);
-      if ((st = hip_check(kv, hipGetLastError(), "compaction launch"))) return st;
-    }
+  for (int cache = 0; cache < 2; ++cache) {
+    if (cm.moves[cache].empty()) continue;
+    const Layout& L = kv->L;
+    std::vector<char> blob(L.commit_bytes);
+    memcpy(blob.data(), cm.btab[cache].data(), cm.btab[cache].size() * 4);
+    memcpy(blob.data() + (L.c_moves - L.c_btab), cm.moves[cache].data(), cm.moves[cache].size() * sizeof(KvMove));
+    if ((st = upload(kv, kv->ws + L.c_btab, blob.data(), L.commit_bytes, s))) return st;
+    const int slots = cache == VIA_CACHE_FULL ? kv->m->d.n_layers : (int)kv->m->route.size();
+    launch_kv_moves(kv->m->bf16, cache == VIA_CACHE_FULL ? kv->d.pool_full : kv->d.pool_slim,
+                    cache == VIA_CACHE_FULL ? kv->d.blocks_full : kv->d.blocks_slim, slots, kv->m->d.n_kv_heads,
+                    kv->m->d.head_dim, (const int32_t*)(kv->ws + L.c_btab), (const KvMove*)(kv->ws + L.c_moves),
+                    (int)cm.moves[cache].size(), s);
+    if ((st = hip_check(kv, hipGetLastError(), "compaction launch"))) return st;
   }
-  for (int b = 0; b < B; ++b) {
-    SeqSt& S = kv->seqs[w.seq[b]];
-    if (hp[b] == 0) {
-      int nv = hp[3 * B + b] - 1;
-      S.valid[VIA_CACHE_SLIM] = nv;
-      if (S.full_ran) S.valid[VIA_CACHE_FULL] = nv;
-    }
-    trim_blocks(kv, VIA_CACHE_SLIM, w.seq[b], S.valid[VIA_CACHE_SLIM]);
-    trim_blocks(kv, VIA_CACHE_FULL, w.seq[b], S.valid[VIA_CACHE_FULL]);
-    S.full_ran = false;
-  }
+  apply_commit(kv->bk, w, hp);
   kv->step_open = false;
   kv->xpref_ok = false;
   return VIA_OK;

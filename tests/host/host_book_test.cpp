@@ -1,0 +1,481 @@
+// CPU tests of the host bookkeeping (paper_2606_12243_amd/csrc/host_book.cpp):
+// the paged block allocator, window validation, row plans with lag rows and
+// tree masks, commit validation, tree-compaction moves and the commit itself.
+// Built with -fsanitize=address,undefined by tests/test_host_book.py.
+#include <cstdio>
+#include <cstdlib>
+#include <random>
+#include <vector>
+
+#include "host_book.h"
+
+using namespace via;
+
+static int g_fail = 0;
+#define CHECK(c)                                                          \
+  do {                                                                    \
+    if (!(c)) {                                                           \
+      std::printf("FAIL %s:%d: %s (%s)\n", __FILE__, __LINE__, #c, last_error()); \
+      ++g_fail;                                                           \
+    }                                                                     \
+  } while (0)
+
+static const int V = 100;
+
+// A window built from plain vectors (chain unless parents are given).
+struct Win {
+  std::vector<int32_t> seq, n_rows, row_tok, row_depth, n_drafts, draft_tok, draft_row, draft_parent, n_lag,
+      lag_tok;
+  std::vector<uint64_t> row_mask;
+  via_window w{};
+  void finish(int max_rows, int max_drafts, int max_lag, bool tree) {
+    w.batch = (int)seq.size();
+    w.max_rows = max_rows;
+    w.max_drafts = max_drafts;
+    w.max_lag = max_lag;
+    w.seq_id = seq.data();
+    w.n_rows = n_rows.data();
+    w.row_tok = row_tok.data();
+    w.row_depth = tree ? row_depth.data() : nullptr;
+    w.row_mask = tree ? row_mask.data() : nullptr;
+    w.n_drafts = n_drafts.data();
+    w.draft_tok = draft_tok.data();
+    w.draft_row = draft_row.data();
+    w.draft_parent = tree ? draft_parent.data() : nullptr;
+    w.n_lag = n_lag.empty() ? nullptr : n_lag.data();
+    w.lag_tok = lag_tok.empty() ? nullptr : lag_tok.data();
+  }
+};
+
+// Chain window: per sequence k drafts, rows [pending, d0..d_{k-2}].
+static Win chain(const std::vector<int>& seqs, int k, int max_drafts = 8) {
+  Win c;
+  for (int s : seqs) {
+    c.seq.push_back(s);
+    c.n_rows.push_back(k);
+    c.n_drafts.push_back(k);
+    for (int r = 0; r < k; ++r) c.row_tok.push_back((s * 7 + r) % V);
+    for (int r = k; r < k; ++r) c.row_tok.push_back(0);
+    for (int j = 0; j < max_drafts; ++j) {
+      c.draft_tok.push_back(j < k ? (s * 11 + j) % V : 0);
+      c.draft_row.push_back(j < k ? j : 0);
+    }
+  }
+  c.finish(k, max_drafts, 1, false);
+  return c;
+}
+
+static bool owned_once(const KvBook& bk, int cache, int n_blocks) {
+  std::vector<int> seen(n_blocks, 0);
+  for (const SeqSt& S : bk.seqs)
+    for (int b : S.table[cache]) {
+      if (b < 0 || b >= n_blocks || seen[b]++) return false;
+    }
+  for (int b : bk.free_[cache]) {
+    if (b < 0 || b >= n_blocks || seen[b]++) return false;
+  }
+  for (int v : seen)
+    if (v != 1) return false;
+  return true;
+}
+
+static void attach(KvBook& bk, int seq, int n) {
+  bk.seqs[seq] = SeqSt();
+  bk.seqs[seq].on = true;
+  CHECK(book_alloc(bk, 0, {{seq, n}}, nullptr) == VIA_OK);
+  CHECK(book_alloc(bk, 1, {{seq, n}}, nullptr) == VIA_OK);
+  bk.seqs[seq].valid[0] = bk.seqs[seq].valid[1] = n;
+}
+
+static void test_allocator() {
+  KvBook bk;
+  book_init(bk, 3, 4, 8, 8);
+  CHECK(book_alloc(bk, 0, {{0, 20}, {1, 16}}, nullptr) == VIA_OK);  // seq 0: 2 blocks, seq 1: 1
+  CHECK((bk.seqs[0].table[0] == std::vector<int>{0, 1}) && (bk.seqs[1].table[0] == std::vector<int>{2}));
+  book_trim(bk, 0, 0, 16);  // keeps block 0
+  CHECK(bk.seqs[0].table[0] == std::vector<int>{0});
+  CHECK(book_alloc(bk, 0, {{1, 48}}, nullptr) == VIA_OK);  // lowest free first: 1, 3
+  CHECK((bk.seqs[1].table[0] == std::vector<int>{2, 1, 3}));
+  // more than max_blocks_per_seq (4) or more than the pool holds: nothing taken
+  KvBook before = bk;
+  CHECK(book_alloc(bk, 0, {{0, 16 * 5}}, nullptr) == VIA_ENOMEM);
+  CHECK(book_alloc(bk, 0, {{0, 64}, {2, 64}}, nullptr) == VIA_ENOMEM);  // 3 + 4 > 4 free
+  CHECK(bk.seqs[0].table[0] == before.seqs[0].table[0] && bk.free_[0] == before.free_[0]);
+  // release_taken undoes exactly what an allocation took
+  std::vector<std::pair<int, int>> taken;
+  CHECK(book_alloc(bk, 0, {{0, 40}, {2, 30}}, &taken) == VIA_OK);
+  CHECK(taken.size() == 4);
+  book_release_taken(bk, 0, taken);
+  CHECK(bk.seqs[0].table[0] == before.seqs[0].table[0] && bk.seqs[2].table[0].empty());
+  CHECK(bk.free_[0] == before.free_[0]);
+  CHECK(owned_once(bk, 0, 8) && owned_once(bk, 1, 8));
+}
+
+static void test_window_validation() {
+  KvBook bk;
+  book_init(bk, 4, 8, 32, 32);
+  attach(bk, 0, 10);
+  attach(bk, 2, 33);
+  WinCopy c;
+  Win ok = chain({0, 2}, 4);
+  CHECK(copy_window(bk, &ok.w, V, 4, 8, c) == VIA_OK);
+  CHECK(c.batch == 2 && c.seq[1] == 2 && c.draft_tok[8 + 3] == (2 * 11 + 3) % V && !c.tree);
+  CHECK(copy_window(bk, nullptr, V, 4, 8, c) == VIA_EINVAL);
+  {
+    Win w = chain({0, 1}, 4);  // 1 not attached
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  {
+    Win w = chain({0, 0}, 4);  // repeated
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  {
+    Win w = chain({0}, 4);
+    CHECK(copy_window(bk, &w.w, V, 0, 8, c) == VIA_EINVAL);  // batch above max_batch
+    CHECK(copy_window(bk, &w.w, V, 4, 4, c) == VIA_EINVAL);  // strides above the handle's max_drafts
+  }
+  {
+    Win w = chain({0}, 4);
+    w.row_tok[1] = V;  // token out of range
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  {
+    Win w = chain({0}, 4);
+    w.draft_tok[2] = -1;
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  {
+    Win w = chain({0}, 4);
+    w.draft_row[2] = 1;  // chain draft j must be verified by row j
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  {
+    Win w = chain({0}, 4);
+    w.n_rows[0] = 5;  // more rows than the stride
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  {
+    Win w = chain({0}, 4);
+    w.w.draft_tok = nullptr;
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+  // tree: root -> {0, 1}; 0 -> {2}; rows: root, node 0
+  {
+    Win w;
+    w.seq = {2};
+    w.n_rows = {2};
+    w.row_tok = {5, 6};
+    w.row_depth = {0, 1};
+    w.row_mask = {1, 3};
+    w.n_drafts = {3};
+    w.draft_tok = {6, 7, 8, 0};
+    w.draft_row = {0, 0, 1, 0};
+    w.draft_parent = {-1, -1, 0, -1};
+    w.finish(2, 4, 1, true);
+    CHECK(copy_window(bk, &w.w, V, 4, 8, c) == VIA_OK && c.tree);
+    Win bad = w;
+    bad.row_mask = {1, 2};  // row 1 misses row 0
+    bad.finish(2, 4, 1, true);
+    CHECK(copy_window(bk, &bad.w, V, 4, 8, c) == VIA_EINVAL);
+    bad = w;
+    bad.draft_row = {0, 1, 1, 0};  // a child of the root verified by row 1
+    bad.finish(2, 4, 1, true);
+    CHECK(copy_window(bk, &bad.w, V, 4, 8, c) == VIA_EINVAL);
+    bad = w;
+    bad.draft_parent = {-1, -1, 2, -1};  // parent index not below j
+    bad.finish(2, 4, 1, true);
+    CHECK(copy_window(bk, &bad.w, V, 4, 8, c) == VIA_EINVAL);
+    bad = w;
+    bad.row_depth = {1, 1};  // row 0 must sit at depth 0
+    bad.finish(2, 4, 1, true);
+    CHECK(copy_window(bk, &bad.w, V, 4, 8, c) == VIA_EINVAL);
+    bad = w;
+    bad.w.row_mask = nullptr;  // half a tree
+    CHECK(copy_window(bk, &bad.w, V, 4, 8, c) == VIA_EINVAL);
+  }
+}
+
+static void test_plans() {
+  KvBook bk;
+  book_init(bk, 2, 8, 16, 16);
+  attach(bk, 0, 20);
+  attach(bk, 1, 5);
+  bk.seqs[1].valid[0] = 3;  // full cache of seq 1 lags 2 tokens
+  WinCopy c;
+  Win w = chain({0, 1}, 4);
+  w.n_lag = {0, 2};
+  w.lag_tok = {0, 0, 41, 42};
+  w.finish(4, 8, 2, false);
+  CHECK(copy_window(bk, &w.w, V, 2, 8, c) == VIA_OK);
+  // slim forward: window rows only, positions n-1 .. n+2, slots after the valid length
+  Plan P;
+  std::vector<std::pair<int, int>> taken;
+  CHECK(build_verify_plan(bk, VIA_CACHE_SLIM, c, {0, 1}, &w.w, true, V, 4, P, &taken) == VIA_OK);
+  CHECK(P.rows.size() == 8 && P.lm.size() == 8 && P.seqs.size() == 2);
+  CHECK(P.rows[0].pos == 20 && P.rows[0].slot == 20 && P.rows[3].vis_len == 24 && P.rows[4].pos == 5);
+  CHECK(P.rows[4].blk == bk.seqs[1].table[1][0]);
+  CHECK(P.lm[5].out == 1 * 4 + 1 && P.lm[5].n_drafts == 1 && P.lm[5].draft_idx[0] == 8 + 1);
+  CHECK(P.items.size() == 2);  // 4 rows x 4 heads = 16 queries per sequence: one item each
+  CHECK(bk.seqs[0].table[1].size() == 2 && bk.seqs[1].table[1].size() == 1);
+  book_release_taken(bk, VIA_CACHE_SLIM, taken);
+  CHECK(owned_once(bk, 1, 16));
+  // full forward of seq 1 only: 2 lag rows first, then the window
+  Plan F;
+  CHECK(build_verify_plan(bk, VIA_CACHE_FULL, c, {1}, &w.w, true, V, 4, F, nullptr) == VIA_OK);
+  CHECK(F.rows.size() == 6 && F.rows[0].tok == 41 && F.rows[1].pos == 4 && F.rows[1].lm == -1);
+  CHECK(F.rows[2].pos == 5 && F.rows[2].slot == 5 && F.rows[2].vis_len == 6 && F.seqs[0].kv_len == 9);
+  CHECK(F.lm.size() == 4 && F.lm[0].row == 2);
+  // a lag that disagrees with the cache: ESTATE, nothing allocated
+  KvBook before = bk;
+  w.n_lag = {0, 1};
+  w.finish(4, 8, 2, false);
+  Plan G;
+  CHECK(build_verify_plan(bk, VIA_CACHE_FULL, c, {1}, &w.w, true, V, 4, G, nullptr) == VIA_ESTATE);
+  CHECK(bk.free_[0] == before.free_[0]);
+  // a lag token out of range
+  w.n_lag = {0, 2};
+  w.lag_tok[3] = V + 3;
+  w.finish(4, 8, 2, false);
+  CHECK(build_verify_plan(bk, VIA_CACHE_FULL, c, {1}, &w.w, true, V, 4, G, nullptr) == VIA_EINVAL);
+  // pool exhaustion: nothing allocated
+  KvBook small;
+  book_init(small, 1, 8, 2, 2);
+  attach(small, 0, 30);
+  Win w2 = chain({0}, 4);
+  WinCopy c2;
+  CHECK(copy_window(small, &w2.w, V, 1, 8, c2) == VIA_OK);
+  Plan H;
+  CHECK(build_verify_plan(small, VIA_CACHE_SLIM, c2, {0}, &w2.w, true, V, 4, H, nullptr) == VIA_ENOMEM);
+  CHECK(small.seqs[0].table[1].size() == 2 && small.free_[1].empty());
+  // prefill plan rows [16, 20) of a 20-token prompt
+  std::vector<int32_t> toks(20);
+  for (int i = 0; i < 20; ++i) toks[i] = i;
+  Plan Q;
+  build_prefill_plan(bk.seqs[0], VIA_CACHE_FULL, toks.data(), 16, 20, 4, Q);
+  CHECK(Q.rows.size() == 4 && Q.rows[0].slot == 16 && Q.rows[0].vis_len == 17 && Q.seqs[0].kv_len == 20);
+}
+
+// Decision block for B sequences, max_drafts D.
+static std::vector<int32_t> decision(int B, int D) { return std::vector<int32_t>(4 * B + B * D, -1); }
+static void set(std::vector<int32_t>& hp, int B, int D, int b, int st, int kappa, int emit, int nl,
+                std::vector<int> path) {
+  hp[b] = st;
+  hp[B + b] = kappa;
+  hp[2 * B + b] = emit;
+  hp[3 * B + b] = nl;
+  for (size_t i = 0; i < path.size(); ++i) hp[4 * B + b * D + i] = path[i];
+}
+
+static void test_commit() {
+  KvBook bk;
+  book_init(bk, 2, 8, 32, 32);
+  attach(bk, 0, 30);
+  attach(bk, 1, 14);
+  Win w = chain({0, 1}, 4);
+  WinCopy c;
+  CHECK(copy_window(bk, &w.w, V, 2, 8, c) == VIA_OK);
+  std::vector<std::pair<int, int>> t0, t1;
+  Plan P;
+  CHECK(build_verify_plan(bk, VIA_CACHE_SLIM, c, {0, 1}, &w.w, true, V, 4, P, nullptr) == VIA_OK);
+  bk.seqs[0].full_ran = true;
+  Plan F;
+  CHECK(build_verify_plan(bk, VIA_CACHE_FULL, c, {0}, &w.w, true, V, 4, F, nullptr) == VIA_OK);
+  const std::vector<int> step_n = {31, 15};
+  const int B = 2, D = 8;
+  CommitMoves cm;
+  // malformed decisions are refused and change nothing
+  auto hp = decision(B, D);
+  set(hp, B, D, 0, 1, 0, -1, 31, {});
+  set(hp, B, D, 1, 0, 0, 5, 16, {});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_ESTATE);  // still needs the full verifier
+  set(hp, B, D, 0, 3, 0, -1, 31, {});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);  // bad status
+  set(hp, B, D, 0, 0, 5, -1, 36, {0, 1, 2, 3, 4});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);  // kappa above n_drafts
+  set(hp, B, D, 0, 0, 2, V, 34, {0, 1});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);  // emit out of range
+  set(hp, B, D, 0, 0, 2, 7, 33, {0, 1});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);  // new_len inconsistent
+  set(hp, B, D, 0, 0, 2, 7, 34, {1, 0});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);  // not a root path
+  set(hp, B, D, 0, 2, 0, -1, 32, {});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);  // status 2 must keep n
+  // a good decision: seq 0 accepts 2 drafts and emits (full ran), seq 1 status 2
+  set(hp, B, D, 0, 0, 2, 7, 34, {0, 1});
+  set(hp, B, D, 1, 2, 0, -1, 15, {});
+  KvBook before = bk;
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_OK);
+  CHECK(cm.moves[0].empty() && cm.moves[1].empty());  // chain: nothing to compact
+  CHECK(bk.seqs[0].valid[0] == before.seqs[0].valid[0]);  // validation alone changes nothing
+  apply_commit(bk, c, hp.data());
+  CHECK(bk.seqs[0].valid[1] == 33 && bk.seqs[0].valid[0] == 33 && bk.seqs[0].table[1].size() == 3);
+  CHECK(bk.seqs[1].valid[1] == 14 && bk.seqs[1].valid[0] == 14 && bk.seqs[1].table[1].size() == 1);
+  CHECK(!bk.seqs[0].full_ran && owned_once(bk, 0, 32) && owned_once(bk, 1, 32));
+}
+
+static void test_tree_moves() {
+  KvBook bk;
+  book_init(bk, 1, 8, 16, 16);
+  attach(bk, 0, 15);
+  // root -> {0, 1}; 1 -> {2, 3}; 3 -> {4}; rows: root, node 1, node 3
+  Win w;
+  w.seq = {0};
+  w.n_rows = {3};
+  w.row_tok = {5, 6, 7};
+  w.row_depth = {0, 1, 2};
+  w.row_mask = {1, 3, 7};
+  w.n_drafts = {5};
+  w.draft_tok = {1, 2, 3, 4, 5, 0, 0, 0};
+  w.draft_row = {0, 0, 1, 1, 2, 0, 0, 0};
+  w.draft_parent = {-1, -1, 1, 1, 3, -1, -1, -1};
+  w.finish(3, 8, 1, true);
+  WinCopy c;
+  CHECK(copy_window(bk, &w.w, V, 1, 8, c) == VIA_OK);
+  Plan P;
+  CHECK(build_verify_plan(bk, VIA_CACHE_SLIM, c, {0}, &w.w, true, V, 4, P, nullptr) == VIA_OK);
+  CHECK(P.rows[0].pos == 15 && P.rows[1].pos == 16 && P.rows[2].pos == 17 && P.rows[2].vis_len == 15 && P.rows[2].mask == 7);
+  const std::vector<int> step_n = {16};
+  auto hp = decision(1, 8);
+  // path 1 -> 3 -> 4, all accepted, no emit: root stays at slot 15, node 1's row (1) to 16, node 3's row (2) to 17
+  set(hp, 1, 8, 0, 0, 3, -1, 19, {1, 3, 4});
+  CommitMoves cm;
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_OK);
+  CHECK(cm.moves[1].empty());  // slots 16 and 17 are rows 1 and 2 already
+  // path 1 -> 2 (node 2 is a leaf, fed by no row): kept rows are root and node 1 only
+  set(hp, 1, 8, 0, 0, 2, -1, 18, {1, 2});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_OK && cm.moves[1].empty());
+  // path 0 (a leaf) then emit: node 0 has no row -> refused
+  set(hp, 1, 8, 0, 0, 1, 9, 18, {0});
+  CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_EINVAL);
+  // a tree where the accepted path skips a fed row: root -> {0, 1}; 0 -> {2}; 1 -> {3}; 3 -> {4}
+  Win t = w;
+  t.n_rows = {4};
+  t.row_tok = {5, 6, 7, 8};
+  t.row_depth = {0, 1, 1, 2};
+  t.row_mask = {1, 3, 5, 13};
+  t.draft_row = {0, 0, 1, 2, 3, 0, 0, 0};
+  t.draft_parent = {-1, -1, 0, 1, 3, -1, -1, -1};
+  t.finish(4, 8, 1, true);
+  KvBook bk2;
+  book_init(bk2, 1, 8, 16, 16);
+  attach(bk2, 0, 15);
+  CHECK(copy_window(bk2, &t.w, V, 1, 8, c) == VIA_OK);
+  Plan P2;
+  CHECK(build_verify_plan(bk2, VIA_CACHE_SLIM, c, {0}, &t.w, true, V, 4, P2, nullptr) == VIA_OK);
+  bk2.seqs[0].full_ran = true;
+  Plan F2;
+  CHECK(build_verify_plan(bk2, VIA_CACHE_FULL, c, {0}, &t.w, true, V, 4, F2, nullptr) == VIA_OK);
+  // path 1 -> 3 -> 4: node 1 is row 2 (slot 17 -> 16), node 3 is row 3 (slot 18 -> 17)
+  set(hp, 1, 8, 0, 0, 3, -1, 19, {1, 3, 4});
+  CHECK(plan_commit(bk2, c, step_n, hp.data(), V, cm) == VIA_OK);
+  for (int cache = 0; cache < 2; ++cache) {
+    CHECK(cm.moves[cache].size() == 2);
+    if (cm.moves[cache].size() == 2) {
+      CHECK(cm.moves[cache][0].src == 17 && cm.moves[cache][0].dst == 16);
+      CHECK(cm.moves[cache][1].src == 18 && cm.moves[cache][1].dst == 17);
+      CHECK(cm.btab[cache].size() == bk2.seqs[0].table[cache].size());
+    }
+  }
+  apply_commit(bk2, c, hp.data());
+  CHECK(bk2.seqs[0].valid[0] == 18 && bk2.seqs[0].valid[1] == 18);
+}
+
+// Random steps: windows of random sizes, random lag catch-up, random
+// decisions; the pools stay partitioned and the tables fit the valid lengths.
+static void test_random_steps() {
+  std::mt19937 rng(7);
+  const int NB = 40, S = 3;
+  KvBook bk;
+  book_init(bk, S, 16, NB, NB);
+  for (int s = 0; s < S; ++s) attach(bk, s, 5 + 17 * s);
+  for (int it = 0; it < 400; ++it) {
+    std::vector<int> seqs;
+    for (int s = 0; s < S; ++s)
+      if (rng() % 3) seqs.push_back(s);
+    if (seqs.empty()) seqs.push_back(it % S);
+    const int k = 1 + rng() % 6;
+    Win w = chain(seqs, k);
+    std::vector<int32_t> lag(seqs.size()), lt(seqs.size() * 64, 1);
+    int ml = 1;
+    for (size_t b = 0; b < seqs.size(); ++b) {
+      lag[b] = bk.seqs[seqs[b]].valid[1] - bk.seqs[seqs[b]].valid[0];
+      ml = std::max(ml, (int)lag[b]);
+    }
+    if (ml > 64) continue;
+    w.n_lag = lag;
+    w.lag_tok = lt;
+    w.finish(k, 8, 64, false);
+    WinCopy c;
+    CHECK(copy_window(bk, &w.w, V, S, 8, c) == VIA_OK);
+    std::vector<int> run;
+    for (size_t b = 0; b < seqs.size(); ++b) run.push_back((int)b);
+    Plan P;
+    KvBook before = bk;
+    via_status st = build_verify_plan(bk, VIA_CACHE_SLIM, c, run, &w.w, true, V, 4, P, nullptr);
+    if (st == VIA_ENOMEM) {
+      CHECK(bk.free_[1] == before.free_[1]);
+      // make room: drop the longest sequence back to a short context
+      int big = 0;
+      for (int s = 1; s < S; ++s)
+        if (bk.seqs[s].valid[1] > bk.seqs[big].valid[1]) big = s;
+      for (int cc = 0; cc < 2; ++cc) {
+        bk.seqs[big].valid[cc] = 3;
+        book_trim(bk, cc, big, 3);
+      }
+      continue;
+    }
+    CHECK(st == VIA_OK);
+    std::vector<int> frun;
+    for (size_t b = 0; b < seqs.size(); ++b)
+      if (rng() % 2) frun.push_back((int)b);
+    if (!frun.empty()) {
+      Plan F;
+      std::vector<std::pair<int, int>> taken;
+      st = build_verify_plan(bk, VIA_CACHE_FULL, c, frun, &w.w, true, V, 4, F, &taken);
+      if (st == VIA_ENOMEM) {
+        frun.clear();
+      } else {
+        CHECK(st == VIA_OK);
+        for (int b : frun) bk.seqs[seqs[b]].full_ran = true;
+      }
+    }
+    std::vector<int> step_n;
+    auto hp = decision((int)seqs.size(), 8);
+    for (size_t b = 0; b < seqs.size(); ++b) {
+      const int n = bk.seqs[seqs[b]].valid[1] + 1;
+      step_n.push_back(n);
+      const bool ran = bk.seqs[seqs[b]].full_ran;
+      const int status = ran && rng() % 10 == 0 ? 2 : 0;
+      const int kappa = status ? 0 : rng() % (k + 1);
+      // every draft accepted: nothing is emitted (no bonus token)
+      const int emit = status || kappa == k ? -1 : (int)(rng() % V);
+      std::vector<int> path;
+      for (int j = 0; j < kappa; ++j) path.push_back(j);
+      set(hp, (int)seqs.size(), 8, (int)b, status, kappa, emit, status ? n : n + kappa + (emit >= 0), path);
+    }
+    CommitMoves cm;
+    CHECK(plan_commit(bk, c, step_n, hp.data(), V, cm) == VIA_OK);
+    apply_commit(bk, c, hp.data());
+    for (int s = 0; s < S; ++s) {
+      const SeqSt& Sq = bk.seqs[s];
+      CHECK(Sq.valid[0] <= Sq.valid[1]);
+      for (int cc = 0; cc < 2; ++cc) CHECK((int)Sq.table[cc].size() == blocks_for(Sq.valid[cc]));
+    }
+    CHECK(owned_once(bk, 0, NB) && owned_once(bk, 1, NB));
+  }
+}
+
+int main() {
+  test_allocator();
+  test_window_validation();
+  test_plans();
+  test_commit();
+  test_tree_moves();
+  test_random_steps();
+  if (g_fail) {
+    std::printf("%d check(s) failed\n", g_fail);
+    return 1;
+  }
+  std::printf("ALL OK\n");
+  return 0;
+}
