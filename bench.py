@@ -11,13 +11,16 @@ step's drafts, then the KV state is reset and the recorded steps are
 replayed; W replayed steps warm up, the next K are timed.
 
 value = accepted (committed) tokens summed over the batch / timed seconds, at
-the workload's logit temperature (calibrated for the bf16 workloads so that
-about half of the greedy drafts clear the accept threshold).  The JSON line
-adds the verify-step latency percentiles, the roofline of the dominant
-kernel (HIP events carried by its dispatches during the timed region), the
-whole step's algorithmic bytes against HBM peak, the same workload at T = 1
-(every drafted position escalated to the full verifier) and the oracle's
-rate on a bounded sample of the same workload.
+the workload's logit temperature (calibrated for the 1B and the 8B chain and
+tree workloads so that about half of the greedy drafts clear the accept
+threshold; the long-context batch runs at its mixed-tier temperature).  The
+JSON line adds the verify-step latency percentiles, the roofline of the
+dominant kernel (HIP events carried by its dispatches during the timed
+region), the whole step's algorithmic bytes against HBM peak, the same
+workload at its mixed-tier temperature (all three tiers, escalations of part
+of the batch with lag rows) and at T = 1 (every drafted position escalated to
+the full verifier), and the oracle's rate on a bounded sample of the same
+workload.
 
     python bench.py [--steps K] [--warmup W] [--config 8b_bf16_chain]
 """
@@ -83,19 +86,34 @@ def attach_context(cfg, sess, synthetic):
             sess.prefill(b, toks)
 
 
-def step_bytes(cfg, kv_slim_tokens, kv_full_tokens, full_ran):
+def shared_layers(route):
+    """Leading layers the slim route shares with the full model (route[i] == i)."""
+    n = 0
+    while n < len(route) and route[n] == n:
+        n += 1
+    return n
+
+
+def step_bytes(cfg, kv_slim_tokens, full_seqs, run):
     """Algorithmic HBM bytes of one step: the routed layers' weights and the
-    head for the slim forward, every layer's weights and the head again when
-    the full verifier ran, plus the cached K/V each forward read (tokens
-    summed over the sequences it covered)."""
+    head for the slim forward plus the cached K/V it read (tokens summed over
+    the batch); when the full verifier ran, the weights of the layers it ran,
+    the head, and the K/V those layers read for the sequences it covered.
+    ``full_seqs[b]`` = (cached + lag tokens, lag tokens) of the full cache
+    before the step.  Without lag rows the full forward starts after the
+    layers the slim route shares with it (their state comes from the slim
+    forward), so those layers' weights and K/V are not read again."""
     from workload.configs import model_bytes
     md = cfg["model"]
     slim = model_bytes(md, cfg["route"])
-    full = model_bytes(md)
     kvb = slim["kv_per_token_layer"]
     tot = slim["layers"] + slim["head"] + kvb * len(cfg["route"]) * kv_slim_tokens
-    if full_ran:
-        tot += full["layers"] + full["head"] + kvb * md["n_layers"] * kv_full_tokens
+    ran = [b for b in range(len(run)) if run[b]]
+    if ran:
+        n_sh = shared_layers(cfg["route"])
+        start = n_sh if all(full_seqs[b][1] == 0 for b in ran) and 0 < n_sh < len(cfg["route"]) else 0
+        layers = md["n_layers"] - start
+        tot += layers * slim["per_layer"] + slim["head"] + kvb * layers * sum(full_seqs[b][0] for b in ran)
     return tot
 
 
@@ -158,7 +176,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
         t_draft += time.time() - ts
         # cached tokens each forward of this step reads (for the step's algorithmic bytes)
         kv_slim = sum(sess.kv.seq_info(b, via.CACHE_SLIM)[0] for b in range(B))
-        kv_full = sum(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)) for b in range(B))
+        kv_full = [(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)), len(sess.lag(b))) for b in range(B)]
         h, run = sess.step(drafts, smp)
         recorded.append((drafts, h["new_len"].copy(), run.copy(), kv_slim, kv_full, smp))
     log(f"T={temperature:.4g}: reference decode of {n_steps} steps, drafting {t_draft:.2f}s")
@@ -213,7 +231,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
 
     lat, accepted, n_full_steps, t_total, mism, _ = replay(None)
     timer = replay(timer_kind)[5] if timer_kind is not None else (0, 0.0)
-    bytes_tot = sum(step_bytes(cfg, r[3], r[4], bool(r[2].any())) for r in recorded[warmup:])
+    bytes_tot = sum(step_bytes(cfg, r[3], r[4], r[2]) for r in recorded[warmup:])
     lat_ms = np.array(lat) * 1e3
     return dict(value=accepted / t_total, t_total=t_total, lat_ms=lat_ms, escalation=n_full_steps / max(1, steps),
                 mismatch=mism, t_draft=t_draft, bytes=bytes_tot, timer=timer, recorded=recorded,
@@ -295,6 +313,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-tier", action="store_true",
                     help="skip the T = 1 variant (every position escalated to the full verifier)")
+    ap.add_argument("--no-mixed", action="store_true",
+                    help="skip the mixed-tier variant (its calibrated temperature: all three tiers)")
     ap.add_argument("--breakdown", action="store_true", help="extra replay timing every kernel kind")
     ap.add_argument("--no-sampling", action="store_true", help="skip the sampling-rules variant")
     ap.add_argument("--no-drafter", action="store_true", help="skip the drafter-model variant")
@@ -364,6 +384,23 @@ def main():
                      "escalation_rate": round(r1["escalation"], 3), "replay_mismatch_steps": r1["mismatch"],
                      "step_roofline_frac": round(r1["bytes"] / r1["t_total"] / 1e9 / HBM_PEAK_GBS, 4)}
 
+    # the same workload at the mixed-tier temperature: all three tiers occur,
+    # escalations cover part of the batch and carry the lag rows of earlier steps
+    from workload import calibrated
+    mixed, rm = None, None
+    Tm = calibrated.MIXED_TEMPERATURE.get(args.config)
+    if not args.no_mixed and Tm is not None and Tm != T:
+        rm = run_workload(cfg, W, max(5, args.steps // 2), 2, Tm)
+        lm = rm["lat_ms"]
+        mixed = {"temperature": Tm, "value": round(rm["value"], 2), "unit": "tokens/s",
+                 "ms_per_step": round(float(lm.mean()), 3),
+                 "latency_ms": {"p10": round(float(np.percentile(lm, 10)), 3),
+                                "p50": round(float(np.percentile(lm, 50)), 3),
+                                "p90": round(float(np.percentile(lm, 90)), 3)},
+                 "steps": len(lm), "tokens_per_step": round(rm["accepted"] / len(lm), 3),
+                 "escalation_rate": round(rm["escalation"], 3), "replay_mismatch_steps": rm["mismatch"],
+                 "step_roofline_frac": round(rm["bytes"] / rm["t_total"] / 1e9 / HBM_PEAK_GBS, 4)}
+
     # the same workload under the sampling rules (App. A, lossless alpha = 0,
     # beta = 1): logits kept, the decision draws the owed samples
     sampled = None
@@ -400,7 +437,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, W, res["recorded"], res["init_tokens"])
+        cpu = cpu_baseline(cfg, W, res["recorded"], res["init_tokens"],
+                           mixed=(Tm, rm["recorded"], rm["init_tokens"]) if rm is not None else None)
 
     out = {
         "metric": METRIC, "value": round(res["value"], 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -415,10 +453,12 @@ def main():
                        "p90": round(float(np.percentile(lat_ms, 90)), 3)},
         "temperature": T,
         "escalation_rate": round(res["escalation"], 3),
+        "tokens_per_step": round(res["accepted"] / args.steps, 3),
         "replay_mismatch_steps": res["mismatch"],
         "drafting_s_untimed": round(res["t_draft"], 3),
         "roofline": roof,
         "step_roofline": step_roof,
+        "mixed_tier_variant": mixed,
         "full_tier_variant": full_tier,
         "sampling_rules_variant": sampled,
         "drafter_model_variant": drafter,
@@ -546,15 +586,31 @@ def measured_traffic(config):
     return rec.get("traffic_bytes_per_launch")
 
 
-def cpu_baseline(cfg, W, recorded, init_tokens):
-    """The oracle, as it stands, on a bounded sample: the first recorded step
-    of sequence 0 (slim forward, decision, full forward if escalated)."""
+def _cpu_backend():
+    """Threading and BLAS backends torch's CPU ops run on, as torch reports them."""
+    import torch
+    info = {}
+    for line in torch.__config__.parallel_info().splitlines():
+        if line.startswith("ATen parallel backend") or line.startswith("ATen/Parallel"):
+            info["parallel"] = line.split(":", 1)[-1].strip()
+    for item in torch.__config__.show().replace("\n", ",").split(","):
+        item = item.strip()
+        if item.startswith("BLAS_INFO=") or item.startswith("LAPACK_INFO="):
+            k, v = item.split("=", 1)
+            info[k.lower()] = v
+    return info
+
+
+def oracle_steps(cfg, W, recorded, init_tokens, T, n_steps, om=None):
+    """Replay the first recorded steps of sequence 0 through the oracle (fp64
+    CPU): per-step seconds, committed tokens, and whether every step agreed
+    with the GPU's committed length."""
     import torch
     from oracle.decode import Draft, TierParams, Verifier
     from oracle.model import OracleModel
     from workload import gen
     md = cfg["model"]
-    om = OracleModel(md, W)
+    om = om or OracleModel(md, W)
     ver = Verifier(om, cfg["route"])
     toks = init_tokens[0]
     if cfg.get("seed_kv") is not None:
@@ -565,16 +621,50 @@ def cpu_baseline(cfg, W, recorded, init_tokens):
         ver.attach_context(toks, kvf, kvs)
     else:
         ver.prefill(toks)
-    tok, par = recorded[0][0][0]
-    d = Draft.chain(tok) if par is None else Draft(list(tok), list(par))
-    t0 = time.perf_counter()
-    dec = ver.step({0: d}, TierParams(0.9, 0.5, cfg["temperature"]))
-    dt = time.perf_counter() - t0
-    acc = dec[0]["new_len"] - len(toks)
-    return {"value": round(acc / dt, 4), "unit": "tokens/s", "cores": torch.get_num_threads(), "kind": "oracle",
-            "sample": f"one verification step of sequence 0 of {cfg['name']} (slim forward, decision"
-                      f"{', full forward' if dec[0]['full_ran'] else ''}) in fp64: {acc} tokens in {dt:.2f}s",
-            "agrees_with_gpu_step": bool(dec[0]["new_len"] == int(recorded[0][1][0]))}
+    times, acc, agree, full = [], 0, True, 0
+    for i in range(min(n_steps, len(recorded))):
+        tok, par = recorded[i][0][0]
+        d = Draft.chain(tok) if par is None else Draft(list(tok), list(par))
+        n0 = ver.seqs[0].n
+        t0 = time.perf_counter()
+        dec = ver.step({0: d}, TierParams(0.9, 0.5, T))
+        times.append(time.perf_counter() - t0)
+        acc += dec[0]["new_len"] - n0
+        full += int(dec[0]["full_ran"])
+        agree = agree and dec[0]["new_len"] == int(recorded[i][1][0])
+        if not agree:
+            break
+    return times, acc, agree, full, om
+
+
+def cpu_baseline(cfg, W, recorded, init_tokens, mixed=None, n_steps=3):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    the first ``n_steps`` recorded steps of sequence 0 (slim forward,
+    decision, full forward when it escalates, commit), replayed in fp64 on
+    the host cores; ``mixed`` = (T, recorded, init_tokens) of the mixed-tier
+    run adds the same figures there.  value = committed tokens / oracle
+    seconds over the sample."""
+    import torch
+    T = float(cfg["temperature"])
+    times, acc, agree, full, om = oracle_steps(cfg, W, recorded, init_tokens, T, n_steps)
+    ms = np.array(times) * 1e3
+    pct = lambda a: {"p10": round(float(np.percentile(a, 10)), 1), "p50": round(float(np.percentile(a, 50)), 1),
+                     "p90": round(float(np.percentile(a, 90)), 1)}
+    out = {"value": round(acc / sum(times), 4), "unit": "tokens/s", "cores": torch.get_num_threads(),
+           "kind": "oracle",
+           "sample": f"first {len(times)} verification steps of sequence 0 of {cfg['name']} at T = {T:.4g} "
+                     f"(slim forward, decision, full forward in {full} of them, commit), fp64 numpy/torch on the "
+                     f"host: {acc} tokens in {sum(times):.2f}s",
+           "precision": "fp64", "step_ms": pct(ms), "steps": len(times), "agrees_with_gpu_steps": bool(agree),
+           "affinity_cpus": len(os.sched_getaffinity(0)), "threads_used": torch.get_num_threads(),
+           "backend": _cpu_backend()}
+    if mixed is not None:
+        Tm, rec_m, init_m = mixed
+        tm, acc_m, agree_m, full_m, _ = oracle_steps(cfg, W, rec_m, init_m, Tm, n_steps, om)
+        out["mixed_tier"] = {"temperature": Tm, "value": round(acc_m / sum(tm), 4), "unit": "tokens/s",
+                             "step_ms": pct(np.array(tm) * 1e3), "steps": len(tm), "full_forward_steps": full_m,
+                             "agrees_with_gpu_steps": bool(agree_m)}
+    return out
 
 
 if __name__ == "__main__":

@@ -63,6 +63,10 @@ class Lockstep:
                                                              self.p.forced), logits=True)
         self.o_id = {}    # GPU sequence id -> oracle sequence index
         self.log = []
+        # per step: which batch entries ran the full forward, with how many lag rows
+        # (sampled sequences), and the committed kappa of each sampled sequence
+        self.steps = []
+        self.gpu_tiers = set()   # tiers the GPU gave any draft of the batch (sampled or not)
         self.seen_tiers = set()
         self.max_logit_err = 0.0
 
@@ -126,6 +130,9 @@ class Lockstep:
         """drafts: {b: Draft}; runs both sides, compares, commits."""
         p = self.p
         order = sorted(drafts)
+        lag_before = {b: self.ver.seqs[self.o_id[b]].n - 1 - self.ver.seqs[self.o_id[b]].full.valid
+                      for b in order if self.sampled(b)}
+        gpu_lag = {b: len(self.sess.lag(b)) for b in order}
         raw = self.ver.step({self.o_id[b]: drafts[b] for b in order if self.sampled(b)}, p)  # oracle decides, commits
         dec_o = {b: raw[self.o_id[b]] for b in order if self.sampled(b)}
         gd = {b: (drafts[b].tok, None if self._is_chain(drafts[b]) else drafts[b].parent) for b in order}
@@ -135,6 +142,10 @@ class Lockstep:
         via.check(via.via_tier_decide(s.kv.h, s.p, s.out_slim.c, None, s.dec.c, s.sp()))
         s.stream.synchronize()
         h1 = s._host(w)
+        D = w.max_drafts
+        tiers_all = s.dec.tier[:w.B * D].cpu().numpy().reshape(w.B, D)
+        for i, b in enumerate(order):
+            self.gpu_tiers.update("ASF"[t] for t in tiers_all[i, :len(drafts[b].tok)])
         exempt = {}   # batch entry -> the near-tie positions that allow it to differ
         T = p.temperature
         for i, b in enumerate(order):
@@ -205,6 +216,10 @@ class Lockstep:
             s.commit(w, gd, hh)
         else:
             s.commit(w, gd)
+        self.steps.append(dict(step=step_idx, run=run.tolist(),
+                               gpu_lag={b: gpu_lag[b] for i, b in enumerate(order) if run[i]},
+                               full_lag={b: lag_before[b] for i, b in enumerate(order) if b in dec_o and run[i]},
+                               kappa={b: dec_o[b]["kappa"] for b in order if b in dec_o}))
         # committed tokens, valid lengths and block tables
         for b in order:
             if b not in dec_o:

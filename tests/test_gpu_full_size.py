@@ -23,7 +23,7 @@ from oracle.decode import Draft, TierParams  # noqa: E402
 from oracle.model import OracleModel  # noqa: E402
 from paper_2606_12243_amd import via  # noqa: E402
 from paper_2606_12243_amd.session import GreedyDrafter as GpuDrafter  # noqa: E402
-from workload import configs, gen  # noqa: E402
+from workload import calibrated, configs, gen  # noqa: E402
 
 from gpu_harness import Lockstep  # noqa: E402
 
@@ -48,16 +48,21 @@ def models():
         gm.close()
 
 
-# (workload, verify steps, sampled sequences, temperature).  At the workloads'
-# calibrated temperatures drafts split between the accept and slim tiers;
-# T = 1 sends every position to the full verifier.
+# (workload, verify steps, sampled sequences, temperature).  At the half-accept
+# temperatures (1B, 8B chain and tree) drafts split between the accept and
+# slim tiers; T = 1 sends every position to the full verifier; at the
+# mixed-tier temperature (the long-context batch's own, and "mixed" for the
+# 8B chain) all three tiers occur, some steps escalate only part of the batch
+# and the full forward of an escalated sequence carries the lag rows its cache
+# missed on earlier steps.  "ends": the shortest- and longest-context sequences.
 CASES = [
-    ("1b_bf16", 3, [0], None),
+    ("1b_bf16", 8, [0], None),
     ("8b_bf16_chain", 2, [3], None),
+    ("8b_bf16_chain", 6, [0, 2], "mixed"),
     ("8b_bf16_chain", 2, [1], 1.0),
     ("8b_bf16_tree", 2, [0], None),
     ("8b_bf16_tree", 2, [0], 1.0),
-    ("8b_bf16_long", 1, None, None),  # None: the sequence with the longest context
+    ("8b_bf16_long", 3, "ends", None),
 ]
 
 
@@ -70,8 +75,10 @@ def test_full_size_sampled_parity(name, steps, sample, temperature, models):
         cfg["seed_kv"] = 4000 + int(cfg["seed_w"]) % 1000
     ctx = gen.context_lengths(cfg)
     B = cfg["batch"]
-    if sample is None:
-        sample = [max(range(B), key=lambda b: ctx[b])]
+    if sample == "ends":
+        sample = sorted({min(range(B), key=lambda b: ctx[b]), max(range(B), key=lambda b: ctx[b])})
+    if temperature == "mixed":
+        temperature = calibrated.MIXED_TEMPERATURE[name]
     tree = cfg["draft"] == "tree"
     k = cfg.get("k", 8)
     # the benchmark's row and block budgets (its default 35 replayed steps)
@@ -79,6 +86,7 @@ def test_full_size_sampled_parity(name, steps, sample, temperature, models):
     rows_per_seq = (64 if tree else k) + grow
     max_blocks = (max(ctx) + grow + rows_per_seq + 16) // 16 + 1
     T = float(cfg["temperature"] if temperature is None else temperature)
+    mixed = T == calibrated.MIXED_TEMPERATURE.get(name)
     print(f"[case] {name} T={T:.4g} B={B} ctx={min(ctx)}..{max(ctx)} sample={sample} steps={steps}", flush=True)
     W, om, gm = models(cfg)
     ls = Lockstep(cfg, weights=W, oracle_model=om, gpu_model=gm, sample=sample, max_rows=B * rows_per_seq,
@@ -98,6 +106,18 @@ def test_full_size_sampled_parity(name, steps, sample, temperature, models):
                 drafts = {b: Draft.chain(list(d[b])) for b in range(B)}
             ls.step(drafts, step)
             print(f"[step] {name} {step}: max logit err {ls.max_logit_err:.3g} tiers {sorted(ls.seen_tiers)} "
-                  f"resyncs {len(ls.log)}", flush=True)
+                  f"resyncs {len(ls.log)} run {ls.steps[-1]['run']} lag {ls.steps[-1]['gpu_lag']} "
+                  f"kappa {ls.steps[-1]['kappa']}", flush=True)
+        if mixed:
+            # the three tiers over the batch, a full forward over part of the batch, and
+            # full forwards carrying lag rows (for a compared sequence when 2+ are followed
+            # over 6+ steps)
+            assert ls.gpu_tiers == {"A", "S", "F"}, ls.gpu_tiers
+            assert any(0 < sum(st["run"]) < B for st in ls.steps), [st["run"] for st in ls.steps]
+            assert any(lg > 0 for st in ls.steps for lg in st["gpu_lag"].values()), \
+                [st["gpu_lag"] for st in ls.steps]
+            if steps >= 6 and len(sample) >= 2:
+                assert any(lg > 0 for st in ls.steps for lg in st["full_lag"].values()), \
+                    [st["full_lag"] for st in ls.steps]
     finally:
         ls.close()
