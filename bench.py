@@ -593,11 +593,11 @@ def _cpu_backend():
     for line in torch.__config__.parallel_info().splitlines():
         if line.startswith("ATen parallel backend") or line.startswith("ATen/Parallel"):
             info["parallel"] = line.split(":", 1)[-1].strip()
-    for item in torch.__config__.show().replace("\n", ",").split(","):
-        item = item.strip()
-        if item.startswith("BLAS_INFO=") or item.startswith("LAPACK_INFO="):
-            k, v = item.split("=", 1)
-            info[k.lower()] = v
+    import re
+    for key in ("BLAS_INFO", "LAPACK_INFO"):
+        m = re.search(key + r"=([^,\s]+)", torch.__config__.show())
+        if m:
+            info[key.lower()] = m.group(1)
     return info
 
 

@@ -58,7 +58,7 @@ def models():
 CASES = [
     ("1b_bf16", 8, [0], None),
     ("8b_bf16_chain", 2, [3], None),
-    ("8b_bf16_chain", 6, [0, 2], "mixed"),
+    ("8b_bf16_chain", 8, [0, 1, 2, 3], "mixed"),
     ("8b_bf16_chain", 2, [1], 1.0),
     ("8b_bf16_tree", 2, [0], None),
     ("8b_bf16_tree", 2, [0], 1.0),
