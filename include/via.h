@@ -373,6 +373,23 @@ via_status via_tier_decide_sampled(via_kv *kv, const via_tier_params *p, const v
 via_status via_sample_rows(via_kv *kv, const via_verify_out *out, int32_t out_rows, int32_t n, const int32_t *row,
                            float temperature, const float *uniforms, int32_t *tokens, float *probs,
                            int32_t probs_ld, void *stream);
+/* via_sample_rows for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same draws and probabilities, without a KV handle.  The requests go to
+ * the device as kernel arguments and the kernels' scratch (request array and
+ * per-slice sums, 66560 bytes) is a static device array of the library, which
+ * each GPU it runs on holds until the process ends; the call allocates and
+ * frees nothing.  Every call on a GPU reuses that GPU's scratch and leaves its
+ * contents behind: calls that overlap on one GPU (two streams, two threads)
+ * race and must be serialised by the caller.  At most
+ * VIA_STATIC_SAMPLE_MAX_ROWS draws per call (EINVAL beyond).  out, out_rows,
+ * n, row, temperature, uniforms, tokens, probs and probs_ld are as for
+ * via_sample_rows; vocab is the logits row length (the model's vocabulary).
+ * EDEVICE if the scratch address cannot be obtained. */
+#define VIA_STATIC_SAMPLE_MAX_ROWS 64
+via_status via_sample_rows_static(const via_verify_out *out, int32_t out_rows, int32_t vocab, int32_t n,
+                                  const int32_t *row, float temperature, const float *uniforms, int32_t *tokens,
+                                  float *probs, int32_t probs_ld, void *stream);
 /* Commit the open step from dec->h_packed (read on the host: synchronise
  * first).  This is the end of a block in Alg. 1 and App. B.1: append the
  * accepted prefix x_t..x_{t+kappa-1} (plus the rewritten token at the

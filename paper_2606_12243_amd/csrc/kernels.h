@@ -208,5 +208,14 @@ void launch_decide(const DecideArgs& a, hipStream_t s);
 // a.tok_out; with probs, also writes each request row's softmax
 // exp((l - max) / T) / s_row_sumexp as probs[i * probs_ld + v].
 void launch_sample_rows(const DecideArgs& a, float* probs, int probs_ld, hipStream_t s);
+// The same draws with the requests passed as kernel arguments and the
+// request array and slice sums in the library's static device scratch
+// (n <= kStaticSampleRows); `scratch` is the address static_scratch gave.
+constexpr int kStaticSampleRows = 64;
+void launch_sample_rows_static(DecideArgs a, const SampleReq* req, int n, void* scratch, float* probs,
+                               int probs_ld, hipStream_t s);
+// Device address and size of the static scratch on the current device
+// (looked up once per device).
+hipError_t static_scratch(void** ptr, size_t* bytes);
 
 }  // namespace via

@@ -2,6 +2,9 @@
 // of the split-K GEMM partials (residual + RMSNorm, SwiGLU, QKV RoPE + paged
 // K/V write), the tier decision with its gate walk, and tree-path K/V
 // compaction.
+#include <mutex>
+#include <vector>
+
 #include "kernels.h"
 
 namespace via {
@@ -601,6 +604,60 @@ void launch_sample_rows(const DecideArgs& a, float* probs, int probs_ld, hipStre
   hipLaunchKernelGGL(sample_sums_kernel, dim3(g.G, a.batch), dim3(kSampleThreads), 0, s, a);
   hipLaunchKernelGGL(sample_pick_kernel, dim3(a.batch), dim3(kSampleThreads), 0, s, a);
   if (probs) hipLaunchKernelGGL(sample_probs_kernel, dim3(g.G, a.batch), dim3(kSampleThreads), 0, s, a, probs, probs_ld);
+}
+
+// ---------------------------------------------------------------- draws without allocation
+// Scratch of the draw entry point that allocates nothing (via_sample_rows_static):
+// the request array, then the per-slice sums [request][slice][2].  Each GPU
+// holds its own copy until the process ends; every call on a GPU reuses it.
+namespace {
+constexpr size_t kStaticReqBytes = (size_t)kStaticSampleRows * sizeof(SampleReq);
+constexpr size_t kStaticScratchBytes = kStaticReqBytes + (size_t)kStaticSampleRows * kSampleSlices * 2 * sizeof(double);
+static_assert(kStaticScratchBytes == 66560, "the size include/via.h states");
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+// Requests travel as kernel arguments (no host buffer, no copy).
+struct StaticReqs {
+  SampleReq r[kStaticSampleRows];
+  int n;
+};
+__global__ __launch_bounds__(kStaticSampleRows) void put_reqs_kernel(StaticReqs q, SampleReq* dst) {
+  const int i = threadIdx.x;
+  if (i < q.n) dst[i] = q.r[i];
+}
+}  // namespace
+
+hipError_t static_scratch(void** ptr, size_t* bytes) {
+  // the array's device address, looked up once per device with that device current
+  static std::mutex mu;
+  static std::vector<void*> addr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((size_t)dev >= addr.size()) addr.resize(dev + 1, nullptr);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kStaticScratchBytes;
+  return hipSuccess;
+}
+
+void launch_sample_rows_static(DecideArgs a, const SampleReq* req, int n, void* scratch_ptr, float* probs,
+                               int probs_ld, hipStream_t s) {
+  StaticReqs q{};
+  for (int i = 0; i < n; ++i) q.r[i] = req[i];
+  q.n = n;
+  char* base = (char*)scratch_ptr;
+  a.req = (SampleReq*)base;
+  a.slice_sum = (double*)(base + kStaticReqBytes);
+  a.batch = n;
+  hipLaunchKernelGGL(put_reqs_kernel, dim3(1), dim3(kStaticSampleRows), 0, s, q, a.req);
+  launch_sample_rows(a, probs, probs_ld, s);
 }
 
 void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KVH, int hd, const int32_t* btab,

@@ -1040,6 +1040,46 @@ via_status via_sample_rows(via_kv* kv, const via_verify_out* out, int32_t out_ro
   return hip_check(kv, hipGetLastError(), "sample launch");
 }
 
+static_assert(VIA_STATIC_SAMPLE_MAX_ROWS == kStaticSampleRows, "the header's limit is the scratch's");
+
+via_status via_sample_rows_static(const via_verify_out* out, int32_t out_rows, int32_t vocab, int32_t n,
+                                  const int32_t* row, float temperature, const float* uniforms, int32_t* tokens,
+                                  float* probs, int32_t probs_ld, void* stream) {
+  if (!out) return fail(VIA_EINVAL, "null argument");
+  if (vocab < 1) return fail(VIA_EINVAL, "vocab must be >= 1");
+  if (n < 0 || n > VIA_STATIC_SAMPLE_MAX_ROWS)
+    return fail(VIA_EINVAL, "n = %d outside [0, %d] (the static scratch holds %d requests)", n,
+                VIA_STATIC_SAMPLE_MAX_ROWS, VIA_STATIC_SAMPLE_MAX_ROWS);
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(VIA_EINVAL, "temperature must be > 0");
+  if (probs && probs_ld < vocab) return fail(VIA_EINVAL, "probs_ld must be >= vocab");
+  if (n == 0) return VIA_OK;
+  if (!out->logits || !out->row_max || !out->row_sumexp || !tokens || !row || !uniforms)
+    return fail(VIA_EINVAL, "logits, row statistics, rows, uniforms and tokens are required");
+  std::vector<SampleReq> req(n);
+  for (int i = 0; i < n; ++i) {
+    if (row[i] < 0 || row[i] >= out_rows) return fail(VIA_EINVAL, "row %d outside [0, %d)", row[i], out_rows);
+    if (!(uniforms[i] >= 0.f && uniforms[i] < 1.f)) return fail(VIA_EINVAL, "uniforms must lie in [0, 1)");
+    req[i] = SampleReq{1, row[i], i, uniforms[i]};
+  }
+  void* scr = nullptr;
+  size_t scr_bytes = 0;
+  hipError_t e = static_scratch(&scr, &scr_bytes);
+  if (e != hipSuccess) return fail(VIA_EDEVICE, "static scratch: %s", hipGetErrorString(e));
+  DecideArgs a{};
+  a.max_drafts = 1;
+  a.s_logits = out->logits;
+  a.s_row_max = out->row_max;
+  a.s_row_sumexp = out->row_sumexp;
+  a.inv_T = 1.0f / temperature;
+  a.beta = 1.f;
+  a.vocab = vocab;
+  a.tok_out = tokens;
+  launch_sample_rows_static(a, req.data(), n, scr, probs, probs_ld, (hipStream_t)stream);
+  e = hipGetLastError();
+  if (e != hipSuccess) return fail(VIA_EDEVICE, "sample launch: %s", hipGetErrorString(e));
+  return VIA_OK;
+}
+
 via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* stream) {
   if (!kv || !dec || !dec->h_packed) return fail(VIA_EINVAL, "null argument");
   if (kv->sticky) return fail(VIA_EDEVICE, "handle has a sticky device error");

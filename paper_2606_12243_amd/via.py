@@ -125,6 +125,8 @@ via_tier_decide_sampled = _sig("via_tier_decide_sampled", I32, P, C.POINTER(Tier
                                C.POINTER(VerifyOut), C.POINTER(SamplingC), C.POINTER(Decision), P)
 via_sample_rows = _sig("via_sample_rows", I32, P, C.POINTER(VerifyOut), I32, I32, PI32, C.c_float, P, P, P, I32,
                        P)
+via_sample_rows_static = _sig("via_sample_rows_static", I32, C.POINTER(VerifyOut), I32, I32, I32, PI32, C.c_float, P,
+                              P, P, I32, P)
 via_kv_commit_rollback = _sig("via_kv_commit_rollback", I32, P, C.POINTER(Decision), P)
 via_kv_timer_enable = _sig("via_kv_timer_enable", I32, P, C.c_uint32)
 via_kv_timer_read = _sig("via_kv_timer_read", I32, P, I32, PI32, C.POINTER(C.c_double))
@@ -135,6 +137,7 @@ EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide", "via_tier_decide_sampled", "via_sample_rows",
+           "via_sample_rows_static",
            "via_kv_commit_rollback", "via_kv_timer_enable", "via_kv_timer_read", "via_last_error",
            "via_version"]
 KERNEL_QKV, KERNEL_ATTN, KERNEL_O, KERNEL_GATEUP, KERNEL_DOWN, KERNEL_HEAD, KERNEL_DECIDE = range(7)
