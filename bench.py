@@ -199,31 +199,52 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
     def replay(timed_kind):
         """Warm-up steps, then the timed steps; with `timed_kind` the kernels of
         that kind carry timing events (a separate pass, so the timed pass runs
-        without them)."""
+        without them).  Greedy steps run as one native via_step call each
+        (window assembly, forwards, decisions and commit in the library); the
+        sampling rules are driven call by call from the session."""
+        import ctypes as C
         s2 = fresh()
+        native = sampling is None
+        if native:
+            for b in range(B):
+                t, tp = via._i32(init_tokens[b])
+                via.check(via.via_kv_seq_set_tokens(s2.kv.h, b, tp, len(init_tokens[b])))
+            bufs = [via.DraftsBuf(r[0]) for r in recorded]   # the drafts, resident before timing
+            hp = s2.dec.h_packed.numpy()
+            args = (s2.m.h, s2.kv.h, None, C.byref(s2.p), C.byref(s2.out_slim.c), C.byref(s2.out_full.c),
+                    C.byref(s2.dec.c), s2.sp())
+
+        def one(i):
+            if native:
+                via.check(via.via_step(args[0], args[1], C.byref(bufs[i].c), *args[3:]))
+                return hp[3 * B:4 * B].copy(), hp[:B].copy()
+            w, h, run = s2.begin(recorded[i][0], recorded[i][5])
+            s2.commit(w, recorded[i][0])
+            return h["new_len"].copy(), run
+
         mism = 0
         for i in range(warmup):
-            h, run = s2.step(recorded[i][0], recorded[i][5])
-            mism += int((h["new_len"] != recorded[i][1]).any())
+            new_len, _ = one(i)
+            mism += int((new_len != recorded[i][1]).any())
         torch.cuda.synchronize()
         if timed_kind is not None:
             s2.kv.timer_enable(1 << timed_kind)
             s2.kv.timer_read(timed_kind)
-        lat, accepted, n_full_steps = [], 0, 0
-        n_prev = [np.array([len(s2.tokens[b]) for b in range(B)])]
+        lat, n_full_steps, outs = [], 0, []
+        n_prev = np.array(recorded[warmup - 1][1] if warmup else [len(init_tokens[b]) for b in range(B)])
         torch.cuda.synchronize()
         t_start = time.perf_counter()
         for i in range(warmup, n_steps):
-            drafts = recorded[i][0]
             ts = time.perf_counter()
-            w, h, run = s2.begin(drafts, recorded[i][5])
-            s2.commit(w, drafts)
+            new_len, run = one(i)
             torch.cuda.synchronize()
             lat.append(time.perf_counter() - ts)
-            mism += int((h["new_len"] != recorded[i][1]).any())
-            n_full_steps += int(run.any())
+            outs.append((new_len, run))
         t_total = time.perf_counter() - t_start
-        accepted = int((np.array([len(s2.tokens[b]) for b in range(B)]) - n_prev[0]).sum())
+        for i, (new_len, run) in zip(range(warmup, n_steps), outs):
+            mism += int((new_len != recorded[i][1]).any())
+            n_full_steps += int(np.asarray(run).any() if not native else recorded[i][2].any())
+        accepted = int((np.asarray(outs[-1][0]) - n_prev).sum())
         timer = s2.kv.timer_read(timed_kind) if timed_kind is not None else (0, 0.0)
         s2.kv.timer_enable(0)
         s2.kv.close()

@@ -19,7 +19,8 @@
  *    an asynchronous copy and are valid once the caller has synchronised the
  *    stream.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *    Calls enqueue work and return; the library never synchronises.
+ *    Calls enqueue work and return; apart from via_step, which drives a
+ *    whole step and waits for its decisions, the library never synchronises.
  *  - Handles are single-stream and not thread-safe.
  *  - Every argument is validated before any work is enqueued.  A non-OK
  *    return leaves model and KV state unchanged; via_last_error() gives a
@@ -402,6 +403,37 @@ via_status via_sample_rows_static(const via_verify_out *out, int32_t out_rows, i
  * contiguous slots (kernel on `stream`).  All-or-nothing: ESTATE (nothing
  * changed) if any status is 1 or no step is open. */
 via_status via_kv_commit_rollback(via_kv *kv, const via_decision *dec, void *stream);
+
+/* ---- a whole step, driven natively --------------------------------------
+ * The loop body of Alg. 1 (App. B.1) in one call: window assembly from the
+ * library's record of each sequence's committed tokens and the caller's
+ * drafts, via_verify_slim, via_tier_decide, and -- when some sequence's walk
+ * escalates -- via_verify_full over those sequences (with the lag rows their
+ * full cache is missing) and the second via_tier_decide, then
+ * via_kv_commit_rollback, which also appends the committed tokens to the
+ * record.  Unlike the calls it composes, via_step synchronises `stream`: once
+ * for the first decision, again after an escalation.  On return dec->h_packed
+ * holds the committed decision.  Errors are those of the composed calls (a
+ * failure after the slim forward leaves the step open, as the individual
+ * calls would); ESTATE for a sequence whose committed tokens were never given.
+ */
+typedef struct {
+  int32_t batch, max_drafts;     /* stride of the draft arrays, 1..VIA_MAX_DRAFTS */
+  const int32_t *seq_id;         /* [batch] */
+  const int32_t *n_drafts;       /* [batch], >= 1 */
+  const int32_t *draft_tok;      /* [batch * max_drafts] */
+  const int32_t *draft_parent;   /* [batch * max_drafts] tree parents (-1 root, < j), or NULL: chain */
+} via_drafts;
+/* Give an attached sequence its committed tokens x[0..n-1] (host, copied):
+ * n must be its slim valid length + 1 (x[n-1] is the pending token).  From
+ * then on every commit appends the sequence's accepted drafts and emitted
+ * token.  ESTATE during a step. */
+via_status via_kv_seq_set_tokens(via_kv *kv, int32_t seq_id, const int32_t *tokens, int32_t n);
+/* Read the committed tokens (host out[0..cap)); *n receives their count.
+ * ESTATE if they were never given. */
+via_status via_kv_seq_tokens(const via_kv *kv, int32_t seq_id, int32_t *out, int32_t cap, int32_t *n);
+via_status via_step(via_model *m, via_kv *kv, const via_drafts *drafts, const via_tier_params *p,
+                    via_verify_out *slim, via_verify_out *full, via_decision *dec, void *stream);
 
 /* ---- kernel timing (profiling aid) --------------------------------------
  * When a kind's bit is set, every launch of that kernel kind is bracketed by

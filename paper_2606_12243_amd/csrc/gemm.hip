@@ -739,6 +739,77 @@ __global__ __launch_bounds__(kThreads) void gemm_ki_part(GemmArgs a) {
   }
 }
 
+// The same decomposition at a fixed shape: NB blocks per work-group and
+// exactly NSW steps per wave, fully unrolled, with the loads of DEPTH steps
+// in flight (a ring of DEPTH register buffers) instead of one.  Used when
+// the K split and the column blocks divide evenly.
+template <int MB, int NT, int NB, int NSW, int DEPTH>
+__global__ __launch_bounds__(kThreads) void gemm_ki_fixed(GemmArgs a) {
+  __shared__ __align__(16) float red[kWaves][16 * MB][NB * 16 + 4];
+  const int blk0 = blockIdx.x * NB;
+  const int split = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
+  const int s_beg = split * NSW * kWaves;
+  const uint4* wt[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int blk = blk0 + j;
+    wt[j] = (const uint4*)a.W + (size_t)min(blk >> 2, t64 - 1) * S * 256 + (blk & 3) * 64 + lane;
+  }
+  const uint4* xg = (const uint4*)a.X + lane;
+  const size_t x_step = (size_t)a.MBn * 64, x_term = (size_t)S * x_step;
+  f32x4 acc[NB][MB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[j][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 w[DEPTH][NB], x[DEPTH][NT][MB];
+  // iteration i multiplies step i - DEPTH (its buffer) and then loads step i into it
+#pragma unroll
+  for (int i = 0; i < NSW + DEPTH; ++i) {
+    if (i >= DEPTH) {
+      const int b = (i - DEPTH) % DEPTH;
+#pragma unroll
+      for (int q = 0; q < NT; ++q)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[j][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x[b][q][mb]), as_bf16x8(w[b][j]),
+                                                                 acc[j][mb], 0, 0, 0);
+    }
+    if (i < NSW) {
+      const int b = i % DEPTH;
+      const size_t st = (size_t)(s_beg + wave + i * kWaves);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) w[b][j] = load_stream(wt[j] + st * 256);
+#pragma unroll
+      for (int q = 0; q < NT; ++q)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) x[b][q][mb] = xg[q * x_term + st * x_step + mb * 64];
+    }
+  }
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][mb * 16 + g * 4 + r][j * 16 + n] = acc[j][mb][r];
+  __syncthreads();
+  float* P = a.part + (size_t)split * a.M * a.N;
+  constexpr int cols = NB * 16;
+  for (int e = threadIdx.x; e < 16 * MB * cols; e += kThreads) {
+    const int r = e / cols, c = e - r * cols;
+    if (r >= a.M) continue;
+    float v = 0.f;
+#pragma unroll
+    for (int wv = 0; wv < kWaves; ++wv) v += red[wv][r][c];
+    P[(size_t)r * a.N + blk0 * 16 + c] = v;
+  }
+}
+
 template <int NT>
 void launch_ki_part(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid(((a.N >> 4) + a.nb - 1) / a.nb, a.ksplit);
@@ -748,6 +819,24 @@ void launch_ki_part(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t 
     else
       hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a);
   };
+  // fixed shapes (the 8B and 1B projections): even K splits and column blocks
+  const int S = a.K >> 5, per = S / a.ksplit, nsw = per / kWaves;
+  if (S % a.ksplit == 0 && per % kWaves == 0 && (a.N >> 4) % a.nb == 0) {
+#define VIA_KI_FIXED(NB_, NSW_)                                                   \
+  if (a.nb == NB_ && nsw == NSW_) {                                              \
+    if (a.M <= 16)                                                               \
+      go(gemm_ki_fixed<1, NT, NB_, NSW_, 2>);                                    \
+    else                                                                         \
+      go(gemm_ki_fixed<2, NT, NB_, NSW_, 2>);                                    \
+    return;                                                                      \
+  }
+    VIA_KI_FIXED(6, 4)
+    VIA_KI_FIXED(4, 4)
+    VIA_KI_FIXED(8, 7)
+    VIA_KI_FIXED(2, 4)
+    VIA_KI_FIXED(1, 4)
+#undef VIA_KI_FIXED
+  }
   if (a.M <= 16)
     go(gemm_ki_part<1, NT>);
   else
@@ -988,7 +1077,10 @@ bool gemm_uses_ki(GemmRole role, int M, int N) {
 
 void gemm_ki_plan(int N, int K, int* nb, int* ksplit) {
   const int S = K / 32, blocks = N / 16;
-  const int ks = std::max(1, std::min(4, S / 32));  // at least 4 steps per wave in a split
+  // at least 4 steps per wave in a split; long K (the down projection) in 8
+  // splits, which with 8 blocks per work-group halves the activation reads
+  // per weight byte and keeps the grid at one round
+  const int ks = S >= 256 ? 8 : std::max(1, std::min(4, S / 32));
   *ksplit = ks;
   *nb = std::max(1, std::min(kWaves, (blocks * ks + 255) / 256));
 }

@@ -341,18 +341,124 @@ via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int
 }
 
 void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp) {
-  const int B = w.batch;
+  const int B = w.batch, Dd = std::max(1, w.max_drafts);
   for (int b = 0; b < B; ++b) {
     SeqSt& S = bk.seqs[w.seq[b]];
     if (hp[b] == 0) {
       const int nv = hp[3 * B + b] - 1;
       S.valid[VIA_CACHE_SLIM] = nv;
       if (S.full_ran) S.valid[VIA_CACHE_FULL] = nv;
+      if (S.has_tokens) {
+        const int kappa = hp[B + b], emit = hp[2 * B + b];
+        for (int i = 0; i < kappa; ++i) S.tokens.push_back(w.draft_tok[(size_t)b * w.max_drafts + hp[4 * B + b * Dd + i]]);
+        if (emit >= 0) S.tokens.push_back(emit);
+      }
     }
     book_trim(bk, VIA_CACHE_SLIM, w.seq[b], S.valid[VIA_CACHE_SLIM]);
     book_trim(bk, VIA_CACHE_FULL, w.seq[b], S.valid[VIA_CACHE_FULL]);
     S.full_ran = false;
   }
+}
+
+via_status build_step_window(const KvBook& bk, const via_drafts* d, bool with_lag, StepWin& sw) {
+  if (!d || !d->seq_id || !d->n_drafts || !d->draft_tok) return fail(VIA_EINVAL, "drafts: arrays missing");
+  if (d->batch < 1 || d->max_drafts < 1 || d->max_drafts > VIA_MAX_DRAFTS)
+    return fail(VIA_EINVAL, "drafts: batch >= 1 and 1 <= max_drafts <= %d", VIA_MAX_DRAFTS);
+  const int B = d->batch, D = d->max_drafts;
+  const bool tree = d->draft_parent != nullptr;
+  sw = StepWin();
+  // rows per sequence: chain k rows; tree the root and every node with children
+  std::vector<std::vector<int>> rows_of(B);
+  int R = 1, Lg = 1;
+  for (int b = 0; b < B; ++b) {
+    const int sid = d->seq_id[b], nd = d->n_drafts[b];
+    if (sid < 0 || sid >= (int)bk.seqs.size() || !bk.seqs[sid].on) return fail(VIA_EINVAL, "sequence %d not attached", sid);
+    const SeqSt& S = bk.seqs[sid];
+    if (!S.has_tokens || (int)S.tokens.size() != S.valid[VIA_CACHE_SLIM] + 1)
+      return fail(VIA_ESTATE, "sequence %d has no committed tokens (via_kv_seq_set_tokens)", sid);
+    if (nd < 1 || nd > D) return fail(VIA_EINVAL, "n_drafts[%d] = %d outside [1, %d]", b, nd, D);
+    std::vector<int>& rn = rows_of[b];
+    rn.push_back(-1);
+    if (tree) {
+      std::vector<char> has_child(nd, 0);
+      for (int j = 0; j < nd; ++j) {
+        const int par = d->draft_parent[(size_t)b * D + j];
+        if (par < -1 || par >= j) return fail(VIA_EINVAL, "draft_parent[%d][%d] must be -1 or < j", b, j);
+        if (par >= 0) has_child[par] = 1;
+      }
+      for (int j = 0; j < nd; ++j)
+        if (has_child[j]) rn.push_back(j);
+      if ((int)rn.size() > VIA_MAX_TREE_ROWS) return fail(VIA_EINVAL, "tree windows hold at most %d rows", VIA_MAX_TREE_ROWS);
+    } else {
+      for (int j = 0; j + 1 < nd; ++j) rn.push_back(j);
+    }
+    R = std::max(R, (int)rn.size());
+    Lg = std::max(Lg, S.valid[VIA_CACHE_SLIM] - S.valid[VIA_CACHE_FULL]);
+  }
+  sw.seq.assign(d->seq_id, d->seq_id + B);
+  sw.n_rows.resize(B);
+  sw.n_drafts.assign(d->n_drafts, d->n_drafts + B);
+  sw.row_tok.assign((size_t)B * R, 0);
+  sw.draft_tok.assign((size_t)B * D, 0);
+  sw.draft_row.assign((size_t)B * D, 0);
+  if (tree) {
+    sw.row_depth.assign((size_t)B * R, 0);
+    sw.row_mask.assign((size_t)B * R, 0);
+    sw.draft_parent.assign((size_t)B * D, -1);
+  }
+  if (with_lag) {
+    sw.n_lag.assign(B, 0);
+    sw.lag_tok.assign((size_t)B * Lg, 0);
+  }
+  for (int b = 0; b < B; ++b) {
+    const SeqSt& S = bk.seqs[d->seq_id[b]];
+    const std::vector<int>& rn = rows_of[b];
+    const int nd = d->n_drafts[b];
+    sw.n_rows[b] = (int)rn.size();
+    std::vector<int> row_of(nd, -1), depth(nd, 0);
+    for (int r = 0; r < (int)rn.size(); ++r) {
+      if (rn[r] >= 0) row_of[rn[r]] = r;
+      sw.row_tok[(size_t)b * R + r] = rn[r] < 0 ? S.tokens.back() : d->draft_tok[(size_t)b * D + rn[r]];
+    }
+    for (int j = 0; j < nd; ++j) {
+      const size_t i = (size_t)b * D + j;
+      const int par = tree ? d->draft_parent[i] : j - 1;
+      sw.draft_tok[i] = d->draft_tok[i];
+      sw.draft_row[i] = par < 0 ? 0 : (tree ? row_of[par] : j);
+      depth[j] = par < 0 ? 1 : depth[par] + 1;
+      if (tree) sw.draft_parent[i] = par;
+    }
+    if (tree) {
+      for (int r = 0; r < (int)rn.size(); ++r) {
+        uint64_t mk = 1ull | (1ull << r);
+        for (int u = rn[r]; u >= 0; u = d->draft_parent[(size_t)b * D + u]) mk |= 1ull << row_of[u];
+        sw.row_mask[(size_t)b * R + r] = mk;
+        sw.row_depth[(size_t)b * R + r] = rn[r] < 0 ? 0 : depth[rn[r]];
+      }
+    }
+    if (with_lag) {
+      const int vf = S.valid[VIA_CACHE_FULL], n1 = S.valid[VIA_CACHE_SLIM];
+      sw.n_lag[b] = n1 - vf;
+      for (int i = vf; i < n1; ++i) sw.lag_tok[(size_t)b * Lg + (i - vf)] = S.tokens[i];
+    }
+  }
+  via_window& w = sw.win;
+  w.batch = B;
+  w.max_rows = R;
+  w.max_drafts = D;
+  w.max_lag = Lg;
+  w.seq_id = sw.seq.data();
+  w.n_rows = sw.n_rows.data();
+  w.row_tok = sw.row_tok.data();
+  w.row_depth = tree ? sw.row_depth.data() : nullptr;
+  w.row_mask = tree ? sw.row_mask.data() : nullptr;
+  w.n_drafts = sw.n_drafts.data();
+  w.draft_tok = sw.draft_tok.data();
+  w.draft_row = sw.draft_row.data();
+  w.draft_parent = tree ? sw.draft_parent.data() : nullptr;
+  w.n_lag = with_lag ? sw.n_lag.data() : nullptr;
+  w.lag_tok = with_lag ? sw.lag_tok.data() : nullptr;
+  return VIA_OK;
 }
 
 }  // namespace via

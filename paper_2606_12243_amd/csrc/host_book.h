@@ -31,6 +31,10 @@ struct SeqSt {
   int valid[2] = {0, 0};
   std::vector<int> table[2];
   bool full_ran = false;  // the full verifier ran for it in the open step
+  // committed tokens x[0..n-1] (n = slim valid length + 1) when the caller
+  // gave them (via_kv_seq_set_tokens); commits then append to them
+  bool has_tokens = false;
+  std::vector<int32_t> tokens;
 };
 
 // Both caches' sequences and free block sets.  Blocks are handed out lowest
@@ -101,7 +105,22 @@ struct CommitMoves {
 via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int>& step_n, const int32_t* hp,
                        int vocab, CommitMoves& cm);
 // Apply a validated commit: valid lengths (slim always, full where it ran),
-// blocks past them freed, full_ran cleared.
+// blocks past them freed, full_ran cleared, and the accepted drafts and the
+// emitted token appended to the committed tokens of sequences that keep them.
 void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp);
+
+// Draft window of a natively driven step (via_step): rows, draft rows,
+// depths and ancestor masks built from each sequence's committed tokens (the
+// pending token x[n-1] is row 0) and its drafts, plus the lag rows (the
+// committed tokens x[valid_full .. n-2] the full cache is missing).  `win`
+// points into the vectors of this object.
+struct StepWin {
+  std::vector<int32_t> seq, n_rows, row_tok, row_depth, n_drafts, draft_tok, draft_row, draft_parent, n_lag, lag_tok;
+  std::vector<uint64_t> row_mask;
+  via_window win{};
+};
+// EINVAL for malformed drafts (sizes, parents, more than VIA_MAX_TREE_ROWS
+// fed rows), ESTATE for a sequence without committed tokens.
+via_status build_step_window(const KvBook& bk, const via_drafts* d, bool with_lag, StepWin& sw);
 
 }  // namespace via

@@ -1040,6 +1040,59 @@ via_status via_sample_rows(via_kv* kv, const via_verify_out* out, int32_t out_ro
   return hip_check(kv, hipGetLastError(), "sample launch");
 }
 
+via_status via_kv_seq_set_tokens(via_kv* kv, int32_t seq_id, const int32_t* tokens, int32_t n) {
+  if (!kv || (n > 0 && !tokens)) return fail(VIA_EINVAL, "null argument");
+  if (kv->step_open) return fail(VIA_ESTATE, "a step is open");
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->bk.seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
+  SeqSt& S = kv->bk.seqs[seq_id];
+  if (n != S.valid[VIA_CACHE_SLIM] + 1)
+    return fail(VIA_EINVAL, "n = %d must be the cached length + 1 = %d", n, S.valid[VIA_CACHE_SLIM] + 1);
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= kv->m->d.vocab) return fail(VIA_EINVAL, "token %d out of range", tokens[i]);
+  S.tokens.assign(tokens, tokens + n);
+  S.has_tokens = true;
+  return VIA_OK;
+}
+
+via_status via_kv_seq_tokens(const via_kv* kv, int32_t seq_id, int32_t* out, int32_t cap, int32_t* n) {
+  if (!kv || !n) return fail(VIA_EINVAL, "null argument");
+  if (seq_id < 0 || seq_id >= kv->d.max_seqs || !kv->bk.seqs[seq_id].on) return fail(VIA_EINVAL, "sequence not attached");
+  const SeqSt& S = kv->bk.seqs[seq_id];
+  if (!S.has_tokens) return fail(VIA_ESTATE, "sequence %d has no committed tokens", seq_id);
+  *n = (int)S.tokens.size();
+  if (out) {
+    if (cap < *n) return fail(VIA_EINVAL, "capacity %d < %d", cap, *n);
+    std::copy(S.tokens.begin(), S.tokens.end(), out);
+  }
+  return VIA_OK;
+}
+
+via_status via_step(via_model* m, via_kv* kv, const via_drafts* drafts, const via_tier_params* p,
+                    via_verify_out* slim, via_verify_out* full, via_decision* dec, void* stream) {
+  via_status st = common_checks(m, kv);
+  if (st) return st;
+  if (!dec || !dec->h_packed || !full) return fail(VIA_EINVAL, "null argument");
+  if (kv->step_open) return fail(VIA_ESTATE, "a step is already open");
+  hipStream_t s = (hipStream_t)stream;
+  StepWin sw;
+  if ((st = build_step_window(kv->bk, drafts, false, sw))) return st;
+  if ((st = via_verify_slim(m, kv, &sw.win, p, slim, stream))) return st;
+  if ((st = via_tier_decide(kv, p, slim, nullptr, dec, stream))) return st;
+  if ((st = hip_check(kv, hipStreamSynchronize(s), "hipStreamSynchronize"))) return st;
+  const int B = drafts->batch;
+  std::vector<int32_t> run(B, 0);
+  bool any = false;
+  for (int b = 0; b < B; ++b) any |= (run[b] = dec->h_packed[b] == 1) != 0;
+  if (any) {
+    StepWin lw;
+    if ((st = build_step_window(kv->bk, drafts, true, lw))) return st;
+    if ((st = via_verify_full(m, kv, &lw.win, run.data(), p, full, stream))) return st;
+    if ((st = via_tier_decide(kv, p, slim, full, dec, stream))) return st;
+    if ((st = hip_check(kv, hipStreamSynchronize(s), "hipStreamSynchronize"))) return st;
+  }
+  return via_kv_commit_rollback(kv, dec, stream);
+}
+
 static_assert(VIA_STATIC_SAMPLE_MAX_ROWS == kStaticSampleRows, "the header's limit is the scratch's");
 
 via_status via_sample_rows_static(const via_verify_out* out, int32_t out_rows, int32_t vocab, int32_t n,

@@ -128,6 +128,8 @@ via_sample_rows = _sig("via_sample_rows", I32, P, C.POINTER(VerifyOut), I32, I32
 via_sample_rows_static = _sig("via_sample_rows_static", I32, C.POINTER(VerifyOut), I32, I32, I32, PI32, C.c_float, P,
                               P, P, I32, P)
 via_kv_commit_rollback = _sig("via_kv_commit_rollback", I32, P, C.POINTER(Decision), P)
+via_kv_seq_set_tokens = _sig("via_kv_seq_set_tokens", I32, P, I32, PI32, I32)
+via_kv_seq_tokens = _sig("via_kv_seq_tokens", I32, P, I32, PI32, I32, PI32)
 via_kv_timer_enable = _sig("via_kv_timer_enable", I32, P, C.c_uint32)
 via_kv_timer_read = _sig("via_kv_timer_read", I32, P, I32, PI32, C.POINTER(C.c_double))
 via_last_error = _sig("via_last_error", C.c_char_p)
@@ -137,7 +139,7 @@ EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide", "via_tier_decide_sampled", "via_sample_rows",
-           "via_sample_rows_static",
+           "via_sample_rows_static", "via_kv_seq_set_tokens", "via_kv_seq_tokens", "via_step",
            "via_kv_commit_rollback", "via_kv_timer_enable", "via_kv_timer_read", "via_last_error",
            "via_version"]
 KERNEL_QKV, KERNEL_ATTN, KERNEL_O, KERNEL_GATEUP, KERNEL_DOWN, KERNEL_HEAD, KERNEL_DECIDE = range(7)
@@ -399,6 +401,39 @@ class Dec:
         h[4 * B:] = np.asarray(path, np.int32).reshape(-1)
 
 
+class Drafts(C.Structure):
+    _fields_ = [("batch", I32), ("max_drafts", I32), ("seq_id", P), ("n_drafts", P), ("draft_tok", P),
+                ("draft_parent", P)]
+
+
+class DraftsBuf:
+    """Host arrays of a via_drafts (kept alive with the struct): {seq: (tokens,
+    parents or None)} in batch order."""
+
+    def __init__(self, drafts: dict):
+        seqs = list(drafts)
+        B = len(seqs)
+        D = max(1, max(len(drafts[q][0]) for q in seqs))
+        tree = any(drafts[q][1] is not None for q in seqs)
+        a = np.zeros(2 * B + (2 if tree else 1) * B * D, np.int32)
+        a[:B] = seqs
+        a[B:2 * B] = [len(drafts[q][0]) for q in seqs]
+        tok = a[2 * B:2 * B + B * D].reshape(B, D)
+        for i, q in enumerate(seqs):
+            tok[i, :len(drafts[q][0])] = drafts[q][0]
+        par_ptr = None
+        if tree:
+            par = a[2 * B + B * D:].reshape(B, D)
+            par[:] = -1
+            for i, q in enumerate(seqs):
+                pp = drafts[q][1] if drafts[q][1] is not None else [j - 1 for j in range(len(drafts[q][0]))]
+                par[i, :len(pp)] = pp
+            par_ptr = a.ctypes.data + 4 * (2 * B + B * D)
+        self._a = a
+        self.B, self.D = B, D
+        self.c = Drafts(B, D, a.ctypes.data, a.ctypes.data + 4 * B, a.ctypes.data + 8 * B, par_ptr)
+
+
 class Sampling:
     """Sampling-rule arguments of one step: alpha, beta, the drafter's
     distributions ``draft_probs`` (device fp32 [batch, max_drafts, vocab],
@@ -412,3 +447,7 @@ class Sampling:
 
 def tier_params(tau_acc=0.9, tau_full=0.5, temperature=1.0, forced=FORCED_NONE):
     return TierParams(tau_acc, tau_full, temperature, forced)
+
+
+via_step = _sig("via_step", I32, P, P, C.POINTER(Drafts), C.POINTER(TierParams), C.POINTER(VerifyOut),
+                C.POINTER(VerifyOut), C.POINTER(Decision), P)

@@ -465,7 +465,72 @@ static void test_random_steps() {
   }
 }
 
+static void test_step_window_and_tokens() {
+  KvBook bk;
+  book_init(bk, 2, 8, 32, 32);
+  attach(bk, 0, 20);
+  attach(bk, 1, 9);
+  bk.seqs[1].valid[0] = 6;  // full cache lags 3 tokens
+  for (int s = 0; s < 2; ++s) {
+    bk.seqs[s].has_tokens = true;
+    for (int i = 0; i <= bk.seqs[s].valid[1]; ++i) bk.seqs[s].tokens.push_back(100 + 10 * s + i % 10);
+  }
+  // chain: seq 0 drafts 4, seq 1 drafts 2
+  std::vector<int32_t> sid = {0, 1}, nd = {4, 2}, tok = {1, 2, 3, 4, 5, 6, 0, 0};
+  via_drafts d{2, 4, sid.data(), nd.data(), tok.data(), nullptr};
+  StepWin sw;
+  CHECK(build_step_window(bk, &d, true, sw) == VIA_OK);
+  CHECK(sw.win.max_rows == 4 && sw.n_rows[0] == 4 && sw.n_rows[1] == 2);
+  CHECK(sw.row_tok[0] == bk.seqs[0].tokens.back() && sw.row_tok[1] == 1 && sw.row_tok[3] == 3);
+  CHECK(sw.row_tok[4] == bk.seqs[1].tokens.back() && sw.row_tok[5] == 5);
+  CHECK(sw.draft_row[3] == 3 && sw.draft_row[4 + 1] == 1 && !sw.win.row_mask);
+  CHECK(sw.n_lag[0] == 0 && sw.n_lag[1] == 3 && sw.win.max_lag == 3);
+  CHECK(sw.lag_tok[3 + 0] == bk.seqs[1].tokens[6] && sw.lag_tok[3 + 2] == bk.seqs[1].tokens[8]);
+  WinCopy c;
+  CHECK(copy_window(bk, &sw.win, 200, 2, 8, c) == VIA_OK);
+  Plan F;
+  CHECK(build_verify_plan(bk, VIA_CACHE_FULL, c, {1}, &sw.win, true, 200, 4, F, nullptr) == VIA_OK);
+  CHECK(F.rows.size() == 5 && F.rows[0].tok == bk.seqs[1].tokens[6]);
+  // tree: root -> {0, 1}; 1 -> {2, 3}; 3 -> {4}
+  std::vector<int32_t> sid1 = {0}, nd1 = {5}, tok1 = {7, 8, 9, 10, 11}, par1 = {-1, -1, 1, 1, 3};
+  via_drafts t{1, 5, sid1.data(), nd1.data(), tok1.data(), par1.data()};
+  StepWin tw;
+  CHECK(build_step_window(bk, &t, false, tw) == VIA_OK);
+  CHECK(tw.n_rows[0] == 3 && tw.row_tok[1] == 8 && tw.row_tok[2] == 10);
+  CHECK(tw.row_depth[1] == 1 && tw.row_depth[2] == 2 && tw.row_mask[2] == 7 && tw.row_mask[1] == 3);
+  CHECK(tw.draft_row[0] == 0 && tw.draft_row[2] == 1 && tw.draft_row[4] == 2);
+  CHECK(copy_window(bk, &tw.win, 200, 2, 8, c) == VIA_OK && c.tree);
+  // a sequence without tokens, bad parents, no drafts
+  bk.seqs[1].has_tokens = false;
+  CHECK(build_step_window(bk, &d, false, sw) == VIA_ESTATE);
+  bk.seqs[1].has_tokens = true;
+  par1[2] = 2;
+  CHECK(build_step_window(bk, &t, false, tw) == VIA_EINVAL);
+  par1[2] = 1;
+  nd1[0] = 0;
+  CHECK(build_step_window(bk, &t, false, tw) == VIA_EINVAL);
+  nd1[0] = 5;
+  // a commit appends the accepted drafts and the emitted token
+  Plan P;
+  CHECK(build_step_window(bk, &d, false, sw) == VIA_OK);
+  CHECK(copy_window(bk, &sw.win, 200, 2, 8, c) == VIA_OK);
+  CHECK(build_verify_plan(bk, VIA_CACHE_SLIM, c, {0, 1}, &sw.win, true, 200, 4, P, nullptr) == VIA_OK);
+  auto hp = decision(2, 4);
+  set(hp, 2, 4, 0, 0, 2, 77, 21 + 3, {0, 1});
+  set(hp, 2, 4, 1, 0, 2, -1, 10 + 2, {0, 1});
+  CommitMoves cm;
+  const std::vector<int> step_n = {21, 10};
+  CHECK(plan_commit(bk, c, step_n, hp.data(), 200, cm) == VIA_OK);
+  const size_t n0 = bk.seqs[0].tokens.size(), n1 = bk.seqs[1].tokens.size();
+  apply_commit(bk, c, hp.data());
+  CHECK(bk.seqs[0].tokens.size() == n0 + 3 && bk.seqs[0].tokens[n0] == 1 && bk.seqs[0].tokens[n0 + 2] == 77);
+  CHECK(bk.seqs[1].tokens.size() == n1 + 2 && bk.seqs[1].tokens.back() == 6);
+  CHECK((int)bk.seqs[0].tokens.size() == bk.seqs[0].valid[1] + 1);
+  CHECK((int)bk.seqs[1].tokens.size() == bk.seqs[1].valid[1] + 1);
+}
+
 int main() {
+  test_step_window_and_tokens();
   test_allocator();
   test_window_validation();
   test_plans();

@@ -142,3 +142,65 @@ def test_nonfinite_full_logits_status2_no_commit():
     finally:
         kv.close()
         gm.close()
+
+
+@pytest.mark.parametrize("tree", [False, True])
+def test_native_step_matches_python_driven_step(tree):
+    """via_step (window assembly from the library's committed tokens, slim
+    forward, decision, escalation with lag rows, commit: one native call)
+    against the same step driven call by call from Python, on two handles of
+    one model: identical decisions, committed tokens, valid lengths and block
+    tables every step (natural tiers at T = 1, so escalations and lag rows
+    occur)."""
+    import ctypes as C
+
+    import numpy as np
+    from paper_2606_12243_amd import via
+    from paper_2606_12243_amd.session import GreedyDrafter, Session
+
+    cfg = configs.get("micro_bf16")
+    cfg.update(seed_c=26, seed_d=36)
+    md = cfg["model"]
+    print(f"[case] native step tree={tree}", flush=True)
+    gm = via.Model(md, gen.model_weights(cfg), cfg["route"])
+    kvs = [via.KV(gm, max_seqs=2, max_blocks_per_seq=16, blocks_full=64, blocks_slim=64, max_rows=128, max_batch=2,
+                  max_drafts=16) for _ in range(2)]
+    try:
+        py, nat = (Session(gm, kv, via.tier_params(0.9, 0.5, 1.0), logits=False) for kv in kvs)
+        for b, n in ((0, 27), (1, 12)):
+            toks = gen.context_tokens(cfg, b, n)
+            py.prefill(b, toks)
+            nat.prefill(b, toks)
+            t, tp = via._i32(toks)
+            via.check(via.via_kv_seq_set_tokens(kvs[1].h, b, tp, len(toks)))
+        drafter = GreedyDrafter(py, lambda b, step, j: gen.corruption(cfg["seed_d"], b, step, j, 0.3,
+                                                                       md["vocab"]))
+        escalated = False
+        for step in range(10):
+            if tree:
+                drafts = drafter.tree([0, 1], [3, 4, 3], 2, step)
+            else:
+                d = drafter.chain([0, 1], 4, step)
+                drafts = {b: (d[b], None) for b in (0, 1)}
+            h, run = py.step(drafts)
+            escalated |= bool(run.any())
+            db = via.DraftsBuf(drafts)
+            via.check(via.via_step(gm.h, kvs[1].h, C.byref(db.c), C.byref(nat.p), C.byref(nat.out_slim.c),
+                                   C.byref(nat.out_full.c), C.byref(nat.dec.c), nat.sp()))
+            B, D = db.B, db.D
+            hp = nat.dec.h_packed.numpy()
+            for k, i in (("status", 0), ("kappa", 1), ("emit", 2), ("new_len", 3)):
+                assert hp[i * B:(i + 1) * B].tolist() == h[k].tolist(), (step, k)
+            assert hp[4 * B:4 * B + B * D].tolist() == np.asarray(h["path"]).reshape(-1)[:B * D].tolist()
+            for b in (0, 1):
+                n = C.c_int32()
+                out = np.zeros(512, np.int32)
+                via.check(via.via_kv_seq_tokens(kvs[1].h, b, out.ctypes.data_as(via.PI32), 512, C.byref(n)))
+                assert out[:n.value].tolist() == py.tokens[b], (step, b)
+                for c in (via.CACHE_FULL, via.CACHE_SLIM):
+                    assert kvs[0].seq_info(b, c) == kvs[1].seq_info(b, c), (step, b, c)
+        assert escalated
+    finally:
+        for kv in kvs:
+            kv.close()
+        gm.close()
