@@ -284,6 +284,17 @@ via_status via_kv_seq_reserve(via_kv *kv, int32_t seq_id, int32_t n_ctx);
  * blocks. */
 via_status via_prefill(via_model *m, via_kv *kv, int32_t seq_id, const int32_t *tokens, int32_t n,
                        void *stream);
+/* via_prefill for several sequences at once: sequence seq_ids[i] caches
+ * its lens[i] tokens, which follow those of the earlier sequences in the
+ * flat host array `tokens`.  The sequences share each forward (up to the
+ * handle's max_rows rows and max_batch sequences per forward; longer
+ * prompts continue in later forwards), so the projections of a batch of
+ * prompts run as one tall GEMM.  All-or-nothing: on any error no sequence
+ * is attached (EINVAL for repeated or attached ids, ENOMEM when the pools
+ * lack the blocks).  Same results as one via_prefill per sequence when
+ * every forward has more than 512 rows either way. */
+via_status via_prefill_batch(via_model *m, via_kv *kv, int32_t n_seqs, const int32_t *seq_ids, const int32_t *lens,
+                             const int32_t *tokens, void *stream);
 /* Detach a sequence and free its blocks.  Not during a step. */
 via_status via_kv_seq_release(via_kv *kv, int32_t seq_id);
 /* Valid lengths and block table of one cache (host outputs; table may be

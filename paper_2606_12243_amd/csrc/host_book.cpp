@@ -254,18 +254,19 @@ via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std:
 
 void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0, int c1, int G, Plan& P) {
   SeqInfo si{};
-  si.row_start = 0;
+  si.row_start = (int)P.rows.size();
   si.n_rows = c1 - c0;
   si.kv_len = c1;
   si.win_base = c0;
-  si.bt = 0;
+  si.bt = (int)P.btab.size();
   si.n_blocks = (int)S.table[cache].size();
+  const int sidx = (int)P.seqs.size();
   for (int blk : S.table[cache]) P.btab.push_back(blk);
   for (int i = c0; i < c1; ++i) {
     RowInfo r{};
     r.tok = tokens[i];
     r.pos = i;
-    r.seq = 0;
+    r.seq = sidx;
     r.slot = i;
     r.blk = S.table[cache][i / kBlock];
     r.vis_len = i + 1;

@@ -88,7 +88,9 @@ struct Plan {
 via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std::vector<int>& run,
                              const via_window* raw, bool head, int vocab, int G, Plan& P,
                              std::vector<std::pair<int, int>>* taken);
-// Plan of prefill rows [c0, c1) of one sequence (causal, positions = slots).
+// Append prefill rows [c0, c1) of one sequence to a plan (causal, positions
+// = slots; the sequence's rows, table and attention items follow those
+// already in P).
 void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0, int c1, int G, Plan& P);
 
 // Commit of an open step from the host copy of a decision (the packed block

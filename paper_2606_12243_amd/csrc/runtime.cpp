@@ -833,37 +833,77 @@ via_status via_kv_seq_reserve(via_kv* kv, int32_t seq_id, int32_t n_ctx) {
   return VIA_OK;
 }
 
-via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* tokens, int32_t n, void* stream) {
-  via_status st = attach_checks(kv, seq_id, n);
+via_status via_prefill_batch(via_model* m, via_kv* kv, int32_t n_seqs, const int32_t* seq_ids, const int32_t* lens,
+                             const int32_t* tokens, void* stream) {
+  via_status st = common_checks(m, kv);
   if (st) return st;
-  if ((st = common_checks(m, kv))) return st;
-  if (n > 0 && !tokens) return fail(VIA_EINVAL, "null tokens");
-  for (int i = 0; i < n; ++i)
+  if (n_seqs < 1 || !seq_ids || !lens) return fail(VIA_EINVAL, "need n_seqs >= 1, seq_ids and lens");
+  std::set<int> ids;
+  std::vector<size_t> off(n_seqs + 1, 0);
+  size_t need[2] = {0, 0};
+  for (int i = 0; i < n_seqs; ++i) {
+    if ((st = attach_checks(kv, seq_ids[i], lens[i]))) return st;
+    if (!ids.insert(seq_ids[i]).second) return fail(VIA_EINVAL, "sequence %d appears twice", seq_ids[i]);
+    if (blocks_for(lens[i]) > kv->d.max_blocks_per_seq)
+      return fail(VIA_ENOMEM, "sequence %d needs %d blocks > max_blocks_per_seq", seq_ids[i], blocks_for(lens[i]));
+    off[i + 1] = off[i] + lens[i];
+    need[0] += blocks_for(lens[i]);
+  }
+  need[1] = need[0];
+  if (off[n_seqs] > 0 && !tokens) return fail(VIA_EINVAL, "null tokens");
+  for (size_t i = 0; i < off[n_seqs]; ++i)
     if (tokens[i] < 0 || tokens[i] >= m->d.vocab) return fail(VIA_EINVAL, "token %d out of range", tokens[i]);
-  if (blocks_for(n) > (int)kv->bk.free_[0].size() || blocks_for(n) > (int)kv->bk.free_[1].size() ||
-      blocks_for(n) > kv->d.max_blocks_per_seq)
-    return fail(VIA_ENOMEM, "not enough KV blocks for %d slots", n);
-  kv->bk.seqs[seq_id] = SeqSt();
-  kv->bk.seqs[seq_id].on = true;
-  SeqSt& S = kv->bk.seqs[seq_id];
+  if (need[0] > kv->bk.free_[0].size() || need[1] > kv->bk.free_[1].size())
+    return fail(VIA_ENOMEM, "not enough KV blocks for the prompts");
+  auto detach_all = [&] {
+    for (int i = 0; i < n_seqs; ++i) {
+      book_trim(kv->bk, 0, seq_ids[i], 0);
+      book_trim(kv->bk, 1, seq_ids[i], 0);
+      kv->bk.seqs[seq_ids[i]] = SeqSt();
+    }
+  };
+  for (int i = 0; i < n_seqs; ++i) {
+    kv->bk.seqs[seq_ids[i]] = SeqSt();
+    kv->bk.seqs[seq_ids[i]].on = true;
+  }
+  for (int cache = 0; cache < 2; ++cache) {
+    std::vector<std::pair<int, int>> want;
+    for (int i = 0; i < n_seqs; ++i) want.push_back({seq_ids[i], lens[i]});
+    if ((st = book_alloc(kv->bk, cache, want, nullptr))) {
+      detach_all();
+      return st;
+    }
+  }
   hipStream_t s = (hipStream_t)stream;
   const int G = m->D.G;
+  // forwards of up to max_rows rows and max_batch sequences; a sequence's
+  // later chunk goes into a later forward (it attends to the earlier chunk)
   for (int cache = 0; cache < 2; ++cache) {
-    book_alloc(kv->bk, cache, {{seq_id, n}}, nullptr);
-    for (int c0 = 0; c0 < n; c0 += kv->d.max_rows) {
-      int c1 = std::min(n, c0 + kv->d.max_rows);
+    std::vector<int> done(n_seqs, 0);
+    for (;;) {
       Plan P;
-      build_prefill_plan(S, cache, tokens, c0, c1, G, P);
+      int used = 0, nseq = 0;
+      for (int i = 0; i < n_seqs && used < kv->d.max_rows && nseq < kv->d.max_batch; ++i) {
+        if (done[i] >= lens[i]) continue;
+        const int c0 = done[i], c1 = std::min(lens[i], c0 + (kv->d.max_rows - used));
+        build_prefill_plan(kv->bk.seqs[seq_ids[i]], cache, tokens + off[i], c0, c1, G, P);
+        used += c1 - c0;
+        done[i] = c1;
+        ++nseq;
+      }
+      if (used == 0) break;
       if ((st = exec_forward(m, kv, cache, P, false, nullptr, 1.f, s))) {
-        book_trim(kv->bk, 0, seq_id, 0);
-        book_trim(kv->bk, 1, seq_id, 0);
-        S = SeqSt();
+        detach_all();
         return st;
       }
     }
-    S.valid[cache] = n;
+    for (int i = 0; i < n_seqs; ++i) kv->bk.seqs[seq_ids[i]].valid[cache] = lens[i];
   }
   return VIA_OK;
+}
+
+via_status via_prefill(via_model* m, via_kv* kv, int32_t seq_id, const int32_t* tokens, int32_t n, void* stream) {
+  return via_prefill_batch(m, kv, 1, &seq_id, &n, tokens, stream);
 }
 
 via_status via_kv_seq_release(via_kv* kv, int32_t seq_id) {

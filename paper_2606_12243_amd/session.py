@@ -62,6 +62,16 @@ class Session:
         via.check(via.via_prefill(self.m.h, self.kv.h, seq, tp, len(tokens) - 1, self.sp()))
         self.tokens[seq] = list(tokens)
 
+    def prefill_batch(self, prompts: dict):
+        """prefill() for several sequences in shared forwards ({seq: tokens})."""
+        seqs = list(prompts)
+        ids, ip = via._i32(seqs)
+        lens, lp = via._i32([len(prompts[q]) - 1 for q in seqs])
+        flat, fp = via._i32([t for q in seqs for t in prompts[q][:-1]] or [0])
+        via.check(via.via_prefill_batch(self.m.h, self.kv.h, len(seqs), ip, lp, fp, self.sp()))
+        for q in seqs:
+            self.tokens[q] = list(prompts[q])
+
     def reserve(self, seq, tokens, kv_values=None):
         """Attach with n-1 context slots whose K/V are supplied by the caller.
 

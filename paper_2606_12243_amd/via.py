@@ -111,6 +111,7 @@ via_kv_create = _sig("via_kv_create", I32, P, C.POINTER(KvDesc), C.POINTER(P))
 via_kv_destroy = _sig("via_kv_destroy", I32, P)
 via_kv_seq_reserve = _sig("via_kv_seq_reserve", I32, P, I32, I32)
 via_prefill = _sig("via_prefill", I32, P, P, I32, PI32, I32, P)
+via_prefill_batch = _sig("via_prefill_batch", I32, P, P, I32, PI32, PI32, PI32, P)
 via_kv_seq_release = _sig("via_kv_seq_release", I32, P, I32)
 via_kv_seq_info = _sig("via_kv_seq_info", I32, P, I32, I32, PI32, PI32, I32, PI32)
 via_verify_slim = _sig("via_verify_slim", I32, P, P, C.POINTER(Window), C.POINTER(TierParams),
@@ -137,7 +138,7 @@ via_version = _sig("via_version", C.c_char_p)
 
 EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_bf16", "via_dimr_cost", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
-           "via_kv_seq_reserve", "via_prefill", "via_kv_seq_release", "via_kv_seq_info",
+           "via_kv_seq_reserve", "via_prefill", "via_prefill_batch", "via_kv_seq_release", "via_kv_seq_info",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide", "via_tier_decide_sampled", "via_sample_rows",
            "via_sample_rows_static", "via_kv_seq_set_tokens", "via_kv_seq_tokens", "via_step",
            "via_kv_commit_rollback", "via_kv_timer_enable", "via_kv_timer_read", "via_last_error",

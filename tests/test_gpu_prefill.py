@@ -89,3 +89,56 @@ def test_prefill_sized_forward_lockstep(name):
               f"resyncs={len(ls.log)}", flush=True)
     finally:
         ls.close()
+
+
+@pytest.mark.parametrize("name,max_rows", [("small_bf16_hd128", 1300), ("micro_bf16", 700)])
+def test_batched_prefill_lockstep(name, max_rows):
+    """via_prefill_batch: three prompts share the forwards (all of them in one
+    1300-row forward, or with 700 rows per forward the second prompt split
+    across two forwards and the third in the second), then lock-step decoding
+    against the oracle's per-sequence prefill."""
+    cfg = configs.get(name)
+    cfg.update(seed_c=27, seed_d=37, corrupt=0.3, temperature=1.0)
+    print(f"[case] batched prefill {name} max_rows={max_rows}", flush=True)
+    ls = Lockstep(cfg, max_rows=max_rows, max_batch=3, max_drafts=8, max_blocks=64, blocks=256)
+    try:
+        prompts = {b: gen.context_tokens(cfg, b, n) for b, n in ((0, 520), (1, 611), (2, 170))}
+        for b, toks in prompts.items():
+            ls.o_id[b] = ls.ver.prefill(toks)
+            ls.drafter.attach(b)
+        ls.sess.prefill_batch(prompts)
+        for b, toks in prompts.items():
+            for c in (via.CACHE_FULL, via.CACHE_SLIM):
+                assert ls.kv.seq_info(b, c)[0] == len(toks) - 1
+        steps = ls.run_chain([0, 1, 2], G=10, k=5)
+        print(f"[done] batched {name} steps={steps} max_logit_err={ls.max_logit_err:.3g} "
+              f"tiers={sorted(ls.seen_tiers)} resyncs={len(ls.log)}", flush=True)
+    finally:
+        ls.close()
+
+
+def test_batched_prefill_is_all_or_nothing():
+    cfg = configs.get("micro_bf16")
+    md = cfg["model"]
+    gm = via.Model(md, gen.model_weights(cfg), cfg["route"])
+    kv = via.KV(gm, max_seqs=3, max_blocks_per_seq=8, blocks_full=10, blocks_slim=10, max_rows=64, max_batch=3,
+                max_drafts=4)
+    try:
+        stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+        toks, tp = via._i32(list(range(1, 200)))
+        ids, ip = via._i32([0, 1])
+        lens, lp = via._i32([100, 99])   # 7 + 7 blocks > 10 free
+        assert via.via_prefill_batch(gm.h, kv.h, 2, ip, lp, tp, stream) == via.ENOMEM
+        ids2, ip2 = via._i32([0, 0])
+        lens2, lp2 = via._i32([5, 5])
+        assert via.via_prefill_batch(gm.h, kv.h, 2, ip2, lp2, tp, stream) == via.EINVAL   # repeated id
+        n, nb = C.c_int32(), C.c_int32()
+        for q in (0, 1):
+            assert via.via_kv_seq_info(kv.h, q, 0, C.byref(n), None, 0, C.byref(nb)) == via.EINVAL  # not attached
+        lens3, lp3 = via._i32([40, 30])
+        via.check(via.via_prefill_batch(gm.h, kv.h, 2, ip, lp3, tp, stream))
+        torch.cuda.synchronize()
+        assert kv.seq_info(0, 0)[0] == 40 and kv.seq_info(1, 1)[0] == 30
+    finally:
+        kv.close()
+        gm.close()
