@@ -200,6 +200,8 @@ struct DecideArgs {
   SampleReq* req;             // [batch]
   double* slice_sum;          // [batch * kSampleSlices * 2] per-slice weight sums
   int32_t* tok_out;           // drawn tokens [batch]; null: the decision's emit slots
+  int32_t* h_packed;          // nullable: device address of the pinned host mirror of `packed`,
+                              // written by the greedy decision itself (system-scope stores)
 };
 // Decision kernel, then (sampling rules) the sampling kernel that fills the
 // emitted tokens it left open.

@@ -59,7 +59,7 @@ __device__ __forceinline__ void split_sum2(const float* P, size_t stride, int ks
 // consumer applies it (row_scale) after the GEMM; here each work-group adds
 // the sum of x^2 over its kNormChunk columns to ss[chunk][out].
 // Grid (ceil(d / kNormChunk), M), 64 threads of 8 columns each.
-template <typename G, bool BF16, int NT>
+template <typename G, bool BF16, int NT, int KS>
 __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P, int ksplit, int M, int d,
                                                        const G* g, void* Y, int MBn, const RowInfo* rows,
                                                        float* ss, int ss_stride, float* Xcopy, const G* E,
@@ -86,7 +86,30 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
     for (int i = 0; i < 8; ++i) sq += v[i] * v[i];
   } else if (k0 < d) {
     float4 acc[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-    if (P) split_sum2(P, stride, ksplit, 0, (size_t)m * d + k0, (size_t)m * d + k0 + 4, acc[0], acc[1]);
+    if constexpr (KS > 0) {
+      // exactly KS splits: all loads in flight, then summed in split order
+      if (P) {
+        float4 v0[KS], v1[KS];
+#pragma unroll
+        for (int q = 0; q < KS; ++q) {
+          v0[q] = *(const float4*)(P + (size_t)q * stride + (size_t)m * d + k0);
+          v1[q] = *(const float4*)(P + (size_t)q * stride + (size_t)m * d + k0 + 4);
+        }
+#pragma unroll
+        for (int q = 0; q < KS; ++q) {
+          acc[0].x += v0[q].x;
+          acc[0].y += v0[q].y;
+          acc[0].z += v0[q].z;
+          acc[0].w += v0[q].w;
+          acc[1].x += v1[q].x;
+          acc[1].y += v1[q].y;
+          acc[1].z += v1[q].z;
+          acc[1].w += v1[q].w;
+        }
+      }
+    } else {
+      if (P) split_sum2(P, stride, ksplit, 0, (size_t)m * d + k0, (size_t)m * d + k0 + 4, acc[0], acc[1]);
+    }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       float4 u = *(float4*)(x + k0 + 4 * h);
@@ -117,38 +140,42 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
 
 // QKV partial sums -> RMSNorm scale of the input row -> rotate-half RoPE at
 // the row's position -> Q (bf16 hi/lo terms, or fp32) and paged K/V (model
-// dtype).  One work-group of 64 threads per (row, head of Q, K or V); thread
-// j owns the rotation pair (j, j + hd/2) and its angle pos * theta^(-2j/hd),
-// computed in fp64 while the loads of the pair's split partials (all in
-// flight at once, summed in split order) are outstanding.
-template <typename T>
-__global__ __launch_bounds__(64) void qkv_finish_kernel(QkvArgs a) {
-  const int m = blockIdx.x, hh = blockIdx.y, j = threadIdx.x;
+// dtype).  A work-group of 256 threads takes four (row, head of Q, K or V)
+// pairs, 64 threads each; thread j owns the rotation pair (j, j + hd/2) and
+// its angle pos * theta^(-2j/hd), computed in fp64 while the loads of the
+// pair's KS split partials (all in flight at once, summed in split order)
+// are outstanding.  KS = 0: the split count is taken from the arguments.
+template <typename T, int KS>
+__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
+  const int m = blockIdx.x, hh = blockIdx.y * 4 + (threadIdx.x >> 6), j = threadIdx.x & 63;
   const int half = a.hd >> 1;
-  if (j >= half) return;
+  if (j >= half || hh >= a.H + 2 * a.KVH) return;
   const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
   const size_t c = (size_t)m * N + (size_t)hh * a.hd + j;
-  float v1[16], v2[16];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const size_t base = (size_t)min(q, a.ksplit - 1) * stride;
-    v1[q] = a.P[base + c];
-    v2[q] = a.P[base + c + half];
-  }
-  const RowInfo ri = a.rows[m];
-  double cs = 1.0, sn = 0.0;
-  if (hh < a.H + a.KVH) sincos((double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), &sn, &cs);
-  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);  // RMSNorm of the input row
   float x1 = 0.f, x2 = 0.f;
+  double cs = 1.0, sn = 0.0;
+  const RowInfo ri = a.rows[m];
+  if constexpr (KS > 0) {
+    float v1[KS], v2[KS];
 #pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    x1 += q < a.ksplit ? v1[q] : 0.f;
-    x2 += q < a.ksplit ? v2[q] : 0.f;
+    for (int q = 0; q < KS; ++q) {
+      v1[q] = a.P[(size_t)q * stride + c];
+      v2[q] = a.P[(size_t)q * stride + c + half];
+    }
+    if (hh < a.H + a.KVH) sincos((double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), &sn, &cs);
+#pragma unroll
+    for (int q = 0; q < KS; ++q) {
+      x1 += v1[q];
+      x2 += v2[q];
+    }
+  } else {
+    if (hh < a.H + a.KVH) sincos((double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), &sn, &cs);
+    for (int q = 0; q < a.ksplit; ++q) {
+      x1 += a.P[(size_t)q * stride + c];
+      x2 += a.P[(size_t)q * stride + c + half];
+    }
   }
-  for (int sp = 16; sp < a.ksplit; ++sp) {
-    x1 += a.P[(size_t)sp * stride + c];
-    x2 += a.P[(size_t)sp * stride + c + half];
-  }
+  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);  // RMSNorm of the input row
   x1 *= sc;
   x2 *= sc;
   float y1 = x1, y2 = x2;
@@ -319,6 +346,16 @@ __global__ __launch_bounds__(64) void decide_kernel(DecideArgs a) {
   emit[b] = st == 0 ? em : -1;
   new_len[b] = st == 2 ? ss.n : ss.n + k + (st == 0 && em >= 0 ? 1 : 0);
   for (int q = k; q < D; ++q) path[q] = -1;
+  if (a.h_packed) {
+    // the host mirror, written past the caches so that it is in host memory
+    // once the stream has been synchronised
+    auto put = [&](int i, int v) { __hip_atomic_store(a.h_packed + i, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM); };
+    put(b, status[b]);
+    put(B + b, kappa[b]);
+    put(2 * B + b, emit[b]);
+    put(3 * B + b, new_len[b]);
+    for (int q = 0; q < D; ++q) put(4 * B + base + q, path[q]);
+  }
 }
 
 // Tree compaction: copy the K/V of slot src to slot dst in every layer slot.
@@ -345,23 +382,44 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
                       void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s, float* Xcopy,
                       const void* E, const RowInfo* erows) {
   const dim3 grid((d + kNormChunk - 1) / kNormChunk, M);
-  if (!bf16)
-    hipLaunchKernelGGL((resid_add_kernel<float, false, 1>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
+  if (!bf16) {
+    hipLaunchKernelGGL((resid_add_kernel<float, false, 1, 0>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
                        (const float*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const float*)E, erows);
-  else if (terms >= 3)
-    hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 3>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const uint16_t*)E, erows);
-  else
-    hipLaunchKernelGGL((resid_add_kernel<uint16_t, true, 2>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
-                       (const uint16_t*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const uint16_t*)E, erows);
+    return;
+  }
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, dim3(64), 0, s, X, P, ksplit, M, d, (const uint16_t*)g, Y, MBn, rows, ss,
+                       ss_stride, Xcopy, (const uint16_t*)E, erows);
+  };
+  // the split counts of the projections that feed it get their exact loads
+  if (terms >= 3) {
+    switch (P ? ksplit : 0) {
+      case 4: go(resid_add_kernel<uint16_t, true, 3, 4>); break;
+      case 8: go(resid_add_kernel<uint16_t, true, 3, 8>); break;
+      default: go(resid_add_kernel<uint16_t, true, 3, 0>); break;
+    }
+  } else {
+    switch (P ? ksplit : 0) {
+      case 4: go(resid_add_kernel<uint16_t, true, 2, 4>); break;
+      case 8: go(resid_add_kernel<uint16_t, true, 2, 8>); break;
+      default: go(resid_add_kernel<uint16_t, true, 2, 0>); break;
+    }
+  }
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
-  const dim3 grid(a.M, a.H + 2 * a.KVH);
-  if (bf16)
-    hipLaunchKernelGGL(qkv_finish_kernel<uint16_t>, grid, dim3(64), 0, s, a);
-  else
-    hipLaunchKernelGGL(qkv_finish_kernel<float>, grid, dim3(64), 0, s, a);
+  const dim3 grid(a.M, (a.H + 2 * a.KVH + 3) / 4);
+  auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(256), 0, s, a); };
+  if (bf16) {
+    switch (a.ksplit) {
+      case 1: go(qkv_finish_kernel<uint16_t, 1>); break;
+      case 2: go(qkv_finish_kernel<uint16_t, 2>); break;
+      case 4: go(qkv_finish_kernel<uint16_t, 4>); break;
+      default: go(qkv_finish_kernel<uint16_t, 0>); break;
+    }
+  } else {
+    go(qkv_finish_kernel<float, 0>);
+  }
 }
 
 namespace {

@@ -173,6 +173,9 @@ struct via_kv {
   std::vector<int> slim_row0; // first row of each batch entry in that slim forward
   std::vector<int> step_n;  // committed length n per batch entry at step start
   bool sticky = false;
+  // device address of the last decision's pinned host mirror (null: copy it)
+  const int32_t* h_packed_host = nullptr;
+  int32_t* h_packed_dev = nullptr;
   hipEvent_t ev[kRing];
   bool ev_used[kRing];
   int ring = 0;
@@ -1025,8 +1028,22 @@ via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_ou
     a.req = (SampleReq*)(kv->ws + L.sreq);
     a.slice_sum = (double*)(kv->ws + L.ssum);
   }
+  // greedy rules: the decision kernel writes the pinned host mirror itself
+  // when that memory is mapped for the device (no copy on the step's
+  // critical path); otherwise, and under the sampling rules (whose draw
+  // completes the decision later), the packed block is copied
+  if (!smp) {
+    if (dec->h_packed != kv->h_packed_host) {
+      void* dp = nullptr;
+      kv->h_packed_host = dec->h_packed;
+      kv->h_packed_dev = hipHostGetDevicePointer(&dp, dec->h_packed, 0) == hipSuccess ? (int32_t*)dp : nullptr;
+      (void)hipGetLastError();  // a host pointer that is not mapped leaves no sticky error
+    }
+    a.h_packed = kv->h_packed_dev;
+  }
   timed_launch(kv, VIA_KERNEL_DECIDE, s, [&] { launch_decide(a, s); });
   if ((st = hip_check(kv, hipGetLastError(), "decide launch"))) return st;
+  if (a.h_packed) return VIA_OK;
   size_t bytes = (size_t)(4 * B + B * Dd) * 4;
   return hip_check(kv, hipMemcpyAsync(dec->h_packed, dec->packed, bytes, hipMemcpyDeviceToHost, s), "decision copy");
 }
