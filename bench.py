@@ -86,23 +86,16 @@ def attach_context(cfg, sess, synthetic):
             sess.prefill(b, toks)
 
 
-def shared_layers(route):
-    """Leading layers the slim route shares with the full model (route[i] == i)."""
-    n = 0
-    while n < len(route) and route[n] == n:
-        n += 1
-    return n
-
-
-def step_bytes(cfg, kv_slim_tokens, full_seqs, run):
+def step_bytes(cfg, kv_slim_tokens, full_seqs, run, full_start):
     """Algorithmic HBM bytes of one step: the routed layers' weights and the
     head for the slim forward plus the cached K/V it read (tokens summed over
     the batch); when the full verifier ran, the weights of the layers it ran,
     the head, and the K/V those layers read for the sequences it covered.
     ``full_seqs[b]`` = (cached + lag tokens, lag tokens) of the full cache
-    before the step.  Without lag rows the full forward starts after the
-    layers the slim route shares with it (their state comes from the slim
-    forward), so those layers' weights and K/V are not read again."""
+    before the step; ``full_start`` = the layer the full forward started at
+    (the library reports it: after the layers the slim route shares with the
+    full model when their states were kept, else 0), so the shared layers'
+    weights and K/V are not counted when they were not read again."""
     from workload.configs import model_bytes
     md = cfg["model"]
     slim = model_bytes(md, cfg["route"])
@@ -110,9 +103,7 @@ def step_bytes(cfg, kv_slim_tokens, full_seqs, run):
     tot = slim["layers"] + slim["head"] + kvb * len(cfg["route"]) * kv_slim_tokens
     ran = [b for b in range(len(run)) if run[b]]
     if ran:
-        n_sh = shared_layers(cfg["route"])
-        start = n_sh if all(full_seqs[b][1] == 0 for b in ran) and 0 < n_sh < len(cfg["route"]) else 0
-        layers = md["n_layers"] - start
+        layers = md["n_layers"] - max(0, full_start)
         tot += layers * slim["per_layer"] + slim["head"] + kvb * layers * sum(full_seqs[b][0] for b in ran)
     return tot
 
@@ -178,7 +169,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
         kv_slim = sum(sess.kv.seq_info(b, via.CACHE_SLIM)[0] for b in range(B))
         kv_full = [(sess.kv.seq_info(b, via.CACHE_FULL)[0] + len(sess.lag(b)), len(sess.lag(b))) for b in range(B)]
         h, run = sess.step(drafts, smp)
-        recorded.append((drafts, h["new_len"].copy(), run.copy(), kv_slim, kv_full, smp))
+        recorded.append((drafts, h["new_len"].copy(), run.copy(), kv_slim, kv_full, smp, sess.kv.last_full_start()))
     log(f"T={temperature:.4g}: reference decode of {n_steps} steps, drafting {t_draft:.2f}s")
 
     # ---- reset: fresh handle on the same pools (context slots untouched)
@@ -224,8 +215,10 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
 
         mism = 0
         for i in range(warmup):
-            new_len, _ = one(i)
+            new_len, run = one(i)
             mism += int((new_len != recorded[i][1]).any())
+            # the replayed full forward starts where the recorded one did
+            mism += int(bool(recorded[i][2].any()) and s2.kv.last_full_start() != recorded[i][6])
         torch.cuda.synchronize()
         if timed_kind is not None:
             s2.kv.timer_enable(1 << timed_kind)
@@ -252,7 +245,7 @@ def run_workload(cfg, W, steps, warmup, temperature, timer_kind=None, sampling=N
 
     lat, accepted, n_full_steps, t_total, mism, _ = replay(None)
     timer = replay(timer_kind)[5] if timer_kind is not None else (0, 0.0)
-    bytes_tot = sum(step_bytes(cfg, r[3], r[4], r[2]) for r in recorded[warmup:])
+    bytes_tot = sum(step_bytes(cfg, r[3], r[4], r[2], r[6]) for r in recorded[warmup:])
     lat_ms = np.array(lat) * 1e3
     return dict(value=accepted / t_total, t_total=t_total, lat_ms=lat_ms, escalation=n_full_steps / max(1, steps),
                 mismatch=mism, t_draft=t_draft, bytes=bytes_tot, timer=timer, recorded=recorded,

@@ -252,8 +252,13 @@ via_status via_dimr_cost(const float *q_logits, const float *p_logits, int32_t r
 
 /* ---- sizes -------------------------------------------------------------- */
 size_t via_pool_bytes(const via_model_desc *desc, int32_t n_layer_slots, int32_t n_blocks, int32_t block_size);
+/* The workspace also holds, per sequence id, a ring of VIA_STATE_ROWS fp32
+ * rows of d_model (the residual stream after the layers the slim route
+ * shares with the full model, saved by the slim forward for each slot it
+ * feeds), so it grows with max_seqs. */
+#define VIA_STATE_ROWS 128
 size_t via_workspace_bytes(const via_model_desc *desc, int32_t max_rows, int32_t max_batch,
-                           int32_t max_blocks_per_seq, int32_t max_drafts);
+                           int32_t max_blocks_per_seq, int32_t max_drafts, int32_t max_seqs);
 size_t via_staging_bytes(const via_model_desc *desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
                          int32_t max_drafts);
 
@@ -295,6 +300,11 @@ via_status via_prefill(via_model *m, via_kv *kv, int32_t seq_id, const int32_t *
  * every forward has more than 512 rows either way. */
 via_status via_prefill_batch(via_model *m, via_kv *kv, int32_t n_seqs, const int32_t *seq_ids, const int32_t *lens,
                              const int32_t *tokens, void *stream);
+/* Route index at which the last full-verifier forward of the current (or
+ * last committed) step started: 0 (every layer), P (after the shared
+ * layers, see via_verify_full), -1 if none ran since the step's slim
+ * forward. */
+via_status via_kv_last_full_start(const via_kv *kv, int32_t *route_index);
 /* Detach a sequence and free its blocks.  Not during a step. */
 via_status via_kv_seq_release(via_kv *kv, int32_t seq_id);
 /* Valid lengths and block table of one cache (host outputs; table may be
@@ -326,7 +336,15 @@ via_status via_verify_slim(via_model *m, via_kv *kv, const via_window *win, cons
  * (committed tokens the full cache has not seen because q was not invoked
  * on earlier steps) are this library's reading of the silent cache policy.
  * win must be the window of the open step; n_lag[b] must equal the full
- * cache's lag for each run sequence (ESTATE otherwise). */
+ * cache's lag for each run sequence (ESTATE otherwise).
+ * When the slim route begins with layers 0..P-1 of the full model, those
+ * layers compute the same K/V and residual stream in both forwards; the
+ * forward then starts at layer P, taking the K/V of layers < P from the slim
+ * cache and the residual stream from the state ring, provided every run
+ * sequence has the state of each lag and window slot there (the ring keeps
+ * the last VIA_STATE_ROWS slots; a tree commit the full verifier did not see
+ * that keeps more than the root clears it).  Otherwise it runs all layers.
+ * via_kv_last_full_start reports which. */
 via_status via_verify_full(via_model *m, via_kv *kv, const via_window *win, const int32_t *run,
                            const via_tier_params *p, via_verify_out *out, void *stream);
 /* Forward of either verifier (cache = VIA_CACHE_*) that leaves the logical

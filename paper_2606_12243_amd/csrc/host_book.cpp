@@ -214,6 +214,7 @@ via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std:
       r.seq = sidx;
       r.slot = valid + i;
       r.blk = S.table[cache][r.slot / kBlock];
+      r.xs = w.seq[b] * kStateRows + r.slot % kStateRows;
       r.vis_len = valid + i + 1;
       r.lm = -1;
       P.rows.push_back(r);
@@ -226,6 +227,7 @@ via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std:
       r.seq = sidx;
       r.slot = win_base + rr;
       r.blk = S.table[cache][r.slot / kBlock];
+      r.xs = w.seq[b] * kStateRows + r.slot % kStateRows;
       r.vis_len = w.tree ? win_base : win_base + rr + 1;
       r.mask = w.tree ? w.row_mask[i] : 0;
       r.lm = -1;
@@ -252,6 +254,25 @@ via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std:
   return VIA_OK;
 }
 
+void note_slim_forward(KvBook& bk, const WinCopy& w, const std::vector<int>& run, bool saved) {
+  for (int b : run) {
+    SeqSt& S = bk.seqs[w.seq[b]];
+    if (!saved || S.valid[VIA_CACHE_SLIM] + w.n_rows[b] - S.valid[VIA_CACHE_FULL] > kStateRows) S.xs_ok = false;
+  }
+}
+
+bool build_prefix_xfer(const KvBook& bk, const WinCopy& w, const std::vector<int>& run, Plan& P) {
+  P.xfer.clear();
+  for (int b : run)
+    if (!bk.seqs[w.seq[b]].xs_ok) return false;
+  for (const RowInfo& r : P.rows) {
+    const SeqSt& S = bk.seqs[w.seq[run[r.seq]]];
+    P.xfer.push_back(PrefixXfer{r.xs, r.slot % kBlock, S.table[VIA_CACHE_SLIM][r.slot / kBlock],
+                                S.table[VIA_CACHE_FULL][r.slot / kBlock]});
+  }
+  return true;
+}
+
 void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0, int c1, int G, Plan& P) {
   SeqInfo si{};
   si.row_start = (int)P.rows.size();
@@ -269,6 +290,7 @@ void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0
     r.seq = sidx;
     r.slot = i;
     r.blk = S.table[cache][i / kBlock];
+    r.xs = -1;
     r.vis_len = i + 1;
     r.lm = -1;
     P.rows.push_back(r);
@@ -347,8 +369,14 @@ void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp) {
     SeqSt& S = bk.seqs[w.seq[b]];
     if (hp[b] == 0) {
       const int nv = hp[3 * B + b] - 1;
+      const int kept = hp[B + b] + (hp[2 * B + b] >= 0 ? 1 : 0);
       S.valid[VIA_CACHE_SLIM] = nv;
-      if (S.full_ran) S.valid[VIA_CACHE_FULL] = nv;
+      if (S.full_ran) {
+        S.valid[VIA_CACHE_FULL] = nv;
+        S.xs_ok = true;
+      } else if (w.tree && kept >= 2) {
+        S.xs_ok = false;
+      }
       if (S.has_tokens) {
         const int kappa = hp[B + b], emit = hp[2 * B + b];
         for (int i = 0; i < kappa; ++i) S.tokens.push_back(w.draft_tok[(size_t)b * w.max_drafts + hp[4 * B + b * Dd + i]]);

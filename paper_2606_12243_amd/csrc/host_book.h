@@ -31,6 +31,10 @@ struct SeqSt {
   int valid[2] = {0, 0};
   std::vector<int> table[2];
   bool full_ran = false;  // the full verifier ran for it in the open step
+  // every slot in [valid full, valid slim) has its state after the shared
+  // layers in the state ring (kStateRows rows per sequence, row slot %
+  // kStateRows), so a full forward can start after those layers
+  bool xs_ok = true;
   // committed tokens x[0..n-1] (n = slim valid length + 1) when the caller
   // gave them (via_kv_seq_set_tokens); commits then append to them
   bool has_tokens = false;
@@ -88,6 +92,16 @@ struct Plan {
 via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std::vector<int>& run,
                              const via_window* raw, bool head, int vocab, int G, Plan& P,
                              std::vector<std::pair<int, int>>* taken);
+// After a slim forward over the batch entries `run` of w that saved (saved)
+// or did not save its rows' states to the state ring: a sequence whose
+// window rows, written at slots valid slim .. + n_rows - 1, overwrite ring
+// rows of slots the full cache still lacks loses xs_ok.
+void note_slim_forward(KvBook& bk, const WinCopy& w, const std::vector<int>& run, bool saved);
+// Row map of a full forward (plan P of the entries `run` of w) that starts
+// after the shared layers: one PrefixXfer per row of P (its state-ring row
+// and the slim and full pages of its slot).  False, with P.xfer left empty,
+// unless every running sequence has xs_ok.
+bool build_prefix_xfer(const KvBook& bk, const WinCopy& w, const std::vector<int>& run, Plan& P);
 // Append prefill rows [c0, c1) of one sequence to a plan (causal, positions
 // = slots; the sequence's rows, table and attention items follow those
 // already in P).
@@ -109,6 +123,9 @@ via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int
 // Apply a validated commit: valid lengths (slim always, full where it ran),
 // blocks past them freed, full_ran cleared, and the accepted drafts and the
 // emitted token appended to the committed tokens of sequences that keep them.
+// xs_ok: set where the full cache caught up; cleared where a tree commit
+// that the full verifier did not see keeps more than the root row (the
+// compaction moves cache slots, the state ring is not moved).
 void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp);
 
 // Draft window of a natively driven step (via_step): rows, draft rows,

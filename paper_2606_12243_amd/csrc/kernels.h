@@ -78,7 +78,8 @@ int gate_up_blocks_per_group(int F);
 // rows[m].lm when `rows` is given (rows with lm < 0 skipped), and the sums of
 // x^2 over column chunks to ss[chunk * ss_stride + row]: the consumer of the
 // next projection multiplies its output row by row_scale() (RMSNorm).
-// Xcopy (nullable): the updated rows are also stored there ([M, d] fp32).
+// Xcopy (nullable): the updated rows are also stored there, row m to row
+// erows[m].xs when erows is given (skipped where xs < 0), else to row m.
 // E (nullable, model dtype [vocab, d]): X[m] is first set to the embedding
 // row of token erows[m].tok (P is then ignored).
 void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit, int M, int d, const void* g,
@@ -88,7 +89,7 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
 struct PrefixArgs {
   const PrefixXfer* xfer;  // [M]
   int M, P, d, KVH, hd;
-  const float* Xpref;      // slim forward's residual stream after layer P - 1, [slim rows, d]
+  const float* xstate;     // state ring [rows][d]: residual streams after layer P - 1
   float* X;                // the full forward's residual stream [M, d]
   const void* slim_pool;
   int slim_blocks;
@@ -96,7 +97,7 @@ struct PrefixArgs {
   int full_blocks;
 };
 // K/V of layers 0..P-1 copied slim -> full cache at every row's position and
-// X[m] = Xpref[xfer[m].src_row].
+// X[m] = xstate[xfer[m].src_row].
 void launch_prefix_copy(bool bf16, const PrefixArgs& a, hipStream_t s);
 
 // DIMR routing cost per row (Eq. 11): q = full verifier logits, p = routed

@@ -68,6 +68,10 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
   const int k0 = chunk * kNormChunk + threadIdx.x * 8;
   const int out = rows ? rows[m].lm : m;
   float* x = X + (size_t)m * d;
+  if (Xcopy) {  // uniform per work-group
+    const int xr = erows ? erows[m].xs : m;
+    Xcopy = xr < 0 ? nullptr : Xcopy + (size_t)xr * d;
+  }
   const size_t stride = (size_t)M * d;
   float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float sq = 0.f;
@@ -79,8 +83,8 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
     *(float4*)(x + k0) = make_float4(v[0], v[1], v[2], v[3]);
     *(float4*)(x + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
     if (Xcopy) {
-      *(float4*)(Xcopy + (size_t)m * d + k0) = make_float4(v[0], v[1], v[2], v[3]);
-      *(float4*)(Xcopy + (size_t)m * d + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      *(float4*)(Xcopy + k0) = make_float4(v[0], v[1], v[2], v[3]);
+      *(float4*)(Xcopy + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) sq += v[i] * v[i];
@@ -120,7 +124,7 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
         u.w = u.w + acc[h].w;
         *(float4*)(x + k0 + 4 * h) = u;
       }
-      if (Xcopy) *(float4*)(Xcopy + (size_t)m * d + k0 + 4 * h) = u;
+      if (Xcopy) *(float4*)(Xcopy + k0 + 4 * h) = u;
       v[4 * h + 0] = u.x;
       v[4 * h + 1] = u.y;
       v[4 * h + 2] = u.z;
@@ -736,13 +740,14 @@ namespace {
 // (route layer i == i for i < a.P): grid (M, P + 1).  y < P: the row's K and
 // V of layer y, copied from the slim cache (slot y) to the full cache (slot
 // y) at the row's position; y == P: the row's residual stream after layer
-// P - 1, taken from the slim forward of the same step.
+// P - 1, taken from the state ring (saved there by the slim forward that fed
+// the slot: this step's for window rows, an earlier one for lag rows).
 template <typename T>
 __global__ __launch_bounds__(256) void prefix_copy_kernel(PrefixArgs a) {
   const int m = blockIdx.x, y = blockIdx.y;
   const PrefixXfer x = a.xfer[m];
   if (y == a.P) {
-    const float* src = a.Xpref + (size_t)x.src_row * a.d;
+    const float* src = a.xstate + (size_t)x.src_row * a.d;
     float* dst = a.X + (size_t)m * a.d;
     for (int i = threadIdx.x; i < a.d; i += 256) dst[i] = src[i];
     return;

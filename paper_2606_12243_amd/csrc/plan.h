@@ -13,6 +13,9 @@ constexpr int kAttnMaxSpan = 8192;  // keys of one split (pages of a split's wor
 constexpr int kAttnTargetGroups = 192;  // attention work-groups a forward aims for (fewer, longer spans than one per compute unit: measured best at the 8B shapes)
 constexpr int kAttnQueries = 32;  // (row, head-in-group) queries per attention work-group
 constexpr int kNormChunk = 512;   // columns per partial sum of squares (RMSNorm)
+// Per-sequence ring of post-shared-layer states: slot p of a sequence keeps
+// its state in ring row p % kStateRows.
+constexpr int kStateRows = 128;
 
 // One fed row of a forward (lag row or window row).
 struct RowInfo {
@@ -23,7 +26,7 @@ struct RowInfo {
   int32_t vis_len;  // slots [0, vis_len) are visible
   int32_t lm;       // index into the head rows, -1 if the row has no head output
   int32_t blk;      // pool block holding `slot` (the sequence's block table entry slot / block size)
-  int32_t pad_;
+  int32_t xs;       // state-store row of (sequence, slot) the slim forward saves the row's state to, -1: none
   uint64_t mask;    // extra visible slots win_base + bit (tree rows)
 };
 
@@ -66,7 +69,7 @@ struct StepSeq {
 // One row of a full forward that starts after the P layers the slim route
 // shares with it (route layer i == i for i < P).
 struct PrefixXfer {
-  int32_t src_row;           // row of the same step's slim forward
+  int32_t src_row;           // state-store row of (sequence, slot)
   int32_t t;                 // slot within the page (position % 16)
   int32_t src_blk, dst_blk;  // page of the position in the slim and the full cache
 };

@@ -73,7 +73,7 @@ Dims dims_of(const via_model_desc* d) {
 
 struct Layout {
   size_t X, Yf, Q, Af, Hf, Ylf, part, att_o, att_ml, lm_part, ss;
-  size_t Xpref;                        // slim forward's residual stream after the shared layers
+  size_t xstate;                       // state ring: [max_seqs][kStateRows][d] residual stream after the shared layers
   size_t rows, seqs, btab, items, lm, xfer;  // plan region
   size_t step_seqs, dtok, drow, dpar, du;  // step region
   size_t sreq, ssum;                   // sampling requests and slice sums of a decision
@@ -83,7 +83,8 @@ struct Layout {
   int max_chunks, max_items;
 };
 
-Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int max_blocks, int max_drafts) {
+Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int max_blocks, int max_drafts,
+                 int max_seqs) {
   Dims D = dims_of(desc);
   const size_t es = esize_of(desc);
   Layout L{};
@@ -117,7 +118,7 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.att_ml = take((size_t)L.max_chunks * R * D.H * 2 * 4);
   L.lm_part = take((size_t)gemm_tiles(D.V) * R * 4 * 4);
   L.ss = take((size_t)ceil_div(D.d, kNormChunk) * R * 4);  // RMSNorm sums of squares [chunk][row]
-  L.Xpref = take(R * D.d * 4);
+  L.xstate = take((size_t)max_seqs * kStateRows * D.d * 4);
   L.max_items = ceil_div(max_rows * D.G, kAttnQueries) + max_batch;
   // plan region (one upload per forward)
   size_t p0 = o;
@@ -169,8 +170,8 @@ struct via_kv {
   KvBook bk;
   bool step_open = false;
   WinCopy win;
-  bool xpref_ok = false;      // the open step's slim forward saved its state after the shared layers
-  std::vector<int> slim_row0; // first row of each batch entry in that slim forward
+  bool xpref_ok = false;      // the open step's slim forward saved its rows' states after the shared layers
+  int last_full_start = -1;   // route index the last full forward started at (-1: none in this step)
   std::vector<int> step_n;  // committed length n per batch entry at step start
   bool sticky = false;
   // device address of the last decision's pinned host mirror (null: copy it)
@@ -360,7 +361,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     pa.d = D.d;
     pa.KVH = D.KVH;
     pa.hd = D.hd;
-    pa.Xpref = (const float*)(ws + L.Xpref);
+    pa.xstate = (const float*)(ws + L.xstate);
     pa.X = X;
     pa.slim_pool = kv->d.pool_slim;
     pa.slim_blocks = kv->d.blocks_slim;
@@ -439,7 +440,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
       launch_resid_add(bf, 3, X, part, ks(D.g_down), M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
-                       ss_stride, s, save_prefix && (int)si + 1 == n_shared ? (float*)(ws + L.Xpref) : nullptr);
+                       ss_stride, s, save_prefix && (int)si + 1 == n_shared ? (float*)(ws + L.xstate) : nullptr,
+                       nullptr, d_rows);
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
@@ -520,32 +522,15 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   std::vector<std::pair<int, int>> taken;
   if ((st = build_verify_plan(kv->bk, cache, *wp, run, win, true, m->d.vocab, m->D.G, P, &taken))) return st;
   // The full forward of a step starts after the layers the slim route shares
-  // with it when no running sequence has lag rows: the slim forward of the
-  // step saved those rows' state, and their K/V of the shared layers are
-  // copied from the slim cache.
+  // with it when every running sequence has the states after those layers
+  // of its lag slots (kept by earlier slim forwards) and window slots (this
+  // step's slim forward) in the state ring; the K/V of the shared layers are
+  // copied from the slim cache.  Otherwise it runs every layer.
   const int n_shared = shared_prefix(m);
   const bool save = !probe && cache == VIA_CACHE_SLIM && n_shared > 0 && n_shared < (int)m->route.size();
   int start_si = 0;
-  if (!probe && cache == VIA_CACHE_FULL && kv->xpref_ok && n_shared > 0) {
-    bool lag0 = true;
-    for (int b : run) {
-      const SeqSt& S = kv->bk.seqs[wp->seq[b]];
-      lag0 = lag0 && S.valid[VIA_CACHE_FULL] == S.valid[VIA_CACHE_SLIM];
-    }
-    if (lag0) {
-      start_si = n_shared;
-      for (size_t q = 0; q < run.size(); ++q) {
-        const int b = run[q];
-        const SeqSt& S = kv->bk.seqs[wp->seq[b]];
-        const SeqInfo& si = P.seqs[q];
-        for (int rr = 0; rr < si.n_rows; ++rr) {
-          const int pos = si.win_base + rr;
-          P.xfer.push_back(PrefixXfer{kv->slim_row0[b] + rr, pos % kBlock, S.table[VIA_CACHE_SLIM][pos / kBlock],
-                                      S.table[VIA_CACHE_FULL][pos / kBlock]});
-        }
-      }
-    }
-  }
+  if (!probe && cache == VIA_CACHE_FULL && kv->xpref_ok && n_shared > 0 && build_prefix_xfer(kv->bk, *wp, run, P))
+    start_si = n_shared;
   st = exec_forward(m, kv, cache, P, true, out, 1.0f / p->temperature, s, start_si, save);
   if (probe) {
     book_release_taken(kv->bk, cache, taken);
@@ -557,8 +542,8 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   }
   if (cache == VIA_CACHE_SLIM) {
     kv->xpref_ok = save;
-    kv->slim_row0.assign(w.batch, 0);
-    for (size_t q = 0; q < run.size(); ++q) kv->slim_row0[run[q]] = P.seqs[q].row_start;
+    kv->last_full_start = -1;
+    note_slim_forward(kv->bk, w, run, save);
     kv->win = w;
     kv->step_open = true;
     kv->step_n.assign(w.batch, 0);
@@ -567,6 +552,7 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
       kv->bk.seqs[w.seq[b]].full_ran = false;
     }
   } else {
+    kv->last_full_start = start_si;
     for (int b : run) kv->bk.seqs[wp->seq[b]].full_ran = true;
   }
   return VIA_OK;
@@ -652,15 +638,15 @@ via_status via_pack_gate_up(const void* src, void* dst, int32_t d_ffn, int32_t d
 }
 
 size_t via_workspace_bytes(const via_model_desc* desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
-                           int32_t max_drafts) {
-  if (!desc || max_rows < 1 || max_batch < 1 || max_blocks_per_seq < 1 || max_drafts < 1) return 0;
-  return layout_of(desc, max_rows, max_batch, max_blocks_per_seq, max_drafts).total;
+                           int32_t max_drafts, int32_t max_seqs) {
+  if (!desc || max_rows < 1 || max_batch < 1 || max_blocks_per_seq < 1 || max_drafts < 1 || max_seqs < 1) return 0;
+  return layout_of(desc, max_rows, max_batch, max_blocks_per_seq, max_drafts, max_seqs).total;
 }
 
 size_t via_staging_bytes(const via_model_desc* desc, int32_t max_rows, int32_t max_batch, int32_t max_blocks_per_seq,
                          int32_t max_drafts) {
   if (!desc || max_rows < 1 || max_batch < 1 || max_blocks_per_seq < 1 || max_drafts < 1) return 0;
-  Layout L = layout_of(desc, max_rows, max_batch, max_blocks_per_seq, max_drafts);
+  Layout L = layout_of(desc, max_rows, max_batch, max_blocks_per_seq, max_drafts, 1);
   return staging_slot_bytes(L) * kRing;
 }
 
@@ -734,7 +720,8 @@ via_status via_kv_create(via_model* m, const via_kv_desc* d, via_kv** out) {
     return fail(VIA_EINVAL, "KV description sizes out of range");
   if (!d->pool_full || !d->pool_slim || !d->workspace || !d->pinned_staging)
     return fail(VIA_EINVAL, "pools, workspace and staging are required");
-  Layout L = layout_of(&m->d, d->max_rows, d->max_batch, d->max_blocks_per_seq, std::max(1, (int)d->max_drafts));
+  Layout L = layout_of(&m->d, d->max_rows, d->max_batch, d->max_blocks_per_seq, std::max(1, (int)d->max_drafts),
+                       d->max_seqs);
   if (d->workspace_bytes < L.total)
     return fail(VIA_ENOMEM, "workspace %zu bytes < required %zu", d->workspace_bytes, L.total);
   size_t slot = staging_slot_bytes(L);
@@ -1151,6 +1138,7 @@ via_status via_step(via_model* m, via_kv* kv, const via_drafts* drafts, const vi
 }
 
 static_assert(VIA_STATIC_SAMPLE_MAX_ROWS == kStaticSampleRows, "the header's limit is the scratch's");
+static_assert(VIA_STATE_ROWS == kStateRows, "the header's ring size is the runtime's");
 
 via_status via_sample_rows_static(const via_verify_out* out, int32_t out_rows, int32_t vocab, int32_t n,
                                   const int32_t* row, float temperature, const float* uniforms, int32_t* tokens,
@@ -1187,6 +1175,12 @@ via_status via_sample_rows_static(const via_verify_out* out, int32_t out_rows, i
   launch_sample_rows_static(a, req.data(), n, scr, probs, probs_ld, (hipStream_t)stream);
   e = hipGetLastError();
   if (e != hipSuccess) return fail(VIA_EDEVICE, "sample launch: %s", hipGetErrorString(e));
+  return VIA_OK;
+}
+
+via_status via_kv_last_full_start(const via_kv* kv, int32_t* route_index) {
+  if (!kv || !route_index) return fail(VIA_EINVAL, "null argument");
+  *route_index = kv->last_full_start;
   return VIA_OK;
 }
 

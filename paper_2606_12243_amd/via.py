@@ -102,7 +102,7 @@ via_pack_gate_up = _sig("via_pack_gate_up", I32, P, P, I32, I32, I32, P)
 via_gemm_bf16 = _sig("via_gemm_bf16", I32, P, P, P, I32, I32, I32, P)
 via_pool_bytes = _sig("via_pool_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32)
 via_dimr_cost = _sig("via_dimr_cost", I32, P, P, I32, I32, I32, C.c_float, C.c_float, C.c_float, P, P)
-via_workspace_bytes = _sig("via_workspace_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
+via_workspace_bytes = _sig("via_workspace_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32, I32)
 via_staging_bytes = _sig("via_staging_bytes", C.c_size_t, C.POINTER(ModelDesc), I32, I32, I32, I32)
 via_model_create = _sig("via_model_create", I32, C.POINTER(ModelDesc), C.POINTER(Weights), C.POINTER(P))
 via_model_set_route = _sig("via_model_set_route", I32, P, PI32, I32)
@@ -114,6 +114,7 @@ via_prefill = _sig("via_prefill", I32, P, P, I32, PI32, I32, P)
 via_prefill_batch = _sig("via_prefill_batch", I32, P, P, I32, PI32, PI32, PI32, P)
 via_kv_seq_release = _sig("via_kv_seq_release", I32, P, I32)
 via_kv_seq_info = _sig("via_kv_seq_info", I32, P, I32, I32, PI32, PI32, I32, PI32)
+via_kv_last_full_start = _sig("via_kv_last_full_start", I32, P, PI32)
 via_verify_slim = _sig("via_verify_slim", I32, P, P, C.POINTER(Window), C.POINTER(TierParams),
                        C.POINTER(VerifyOut), P)
 via_verify_full = _sig("via_verify_full", I32, P, P, C.POINTER(Window), PI32, C.POINTER(TierParams),
@@ -139,6 +140,7 @@ via_version = _sig("via_version", C.c_char_p)
 EXPORTS = ["via_packed_bytes", "via_pack_weight", "via_pack_gate_up", "via_gemm_bf16", "via_dimr_cost", "via_pool_bytes", "via_workspace_bytes", "via_staging_bytes", "via_model_create",
            "via_model_set_route", "via_model_destroy", "via_kv_create", "via_kv_destroy",
            "via_kv_seq_reserve", "via_prefill", "via_prefill_batch", "via_kv_seq_release", "via_kv_seq_info",
+           "via_kv_last_full_start",
            "via_verify_slim", "via_verify_full", "via_verify_probe", "via_tier_decide", "via_tier_decide_sampled", "via_sample_rows",
            "via_sample_rows_static", "via_kv_seq_set_tokens", "via_kv_seq_tokens", "via_step",
            "via_kv_commit_rollback", "via_kv_timer_enable", "via_kv_timer_read", "via_last_error",
@@ -253,7 +255,7 @@ class KV:
         else:
             self.pool_full = mk(nb_full // esz, dtype=dt, device=device)
             self.pool_slim = mk(nb_slim // esz, dtype=dt, device=device)
-        wsb = via_workspace_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts)
+        wsb = via_workspace_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts, max_seqs)
         stb = via_staging_bytes(C.byref(d), max_rows, max_batch, max_blocks_per_seq, max_drafts)
         self.workspace = torch.empty(wsb, dtype=torch.uint8, device=device)
         self.staging = torch.empty(stb, dtype=torch.uint8, pin_memory=True)
@@ -282,6 +284,12 @@ class KV:
         check(via_kv_seq_info(self.h, seq, cache, C.byref(valid), tab.ctypes.data_as(PI32), len(tab),
                               C.byref(nb)))
         return valid.value, tab[:nb.value].tolist()
+
+    def last_full_start(self):
+        """Route index the last full forward started at (0, the shared-prefix length, or -1)."""
+        v = C.c_int32()
+        check(via_kv_last_full_start(self.h, C.byref(v)))
+        return v.value
 
     def timer_enable(self, mask):
         check(via_kv_timer_enable(self.h, mask))

@@ -70,6 +70,11 @@ class Lockstep:
         self.seen_tiers = set()
         self.max_logit_err = 0.0
 
+    def set_params(self, params):
+        """Tier parameters of the following steps (both sides)."""
+        self.p = params
+        self.sess.p = via.tier_params(params.tau_acc, params.tau_full, params.temperature, params.forced)
+
     def close(self):
         self.kv.close()
         if self.own_gm:
@@ -217,6 +222,7 @@ class Lockstep:
         else:
             s.commit(w, gd)
         self.steps.append(dict(step=step_idx, run=run.tolist(),
+                               full_start=s.kv.last_full_start() if run.any() else None,
                                gpu_lag={b: gpu_lag[b] for i, b in enumerate(order) if run[i]},
                                full_lag={b: lag_before[b] for i, b in enumerate(order) if b in dec_o and run[i]},
                                kappa={b: dec_o[b]["kappa"] for b in order if b in dec_o}))

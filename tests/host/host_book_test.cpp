@@ -529,6 +529,111 @@ static void test_step_window_and_tokens() {
   CHECK((int)bk.seqs[1].tokens.size() == bk.seqs[1].valid[1] + 1);
 }
 
+// The state ring: ring rows of every planned row, the slim forward's
+// overwrite check, the row map of a full forward that starts after the
+// shared layers, and the commits that set and clear xs_ok.
+static void test_state_ring() {
+  KvBook bk;
+  book_init(bk, 2, 16, 64, 64);
+  attach(bk, 0, 20);
+  attach(bk, 1, 130);
+  Win w = chain({0, 1}, 4);
+  WinCopy c;
+  CHECK(copy_window(bk, &w.w, V, 2, 8, c) == VIA_OK);
+  Plan P;
+  CHECK(build_verify_plan(bk, VIA_CACHE_SLIM, c, {0, 1}, &w.w, true, V, 4, P, nullptr) == VIA_OK);
+  CHECK(P.rows[0].xs == 20 && P.rows[3].xs == 23);                              // seq 0, slots 20..23
+  CHECK(P.rows[4].xs == kStateRows + 130 % kStateRows && P.rows[7].xs == kStateRows + 133 % kStateRows);
+  note_slim_forward(bk, c, {0, 1}, true);
+  CHECK(bk.seqs[0].xs_ok && bk.seqs[1].xs_ok);
+  // commit without the full verifier: seq 0 keeps pending + 2 drafts + emit (lag 3), seq 1 pending + emit
+  const int B = 2, D = 8;
+  auto hp = decision(B, D);
+  set(hp, B, D, 0, 0, 2, 7, 24, {0, 1});
+  set(hp, B, D, 1, 0, 0, 9, 132, {});
+  CommitMoves cm;
+  CHECK(plan_commit(bk, c, {21, 131}, hp.data(), V, cm) == VIA_OK);
+  apply_commit(bk, c, hp.data());
+  CHECK(bk.seqs[0].valid[VIA_CACHE_SLIM] == 23 && bk.seqs[0].valid[VIA_CACHE_FULL] == 20 && bk.seqs[0].xs_ok);
+  // next step: seq 0 escalates; its full forward has lag rows 20..22 then window slots 23..26
+  Win w2 = chain({0, 1}, 4);
+  w2.n_lag = {3, 1};
+  w2.lag_tok = {1, 2, 3, 4, 0, 0};
+  w2.finish(4, 8, 3, false);
+  WinCopy c2;
+  CHECK(copy_window(bk, &w2.w, V, 2, 8, c2) == VIA_OK);
+  Plan S2;
+  CHECK(build_verify_plan(bk, VIA_CACHE_SLIM, c2, {0, 1}, &w2.w, true, V, 4, S2, nullptr) == VIA_OK);
+  note_slim_forward(bk, c2, {0, 1}, true);
+  CHECK(bk.seqs[0].xs_ok && bk.seqs[1].xs_ok);  // 23 + 4 - 20 and 131 + 4 - 130 slots fit the ring
+  Plan F;
+  CHECK(build_verify_plan(bk, VIA_CACHE_FULL, c2, {0}, &w2.w, true, V, 4, F, nullptr) == VIA_OK);
+  CHECK(build_prefix_xfer(bk, c2, {0}, F));
+  CHECK(F.xfer.size() == 7);
+  if (F.xfer.size() == 7) {
+    CHECK(F.xfer[0].src_row == 20 && F.xfer[0].t == 4 && F.xfer[0].src_blk == bk.seqs[0].table[VIA_CACHE_SLIM][1] &&
+          F.xfer[0].dst_blk == bk.seqs[0].table[VIA_CACHE_FULL][1]);
+    CHECK(F.xfer[3].src_row == 23 && F.xfer[6].src_row == 26 && F.xfer[6].t == 26 % 16);
+  }
+  // a window that would overwrite ring rows of lag slots: seq 1 lags 121 slots, 8 rows need 129
+  bk.seqs[1].valid[VIA_CACHE_FULL] = 10;
+  note_slim_forward(bk, c2, {1}, true);
+  CHECK(bk.seqs[1].xs_ok);  // 131 + 4 - 10 = 125 slots
+  Win w3 = chain({1}, 8);
+  WinCopy c3;
+  CHECK(copy_window(bk, &w3.w, V, 2, 8, c3) == VIA_OK);
+  note_slim_forward(bk, c3, {0}, true);
+  CHECK(!bk.seqs[1].xs_ok);
+  Plan F3;
+  F3.rows = F.rows;
+  F3.xfer.push_back(PrefixXfer{0, 0, 0, 0});
+  CHECK(!build_prefix_xfer(bk, c3, {0}, F3) && F3.xfer.empty());
+  // a slim forward that saved nothing clears it too
+  note_slim_forward(bk, c2, {0}, false);
+  CHECK(!bk.seqs[0].xs_ok);
+  // the full verifier's commit sets it again
+  bk.seqs[0].full_ran = true;
+  auto h2 = decision(1, 8);
+  set(h2, 1, 8, 0, 0, 0, 5, 24, {});
+  Win w4 = chain({0}, 4);
+  WinCopy c4;
+  CHECK(copy_window(bk, &w4.w, V, 2, 8, c4) == VIA_OK);
+  apply_commit(bk, c4, h2.data());
+  CHECK(bk.seqs[0].xs_ok && bk.seqs[0].valid[VIA_CACHE_FULL] == 23);
+  // tree commits the full verifier did not see: keeping the root alone leaves the ring valid, keeping
+  // more clears it (compaction moves cache slots, not ring rows)
+  for (int keep_more = 0; keep_more < 2; ++keep_more) {
+    KvBook tb;
+    book_init(tb, 1, 8, 16, 16);
+    attach(tb, 0, 15);
+    Win t;
+    t.seq = {0};
+    t.n_rows = {3};
+    t.row_tok = {5, 6, 7};
+    t.row_depth = {0, 1, 2};
+    t.row_mask = {1, 3, 7};
+    t.n_drafts = {5};
+    t.draft_tok = {1, 2, 3, 4, 5, 0, 0, 0};
+    t.draft_row = {0, 0, 1, 1, 2, 0, 0, 0};
+    t.draft_parent = {-1, -1, 1, 1, 3, -1, -1, -1};
+    t.finish(3, 8, 1, true);
+    WinCopy tc;
+    CHECK(copy_window(tb, &t.w, V, 1, 8, tc) == VIA_OK);
+    Plan TP;
+    CHECK(build_verify_plan(tb, VIA_CACHE_SLIM, tc, {0}, &t.w, true, V, 4, TP, nullptr) == VIA_OK);
+    note_slim_forward(tb, tc, {0}, true);
+    auto th = decision(1, 8);
+    if (keep_more)
+      set(th, 1, 8, 0, 0, 2, -1, 18, {1, 2});  // root + node 1 kept
+    else
+      set(th, 1, 8, 0, 0, 0, 9, 17, {});  // root only
+    CommitMoves tm;
+    CHECK(plan_commit(tb, tc, {16}, th.data(), V, tm) == VIA_OK);
+    apply_commit(tb, tc, th.data());
+    CHECK(tb.seqs[0].xs_ok == !keep_more);
+  }
+}
+
 int main() {
   test_step_window_and_tokens();
   test_allocator();
@@ -536,6 +641,7 @@ int main() {
   test_plans();
   test_commit();
   test_tree_moves();
+  test_state_ring();
   test_random_steps();
   if (g_fail) {
     std::printf("%d check(s) failed\n", g_fail);

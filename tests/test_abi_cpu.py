@@ -79,7 +79,10 @@ def test_sizes(via):
     d = _desc(via)
     pb = via.via_pool_bytes(C.byref(d), 2, 10, 16)
     assert pb == 2 * 10 * 2 * 1 * 16 * 64 * 2
-    ws = via.via_workspace_bytes(C.byref(d), 64, 2, 32, 8)
+    ws = via.via_workspace_bytes(C.byref(d), 64, 2, 32, 8, 1)
     assert ws > 0 and ws % 256 == 0
-    assert via.via_workspace_bytes(C.byref(d), 0, 2, 32, 8) == 0
+    assert via.via_workspace_bytes(C.byref(d), 0, 2, 32, 8, 1) == 0
+    assert via.via_workspace_bytes(C.byref(d), 64, 2, 32, 8, 0) == 0
+    # each sequence id adds its ring of post-shared-layer states (VIA_STATE_ROWS fp32 rows of d_model)
+    assert via.via_workspace_bytes(C.byref(d), 64, 2, 32, 8, 3) - ws == 2 * 128 * d.d_model * 4
     assert via.via_staging_bytes(C.byref(d), 64, 2, 32, 8) > 0

@@ -107,7 +107,7 @@ def test_full_size_sampled_parity(name, steps, sample, temperature, models):
             ls.step(drafts, step)
             print(f"[step] {name} {step}: max logit err {ls.max_logit_err:.3g} tiers {sorted(ls.seen_tiers)} "
                   f"resyncs {len(ls.log)} run {ls.steps[-1]['run']} lag {ls.steps[-1]['gpu_lag']} "
-                  f"kappa {ls.steps[-1]['kappa']}", flush=True)
+                  f"full start {ls.steps[-1]['full_start']} kappa {ls.steps[-1]['kappa']}", flush=True)
         if mixed:
             # the three tiers over the batch, a full forward over part of the batch, and
             # full forwards carrying lag rows (for a compared sequence when 2+ are followed
@@ -119,5 +119,10 @@ def test_full_size_sampled_parity(name, steps, sample, temperature, models):
             if steps >= 6 and len(sample) >= 2:
                 assert any(lg > 0 for st in ls.steps for lg in st["full_lag"].values()), \
                     [st["full_lag"] for st in ls.steps]
+            # a full forward with lag rows that started after the layers the slim route shares
+            # with the full model (the lag slots' states taken from the state ring)
+            n_sh = next(i for i, l in enumerate(list(cfg["route"]) + [-1]) if l != i)
+            assert any(st["full_start"] == n_sh and any(lg > 0 for lg in st["gpu_lag"].values())
+                       for st in ls.steps), [(st["full_start"], st["gpu_lag"]) for st in ls.steps]
     finally:
         ls.close()

@@ -48,6 +48,54 @@ def test_tiny_fp32_workload_end_to_end():
         ls.close()
 
 
+@pytest.mark.parametrize("name", ["micro_f32", "micro_bf16", "small_bf16_hd128"])
+def test_lag_rows_start_after_shared_layers(name):
+    """Full forwards of sequences whose full caches lag: the states of the lag
+    slots after the layers the slim route shares with the full model are kept
+    in the state ring, so the forward starts after those layers and still
+    matches the oracle's all-layer forward, block tables included.  A lag
+    that exactly fills the ring with the window still starts there; one more
+    step of lag overflows it, and the forward runs every layer again."""
+    from oracle.decode import FORCED_ACCEPT, FORCED_NONE
+
+    cfg = configs.get(name)
+    cfg.update(seed_c=26, seed_d=36, corrupt=0.3)
+    route = list(cfg["route"])
+    n_sh = next(i for i, l in enumerate(route + [-1]) if l != i)
+    assert 0 < n_sh < len(route)
+    k = 4
+    print(f"[case] lag rows via the state ring {name}", flush=True)
+    ls = Lockstep(cfg, max_rows=2 * (128 + k), max_batch=2, max_drafts=8, max_blocks=32, blocks=128)
+    accept, full = TierParams(0.9, 0.5, 1.0, FORCED_ACCEPT), TierParams(0.9, 0.5, 1.0, FORCED_FULL)
+    step = 0
+
+    def run(params, n):
+        nonlocal step
+        ls.set_params(params)
+        for _ in range(n):
+            drafts = {b: ls.drafter.chain(b, ls.ver.seqs[b].tokens, k, step) for b in (0, 1)}
+            ls.step(drafts, step)
+            step += 1
+        return ls.steps[-1]
+
+    try:
+        ls.add_prompt(0, gen.context_tokens(cfg, 0, 30))
+        ls.add_prompt(1, gen.context_tokens(cfg, 1, 19))
+        # (accepted steps before the escalation, lag rows it carries, expected start)
+        for n_acc, lag, start in ((2, 2 * k, n_sh), (31, 31 * k, n_sh), (32, 32 * k, 0)):
+            run(accept, n_acc)
+            st = run(full, 1)
+            assert st["run"] == [1, 1] and st["gpu_lag"] == {0: lag, 1: lag}, st
+            assert st["full_start"] == start, (n_acc, st)
+            print(f"[step] {step}: lag {lag} full forward from route index {st['full_start']}", flush=True)
+        # natural tiers afterwards (the caches caught up)
+        run(TierParams(0.9, 0.5, 1.0, FORCED_NONE), 4)
+        print(f"[done] {name} steps={step} max_logit_err={ls.max_logit_err:.3g} resyncs={len(ls.log)}",
+              flush=True)
+    finally:
+        ls.close()
+
+
 def test_forced_full_matches_greedy_on_gpu():
     cfg = configs.get("micro_bf16")
     cfg.update(seed_c=22, seed_d=32, corrupt=0.3, temperature=1.0)
