@@ -651,7 +651,7 @@ VIA_GEMM_LAUNCH(gemm_head, 2)
 
 // QKV, O and down projections of forwards of up to 32 rows (bf16): the
 // weight-streaming decomposition of the gate/up kernel with split-K partials.
-// A work-group owns a.nb 16-column blocks and K split blockIdx.y (a.ksplit
+// A work-group owns a.nb 16-column blocks and K split blockIdx.x % a.ksplit (a.ksplit
 // equal ranges of 32-wide steps); its 8 waves interleave the split's steps
 // (wave w takes steps w, w+8, ...) over all its blocks, loading X fragments
 // straight from global memory (each is used by one wave; they stay in L2)
@@ -664,8 +664,8 @@ __global__ __launch_bounds__(kThreads) void gemm_ki_part(GemmArgs a) {
   constexpr int NBM = kWaves;
   __shared__ __align__(16) float red[kWaves][16 * MB][NBM * 16 + 4];
   const int nblocks = a.N >> 4;
-  const int blk0 = blockIdx.x * a.nb;
-  const int split = blockIdx.y;
+  const int split = blockIdx.x % a.ksplit;
+  const int blk0 = (blockIdx.x / a.ksplit) * a.nb;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nb = min(a.nb, nblocks - blk0);
   const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
@@ -746,8 +746,8 @@ __global__ __launch_bounds__(kThreads) void gemm_ki_part(GemmArgs a) {
 template <int MB, int NT, int NB, int NSW, int DEPTH>
 __global__ __launch_bounds__(kThreads) void gemm_ki_fixed(GemmArgs a) {
   __shared__ __align__(16) float red[kWaves][16 * MB][NB * 16 + 4];
-  const int blk0 = blockIdx.x * NB;
-  const int split = blockIdx.y;
+  const int split = blockIdx.x % a.ksplit;
+  const int blk0 = (blockIdx.x / a.ksplit) * NB;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
   const int s_beg = split * NSW * kWaves;
@@ -812,7 +812,11 @@ __global__ __launch_bounds__(kThreads) void gemm_ki_fixed(GemmArgs a) {
 
 template <int NT>
 void launch_ki_part(const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const dim3 grid(((a.N >> 4) + a.nb - 1) / a.nb, a.ksplit);
+  // split-major order: work-group i takes K split i % ksplit, so with the
+  // round-robin dispatch of work-groups over the 8 XCDs each XCD's
+  // work-groups share 8 / ksplit splits (one for 8 splits) and its L2 holds
+  // only their slices of the activations
+  const dim3 grid((((a.N >> 4) + a.nb - 1) / a.nb) * a.ksplit);
   auto go = [&](auto kernel) {
     if (e0)
       hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, a);
