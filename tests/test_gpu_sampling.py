@@ -71,7 +71,7 @@ def pick_uniform(w, err, rng):
 
 class SampledLockstep:
     def __init__(self, name, params, alpha, beta, greedy_drafts=False, seed=0, batch=3, k=4, drafter_route=None,
-                 drafter_T=1.0):
+                 drafter_T=1.0, drafter_cfg=None):
         cfg = configs.get(name)
         cfg["seed_c"] = 21 + seed
         cfg["seed_d"] = 31 + seed
@@ -93,16 +93,25 @@ class SampledLockstep:
             V = self.md["vocab"]
             self.drafter = GreedyDrafter(self.om, lambda b, step, j: gen.corruption(cfg["seed_d"], b, step, j,
                                                                                       0.3, V))
-        # drafter model on the same weights under a shallower route (GPU:
-        # ModelDrafter; oracle: cache-free forwards of that route)
+        # drafter model (GPU: ModelDrafter; oracle: cache-free forwards of its
+        # route): the verifier's weights under a shallower route, or a model of
+        # its own (drafter_cfg: own weights and dimensions, same vocabulary)
         self.dr, self.rel_p = None, 0.0
+        if drafter_cfg is not None:
+            dmd = drafter_cfg["model"]
+            assert dmd["vocab"] == self.md["vocab"]
+            dW = gen.model_weights(drafter_cfg)
+            self.dr_om, self.dr_md = OracleModel(dmd, dW), dmd
+            drafter_route = list(range(dmd["n_layers"])) if drafter_route is None else drafter_route
+        else:
+            dW, self.dr_om, self.dr_md = W, self.om, self.md
         if drafter_route is not None:
             self.dr_route, self.dr_T = list(drafter_route), float(drafter_T)
-            self.dr_model = via.Model(self.md, W, self.dr_route)
+            self.dr_model = via.Model(self.dr_md, dW, self.dr_route)
             self.dr_kv = via.KV(self.dr_model, max_seqs=batch, max_blocks_per_seq=16, blocks_full=64,
                                 blocks_slim=64, max_rows=64, max_batch=batch, max_drafts=8)
             self.dr = ModelDrafter(self.dr_model, self.dr_kv, self.dr_T)
-            self.rel_p = math.exp(2 * logit_tol(self.md) / self.dr_T) - 1
+            self.rel_p = math.exp(2 * logit_tol(self.dr_md) / self.dr_T) - 1
         self.oid = {}
         for b in range(batch):
             toks = gen.context_tokens(cfg, b, 9 + 5 * b)
@@ -132,7 +141,7 @@ class SampledLockstep:
             pre = list(self.ver.seqs[self.oid[b]].tokens)
             d, rows = [], []
             for j in range(self.k):
-                lg = self.om.forward_sequence(pre + d, self.dr_route)[-1]
+                lg = self.dr_om.forward_sequence(pre + d, self.dr_route)[-1]
                 p = tempered(lg, self.dr_T)
                 u, exact, lo, hi = pick_uniform(p, 2 * self.rel_p, self.rng)
                 assert exact, "no token interval is wide enough for an exact draw"
@@ -333,6 +342,26 @@ def test_model_drafter_and_sampled_verification(params, alpha, beta, drafter_T):
     print(f"[case] model drafter forced={params.forced} alpha={alpha} drafter T={drafter_T}", flush=True)
     ls = SampledLockstep("micro_f32", params, alpha, beta, seed=5 + params.forced, drafter_route=[0],
                          drafter_T=drafter_T)
+    try:
+        for step in range(4):
+            ls.step(step)
+        print(f"[done] {ls.stats}", flush=True)
+        assert ls.stats["drafted"] == 4 * ls.B * ls.k and ls.stats["exact"] > 0
+    finally:
+        ls.close()
+
+
+@pytest.mark.parametrize("alpha,beta", [(0.0, 1.0), (0.2, 1.0)])
+def test_independent_drafter_model_and_sampled_verification(alpha, beta):
+    """A drafter with weights and dimensions of its own (2 layers, d_model 64,
+    one head, the verifier's vocabulary): its drafts and p against the
+    oracle's forwards of that model, then the sampled verification of those
+    drafts by the micro model, over four steps (the drafter's cache follows
+    the committed tokens)."""
+    params = TierParams(0.9, 0.5, 1.0, FORCED_NONE)
+    print(f"[case] independent drafter alpha={alpha}", flush=True)
+    ls = SampledLockstep("micro_f32", params, alpha, beta, seed=9, drafter_T=1.0,
+                         drafter_cfg=configs.get("micro_f32_drafter"))
     try:
         for step in range(4):
             ls.step(step)

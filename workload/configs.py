@@ -76,6 +76,11 @@ SMALL = {
         model=dict(n_layers=3, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ffn=512,
                    vocab=1000, dtype="bf16", rms_eps=1e-5, rope_theta=10000.0),
         route=[0, 2], seed_w=12),
+    # a drafter with its own weights and dimensions for micro_f32 (same vocabulary)
+    "micro_f32_drafter": dict(
+        model=dict(n_layers=2, d_model=64, n_heads=1, n_kv_heads=1, head_dim=64, d_ffn=192,
+                   vocab=500, dtype="f32", rms_eps=1e-5, rope_theta=10000.0),
+        route=[0, 1], seed_w=14),
     "small_bf16_hd128": dict(
         model=dict(n_layers=4, d_model=512, n_heads=8, n_kv_heads=2, head_dim=128, d_ffn=1408,
                    vocab=3001, dtype="bf16", rms_eps=1e-5, rope_theta=10000.0),
