@@ -8,8 +8,8 @@
 // linear order and the item index is the grid's slowest, so when splits x
 // KV heads is a multiple of 8 the items of a sequence that share a (KV head,
 // split) run on one XCD and their repeated K/V reads can hit its L2.  The keys of a sequence are split into spans of `span` keys (a
-// multiple of 32 the host picks so that the whole launch has about one
-// work-group per compute unit); a work-group streams its span and writes
+// multiple of 32 the host picks so that the whole launch has about 192
+// work-groups, or more when that would take spans well past 4096 keys); a work-group streams its span and writes
 // one (max, sum, output) partial per query, and a combine kernel merges the
 // partials of a query in split order.  Visibility of slot p for row r:
 // p < vis_len[r], or p is a window slot whose bit is set in the row's tree
@@ -443,6 +443,9 @@ int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int ta
   }
   long long per = std::max<long long>(1, (blocks + target_groups - 1) / target_groups);
   int span = (int)std::min<long long>(per * 32, kAttnMaxSpan);
+  // a forward whose spans would run well past kAttnPrefSpan keys (long
+  // contexts with several query items per sequence) takes more work-groups
+  if (span > kAttnPrefSpan * 3 / 2) span = kAttnPrefSpan;
   const int need = ((max_kv + 31) / 32 + max_splits - 1) / max_splits * 32;  // at most max_splits splits
   span = std::max(span, need);
   if (span > kAttnMaxSpan) return -1;

@@ -10,6 +10,7 @@ constexpr int kBlock = 16;        // tokens per KV page
 constexpr int kMaxChildren = 8;   // drafts verified by one row
 constexpr int kAttnMaxSplits = 32;  // key splits per sequence (partials one query's combine merges)
 constexpr int kAttnMaxSpan = 8192;  // keys of one split (pages of a split's work-group, x16)
+constexpr int kAttnPrefSpan = 4096;  // keys per work-group beyond which a forward takes more work-groups than the target
 constexpr int kAttnTargetGroups = 192;  // attention work-groups a forward aims for (fewer, longer spans than one per compute unit: measured best at the 8B shapes)
 constexpr int kAttnQueries = 32;  // (row, head-in-group) queries per attention work-group
 constexpr int kNormChunk = 512;   // columns per partial sum of squares (RMSNorm)
