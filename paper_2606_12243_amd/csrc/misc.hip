@@ -345,20 +345,32 @@ __global__ __launch_bounds__(64) void decide_kernel(DecideArgs a) {
     em = gtok;
     break;
   }
+  const int ev = st == 0 ? em : -1;
+  const int nv = st == 2 ? ss.n : ss.n + k + (st == 0 && em >= 0 ? 1 : 0);
   status[b] = st;
   kappa[b] = k;
-  emit[b] = st == 0 ? em : -1;
-  new_len[b] = st == 2 ? ss.n : ss.n + k + (st == 0 && em >= 0 ? 1 : 0);
+  emit[b] = ev;
+  new_len[b] = nv;
   for (int q = k; q < D; ++q) path[q] = -1;
   if (a.h_packed) {
     // the host mirror, written past the caches so that it is in host memory
-    // once the stream has been synchronised
+    // once the stream has been synchronised.  Values come from registers
+    // (the path in rounds of 8 loads, then 8 stores): a value re-read from
+    // device memory after each store would make every system-scope store
+    // wait for a load, one host round trip per value.
     auto put = [&](int i, int v) { __hip_atomic_store(a.h_packed + i, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM); };
-    put(b, status[b]);
-    put(B + b, kappa[b]);
-    put(2 * B + b, emit[b]);
-    put(3 * B + b, new_len[b]);
-    for (int q = 0; q < D; ++q) put(4 * B + base + q, path[q]);
+    put(b, st);
+    put(B + b, k);
+    put(2 * B + b, ev);
+    put(3 * B + b, nv);
+    for (int q0 = 0; q0 < D; q0 += 8) {
+      int pv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pv[j] = q0 + j < D ? path[q0 + j] : 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (q0 + j < D) put(4 * B + base + q0 + j, pv[j]);
+    }
   }
 }
 
