@@ -639,7 +639,7 @@ def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None):
             "one_sequence_per_call": {"ms": round(ms_seq, 2),
                                       "frac": round((gemm_flop + attn_flop) / (ms_seq * 1e-3) / 1e12
                                                     / MFMA_BF16_PEAK_TFLOPS, 4)},
-            "note": "projections run as 3 (QKV) or 2 bf16-term passes of the prefill GEMM (fp32-activation "
+            "note": "projections run as 2 bf16-term passes of the prefill GEMM (fp32-activation "
                     "contract); the frac counts each product's 2MNK once"}
 
 

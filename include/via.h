@@ -223,7 +223,7 @@ via_status via_pack_gate_up(const void *src, void *dst, int32_t d_ffn, int32_t d
  * C = X W^T for bf16 X [M, K] and W [N, K], fp32 accumulation and output:
  * the compute-bound tile kernel that runs every projection of a forward of
  * more than 512 rows (a prefill), exposed for measurement and tests.  (A
- * forward feeds it its fp32 activations as 2 or 3 bf16 terms, one pass each;
+ * forward feeds it its fp32 activations as 2 bf16 terms, one pass each;
  * this call runs one.)
  *   X  device bf16, ceil(M/16)*16 rows, in the activation-fragment layout:
  *      element (m, k) is at 8-element group

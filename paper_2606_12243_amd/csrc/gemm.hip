@@ -20,7 +20,8 @@
 // as fragments (afrag_group), so every global load of a wave reads one
 // contiguous 1 KB block and every LDS read is conflict-free.  fp32
 // activations enter the matrix cores as NT bf16 terms (x = hi + [mid +] lo),
-// NT = 3 keeping ~24 significant bits and NT = 2 ~16.  Output register r of
+// NT = 3 keeping ~24 significant bits and NT = 2 ~16 (every projection
+// takes 2; the kernels also build for 3).  Output register r of
 // lane l is row (l/16)*4 + r, column l%16.  The head GEMM (split 1) reduces
 // its tile to per-row (max, second, sum-exp, argmax) partials and
 // draft-token logits in place.
@@ -569,7 +570,7 @@ __global__ __launch_bounds__(kThreads) void gemm_gate_up_ki(GemmArgs a) {
   __global__ __launch_bounds__(kThreads) void NAME(GemmArgs a) {                         \
     gemm_body<T, MB, (sizeof(T) == 2 ? NT_BF16 : 1), kNBW, C, STATS>(a);                 \
   }
-VIA_GEMM_ENTRY(gemm_qkv, 3, false)
+VIA_GEMM_ENTRY(gemm_qkv, kQkvTerms, false)
 VIA_GEMM_ENTRY(gemm_o, 2, false)
 VIA_GEMM_ENTRY(gemm_down, 2, false)
 VIA_GEMM_ENTRY(gemm_head, 2, true)
@@ -607,7 +608,7 @@ constexpr int chunk_steps() {
       default: go(NAME<T, 8, chunk_steps<T, 8, NT>()>); break;                               \
     }                                                                                        \
   }
-VIA_GEMM_LAUNCH(gemm_qkv, 3)
+VIA_GEMM_LAUNCH(gemm_qkv, kQkvTerms)
 VIA_GEMM_LAUNCH(gemm_o, 2)
 
 // Gate/up with SwiGLU: grid (work-groups of a.nb blocks, row groups).
@@ -1103,7 +1104,7 @@ bool gemm_is_prefill(bool bf16, int M) { return bf16 && M > kPrefillMinRows; }
 void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (role != GemmRole::kHead && gemm_is_prefill(bf16, a.M)) {
     // many rows: the compute-bound tile kernel (one partial, ksplit 1)
-    const int nt = role == GemmRole::kQkv ? 3 : 2;
+    const int nt = role == GemmRole::kQkv ? kQkvTerms : 2;
     launch_prefill(a, nt, s, e0, e1);
     if (role == GemmRole::kGateUp) {
       const int n = a.M * (a.F >> 3);
@@ -1113,7 +1114,7 @@ void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hip
   }
   if (bf16 && a.nb > 0 && gemm_uses_ki(role, a.M, a.N)) {
     if (role == GemmRole::kQkv)
-      launch_ki_part<3>(a, s, e0, e1);
+      launch_ki_part<kQkvTerms>(a, s, e0, e1);
     else
       launch_ki_part<2>(a, s, e0, e1);
     return;

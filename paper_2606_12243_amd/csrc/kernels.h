@@ -35,10 +35,12 @@ struct GemmArgs {
 };
 
 // Projection a GEMM computes.  Each has its own kernel entry point; the QKV
-// input carries 3 bf16 terms per fp32 activation, the others 2; the head
+// input carries kQkvTerms bf16 terms per fp32 activation, the others 2; the head
 // reduces its tiles to row statistics instead of writing partials; the
 // gate/up projection runs over all of K and applies SwiGLU itself.
 enum class GemmRole { kQkv, kO, kGateUp, kDown, kHead };
+// bf16 terms per fp32 activation at the QKV projection's input (the others take 2).
+constexpr int kQkvTerms = 2;
 // e0/e1 (both or neither): timing events recorded at the kernel's own start
 // and end.
 void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,

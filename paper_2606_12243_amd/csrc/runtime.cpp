@@ -96,11 +96,11 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   };
   const size_t R = max_rows;
   // activation fragments: rows padded to the GEMM row group; bf16 models
-  // keep 3 bf16 terms for the QKV input, 2 elsewhere; fp32 models 1 fp32
+  // keep kQkvTerms bf16 terms for the QKV input, 2 elsewhere; fp32 models 1 fp32
   const size_t Rp = (size_t)gemm_padded_rows(max_rows);
-  const size_t f3 = es == 2 ? 6 : 4, f2 = 4;
+  const size_t fq = es == 2 ? 2 * std::max(2, kQkvTerms) : 4, f2 = 4;
   L.X = take(R * D.d * 4);
-  L.Yf = take(Rp * D.d * f3);
+  L.Yf = take(Rp * D.d * fq);
   L.Q = take(R * D.H * D.hd * 4);
   L.Af = take(Rp * D.H * D.hd * f2);
   L.Hf = take(Rp * D.F * f2);
@@ -370,7 +370,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     launch_prefix_copy(bf, pa, s);
   }
   // first layer's input norm; from layer 0 it also gathers the embedding rows into X
-  launch_resid_add(bf, 3, X, nullptr, 1, M, D.d, m->attn_norm[route[start_si]], Yf, MBn, nullptr, ss, ss_stride, s,
+  launch_resid_add(bf, kQkvTerms, X, nullptr, 1, M, D.d, m->attn_norm[route[start_si]], Yf, MBn, nullptr, ss, ss_stride, s,
                    nullptr, start_si > 0 ? nullptr : m->embed, d_rows);
   at.q_hi = Q;
   at.q_lo = Qlo;
@@ -411,7 +411,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   qa.eps = eps;
   for (size_t si = start_si; si < route.size(); ++si) {
     const int l = route[si];
-    // Q/K/V: three bf16 terms per activation (the K/V are rounded to the cache's bf16)
+    // Q/K/V from kQkvTerms bf16 terms per activation (the K/V are rounded to the cache's bf16)
     gemm(Yf, m->w_qkv[l], D.g_qkv, GemmRole::kQkv, VIA_KERNEL_QKV);
     qa.layer_slot = (int)si;
     launch_qkv_finish(bf, qa, s);
@@ -439,7 +439,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     }
     gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
     if (si + 1 < route.size())
-      launch_resid_add(bf, 3, X, part, ks(D.g_down), M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
+      launch_resid_add(bf, kQkvTerms, X, part, ks(D.g_down), M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
                        ss_stride, s, save_prefix && (int)si + 1 == n_shared ? (float*)(ws + L.xstate) : nullptr,
                        nullptr, d_rows);
   }
