@@ -82,6 +82,7 @@ struct Plan {
   std::vector<AttnItem> items;
   std::vector<LmRow> lm;
   std::vector<PrefixXfer> xfer;  // forwards that start after the shared layers
+  std::vector<char> extra;       // bytes uploaded with the plan (the decision's step data)
 };
 // Plan of a verify forward of `cache` over the batch entries `run` of w: the
 // full cache's lag rows (raw->n_lag / lag_tok, which must equal the cache's

@@ -172,6 +172,10 @@ struct via_kv {
   WinCopy win;
   bool xpref_ok = false;      // the open step's slim forward saved its rows' states after the shared layers
   int last_full_start = -1;   // route index the last full forward started at (-1: none in this step)
+  // device copy of the open step's decision inputs uploaded with the slim
+  // forward's plan (greedy rule, before the full verifier ran), or null
+  char* extra_dev = nullptr;
+  const char* staged_step = nullptr;
   std::vector<int> step_n;  // committed length n per batch entry at step start
   bool sticky = false;
   // device address of the last decision's pinned host mirror (null: copy it)
@@ -297,17 +301,22 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   const size_t o_xfer = al(o_lm + P.lm.size() * sizeof(LmRow));
   const size_t plan_used = al(o_xfer + P.xfer.size() * sizeof(PrefixXfer));
   if (plan_used > L.plan_bytes) return fail(VIA_EINVAL, "plan of %zu bytes exceeds its region", plan_used);
-  std::vector<char> blob(plan_used);
+  // extra bytes ride in the same copy when the plan region has room for them
+  const bool extra = !P.extra.empty() && plan_used + P.extra.size() <= L.plan_bytes;
+  std::vector<char> blob(plan_used + (extra ? P.extra.size() : 0));
   put(blob, o_rows, P.rows);
   put(blob, o_seqs, P.seqs);
   put(blob, o_btab, P.btab);
   put(blob, o_items, P.items);
   put(blob, o_lm, P.lm);
   put(blob, o_xfer, P.xfer);
+  if (extra) memcpy(blob.data() + plan_used, P.extra.data(), P.extra.size());
   char* ws = kv->ws;
   char* plan = ws + L.rows;
-  via_status st = upload(kv, plan, blob.data(), plan_used, s);
+  via_status st = upload(kv, plan, blob.data(), blob.size(), s);
   if (st) return st;
+  kv->extra_dev = extra ? plan + plan_used : nullptr;
+  if (!extra) kv->staged_step = nullptr;  // this plan overwrote any staged decision inputs
 
   const bool bf = m->bf16;
   const RowInfo* d_rows = (const RowInfo*)(plan + o_rows);
@@ -475,6 +484,28 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   return hip_check(kv, hipGetLastError(), "kernel launch");
 }
 
+// The decision's per-step inputs in the step region's layout: a StepSeq per
+// batch entry (committed length n, drafts, whether the full verifier ran),
+// the draft tokens, rows and parents, and the sampling uniforms when given.
+std::vector<char> step_blob(const via_kv* kv, const WinCopy& w, const std::vector<int>& step_n,
+                            const float* uniforms) {
+  const Layout& L = kv->L;
+  const int B = w.batch, Dd = std::max(1, w.max_drafts);
+  std::vector<char> blob(uniforms ? L.step_bytes : L.du - L.step_seqs);
+  std::vector<StepSeq> ss(B);
+  for (int b = 0; b < B; ++b) {
+    ss[b].n = step_n[b];
+    ss[b].n_drafts = w.n_drafts[b];
+    ss[b].full_ran = kv->bk.seqs[w.seq[b]].full_ran ? 1 : 0;
+  }
+  memcpy(blob.data(), ss.data(), B * sizeof(StepSeq));
+  memcpy(blob.data() + (L.dtok - L.step_seqs), w.draft_tok.data(), (size_t)B * Dd * 4);
+  memcpy(blob.data() + (L.drow - L.step_seqs), w.draft_row.data(), (size_t)B * Dd * 4);
+  memcpy(blob.data() + (L.dpar - L.step_seqs), w.draft_parent.data(), (size_t)B * Dd * 4);
+  if (uniforms) memcpy(blob.data() + (L.du - L.step_seqs), uniforms, (size_t)B * Dd * 3 * 4);
+  return blob;
+}
+
 via_status check_params(const via_tier_params* p) {
   if (!p) return fail(VIA_EINVAL, "null tier params");
   if (!(p->temperature > 0.f) || !std::isfinite(p->temperature)) return fail(VIA_EINVAL, "temperature must be > 0");
@@ -531,6 +562,13 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
   int start_si = 0;
   if (!probe && cache == VIA_CACHE_FULL && kv->xpref_ok && n_shared > 0 && build_prefix_xfer(kv->bk, *wp, run, P))
     start_si = n_shared;
+  // the first decision of the step reads its inputs from the slim forward's
+  // plan upload (one host-to-device copy fewer between the forward and it)
+  if (!probe && cache == VIA_CACHE_SLIM) {
+    std::vector<int> n0(w.batch);
+    for (int b = 0; b < w.batch; ++b) n0[b] = kv->bk.seqs[w.seq[b]].valid[VIA_CACHE_SLIM] + 1;
+    P.extra = step_blob(kv, w, n0, nullptr);
+  }
   st = exec_forward(m, kv, cache, P, true, out, 1.0f / p->temperature, s, start_si, save);
   if (probe) {
     book_release_taken(kv->bk, cache, taken);
@@ -541,6 +579,7 @@ via_status verify_impl(via_model* m, via_kv* kv, int cache, const via_window* wi
     return st;
   }
   if (cache == VIA_CACHE_SLIM) {
+    kv->staged_step = kv->extra_dev;
     kv->xpref_ok = save;
     kv->last_full_start = -1;
     note_slim_forward(kv->bk, w, run, save);
@@ -952,18 +991,6 @@ via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_ou
   const Layout& L = kv->L;
   hipStream_t s = (hipStream_t)stream;
   const int B = w.batch, Dd = std::max(1, w.max_drafts);
-  // step region: per-sequence state + draft arrays
-  std::vector<char> blob(L.step_bytes);
-  std::vector<StepSeq> ss(B);
-  for (int b = 0; b < B; ++b) {
-    ss[b].n = kv->step_n[b];
-    ss[b].n_drafts = w.n_drafts[b];
-    ss[b].full_ran = kv->bk.seqs[w.seq[b]].full_ran ? 1 : 0;
-  }
-  memcpy(blob.data(), ss.data(), B * sizeof(StepSeq));
-  memcpy(blob.data() + (L.dtok - L.step_seqs), w.draft_tok.data(), (size_t)B * Dd * 4);
-  memcpy(blob.data() + (L.drow - L.step_seqs), w.draft_row.data(), (size_t)B * Dd * 4);
-  memcpy(blob.data() + (L.dpar - L.step_seqs), w.draft_parent.data(), (size_t)B * Dd * 4);
   if (smp) {
     if (w.tree) return fail(VIA_EUNSUPPORTED, "sampling rules take chain drafts");
     // the residual of Eq. A.3 is defined for beta >= 1 - alpha (App. A)
@@ -974,17 +1001,25 @@ via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_ou
     if (!slim->logits || (full && !full->logits)) return fail(VIA_EINVAL, "sampling needs the logits outputs");
     for (size_t i = 0; i < (size_t)B * Dd * 3; ++i)
       if (!(smp->uniforms[i] >= 0.f && smp->uniforms[i] < 1.f)) return fail(VIA_EINVAL, "uniforms must lie in [0, 1)");
-    memcpy(blob.data() + (L.du - L.step_seqs), smp->uniforms, (size_t)B * Dd * 3 * 4);
   }
-  if ((st = upload(kv, kv->ws + L.step_seqs, blob.data(), L.step_bytes, s))) return st;
+  // step region: per-sequence state + draft arrays (+ uniforms).  The
+  // greedy decision after the slim forward finds them in that forward's
+  // plan upload; otherwise (sampling rules, or after the full verifier ran)
+  // they are uploaded here.
+  const char* base = kv->staged_step;
+  if (smp || full || !base) {
+    std::vector<char> blob = step_blob(kv, w, kv->step_n, smp ? smp->uniforms : nullptr);
+    if ((st = upload(kv, kv->ws + L.step_seqs, blob.data(), blob.size(), s))) return st;
+    base = kv->ws + L.step_seqs;
+  }
   DecideArgs a{};
-  a.seqs = (const StepSeq*)(kv->ws + L.step_seqs);
+  a.seqs = (const StepSeq*)base;
   a.batch = B;
   a.max_rows = w.max_rows;
   a.max_drafts = Dd;
-  a.draft_tok = (const int32_t*)(kv->ws + L.dtok);
-  a.draft_row = (const int32_t*)(kv->ws + L.drow);
-  a.draft_parent = (const int32_t*)(kv->ws + L.dpar);
+  a.draft_tok = (const int32_t*)(base + (L.dtok - L.step_seqs));
+  a.draft_row = (const int32_t*)(base + (L.drow - L.step_seqs));
+  a.draft_parent = (const int32_t*)(base + (L.dpar - L.step_seqs));
   a.s_row_max = slim->row_max;
   a.s_row_argmax = slim->row_argmax;
   a.s_draft_logit = slim->draft_logit;
@@ -1002,7 +1037,7 @@ via_status decide_impl(via_kv* kv, const via_tier_params* p, const via_verify_ou
   a.packed = dec->packed;
   if (smp) {
     a.draft_probs = smp->draft_probs;
-    a.u = (const float*)(kv->ws + L.du);
+    a.u = (const float*)(base + (L.du - L.step_seqs));
     a.s_logits = slim->logits;
     a.s_row_sumexp = slim->row_sumexp;
     if (full) {
@@ -1213,6 +1248,7 @@ via_status via_kv_commit_rollback(via_kv* kv, const via_decision* dec, void* str
   apply_commit(kv->bk, w, hp);
   kv->step_open = false;
   kv->xpref_ok = false;
+  kv->staged_step = nullptr;
   return VIA_OK;
 }
 
