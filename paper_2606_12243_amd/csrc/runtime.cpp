@@ -487,6 +487,9 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
 // The decision's per-step inputs in the step region's layout: a StepSeq per
 // batch entry (committed length n, drafts, whether the full verifier ran),
 // the draft tokens, rows and parents, and the sampling uniforms when given.
+// Between steps every full_ran flag is false (the commit clears them), so
+// the copy staged with a step's slim forward carries 0, which is what the
+// decision after that forward needs.
 std::vector<char> step_blob(const via_kv* kv, const WinCopy& w, const std::vector<int>& step_n,
                             const float* uniforms) {
   const Layout& L = kv->L;
