@@ -944,15 +944,26 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int row
 // round-robin over the 8 XCDs; XCD x takes a contiguous range of tiles, taken
 // in groups of 8 row tiles so that co-resident work-groups share operand
 // blocks in its L2.
+//
+// SWIGLU (the gate/up projection): instead of the fp32 product the tile's
+// epilogue writes h = silu(g s) * (u s) with the input row's RMSNorm scale
+// s, as 2-term fragments of the down projection's input.  A 16-column block
+// of the packed gate/up weight holds the gate (columns 0-7) and up (8-15)
+// rows of the same 8 FFN indices, so lane n < 8 of an output block takes its
+// up value from lane n + 8; h of the tile's 128 FFN indices is staged in LDS
+// (the freed operand stages) and written 8 indices per fragment group.
 constexpr int kPfBM = 256, kPfBN = 256, kPfStages = 4, kPfStage = 32 * 1024;
 constexpr int kPfGroupM = 8;
+constexpr int kPfHStride = kPfBN / 2 + 4;  // fp32 per staged h row (padded: no bank conflicts)
+constexpr int kPfLds = kPfStages * kPfStage > kPfBM * kPfHStride * 4 ? kPfStages * kPfStage : kPfBM * kPfHStride * 4;
 
 __device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
 }
 
+template <bool SWIGLU>
 __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) {
-  __shared__ __align__(1024) unsigned char smem[kPfStages * kPfStage];
+  __shared__ __align__(1024) unsigned char smem[SWIGLU ? kPfLds : kPfStages * kPfStage];
   const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
   const int tiles_n = (a.N + kPfBN - 1) / kPfBN, tiles_m = (a.M + kPfBM - 1) / kPfBM;
   const int ntiles = tiles_m * tiles_n;
@@ -991,6 +1002,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < kPfStages - 1; ++p) issue(min(p, iters - 1));
+  // SwiGLU: the RMSNorm scales of the tile's input rows, read while the
+  // first stages are in flight (the compiler's wait for these loads also
+  // covers the copies, which the first iteration waits for anyway)
+  __shared__ float rscale[SWIGLU ? kPfBM : 1];
+  if constexpr (SWIGLU)
+    for (int r = threadIdx.x; r < kPfBM; r += kThreads)
+      rscale[r] = m0 + r < a.M ? row_scale(a.ss, a.ss_stride, m0 + r, a.K, a.eps) : 0.f;
   for (int it = 0; it < iters; ++it) {
     // this wave's copies of stage `it` are the oldest 4 of its 4 * (stages - 1)
     // outstanding ones; its LDS reads of stage it - 1 are complete.  After the
@@ -1014,46 +1032,62 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
   }
   __builtin_amdgcn_s_waitcnt(0);  // the trailing copies land before the work-group ends
   const int n = lane & 15, g = lane >> 4;
+  if constexpr (SWIGLU) {
+    __syncthreads();  // every wave's copies have landed and its stage reads are done
+    float* hl = (float*)smem;  // [row][FFN index of the tile]
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = n0 + wn * 64 + j * 16 + n;
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * 128 + i * 16 + g * 4 + r;
-        if (row < a.M && col < a.N) a.part[(size_t)row * a.N + col] = acc[i][j][r];
-      }
+        for (int r = 0; r < 4; ++r) {
+          const float up = __shfl_xor(acc[i][j][r], 8, 64);
+          const int rl = wm * 128 + i * 16 + g * 4 + r;
+          if (n < 8) {
+            const float sc = rscale[rl], gt = acc[i][j][r] * sc, u = up * sc;
+            hl[rl * kPfHStride + wn * 32 + j * 8 + n] = gt / (1.0f + expf(-gt)) * u;
+          }
+        }
+    __syncthreads();
+    // consecutive lanes take consecutive rows of one 8-index group: 16 of
+    // them write 256 contiguous bytes of a fragment term
+    const int f0 = n0 >> 1;
+    for (int e = threadIdx.x; e < kPfBM * (kPfBN / 16); e += kThreads) {
+      const int rl = e % kPfBM, gq = e / kPfBM, m = m0 + rl, f = f0 + gq * 8;
+      if (m >= a.M || f >= a.F) continue;
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = hl[rl * kPfHStride + gq * 8 + t];
+      put_afrag<true, 2>(a.H, m, f, v, a.F >> 5, a.MBn);
     }
-}
-
-// SwiGLU over a prefill gate/up product P[M, 2F] whose columns interleave
-// gate and up by 8 (the packed gate/up order): h = silu(g s) * (u s) with the
-// input row's RMSNorm scale s, written as 2-term fragments.  One thread per
-// (row, 8-f group).
-__global__ __launch_bounds__(256) void swiglu_rows_kernel(GemmArgs a) {
-  const int groups = a.F >> 3;
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= a.M * groups) return;
-  const int m = e / groups, j = e - m * groups;
-  const float* t = a.part + (size_t)m * a.N + j * 16;
-  const float sc = row_scale(a.ss, a.ss_stride, m, a.K, a.eps);
-  float v[8];
+  } else {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const float gt = t[i] * sc, up = t[8 + i] * sc;
-    v[i] = gt / (1.0f + expf(-gt)) * up;
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = n0 + wn * 64 + j * 16 + n;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + wm * 128 + i * 16 + g * 4 + r;
+          if (row < a.M && col < a.N) a.part[(size_t)row * a.N + col] = acc[i][j][r];
+        }
+      }
   }
-  put_afrag<true, 2>(a.H, m, j * 8, v, a.F >> 5, a.MBn);
 }
 
-void launch_prefill(const GemmArgs& a, int nt, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+void launch_prefill(const GemmArgs& a, int nt, bool swiglu, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const int ntiles = ((a.M + kPfBM - 1) / kPfBM) * ((a.N + kPfBN - 1) / kPfBN);
   const dim3 grid((ntiles + 7) / 8 * 8);
-  if (e0)
-    hipExtLaunchKernelGGL(gemm_prefill, grid, dim3(kThreads), 0, s, e0, e1, 0, a, nt);
+  auto go = [&](auto kernel) {
+    if (e0)
+      hipExtLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, e0, e1, 0, a, nt);
+    else
+      hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a, nt);
+  };
+  if (swiglu)
+    go(gemm_prefill<true>);
   else
-    hipLaunchKernelGGL(gemm_prefill, grid, dim3(kThreads), 0, s, a, nt);
+    go(gemm_prefill<false>);
 }
 
 }  // namespace
@@ -1103,13 +1137,10 @@ bool gemm_is_prefill(bool bf16, int M) { return bf16 && M > kPrefillMinRows; }
 
 void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (role != GemmRole::kHead && gemm_is_prefill(bf16, a.M)) {
-    // many rows: the compute-bound tile kernel (one partial, ksplit 1)
+    // many rows: the compute-bound tile kernel (one partial, ksplit 1; the
+    // gate/up projection writes h itself)
     const int nt = role == GemmRole::kQkv ? kQkvTerms : 2;
-    launch_prefill(a, nt, s, e0, e1);
-    if (role == GemmRole::kGateUp) {
-      const int n = a.M * (a.F >> 3);
-      hipLaunchKernelGGL(swiglu_rows_kernel, dim3((n + 255) / 256), dim3(256), 0, s, a);
-    }
+    launch_prefill(a, nt, role == GemmRole::kGateUp, s, e0, e1);
     return;
   }
   if (bf16 && a.nb > 0 && gemm_uses_ki(role, a.M, a.N)) {
@@ -1125,7 +1156,7 @@ void launch_gemm(bool bf16, GemmRole role, const GemmArgs& a, hipStream_t s, hip
     launch_role<float>(role, a, s, e0, e1);
 }
 
-void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) { launch_prefill(a, 1, s, nullptr, nullptr); }
+void launch_gemm_bf16(const GemmArgs& a, hipStream_t s) { launch_prefill(a, 1, false, s, nullptr, nullptr); }
 
 void launch_lm_finalize(const LmRow* lm, const float* lm_part, int n_lm, int ntiles, float inv_T, int32_t* row_argmax,
                         float* row_max, float* row_sumexp, float* row_gap, hipStream_t s) {

@@ -106,9 +106,10 @@ Layout layout_of(const via_model_desc* desc, int max_rows, int max_batch, int ma
   L.Hf = take(Rp * D.F * f2);
   L.Ylf = take(Rp * D.d * f2);
   // split-K partials of forwards of up to kPrefillMinRows rows; longer
-  // (prefill-sized) forwards write one partial of all their rows
+  // (prefill-sized) forwards write one partial of all their rows.  The
+  // gate/up kernels write h directly and need none.
   size_t part = 0;
-  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_gu, D.g_down}) {
+  for (const GemmShape& g : {D.g_qkv, D.g_o, D.g_down}) {
     part = std::max(part, (size_t)std::max(g.ks, g.ks_ki) * std::min<size_t>(R, kPrefillMinRows) * g.N * 4);
     if (gemm_is_prefill(es == 2, (int)R)) part = std::max(part, R * g.N * 4);
   }
@@ -437,7 +438,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
       g.K = D.d;
       g.N = 2 * D.F;
       g.ksplit = 1;
-      g.part = part;  // the prefill GEMM's gate/up product (consumed by its SwiGLU pass)
+      g.part = part;
       g.H = Hf;
       g.F = D.F;
       g.nb = gate_up_blocks_per_group(D.F);

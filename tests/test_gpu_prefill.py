@@ -6,8 +6,8 @@ of a forward of more than 512 rows.
   products, |err| <= K * 2^-24 * (|X| |W|^T); shapes cover one row, ragged
   M/N tails of the 256 x 256 tiles, K of one stage, and full prefill sizes.
 * A prefill-sized forward (prompts of 600 and 514 tokens, so the prefill GEMM
-  with its 2-term activations and the separate SwiGLU pass builds the
-  caches), followed by lock-step decoding against the oracle.
+  with its 2-term activations, and the SwiGLU epilogue of its gate/up tiles,
+  builds the caches), followed by lock-step decoding against the oracle.
 """
 import ctypes as C
 
