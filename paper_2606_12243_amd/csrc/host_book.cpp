@@ -160,10 +160,22 @@ via_status copy_window(const KvBook& bk, const via_window* w, int vocab, int max
   return VIA_OK;
 }
 
+// One item per kAttnQueries queries of the sequence.  An item streams keys
+// up to the last one any of its rows sees (its causal prefix and tree-mask
+// bits), not the whole sequence: the items of a long prefill then read
+// about half the keys, and a block no row sees would add exactly nothing.
 static void push_items(Plan& P, const SeqInfo& si, int G) {
   const int nq = si.n_rows * G;
-  for (int q0 = 0; q0 < nq; q0 += kAttnQueries)
-    P.items.push_back(AttnItem{q0, 0, si.kv_len, si.row_start, si.n_rows, si.win_base, si.bt, si.n_blocks});
+  for (int q0 = 0; q0 < nq; q0 += kAttnQueries) {
+    int kv = 1;
+    const int r1 = std::min(si.n_rows, (q0 + kAttnQueries + G - 1) / G);
+    for (int rl = q0 / G; rl < r1; ++rl) {
+      const RowInfo& r = P.rows[si.row_start + rl];
+      kv = std::max(kv, r.vis_len);
+      if (r.mask) kv = std::max(kv, si.win_base + 64 - __builtin_clzll(r.mask));
+    }
+    P.items.push_back(AttnItem{q0, 0, std::min(kv, si.kv_len), si.row_start, si.n_rows, si.win_base, si.bt, si.n_blocks});
+  }
 }
 
 via_status build_verify_plan(KvBook& bk, int cache, const WinCopy& w, const std::vector<int>& run,

@@ -253,6 +253,39 @@ static void test_plans() {
   Plan Q;
   build_prefill_plan(bk.seqs[0], VIA_CACHE_FULL, toks.data(), 16, 20, 4, Q);
   CHECK(Q.rows.size() == 4 && Q.rows[0].slot == 16 && Q.rows[0].vis_len == 17 && Q.seqs[0].kv_len == 20);
+  // attention items stop at the last key their rows see: rows [0, 20) of a
+  // prompt with G = 4 queries per row make items of rows 0-7, 8-15 and 16-19
+  CHECK(Q.items.size() == 1 && Q.items[0].kv_len == 20);
+  Plan Q2;
+  build_prefill_plan(bk.seqs[0], VIA_CACHE_FULL, toks.data(), 0, 20, 4, Q2);
+  CHECK(Q2.items.size() == 3 && Q2.items[0].kv_len == 8 && Q2.items[1].kv_len == 16 && Q2.items[2].kv_len == 20);
+  // a 10-row tree window shaped as a chain: the first item's rows see the
+  // committed prefix and, through their mask bits, window slots up to row 7
+  {
+    KvBook tb;
+    book_init(tb, 1, 8, 16, 16);
+    attach(tb, 0, 30);
+    Win t;
+    t.seq = {0};
+    t.n_rows = {10};
+    t.n_drafts = {10};
+    for (int i = 0; i < 10; ++i) {
+      t.row_tok.push_back(i == 0 ? 5 : 10 + i - 1);
+      t.row_depth.push_back(i);
+      t.row_mask.push_back((2ull << i) - 1);
+      t.draft_tok.push_back(10 + i);
+      t.draft_row.push_back(i);
+      t.draft_parent.push_back(i - 1);
+    }
+    t.finish(10, 10, 1, true);
+    WinCopy tc;
+    CHECK(copy_window(tb, &t.w, V, 1, 10, tc) == VIA_OK);
+    Plan T;
+    CHECK(build_verify_plan(tb, VIA_CACHE_SLIM, tc, {0}, &t.w, true, V, 4, T, nullptr) == VIA_OK);
+    const int base = T.seqs[0].win_base;
+    CHECK(T.items.size() == 2 && T.items[0].kv_len == base + 8 && T.items[1].kv_len == T.seqs[0].kv_len);
+    CHECK(T.seqs[0].kv_len == base + 10 && T.rows[7].vis_len <= base + 8);
+  }
 }
 
 // Decision block for B sequences, max_drafts D.
