@@ -142,46 +142,14 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
   put_afrag<BF16, NT>(Y, out, k0, v, d >> 5, MBn);
 }
 
-// QKV partial sums -> RMSNorm scale of the input row -> rotate-half RoPE at
-// the row's position -> Q (bf16 hi/lo terms, or fp32) and paged K/V (model
-// dtype).  A work-group of 256 threads takes four (row, head of Q, K or V)
-// pairs, 64 threads each; thread j owns the rotation pair (j, j + hd/2) and
-// its angle pos * theta^(-2j/hd), computed in fp64 while the loads of the
-// pair's KS split partials (all in flight at once, summed in split order)
-// are outstanding.  KS = 0: the split count is taken from the arguments.
-template <typename T, int KS>
-__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
-  const int m = blockIdx.x, hh = blockIdx.y * 4 + (threadIdx.x >> 6), j = threadIdx.x & 63;
+// Rotate-half RoPE of the pair (j, j + hd/2) of head hh of row m (Q and K
+// heads; V passes through) with the angle's cosine and sine, then the store:
+// Q as bf16 hi/lo terms (fp32 models: fp32), K and V into the row's paged
+// cache slot in the model dtype.
+template <typename T>
+__device__ __forceinline__ void qkv_store(const QkvArgs& a, const RowInfo& ri, int m, int hh, int j, float x1,
+                                          float x2, double cs, double sn) {
   const int half = a.hd >> 1;
-  if (j >= half || hh >= a.H + 2 * a.KVH) return;
-  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
-  const size_t c = (size_t)m * N + (size_t)hh * a.hd + j;
-  float x1 = 0.f, x2 = 0.f;
-  double cs = 1.0, sn = 0.0;
-  const RowInfo ri = a.rows[m];
-  if constexpr (KS > 0) {
-    float v1[KS], v2[KS];
-#pragma unroll
-    for (int q = 0; q < KS; ++q) {
-      v1[q] = a.P[(size_t)q * stride + c];
-      v2[q] = a.P[(size_t)q * stride + c + half];
-    }
-    if (hh < a.H + a.KVH) sincos((double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), &sn, &cs);
-#pragma unroll
-    for (int q = 0; q < KS; ++q) {
-      x1 += v1[q];
-      x2 += v2[q];
-    }
-  } else {
-    if (hh < a.H + a.KVH) sincos((double)ri.pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), &sn, &cs);
-    for (int q = 0; q < a.ksplit; ++q) {
-      x1 += a.P[(size_t)q * stride + c];
-      x2 += a.P[(size_t)q * stride + c + half];
-    }
-  }
-  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);  // RMSNorm of the input row
-  x1 *= sc;
-  x2 *= sc;
   float y1 = x1, y2 = x2;
   if (hh < a.H + a.KVH) {
     y1 = (float)((double)x1 * cs - (double)x2 * sn);
@@ -213,6 +181,80 @@ __global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
     const int gv = hh - a.H - a.KVH;
     pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, j)] = from_f<T>(y1);
     pool[v_off(a.layer_slot, blk, a.pool_blocks, a.KVH, a.hd, gv, t, j + half)] = from_f<T>(y2);
+  }
+}
+
+// The rotation angle of pair j at position pos, pos * theta^(-2j/hd), in fp64.
+__device__ __forceinline__ void rope_angle(int pos, int j, const QkvArgs& a, double* sn, double* cs) {
+  sincos((double)pos * pow((double)a.theta, -2.0 * (double)j / (double)a.hd), sn, cs);
+}
+
+// QKV partial sums -> RMSNorm scale of the input row -> rotate-half RoPE at
+// the row's position -> Q (bf16 hi/lo terms, or fp32) and paged K/V (model
+// dtype).  A work-group of 256 threads takes four (row, head of Q, K or V)
+// pairs, 64 threads each; thread j owns the rotation pair (j, j + hd/2) and
+// its angle pos * theta^(-2j/hd), computed in fp64 while the loads of the
+// pair's KS split partials (all in flight at once, summed in split order)
+// are outstanding.  KS = 0: the split count is taken from the arguments.
+template <typename T, int KS>
+__global__ __launch_bounds__(256) void qkv_finish_kernel(QkvArgs a) {
+  const int m = blockIdx.x, hh = blockIdx.y * 4 + (threadIdx.x >> 6), j = threadIdx.x & 63;
+  const int half = a.hd >> 1;
+  if (j >= half || hh >= a.H + 2 * a.KVH) return;
+  const size_t N = (size_t)(a.H + 2 * a.KVH) * a.hd, stride = (size_t)a.M * N;
+  const size_t c = (size_t)m * N + (size_t)hh * a.hd + j;
+  float x1 = 0.f, x2 = 0.f;
+  double cs = 1.0, sn = 0.0;
+  const RowInfo ri = a.rows[m];
+  if constexpr (KS > 0) {
+    float v1[KS], v2[KS];
+#pragma unroll
+    for (int q = 0; q < KS; ++q) {
+      v1[q] = a.P[(size_t)q * stride + c];
+      v2[q] = a.P[(size_t)q * stride + c + half];
+    }
+    if (hh < a.H + a.KVH) rope_angle(ri.pos, j, a, &sn, &cs);
+#pragma unroll
+    for (int q = 0; q < KS; ++q) {
+      x1 += v1[q];
+      x2 += v2[q];
+    }
+  } else {
+    if (hh < a.H + a.KVH) rope_angle(ri.pos, j, a, &sn, &cs);
+    for (int q = 0; q < a.ksplit; ++q) {
+      x1 += a.P[(size_t)q * stride + c];
+      x2 += a.P[(size_t)q * stride + c + half];
+    }
+  }
+  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);  // RMSNorm of the input row
+  qkv_store<T>(a, ri, m, hh, j, x1 * sc, x2 * sc, cs, sn);
+}
+
+// The same for many-row forwards (prefill): one work-group per row.  The
+// row's hd/2 angles are computed once and shared through LDS by all its Q and
+// K heads (the per-pair form recomputes each one H + KVH times, which makes
+// the fp64 transcendentals the cost at thousands of rows); consecutive
+// threads then take consecutive pairs of the row's heads.  Same arithmetic,
+// same results.
+template <typename T>
+__global__ __launch_bounds__(256) void qkv_finish_rows_kernel(QkvArgs a) {
+  __shared__ double s_cs[64], s_sn[64];  // hd <= 128
+  const int m = blockIdx.x, half = a.hd >> 1;
+  const RowInfo ri = a.rows[m];
+  for (int j = threadIdx.x; j < half; j += 256) rope_angle(ri.pos, j, a, &s_sn[j], &s_cs[j]);
+  const float sc = row_scale(a.ss, a.ss_stride, m, a.d, a.eps);  // RMSNorm of the input row
+  __syncthreads();
+  const int nh = a.H + 2 * a.KVH;
+  const size_t N = (size_t)nh * a.hd, stride = (size_t)a.M * N;
+  for (int e = threadIdx.x; e < nh * half; e += 256) {
+    const int hh = e / half, j = e - hh * half;
+    const size_t c = (size_t)m * N + (size_t)hh * a.hd + j;
+    float x1 = 0.f, x2 = 0.f;
+    for (int q = 0; q < a.ksplit; ++q) {
+      x1 += a.P[(size_t)q * stride + c];
+      x2 += a.P[(size_t)q * stride + c + half];
+    }
+    qkv_store<T>(a, ri, m, hh, j, x1 * sc, x2 * sc, s_cs[j], s_sn[j]);
   }
 }
 
@@ -424,6 +466,13 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
 }
 
 void launch_qkv_finish(bool bf16, const QkvArgs& a, hipStream_t s) {
+  if (a.M > kPrefillMinRows && a.hd <= 128) {  // many rows: angles shared per row
+    if (bf16)
+      hipLaunchKernelGGL(qkv_finish_rows_kernel<uint16_t>, dim3(a.M), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(qkv_finish_rows_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
+    return;
+  }
   const dim3 grid(a.M, (a.H + 2 * a.KVH + 3) / 4);
   auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(256), 0, s, a); };
   if (bf16) {
