@@ -179,6 +179,7 @@ struct via_kv {
   const char* staged_step = nullptr;
   std::vector<int> step_n;  // committed length n per batch entry at step start
   bool sticky = false;
+  int n_cu = 256;  // compute units of the device (attention work-groups of one round)
   // device address of the last decision's pinned host mirror (null: copy it)
   const int32_t* h_packed_host = nullptr;
   int32_t* h_packed_dev = nullptr;
@@ -290,7 +291,7 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   if ((int)P.items.size() > L.max_items) return fail(VIA_EINVAL, "too many attention tiles");
   // key splits of the attention items: about one work-group per compute unit
   AttnArgs at{};
-  if (plan_attention(P.items.data(), (int)P.items.size(), D.KVH, L.max_chunks, kAttnTargetGroups, at))
+  if (plan_attention(P.items.data(), (int)P.items.size(), D.KVH, L.max_chunks, kAttnTargetGroups, kv->n_cu, at))
     return fail(VIA_EINVAL, "a sequence is too long for %d attention splits", L.max_chunks);
   // one upload of the plan: its parts packed back to back (256-byte aligned)
   // at the start of the plan region, which has room for the largest plan
@@ -778,6 +779,13 @@ via_status via_kv_create(via_model* m, const via_kv_desc* d, via_kv** out) {
   kv->stage = (char*)d->pinned_staging;
   kv->slot_bytes = slot;
   book_init(kv->bk, d->max_seqs, d->max_blocks_per_seq, d->blocks_full, d->blocks_slim);
+  {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      kv->n_cu = n;
+    (void)hipGetLastError();
+  }
   for (int r = 0; r < kRing; ++r) {
     kv->ev_used[r] = false;
     if (hipEventCreateWithFlags(&kv->ev[r], hipEventDisableTiming) != hipSuccess) {
