@@ -434,53 +434,4 @@ void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {
   }
 }
 
-int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int target_groups, int max_groups,
-                   AttnArgs& at) {
-  long long blocks = 0;
-  int max_kv = 0;
-  for (int i = 0; i < n_items; ++i) {
-    blocks += (long long)KVH * ((items[i].kv_len + 31) / 32);
-    max_kv = std::max(max_kv, items[i].kv_len);
-  }
-  long long per = std::max<long long>(1, (blocks + target_groups - 1) / target_groups);
-  int span = (int)std::min<long long>(per * 32, kAttnMaxSpan);
-  // a forward whose spans would run well past kAttnPrefSpan keys (long
-  // contexts with several query items per sequence) takes more work-groups
-  if (span > kAttnPrefSpan * 3 / 2) span = kAttnPrefSpan;
-  const int need = ((max_kv + 31) / 32 + max_splits - 1) / max_splits * 32;  // at most max_splits splits
-  span = std::max(span, need);
-  if (span > kAttnMaxSpan) return -1;
-  // One round: when these spans leave more work-groups than the GPU has
-  // compute units (ragged lengths round up to an extra split; a second
-  // work-group on a compute unit halves the bandwidth of both) and one split
-  // per item would fit, widen the span to the smallest multiple of 32 that
-  // fits, up to the preferred cap.
-  auto groups = [&](int sp) {
-    long long g = 0;
-    for (int i = 0; i < n_items; ++i) g += (long long)KVH * ((items[i].kv_len + sp - 1) / sp);
-    return g;
-  };
-  const int cap = kAttnPrefSpan * 3 / 2;
-  if (span < cap && (long long)n_items * KVH <= max_groups && groups(span) > max_groups) {
-    int lo = span, hi = std::min(cap, (max_kv + 31) / 32 * 32);
-    if (hi > lo && groups(hi) <= max_groups) {
-      while (hi - lo > 32) {  // groups(lo) > max_groups >= groups(hi)
-        const int mid = (lo + hi) / 64 * 32;
-        if (groups(mid) <= max_groups)
-          hi = mid;
-        else
-          lo = mid;
-      }
-      span = hi;
-    }
-  }
-  at.span = span;
-  at.max_chunks = 0;
-  for (int i = 0; i < n_items; ++i) {
-    items[i].n_chunks = (items[i].kv_len + span - 1) / span;
-    at.max_chunks = std::max(at.max_chunks, items[i].n_chunks);
-  }
-  return 0;
-}
-
 }  // namespace via

@@ -129,6 +129,15 @@ via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int
 // compaction moves cache slots, the state ring is not moved).
 void apply_commit(KvBook& bk, const WinCopy& w, const int32_t* hp);
 
+// The key-split span of a forward's attention items: about target_groups
+// work-groups over all items and KV heads, at most max_splits splits per
+// sequence, spans capped near kAttnPrefSpan, and widened so that the
+// work-groups fit one round of max_groups (the device's compute units) when
+// one split per item would.  Sets every item's n_chunks, *span_out and
+// *max_chunks_out; returns -1 if a sequence needs a span above kAttnMaxSpan.
+int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int target_groups, int max_groups,
+                   int* span_out, int* max_chunks_out);
+
 // Draft window of a natively driven step (via_step): rows, draft rows,
 // depths and ancestor masks built from each sequence's committed tokens (the
 // pending token x[n-1] is row 0) and its drafts, plus the lag rows (the

@@ -155,12 +155,6 @@ struct AttnArgs {
   int MBn;
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
-// Host: pick the split span for a forward's attention items (about
-// target_groups work-groups over all items and KV heads, at most max_splits
-// splits per sequence), set every item's n_chunks and at.span,
-// at.max_chunks.  Returns -1 if a sequence needs a span above kAttnMaxSpan.
-int plan_attention(AttnItem* items, int n_items, int KVH, int max_splits, int target_groups, int max_groups,
-                   AttnArgs& at);
 
 // Tree compaction: KvMove (plan.h) copies K/V of slot src -> dst for every layer slot.
 void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KVH, int hd,

@@ -291,7 +291,8 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   if ((int)P.items.size() > L.max_items) return fail(VIA_EINVAL, "too many attention tiles");
   // key splits of the attention items: about one work-group per compute unit
   AttnArgs at{};
-  if (plan_attention(P.items.data(), (int)P.items.size(), D.KVH, L.max_chunks, kAttnTargetGroups, kv->n_cu, at))
+  if (plan_attention(P.items.data(), (int)P.items.size(), D.KVH, L.max_chunks, kAttnTargetGroups, kv->n_cu, &at.span,
+                     &at.max_chunks))
     return fail(VIA_EINVAL, "a sequence is too long for %d attention splits", L.max_chunks);
   // one upload of the plan: its parts packed back to back (256-byte aligned)
   // at the start of the plan region, which has room for the largest plan

@@ -667,7 +667,60 @@ static void test_state_ring() {
   }
 }
 
+
+// Attention split spans (plan_attention): the cfg3 shape, the one-round
+// widening of a ragged long batch, the cap it must not undo, the split
+// limit and the error for a sequence too long for any span.
+static void test_attention_plan() {
+  auto items = [](const std::vector<int>& kv) {
+    std::vector<AttnItem> v;
+    for (int k : kv) {
+      AttnItem a{};
+      a.kv_len = k;
+      v.push_back(a);
+    }
+    return v;
+  };
+  auto groups = [](const std::vector<AttnItem>& v, int kvh, int span) {
+    long long g = 0;
+    for (const AttnItem& a : v) g += (long long)kvh * ((a.kv_len + span - 1) / span);
+    return g;
+  };
+  int span = 0, mc = 0;
+  // 4 sequences of 2056 keys, 8 KV heads, about 192 work-groups: 6 splits of 352 keys
+  std::vector<AttnItem> c3 = items({2056, 2056, 2056, 2056});
+  CHECK(plan_attention(c3.data(), 4, 8, 32, 192, 256, &span, &mc) == 0);
+  CHECK(span == 352 && mc == 6 && c3[0].n_chunks == 6 && groups(c3, 8, span) == 192);
+  // 15 sequences of 5000 keys and one of 9100: the target's span (3520) leaves 264 work-groups; the
+  // planner widens it to the narrowest multiple of 32 that fits one round of 256
+  std::vector<int> kv(15, 5000);
+  kv.push_back(9100);
+  std::vector<AttnItem> lg = items(kv);
+  {
+    std::vector<AttnItem> probe = lg;
+    int s0 = 0, m0 = 0;
+    CHECK(plan_attention(probe.data(), 16, 8, 32, 192, 1 << 20, &s0, &m0) == 0);  // no round limit
+    CHECK(groups(probe, 8, s0) > 256);  // the case the widening is for
+  }
+  CHECK(plan_attention(lg.data(), 16, 8, 32, 192, 256, &span, &mc) == 0);
+  CHECK(span % 32 == 0 && span <= 6144 && groups(lg, 8, span) <= 256 && groups(lg, 8, span - 32) > 256);
+  long long n = 0;
+  for (const AttnItem& a : lg) n += 8LL * a.n_chunks;
+  CHECK(n == groups(lg, 8, span) && mc == (kv.back() + span - 1) / span && span == 4576 && mc == 2);
+  // two query items per sequence of 8192 keys: one round cannot hold them below the cap, so the
+  // 4096-key spans stay
+  std::vector<AttnItem> two = items(std::vector<int>(32, 8192));
+  CHECK(plan_attention(two.data(), 32, 8, 32, 192, 256, &span, &mc) == 0 && span == 4096 && mc == 2);
+  // at most max_splits splits per sequence
+  std::vector<AttnItem> one = items({9000});
+  CHECK(plan_attention(one.data(), 1, 8, 2, 192, 256, &span, &mc) == 0 && mc <= 2 && span >= 4500);
+  // a sequence longer than max_splits spans of kAttnMaxSpan keys
+  std::vector<AttnItem> too = items({2 * kAttnMaxSpan + 32});
+  CHECK(plan_attention(too.data(), 1, 8, 2, 192, 256, &span, &mc) == -1);
+}
+
 int main() {
+  test_attention_plan();
   test_step_window_and_tokens();
   test_allocator();
   test_window_validation();
