@@ -34,6 +34,30 @@ def test_small_decode_lockstep(name):
         ls.close()
 
 
+@pytest.mark.parametrize("name", ["micro_f32", "micro_bf16"])
+def test_degenerate_windows_lockstep(name):
+    """Edge cases of the window, in lock-step with the oracle: a sequence whose
+    prompt is one token (nothing cached: its first window attends only to
+    itself), one-row windows (k = 1), window lengths that differ across the
+    batch within a step (1, 3, 8), and a 32-draft window."""
+    cfg = configs.get(name)
+    cfg.update(seed_c=23, seed_d=37, corrupt=0.3, temperature=1.0)
+    print(f"[case] {name} degenerate windows", flush=True)
+    ls = Lockstep(cfg, max_rows=192, max_batch=3, max_drafts=32, max_blocks=16, blocks=96)
+    try:
+        ls.add_prompt(0, gen.context_tokens(cfg, 0, 1))
+        ls.add_prompt(1, gen.context_tokens(cfg, 1, 9))
+        ls.add_prompt(2, gen.context_tokens(cfg, 2, 30))
+        ks = [(1, 3, 8), (8, 1, 3), (3, 8, 1), (1, 1, 1), (32, 2, 5), (2, 32, 1)]
+        for step in range(len(ks)):
+            drafts = {b: ls.drafter.chain(b, ls.ver.seqs[b].tokens, ks[step][b], step) for b in (0, 1, 2)}
+            ls.step(drafts, step)
+        print(f"[done] {name} max_logit_err={ls.max_logit_err:.3g} tiers={sorted(ls.seen_tiers)} "
+              f"resyncs={len(ls.log)}", flush=True)
+    finally:
+        ls.close()
+
+
 def test_tiny_fp32_workload_end_to_end():
     cfg = configs.get("tiny_fp32")
     print("[case] tiny_fp32 G=64", flush=True)
