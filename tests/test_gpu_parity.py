@@ -58,6 +58,29 @@ def test_degenerate_windows_lockstep(name):
         ls.close()
 
 
+def test_largest_windows_lockstep():
+    """Windows at the 64-draft limit, in lock-step with the oracle: a tree of
+    64 drafts (two children of the root, then one child per node) that feeds
+    63 rows through the tree-mask path, next to a 64-draft chain window in the
+    same batch."""
+    cfg = configs.get("micro_bf16")
+    cfg.update(seed_c=29, seed_d=41, corrupt=0.3, temperature=1.0)
+    print("[case] micro_bf16 largest windows", flush=True)
+    ls = Lockstep(cfg, max_rows=320, max_batch=2, max_drafts=64, max_blocks=32, blocks=128)
+    try:
+        ls.add_prompt(0, gen.context_tokens(cfg, 0, 20))
+        ls.add_prompt(1, gen.context_tokens(cfg, 1, 11))
+        for step in range(4):
+            t0, t1 = ls.ver.seqs[0].tokens, ls.ver.seqs[1].tokens
+            tree = ls.drafter.tree(0, t0, [2] + [1] * 62, 2, step)
+            assert len(tree.tok) == 64 and not Lockstep._is_chain(tree)
+            ls.step({0: tree, 1: ls.drafter.chain(1, t1, 64, step)}, step)
+        print(f"[done] largest windows max_logit_err={ls.max_logit_err:.3g} tiers={sorted(ls.seen_tiers)} "
+              f"resyncs={len(ls.log)}", flush=True)
+    finally:
+        ls.close()
+
+
 def test_tiny_fp32_workload_end_to_end():
     cfg = configs.get("tiny_fp32")
     print("[case] tiny_fp32 G=64", flush=True)
