@@ -54,13 +54,17 @@ def models():
 # mixed-tier temperature (the long-context batch's own, and "mixed" for the
 # 8B chain) all three tiers occur, some steps escalate only part of the batch
 # and the full forward of an escalated sequence carries the lag rows its cache
-# missed on earlier steps.  "ends": the shortest- and longest-context sequences.
+# missed on earlier steps; the tree workload (one sequence) at the chain's
+# mixed-tier temperature has all three tiers inside one tree window, so a tree
+# commit follows a full forward.  "ends": the shortest- and longest-context
+# sequences.
 CASES = [
     ("1b_bf16", 8, [0], None),
     ("8b_bf16_chain", 2, [3], None),
     ("8b_bf16_chain", 8, [0, 1, 2, 3], "mixed"),
     ("8b_bf16_chain", 2, [1], 1.0),
     ("8b_bf16_tree", 2, [0], None),
+    ("8b_bf16_tree", 4, [0], "chain_mixed"),
     ("8b_bf16_tree", 2, [0], 1.0),
     ("8b_bf16_long", 3, "ends", None),
 ]
@@ -79,6 +83,8 @@ def test_full_size_sampled_parity(name, steps, sample, temperature, models):
         sample = sorted({min(range(B), key=lambda b: ctx[b]), max(range(B), key=lambda b: ctx[b])})
     if temperature == "mixed":
         temperature = calibrated.MIXED_TEMPERATURE[name]
+    elif temperature == "chain_mixed":  # tree drafts where the chain's mix of tiers occurs
+        temperature = calibrated.MIXED_TEMPERATURE["8b_bf16_chain"]
     tree = cfg["draft"] == "tree"
     k = cfg.get("k", 8)
     # the benchmark's row and block budgets (its default 35 replayed steps)
