@@ -937,10 +937,16 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* src, T* dst, int row
 // stage is one 32-wide K step of the tile: 16 row blocks of X and 16 column
 // blocks of W, each a contiguous 1 KB fragment in both layouts, copied
 // verbatim into LDS by global_load_lds_dwordx4 (16 bytes per lane written at
-// m0 + 16 * lane).  Four stages rotate in LDS, loaded three steps ahead.  The
-// copies are issued by inline asm so that the compiler, which would otherwise
-// make every LDS read wait for all outstanding copies, leaves their
-// completion to the explicit vmcnt waits below.  Work-groups are dispatched
+// m0 + 16 * lane).  Four stages rotate in LDS, two K steps per barrier:
+// stage s is copied two to four steps ahead, read into registers during step
+// s - 1 and multiplied in step s, so a wave's products never wait for LDS
+// after a barrier; the reads of the next step are pinned between the
+// products (one read per two MFMAs) so that the compiler cannot sink them
+// next to their use again.  The copies are issued
+// by inline asm with wave-uniform bases in SGPRs (one lane-offset VGPR for
+// all of them) so that the compiler, which would otherwise make every LDS
+// read wait for all outstanding copies, leaves their completion to the
+// explicit vmcnt waits below.  Work-groups are dispatched
 // round-robin over the 8 XCDs; XCD x takes a contiguous range of tiles, taken
 // in groups of 8 row tiles so that co-resident work-groups share operand
 // blocks in its L2.
@@ -957,8 +963,9 @@ constexpr int kPfGroupM = 8;
 constexpr int kPfHStride = kPfBN / 2 + 4;  // fp32 per staged h row (padded: no bank conflicts)
 constexpr int kPfLds = kPfStages * kPfStage > kPfBM * kPfHStride * 4 ? kPfStages * kPfStage : kPfBM * kPfHStride * 4;
 
-__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+// 16 bytes per lane from base + voff to LDS at lds + 16 * lane (base wave-uniform)
+__device__ __forceinline__ void lds_dma16(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "s"(lds) : "memory", "m0");
 }
 
 template <bool SWIGLU>
@@ -973,63 +980,92 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
   const int grp = tile / (kPfGroupM * tiles_n), in = tile % (kPfGroupM * tiles_n);
   const int gm = min(kPfGroupM, tiles_m - grp * kPfGroupM);
   const int m0 = (grp * kPfGroupM + in % gm) * kPfBM, n0 = (in / gm) * kPfBN;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave >> 2, wn = wave & 3;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
   const int iters = nt * S;  // K32 steps over all terms
   // wave w copies row blocks w, w + 8 and column blocks w, w + 8 of each stage;
   // blocks past the matrix are clamped (their products are never stored)
-  const uint4* xa[2];
-  const uint4* wb[2];
+  const uint4* xs[2];
+  const uint4* ws[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    xa[h] = (const uint4*)a.X + (size_t)min((m0 >> 4) + h * 8 + wave, a.MBn - 1) * 64 + lane;
+    xs[h] = (const uint4*)a.X + (size_t)min((m0 >> 4) + h * 8 + wave, a.MBn - 1) * 64;
     const int cb = (n0 >> 4) + h * 8 + wave;
-    wb[h] = (const uint4*)a.W + (size_t)min(cb >> 2, t64 - 1) * S * 256 + (cb & 3) * 64 + lane;
+    ws[h] = (const uint4*)a.W + (size_t)min(cb >> 2, t64 - 1) * S * 256 + (cb & 3) * 64;
   }
   const size_t xstep = (size_t)a.MBn * 64;
+  const uint32_t voff = lane * 16;
   const uint32_t lds_base =
       __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(__attribute__((address_space(3))) void*)(smem + wave * 1024));
   auto issue = [&](int it) {
     const int q = it / S, ks = it - q * S;
     const uint32_t d = lds_base + (it % kPfStages) * kPfStage;
-    lds_dma16(xa[0] + ((size_t)q * S + ks) * xstep, d);
-    lds_dma16(xa[1] + ((size_t)q * S + ks) * xstep, d + 8 * 1024);
-    lds_dma16(wb[0] + (size_t)ks * 256, d + 16 * 1024);
-    lds_dma16(wb[1] + (size_t)ks * 256, d + 24 * 1024);
+    lds_dma16(xs[0] + ((size_t)q * S + ks) * xstep, voff, d);
+    lds_dma16(xs[1] + ((size_t)q * S + ks) * xstep, voff, d + 8 * 1024);
+    lds_dma16(ws[0] + (size_t)ks * 256, voff, d + 16 * 1024);
+    lds_dma16(ws[1] + (size_t)ks * 256, voff, d + 24 * 1024);
   };
   f32x4 acc[8][4];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
   for (int p = 0; p < kPfStages - 1; ++p) issue(min(p, iters - 1));
   // SwiGLU: the RMSNorm scales of the tile's input rows, read while the
-  // first stages are in flight (the compiler's wait for these loads also
-  // covers the copies, which the first iteration waits for anyway)
+  // first stages are in flight
   __shared__ float rscale[SWIGLU ? kPfBM : 1];
   if constexpr (SWIGLU)
     for (int r = threadIdx.x; r < kPfBM; r += kThreads)
       rscale[r] = m0 + r < a.M ? row_scale(a.ss, a.ss_stride, m0 + r, a.K, a.eps) : 0.f;
-  for (int it = 0; it < iters; ++it) {
-    // this wave's copies of stage `it` are the oldest 4 of its 4 * (stages - 1)
-    // outstanding ones; its LDS reads of stage it - 1 are complete.  After the
-    // barrier every wave's part of stage `it` is in LDS and stage it - 1's
-    // buffer is free for stage it + 3 (past the end the last stage is copied
-    // again into a buffer nothing reads).
-    __builtin_amdgcn_s_waitcnt((4 * (kPfStages - 2)) | (0x7 << 4) | (0x0 << 8));
-    __builtin_amdgcn_s_barrier();
-    issue(min(it + kPfStages - 1, iters - 1));
+  // operands of one step: 8 row blocks of X, 4 column blocks of W
+  uint4 pa[8], pb[4], qa[8], qb[4];
+  auto read = [&](int it, uint4* A, uint4* B) {
     const uint4* st = (const uint4*)(smem + (it % kPfStages) * kPfStage);
-    uint4 af[8], bfr[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) af[i] = st[(wm * 8 + i) * 64 + lane];
+    for (int i = 0; i < 8; ++i) A[i] = st[(wm * 8 + i) * 64 + lane];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bfr[j] = st[(16 + wn * 4 + j) * 64 + lane];
+    for (int j = 0; j < 4; ++j) B[j] = st[(16 + wn * 4 + j) * 64 + lane];
+  };
+  auto mma = [&](const uint4* A, const uint4* B) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(af[i]), as_bf16x8(bfr[j]), acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A[i]), as_bf16x8(B[j]), acc[i][j], 0, 0, 0);
+  };
+  // the products of one step with the reads of the next pinned between them
+#define VIA_PF_PIN                                                                     \
+  _Pragma("unroll") for (int g = 0; g < 12; ++g) {                                     \
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0); /* 2 MFMAs */                   \
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* 1 LDS read */                \
+  }                                                                                    \
+  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  // stage 0 in LDS (the oldest 4 of 12 copies) and in registers
+  __builtin_amdgcn_s_waitcnt((4 * (kPfStages - 2)) | (0x7 << 4) | (0xF << 8));
+  __builtin_amdgcn_s_barrier();
+  read(0, pa, pb);
+  // two steps per barrier, it and it + 1, with the register sets swapped: at
+  // the barrier every copy has landed (stages it + 1 and it + 2 are read in
+  // this trip) and every wave's reads of stages it - 1 and it are back
+  // (lgkmcnt 0), so their buffers take stages it + 3 and it + 4 (past the end
+  // the last stage is copied again into a buffer nothing reads).  One exit
+  // only: an exit between the halves makes the compiler spill.
+  int it = 0;
+  for (; it + 1 < iters; it += 2) {
+    __builtin_amdgcn_s_waitcnt(0x0 | (0x7 << 4) | (0x0 << 8));
+    __builtin_amdgcn_s_barrier();
+    issue(min(it + 3, iters - 1));
+    issue(min(it + 4, iters - 1));
+    read(min(it + 1, iters - 1), qa, qb);
+    mma(pa, pb);
+    VIA_PF_PIN
+    read(min(it + 2, iters - 1), pa, pb);
+    mma(qa, qb);
+    VIA_PF_PIN
   }
+#undef VIA_PF_PIN
+  if (it < iters) mma(pa, pb);  // odd step count: the last stage is in pa, pb
   __builtin_amdgcn_s_waitcnt(0);  // the trailing copies land before the work-group ends
   const int n = lane & 15, g = lane >> 4;
   if constexpr (SWIGLU) {
