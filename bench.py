@@ -595,9 +595,11 @@ def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None):
     at 2048 tokens) cached in both caches, full model then slim route, all
     sequences in one forward per cache (via_prefill_batch), and for
     comparison one via_prefill call per sequence.
-    Algorithmic FLOPs = 2 * (parameters of the layers run) * rows for the
-    projections, counted once, plus the causal attention products (QK^T and
-    PV, 4 * rows^2 / 2 * H * hd per layer); the product computes the
+    Algorithmic FLOPs = 2 * (parameters of the distinct layers run) * rows
+    for the projections, counted once, plus the causal attention products
+    (QK^T and PV, 4 * rows^2 / 2 * H * hd per layer).  The slim route's
+    leading layers that are the full model's own (route[i] == i) compute the
+    same values in both caches and count once.  The product computes the
     projections in 2 or 3 passes of bf16 terms (its fp32-activation
     contract), which is cost, not work."""
     import torch
@@ -634,12 +636,17 @@ def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None):
     kv.close()
     d, H, KVH, hd, F = md["d_model"], md["n_heads"], md["n_kv_heads"], md["head_dim"], md["d_ffn"]
     per_layer = d * (H + 2 * KVH) * hd + H * hd * d + 3 * F * d
-    layers = md["n_layers"] + len(cfg["route"])
+    route = list(cfg["route"])
+    n_shared = 0
+    while n_shared < len(route) and route[n_shared] == n_shared:
+        n_shared += 1
+    layers = md["n_layers"] + len(route) - n_shared
     gemm_flop = 2.0 * per_layer * n * layers * B
     attn_flop = 2.0 * n * n * H * hd * layers * B   # causal half of 4 * n^2 * H * hd
     tf = (gemm_flop + attn_flop) / (ms * 1e-3) / 1e12
     return {"what": "via_prefill_batch of the workload's prompts (full model and slim route, all sequences in "
-                    "one forward per cache)", "sequences": B,
+                    "one forward per cache; the slim route's shared leading layers run once)", "sequences": B,
+            "distinct_layers": layers,
             "tokens_per_sequence": n, "ms": round(ms, 2), "algorithmic_TFLOP": round((gemm_flop + attn_flop) / 1e12, 2),
             "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),

@@ -285,8 +285,12 @@ via_status via_kv_seq_reserve(via_kv *kv, int32_t seq_id, int32_t n_ctx);
  * not discuss the cache itself, so both verifiers keeping their own cache of
  * that prefix is this library's reading.  Forwards of more than 512 rows run
  * on the compute-bound tile GEMM; longer prompts are fed in chunks of the
- * handle's max_rows.  ENOMEM (nothing attached) when either pool lacks the
- * blocks. */
+ * handle's max_rows.  When the slim route starts with the full model's own
+ * leading layers (route[i] == i for i < P, 0 < P < route length), those
+ * layers run once: each chunk's slim forward starts at route index P from
+ * the full forward's residual stream, and the K/V of layers 0..P-1 are
+ * copied from the full cache (the values the slim forward would compute).
+ * ENOMEM (nothing attached) when either pool lacks the blocks. */
 via_status via_prefill(via_model *m, via_kv *kv, int32_t seq_id, const int32_t *tokens, int32_t n,
                        void *stream);
 /* via_prefill for several sequences at once: sequence seq_ids[i] caches

@@ -311,6 +311,16 @@ void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0
   push_items(P, si, G);
 }
 
+void build_prefill_xfer(const KvBook& bk, const std::vector<int>& seq_of, Plan& P) {
+  P.xfer.clear();
+  for (size_t m = 0; m < P.rows.size(); ++m) {
+    const RowInfo& r = P.rows[m];
+    const SeqSt& S = bk.seqs[seq_of[r.seq]];
+    P.xfer.push_back(PrefixXfer{(int32_t)m, r.slot % kBlock, S.table[VIA_CACHE_FULL][r.slot / kBlock],
+                                S.table[VIA_CACHE_SLIM][r.slot / kBlock]});
+  }
+}
+
 via_status plan_commit(const KvBook& bk, const WinCopy& w, const std::vector<int>& step_n, const int32_t* hp,
                        int vocab, CommitMoves& cm) {
   const int B = w.batch, Dd = std::max(1, w.max_drafts);

@@ -107,6 +107,11 @@ bool build_prefix_xfer(const KvBook& bk, const WinCopy& w, const std::vector<int
 // = slots; the sequence's rows, table and attention items follow those
 // already in P).
 void build_prefill_plan(const SeqSt& S, int cache, const int32_t* tokens, int c0, int c1, int G, Plan& P);
+// Row map of a prefill's slim forward (plan P, whose plan-sequence i is
+// sequence id seq_of[i]) that starts after the shared layers from its full
+// forward over the same rows: row m takes the full forward's state row m and
+// the full and slim pages of its slot.
+void build_prefill_xfer(const KvBook& bk, const std::vector<int>& seq_of, Plan& P);
 
 // Commit of an open step from the host copy of a decision (the packed block
 // of include/via.h).  Validation (nothing changes on error): no status 1,

@@ -91,15 +91,17 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
 struct PrefixArgs {
   const PrefixXfer* xfer;  // [M]
   int M, P, d, KVH, hd;
-  const float* xstate;     // state ring [rows][d]: residual streams after layer P - 1
-  float* X;                // the full forward's residual stream [M, d]
-  const void* slim_pool;
-  int slim_blocks;
-  void* full_pool;
-  int full_blocks;
+  const float* xstate;     // [rows][d]: residual streams after layer P - 1
+  float* X;                // the forward's residual stream [M, d]
+  const void* src_pool;    // K/V of layers 0..P-1 are read here ...
+  int src_blocks;
+  void* dst_pool;          // ... and written here
+  int dst_blocks;
 };
-// K/V of layers 0..P-1 copied slim -> full cache at every row's position and
-// X[m] = xstate[xfer[m].src_row].
+// K/V of layers 0..P-1 copied src -> dst cache at every row's position and
+// X[m] = xstate[xfer[m].src_row] (a verify step's full forward: slim -> full
+// from the state ring; a prefill's slim forward: full -> slim from the full
+// forward's saved rows).
 void launch_prefix_copy(bool bf16, const PrefixArgs& a, hipStream_t s);
 
 // DIMR routing cost per row (Eq. 11): q = full verifier logits, p = routed

@@ -797,12 +797,15 @@ void launch_kv_moves(bool bf16, void* pool, int pool_blocks, int n_slots, int KV
 
 namespace {
 
-// Full forward that starts after the layers it shares with the slim route
-// (route layer i == i for i < a.P): grid (M, P + 1).  y < P: the row's K and
-// V of layer y, copied from the slim cache (slot y) to the full cache (slot
-// y) at the row's position; y == P: the row's residual stream after layer
-// P - 1, taken from the state ring (saved there by the slim forward that fed
-// the slot: this step's for window rows, an earlier one for lag rows).
+// Forward that starts after the layers the two routes share (route layer
+// i == i for i < a.P): grid (M, P + 1).  y < P: the row's K and V of layer
+// y, copied from the source cache (slot y) to the destination cache (slot y)
+// at the row's position; y == P: the row's residual stream after layer
+// P - 1.  A verify step's full forward copies slim -> full and takes the
+// state from the state ring (saved there by the slim forward that fed the
+// slot: this step's for window rows, an earlier one for lag rows); a
+// prefill's slim forward copies full -> slim and takes the state its full
+// forward saved for the same rows.
 template <typename T>
 __global__ __launch_bounds__(256) void prefix_copy_kernel(PrefixArgs a) {
   const int m = blockIdx.x, y = blockIdx.y;
@@ -813,17 +816,17 @@ __global__ __launch_bounds__(256) void prefix_copy_kernel(PrefixArgs a) {
     for (int i = threadIdx.x; i < a.d; i += 256) dst[i] = src[i];
     return;
   }
-  const T* sp = (const T*)a.slim_pool;
-  T* dp = (T*)a.full_pool;
+  const T* sp = (const T*)a.src_pool;
+  T* dp = (T*)a.dst_pool;
   const int n = a.KVH * a.hd;
   for (int e = threadIdx.x; e < 2 * n; e += 256) {
     const int g = (e % n) / a.hd, i = e % a.hd;
     if (e < n)
-      dp[k_off(y, x.dst_blk, a.full_blocks, a.KVH, a.hd, g, x.t, i)] =
-          sp[k_off(y, x.src_blk, a.slim_blocks, a.KVH, a.hd, g, x.t, i)];
+      dp[k_off(y, x.dst_blk, a.dst_blocks, a.KVH, a.hd, g, x.t, i)] =
+          sp[k_off(y, x.src_blk, a.src_blocks, a.KVH, a.hd, g, x.t, i)];
     else
-      dp[v_off(y, x.dst_blk, a.full_blocks, a.KVH, a.hd, g, x.t, i)] =
-          sp[v_off(y, x.src_blk, a.slim_blocks, a.KVH, a.hd, g, x.t, i)];
+      dp[v_off(y, x.dst_blk, a.dst_blocks, a.KVH, a.hd, g, x.t, i)] =
+          sp[v_off(y, x.src_blk, a.src_blocks, a.KVH, a.hd, g, x.t, i)];
   }
 }
 

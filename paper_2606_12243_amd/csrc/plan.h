@@ -70,9 +70,9 @@ struct StepSeq {
 // One row of a full forward that starts after the P layers the slim route
 // shares with it (route layer i == i for i < P).
 struct PrefixXfer {
-  int32_t src_row;           // state-store row of (sequence, slot)
+  int32_t src_row;           // state row of (sequence, slot)
   int32_t t;                 // slot within the page (position % 16)
-  int32_t src_blk, dst_blk;  // page of the position in the slim and the full cache
+  int32_t src_blk, dst_blk;  // page of the position in the source and the destination cache
 };
 
 // Tree compaction: copy K/V of slot src -> dst for every layer slot.

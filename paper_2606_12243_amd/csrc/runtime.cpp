@@ -277,12 +277,17 @@ int shared_prefix(const via_model* m) {
   return n;
 }
 
-// start_si > 0: the forward begins at route position start_si from the
-// slim forward's saved state (P.xfer gives each row's source and pages);
-// save_prefix: store the residual stream after the shared layers (slim
-// forwards of a step).
+// start_si > 0: the forward begins at route position start_si (the shared
+// layers) from a saved state, with the shared layers' K/V copied from the
+// other cache (P.xfer gives each row's source and pages): a step's full
+// forward from the slim forward's state ring, a prefill's slim forward from
+// its full forward's rows.  save_prefix: store the residual stream after
+// the shared layers in the state ring (slim forwards of a step);
+// save_rows: store it per row in the head-input region (full forwards of a
+// prefill, which run no head).
 via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head, const via_verify_out* out,
-                        float inv_T, hipStream_t s, int start_si = 0, bool save_prefix = false) {
+                        float inv_T, hipStream_t s, int start_si = 0, bool save_prefix = false,
+                        bool save_rows = false) {
   const Layout& L = kv->L;
   const Dims& D = m->D;
   const int M = (int)P.rows.size();
@@ -363,9 +368,12 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
   float* ss = (float*)(ws + L.ss);
   const int ss_stride = kv->d.max_rows;
   const int n_shared = shared_prefix(m);
+  if (save_rows && (head || cache != VIA_CACHE_FULL || save_prefix))
+    return fail(VIA_EINVAL, "internal: per-row states are kept by prefill full forwards only");
   if (start_si > 0) {
-    if (start_si != n_shared || (int)P.xfer.size() != M || cache != VIA_CACHE_FULL)
+    if (start_si != n_shared || (int)P.xfer.size() != M || (cache == VIA_CACHE_SLIM && head))
       return fail(VIA_EINVAL, "internal: forward from the shared layers without its row map");
+    const bool from_full = cache == VIA_CACHE_SLIM;  // a prefill's slim forward
     PrefixArgs pa{};
     pa.xfer = (const PrefixXfer*)(plan + o_xfer);
     pa.M = M;
@@ -373,12 +381,12 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
     pa.d = D.d;
     pa.KVH = D.KVH;
     pa.hd = D.hd;
-    pa.xstate = (const float*)(ws + L.xstate);
+    pa.xstate = (const float*)(ws + (from_full ? L.Ylf : L.xstate));
     pa.X = X;
-    pa.slim_pool = kv->d.pool_slim;
-    pa.slim_blocks = kv->d.blocks_slim;
-    pa.full_pool = kv->d.pool_full;
-    pa.full_blocks = kv->d.blocks_full;
+    pa.src_pool = from_full ? kv->d.pool_full : kv->d.pool_slim;
+    pa.src_blocks = from_full ? kv->d.blocks_full : kv->d.blocks_slim;
+    pa.dst_pool = from_full ? kv->d.pool_slim : kv->d.pool_full;
+    pa.dst_blocks = from_full ? kv->d.blocks_slim : kv->d.blocks_full;
     launch_prefix_copy(bf, pa, s);
   }
   // first layer's input norm; from layer 0 it also gathers the embedding rows into X
@@ -450,10 +458,16 @@ via_status exec_forward(via_model* m, via_kv* kv, int cache, Plan& P, bool head,
       timed_gemm(kv, VIA_KERNEL_GATEUP, bf, GemmRole::kGateUp, g, s);
     }
     gemm(Hf, m->w_down[l], D.g_down, GemmRole::kDown, VIA_KERNEL_DOWN);
-    if (si + 1 < route.size())
+    if (si + 1 < route.size()) {
+      // after the shared layers: the state ring (slot per row via d_rows) or
+      // the prefill's per-row copy in the head-input region
+      const bool at_shared = (int)si + 1 == n_shared;
+      float* xcopy = at_shared && save_prefix ? (float*)(ws + L.xstate)
+                     : at_shared && save_rows ? (float*)(ws + L.Ylf)
+                                              : nullptr;
       launch_resid_add(bf, kQkvTerms, X, part, ks(D.g_down), M, D.d, m->attn_norm[route[si + 1]], Yf, MBn, nullptr, ss,
-                       ss_stride, s, save_prefix && (int)si + 1 == n_shared ? (float*)(ws + L.xstate) : nullptr,
-                       nullptr, d_rows);
+                       ss_stride, s, xcopy, nullptr, save_rows ? nullptr : d_rows);
+    }
   }
   if (head && !P.lm.empty()) {
     const int nlm = (int)P.lm.size();
@@ -918,8 +932,42 @@ via_status via_prefill_batch(via_model* m, via_kv* kv, int32_t n_seqs, const int
   }
   hipStream_t s = (hipStream_t)stream;
   const int G = m->D.G;
-  // forwards of up to max_rows rows and max_batch sequences; a sequence's
-  // later chunk goes into a later forward (it attends to the earlier chunk)
+  // With layers shared by both routes (route layer i == i for i < n_shared),
+  // each chunk runs the full forward, which keeps every row's residual
+  // stream after the shared layers, then the slim forward from there with
+  // the shared layers' K/V copied from the full cache: the same values the
+  // slim forward would compute for those layers, without running them twice.
+  const int n_shared = shared_prefix(m);
+  if (n_shared > 0 && n_shared < (int)m->route.size()) {
+    std::vector<int> done(n_seqs, 0);
+    for (;;) {
+      Plan Pf, Ps;
+      std::vector<int> seq_of;
+      int used = 0;
+      for (int i = 0; i < n_seqs && used < kv->d.max_rows && (int)seq_of.size() < kv->d.max_batch; ++i) {
+        if (done[i] >= lens[i]) continue;
+        const int c0 = done[i], c1 = std::min(lens[i], c0 + (kv->d.max_rows - used));
+        build_prefill_plan(kv->bk.seqs[seq_ids[i]], VIA_CACHE_FULL, tokens + off[i], c0, c1, G, Pf);
+        build_prefill_plan(kv->bk.seqs[seq_ids[i]], VIA_CACHE_SLIM, tokens + off[i], c0, c1, G, Ps);
+        seq_of.push_back(seq_ids[i]);
+        used += c1 - c0;
+        done[i] = c1;
+      }
+      if (used == 0) break;
+      build_prefill_xfer(kv->bk, seq_of, Ps);
+      if ((st = exec_forward(m, kv, VIA_CACHE_FULL, Pf, false, nullptr, 1.f, s, 0, false, true)) ||
+          (st = exec_forward(m, kv, VIA_CACHE_SLIM, Ps, false, nullptr, 1.f, s, n_shared))) {
+        detach_all();
+        return st;
+      }
+    }
+    for (int i = 0; i < n_seqs; ++i)
+      for (int cache = 0; cache < 2; ++cache) kv->bk.seqs[seq_ids[i]].valid[cache] = lens[i];
+    return VIA_OK;
+  }
+  // otherwise one pass per cache: forwards of up to max_rows rows and
+  // max_batch sequences; a sequence's later chunk goes into a later forward
+  // (it attends to the earlier chunk)
   for (int cache = 0; cache < 2; ++cache) {
     std::vector<int> done(n_seqs, 0);
     for (;;) {

@@ -671,6 +671,40 @@ static void test_state_ring() {
 // Attention split spans (plan_attention): the cfg3 shape, the one-round
 // widening of a ragged long batch, the cap it must not undo, the split
 // limit and the error for a sequence too long for any span.
+// Prefill row map: the slim forward of a chunk takes row m's state from row m
+// of its full forward and copies K/V between the pages of the same slot.
+static void test_prefill_xfer() {
+  KvBook bk;
+  book_init(bk, 4, 16, 16, 16);
+  bk.seqs[2] = SeqSt();
+  bk.seqs[2].on = true;
+  bk.seqs[0] = SeqSt();
+  bk.seqs[0].on = true;
+  bk.seqs[3] = SeqSt();
+  bk.seqs[3].on = true;
+  // the caches hand out different pages: take one extra full page first
+  CHECK(book_alloc(bk, 0, {{3, 1}}, nullptr) == VIA_OK);
+  for (int cache = 0; cache < 2; ++cache) CHECK(book_alloc(bk, cache, {{2, 37}, {0, 9}}, nullptr) == VIA_OK);
+  const int32_t tok[64] = {0};
+  Plan F, S;
+  // chunk rows [16, 37) of seq 2, then [0, 9) of seq 0
+  build_prefill_plan(bk.seqs[2], VIA_CACHE_FULL, tok, 16, 37, 4, F);
+  build_prefill_plan(bk.seqs[0], VIA_CACHE_FULL, tok, 0, 9, 4, F);
+  build_prefill_plan(bk.seqs[2], VIA_CACHE_SLIM, tok, 16, 37, 4, S);
+  build_prefill_plan(bk.seqs[0], VIA_CACHE_SLIM, tok, 0, 9, 4, S);
+  build_prefill_xfer(bk, {2, 0}, S);
+  CHECK(S.xfer.size() == 30 && S.rows.size() == F.rows.size());
+  for (size_t m = 0; m < S.rows.size(); ++m) {
+    const PrefixXfer& x = S.xfer[m];
+    CHECK(x.src_row == (int)m && F.rows[m].slot == S.rows[m].slot && x.t == S.rows[m].slot % kBlock);
+    CHECK(x.src_blk == F.rows[m].blk && x.dst_blk == S.rows[m].blk);
+  }
+  // first row: seq 2, slot 16 (its second page); last row: seq 0, slot 8
+  CHECK(S.xfer[0].src_blk == bk.seqs[2].table[VIA_CACHE_FULL][1] && S.xfer[0].dst_blk == bk.seqs[2].table[VIA_CACHE_SLIM][1]);
+  CHECK(S.xfer[29].t == 8 && S.xfer[29].dst_blk == bk.seqs[0].table[VIA_CACHE_SLIM][0]);
+  CHECK(S.xfer[0].src_blk != S.xfer[0].dst_blk);
+}
+
 static void test_attention_plan() {
   auto items = [](const std::vector<int>& kv) {
     std::vector<AttnItem> v;
@@ -720,6 +754,7 @@ static void test_attention_plan() {
 }
 
 int main() {
+  test_prefill_xfer();
   test_attention_plan();
   test_step_window_and_tokens();
   test_allocator();
