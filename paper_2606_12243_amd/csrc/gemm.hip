@@ -968,7 +968,7 @@ __device__ __forceinline__ void lds_dma16(const void* base, uint32_t voff, uint3
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "s"(lds) : "memory", "m0");
 }
 
-template <bool SWIGLU>
+template <bool SWIGLU, bool PAIR>
 __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) {
   __shared__ __align__(1024) unsigned char smem[SWIGLU ? kPfLds : kPfStages * kPfStage];
   const int S = a.K >> 5, t64 = (a.N + 63) >> 6;
@@ -982,7 +982,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
   const int m0 = (grp * kPfGroupM + in % gm) * kPfBM, n0 = (in / gm) * kPfBN;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 2, wn = wave & 3;
-  const int iters = nt * S;  // K32 steps over all terms
+  // K32 steps over all terms.  PAIR (two terms): step it is term it % 2 of
+  // K step it / 2, so a K step's two terms run back to back and the second
+  // reuses the first's W operands (no W copy or W read for it); otherwise
+  // term-major, step it is term it / S of K step it % S.
+  const int iters = nt * S;
   // wave w copies row blocks w, w + 8 and column blocks w, w + 8 of each stage;
   // blocks past the matrix are clamped (their products are never stored)
   const uint4* xs[2];
@@ -998,12 +1002,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
   const uint32_t lds_base =
       __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(__attribute__((address_space(3))) void*)(smem + wave * 1024));
   auto issue = [&](int it) {
-    const int q = it / S, ks = it - q * S;
+    const int q = PAIR ? (it & 1) : it / S, ks = PAIR ? it >> 1 : it - q * S;
     const uint32_t d = lds_base + (it % kPfStages) * kPfStage;
     lds_dma16(xs[0] + ((size_t)q * S + ks) * xstep, voff, d);
     lds_dma16(xs[1] + ((size_t)q * S + ks) * xstep, voff, d + 8 * 1024);
-    lds_dma16(ws[0] + (size_t)ks * 256, voff, d + 16 * 1024);
-    lds_dma16(ws[1] + (size_t)ks * 256, voff, d + 24 * 1024);
+    if (!PAIR || q == 0) {
+      lds_dma16(ws[0] + (size_t)ks * 256, voff, d + 16 * 1024);
+      lds_dma16(ws[1] + (size_t)ks * 256, voff, d + 24 * 1024);
+    }
   };
   f32x4 acc[8][4];
 #pragma unroll
@@ -1020,12 +1026,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
       rscale[r] = m0 + r < a.M ? row_scale(a.ss, a.ss_stride, m0 + r, a.K, a.eps) : 0.f;
   // operands of one step: 8 row blocks of X, 4 column blocks of W
   uint4 pa[8], pb[4], qa[8], qb[4];
-  auto read = [&](int it, uint4* A, uint4* B) {
+  auto read = [&](int it, uint4* A, uint4* B) {  // B null: X only
     const uint4* st = (const uint4*)(smem + (it % kPfStages) * kPfStage);
 #pragma unroll
     for (int i = 0; i < 8; ++i) A[i] = st[(wm * 8 + i) * 64 + lane];
+    if (B)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) B[j] = st[(16 + wn * 4 + j) * 64 + lane];
+      for (int j = 0; j < 4; ++j) B[j] = st[(16 + wn * 4 + j) * 64 + lane];
   };
   auto mma = [&](const uint4* A, const uint4* B) {
 #pragma unroll
@@ -1034,15 +1041,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A[i]), as_bf16x8(B[j]), acc[i][j], 0, 0, 0);
   };
-  // the products of one step with the reads of the next pinned between them
-#define VIA_PF_PIN                                                                     \
-  _Pragma("unroll") for (int g = 0; g < 12; ++g) {                                     \
+  // the products of one step with the reads of the next (NR of them) pinned
+  // between them
+#define VIA_PF_PIN(NR)                                                                 \
+  _Pragma("unroll") for (int g = 0; g < (NR); ++g) {                                   \
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0); /* 2 MFMAs */                   \
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* 1 LDS read */                \
   }                                                                                    \
-  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-  // stage 0 in LDS (the oldest 4 of 12 copies) and in registers
-  __builtin_amdgcn_s_waitcnt((4 * (kPfStages - 2)) | (0x7 << 4) | (0xF << 8));
+  __builtin_amdgcn_sched_group_barrier(0x008, 32 - 2 * (NR), 0);
+  // stage 0 in LDS (the oldest 4 copies of the 12, PAIR: of 10) and in registers
+  __builtin_amdgcn_s_waitcnt((PAIR ? 6 : 4 * (kPfStages - 2)) | (0x7 << 4) | (0xF << 8));
   __builtin_amdgcn_s_barrier();
   read(0, pa, pb);
   // two steps per barrier, it and it + 1, with the register sets swapped: at
@@ -1057,15 +1065,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
     __builtin_amdgcn_s_barrier();
     issue(min(it + 3, iters - 1));
     issue(min(it + 4, iters - 1));
-    read(min(it + 1, iters - 1), qa, qb);
+    // PAIR: step it + 1 (second term) multiplies its X with step it's W
+    // (pb), and the next K step's W goes to qb, moved to pb afterwards
+    read(min(it + 1, iters - 1), qa, PAIR ? nullptr : qb);
     mma(pa, pb);
-    VIA_PF_PIN
-    read(min(it + 2, iters - 1), pa, pb);
-    mma(qa, qb);
-    VIA_PF_PIN
+    VIA_PF_PIN(PAIR ? 8 : 12)
+    read(min(it + 2, iters - 1), pa, PAIR ? qb : pb);
+    mma(qa, PAIR ? pb : qb);
+    VIA_PF_PIN(12)
+    if constexpr (PAIR)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pb[j] = qb[j];
   }
 #undef VIA_PF_PIN
-  if (it < iters) mma(pa, pb);  // odd step count: the last stage is in pa, pb
+  if (it < iters) mma(pa, pb);  // odd step count (not PAIR): the last stage is in pa, pb
   __builtin_amdgcn_s_waitcnt(0);  // the trailing copies land before the work-group ends
   const int n = lane & 15, g = lane >> 4;
   if constexpr (SWIGLU) {
@@ -1120,10 +1133,14 @@ void launch_prefill(const GemmArgs& a, int nt, bool swiglu, hipStream_t s, hipEv
     else
       hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, s, a, nt);
   };
-  if (swiglu)
-    go(gemm_prefill<true>);
+  if (swiglu && nt == 2)
+    go(gemm_prefill<true, true>);
+  else if (swiglu)
+    go(gemm_prefill<true, false>);
+  else if (nt == 2)
+    go(gemm_prefill<false, true>);
   else
-    go(gemm_prefill<false>);
+    go(gemm_prefill<false, false>);
 }
 
 }  // namespace
