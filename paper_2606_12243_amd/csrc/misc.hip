@@ -142,6 +142,68 @@ __global__ __launch_bounds__(64) void resid_add_kernel(float* X, const float* P,
   put_afrag<BF16, NT>(Y, out, k0, v, d >> 5, MBn);
 }
 
+// Many-row form of the residual update (forwards of more than
+// kPrefillMinRows rows, one partial P, no head rows or embedding gather):
+// a work-group of 64 threads owns one 16-row block of the fragment layout and
+// one kNormChunk of columns.  Thread t takes row t % 16 and, in each of the
+// chunk's K32 steps s, the 8-column group t / 16, so every fragment store of
+// the wave writes one contiguous 1 KB block (the one-row form writes 16 bytes
+// every 256).  The values are those of resid_add_kernel: the 8-column group
+// 4 s + t / 16 is that kernel's thread, and its partial sums of squares are
+// added in that kernel's wave_sum order (three levels within the thread, two
+// across lanes).
+template <int NT>
+__global__ __launch_bounds__(64) void resid_add_rows_kernel(float* X, const float* P, int M, int d, const uint16_t* g,
+                                                            void* Y, int MBn, float* ss, int ss_stride, float* Xcopy) {
+  constexpr int kSteps = kNormChunk / 32;
+  const int chunk = blockIdx.x, t = threadIdx.x, r = t & 15, j = t >> 4;
+  const int m = blockIdx.y * 16 + r;
+  const bool live = m < M;
+  float p[kSteps];
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int k0 = chunk * kNormChunk + st * 32 + j * 8;
+    p[st] = 0.f;
+    if (!live || k0 >= d) continue;
+    float* x = X + (size_t)m * d + k0;
+    const float* a = P + (size_t)m * d + k0;
+    float v[8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float4 u = *(float4*)(x + 4 * h);
+      const float4 b = *(const float4*)(a + 4 * h);
+      u.x = u.x + (0.f + b.x);
+      u.y = u.y + (0.f + b.y);
+      u.z = u.z + (0.f + b.z);
+      u.w = u.w + (0.f + b.w);
+      *(float4*)(x + 4 * h) = u;
+      if (Xcopy) *(float4*)(Xcopy + (size_t)m * d + k0 + 4 * h) = u;
+      v[4 * h + 0] = u.x;
+      v[4 * h + 1] = u.y;
+      v[4 * h + 2] = u.z;
+      v[4 * h + 3] = u.w;
+    }
+    float sq = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sq += v[e] * v[e];
+    p[st] = sq;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] * to_f<uint16_t>(g[k0 + e]);
+    put_afrag<true, NT>(Y, m, k0, v, d >> 5, MBn);
+  }
+  // wave_sum over the one-row form's threads T = 4 s + j: lane xor 32, 16, 8
+  // and 4 pair steps s ^ 8, s ^ 4, s ^ 2, s ^ 1 (this thread), xor 2 and 1
+  // pair groups j ^ 2 and j ^ 1 (lanes t ^ 32 and t ^ 16)
+#pragma unroll
+  for (int o = kSteps / 2; o > 0; o >>= 1)
+#pragma unroll
+    for (int st = 0; st < o; ++st) p[st] = p[st] + p[st + o];
+  float sq = p[0];
+  sq += __shfl_xor(sq, 32, 64);
+  sq += __shfl_xor(sq, 16, 64);
+  if (j == 0 && live) ss[(size_t)chunk * ss_stride + m] = sq;
+}
+
 // Rotate-half RoPE of the pair (j, j + hd/2) of head hh of row m (Q and K
 // heads; V passes through) with the angle's cosine and sine, then the store:
 // Q as bf16 hi/lo terms (fp32 models: fp32), K and V into the row's paged
@@ -440,6 +502,16 @@ void launch_resid_add(bool bf16, int terms, float* X, const float* P, int ksplit
                       void* Y, int MBn, const RowInfo* rows, float* ss, int ss_stride, hipStream_t s, float* Xcopy,
                       const void* E, const RowInfo* erows) {
   const dim3 grid((d + kNormChunk - 1) / kNormChunk, M);
+  if (bf16 && P && ksplit == 1 && !rows && !E && !erows && M > kPrefillMinRows && (terms == 2 || terms == 3)) {
+    const dim3 rgrid((d + kNormChunk - 1) / kNormChunk, (M + 15) / 16);
+    if (terms == 3)
+      hipLaunchKernelGGL(resid_add_rows_kernel<3>, rgrid, dim3(64), 0, s, X, P, M, d, (const uint16_t*)g, Y, MBn, ss,
+                         ss_stride, Xcopy);
+    else
+      hipLaunchKernelGGL(resid_add_rows_kernel<2>, rgrid, dim3(64), 0, s, X, P, M, d, (const uint16_t*)g, Y, MBn, ss,
+                         ss_stride, Xcopy);
+    return;
+  }
   if (!bf16) {
     hipLaunchKernelGGL((resid_add_kernel<float, false, 1, 0>), grid, dim3(64), 0, s, X, P, ksplit, M, d,
                        (const float*)g, Y, MBn, rows, ss, ss_stride, Xcopy, (const float*)E, erows);
