@@ -11,7 +11,9 @@
 // multiple of 32 the host picks so that the whole launch has about 192
 // work-groups, or more when that would take spans well past 4096 keys); a work-group streams its span and writes
 // one (max, sum, output) partial per query, and a combine kernel merges the
-// partials of a query in split order.  Visibility of slot p for row r:
+// partials of a query in split order.  When every item has one split (long
+// forwards: prefills), the work-group applies the combine's arithmetic to its
+// one partial and writes the output itself, and no combine runs.  Visibility of slot p for row r:
 // p < vis_len[r], or p is a window slot whose bit is set in the row's tree
 // mask.
 //
@@ -281,7 +283,39 @@ __global__ __launch_bounds__(256, 2) void attn_split_kernel(AttnArgs a) {
   __syncthreads();
   if (wave == 1) store_to(0);
   __syncthreads();
-  if (wave == 0) {
+  if (wave == 0 && a.direct) {
+    // one split: the combine's arithmetic for a single partial (weight
+    // exp2(max - max), sum and outputs accumulated from zero, then scaled by
+    // 1 / sum), written as activation fragments here.  The 8 dims of a
+    // fragment group are split over lanes l and l ^ 32: lane half 0 writes
+    // group 2p of each pair of groups, half 1 group 2p + 1.
+    merge_from(0);
+    const float w = __builtin_amdgcn_exp2f(mx - mx);
+    float L = 0.f;
+    L += lt * w;
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        float v[8];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float own0 = o[dt][8 * p + c], own1 = o[dt][8 * p + 4 + c];
+          const float recv = __shfl_xor(half ? own0 : own1, 32, 64);
+          v[c] = half ? recv : own0;
+          v[4 + c] = half ? own1 : recv;
+        }
+        float O[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          O[e] = 0.f;
+          O[e] += v[e] * w;
+          O[e] *= inv;
+        }
+        if (qs.valid) put_afrag<true, 2>(a.out, qs.row, qs.head * HD + dt * 32 + (2 * p + half) * 8, O, (a.H * HD) >> 5, a.MBn);
+      }
+  } else if (wave == 0) {
     merge_from(0);
     if (qs.valid) {
       // O^T lane l, register i of d tile dt -> dim dt*32 + (i/4)*8 + (l/32)*4 + i%4
@@ -417,13 +451,17 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s) {
   if (bf16) {
+    AttnArgs b = a;
+    b.direct = a.max_chunks == 1;
     dim3 grid(a.max_chunks, a.KVH, a.n_items);
     if (a.hd == 128) {
-      hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_items * (kAttnQueries / 8), a.KVH), dim3(128), 0, s, a);
+      hipLaunchKernelGGL(attn_split_kernel<128>, grid, dim3(256), 0, s, b);
+      if (!b.direct)
+        hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(a.n_items * (kAttnQueries / 8), a.KVH), dim3(128), 0, s, b);
     } else {
-      hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(a.n_items * (kAttnQueries / 16), a.KVH), dim3(128), 0, s, a);
+      hipLaunchKernelGGL(attn_split_kernel<64>, grid, dim3(256), 0, s, b);
+      if (!b.direct)
+        hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(a.n_items * (kAttnQueries / 16), a.KVH), dim3(128), 0, s, b);
     }
   } else {
     dim3 grid(a.M, a.H);

@@ -155,6 +155,7 @@ struct AttnArgs {
   float* part_ml;          // [split][M][H][2]: max (log2 units), sum
   void* out;               // activation fragments of [M, H * hd] (2 bf16 terms, or fp32)
   int MBn;
+  int direct;              // set by launch_attention: every item has one split, whose work-group writes `out`
 };
 void launch_attention(bool bf16, const AttnArgs& a, hipStream_t s);
 
