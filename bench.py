@@ -333,6 +333,9 @@ def main():
     ap.add_argument("--no-sampling", action="store_true", help="skip the sampling-rules variant")
     ap.add_argument("--no-drafter", action="store_true", help="skip the drafter-model variant")
     ap.add_argument("--no-prefill-gemm", action="store_true", help="skip the prefill GEMM roofline")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="only the batched prefill of the workload's prompts (one warm-up call, one timed call), "
+                         "as one JSON line; for kernel traces of a prefill")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (the reference kernel for HBM counter scaling)")
     args = ap.parse_args()
@@ -364,6 +367,9 @@ def main():
     cfg["_model"] = via.Model(md, W, cfg["route"])
     torch.cuda.synchronize()
     log(f"weights on device in {time.time() - t0:.1f}s")
+    if args.prefill_only:
+        print(json.dumps(prefill_forward_roofline(cfg, W, per_sequence=False)), flush=True)
+        return
     kinds = {"qkv": via.KERNEL_QKV, "attn": via.KERNEL_ATTN, "o": via.KERNEL_O, "gateup": via.KERNEL_GATEUP,
              "down": via.KERNEL_DOWN, "head": via.KERNEL_HEAD, "decide": via.KERNEL_DECIDE}
     DOM = "gateup"
@@ -590,7 +596,7 @@ def prefill_gemm_roofline(md, M, reps=10):
             "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None, "M": M, "shapes": out}
 
 
-def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None):
+def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None, per_sequence=True):
     """Real prefills: the workload's sequences (their context lengths, capped
     at 2048 tokens) cached in both caches, full model then slim route, all
     sequences in one forward per cache (via_prefill_batch), and for
@@ -631,7 +637,7 @@ def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None):
                 sess.release(b)
         return e0.elapsed_time(e1)
 
-    ms_seq = timed(False)
+    ms_seq = timed(False) if per_sequence else None
     ms = timed(True)
     kv.close()
     d, H, KVH, hd, F = md["d_model"], md["n_heads"], md["n_kv_heads"], md["head_dim"], md["d_ffn"]
@@ -650,9 +656,9 @@ def prefill_forward_roofline(cfg, W, n_seq=None, ctx=None):
             "tokens_per_sequence": n, "ms": round(ms, 2), "algorithmic_TFLOP": round((gemm_flop + attn_flop) / 1e12, 2),
             "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
-            "one_sequence_per_call": {"ms": round(ms_seq, 2),
-                                      "frac": round((gemm_flop + attn_flop) / (ms_seq * 1e-3) / 1e12
-                                                    / MFMA_BF16_PEAK_TFLOPS, 4)},
+            "one_sequence_per_call": None if ms_seq is None else {
+                "ms": round(ms_seq, 2),
+                "frac": round((gemm_flop + attn_flop) / (ms_seq * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)},
             "note": "projections run as 2 bf16-term passes of the prefill GEMM (fp32-activation "
                     "contract); the frac counts each product's 2MNK once"}
 
