@@ -1084,19 +1084,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_prefill(GemmArgs a, int nt) 
   if constexpr (SWIGLU) {
     __syncthreads();  // every wave's copies have landed and its stage reads are done
     float* hl = (float*)smem;  // [row][FFN index of the tile]
+    // lane n < 8 of a 16-lane row holds the gate value of FFN index n, lane
+    // n + 8 its up value (rows g * 4 + r).  The pair swaps its four values
+    // with a DPP rotate by 8 within the row (xor 8: no LDS round trip), and
+    // lane n < 8 computes h for rows r = 0, 1, lane n + 8 for rows 2, 3, so
+    // every lane runs the same instructions.
+    const bool lo8 = n < 8;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j) {
+        float other[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float up = __shfl_xor(acc[i][j][r], 8, 64);
-          const int rl = wm * 128 + i * 16 + g * 4 + r;
-          if (n < 8) {
-            const float sc = rscale[rl], gt = acc[i][j][r] * sc, u = up * sc;
-            hl[rl * kPfHStride + wn * 32 + j * 8 + n] = gt / (1.0f + expf(-gt)) * u;
-          }
+        for (int r = 0; r < 4; ++r)
+          other[r] = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(acc[i][j][r]), 0x128, 0xf, 0xf, false));
+#pragma unroll
+        for (int rr = 0; rr < 2; ++rr) {
+          const float gv = lo8 ? acc[i][j][rr] : other[rr + 2];
+          const float uv = lo8 ? other[rr] : acc[i][j][rr + 2];
+          const int rl = wm * 128 + i * 16 + g * 4 + rr + (lo8 ? 0 : 2);
+          const float sc = rscale[rl], gt = gv * sc, u = uv * sc;
+          hl[rl * kPfHStride + wn * 32 + j * 8 + (n & 7)] = gt / (1.0f + expf(-gt)) * u;
         }
+      }
     __syncthreads();
     // consecutive lanes take consecutive rows of one 8-index group: 16 of
     // them write 256 contiguous bytes of a fragment term
