@@ -127,11 +127,11 @@ typedef struct {
   int32_t max_seqs;           /* sequence ids are in [0, max_seqs) */
   int32_t max_blocks_per_seq; /* block-table capacity per sequence */
   int32_t blocks_full, blocks_slim;
-  void *pool_full, *pool_slim; /* device */
+  void *pool_full, *pool_slim; /* device, 16-byte aligned */
   int32_t max_rows;   /* rows per forward (lag + window, summed over batch) */
   int32_t max_batch;  /* sequences per window */
   int32_t max_drafts; /* drafts per sequence per window, 1..VIA_MAX_DRAFTS */
-  void *workspace;    /* device, >= via_workspace_bytes(...) */
+  void *workspace;    /* device, >= via_workspace_bytes(...), 256-byte aligned */
   size_t workspace_bytes;
   void *pinned_staging; /* pinned host, >= via_staging_bytes(...) */
   size_t staging_bytes;

@@ -779,6 +779,8 @@ via_status via_kv_create(via_model* m, const via_kv_desc* d, via_kv** out) {
     return fail(VIA_EINVAL, "KV description sizes out of range");
   if (!d->pool_full || !d->pool_slim || !d->workspace || !d->pinned_staging)
     return fail(VIA_EINVAL, "pools, workspace and staging are required");
+  if ((uintptr_t)d->workspace % kAlign || (uintptr_t)d->pool_full % 16 || (uintptr_t)d->pool_slim % 16)
+    return fail(VIA_EINVAL, "workspace must be %zu-byte and the pools 16-byte aligned", kAlign);
   Layout L = layout_of(&m->d, d->max_rows, d->max_batch, d->max_blocks_per_seq, std::max(1, (int)d->max_drafts),
                        d->max_seqs);
   if (d->workspace_bytes < L.total)

@@ -142,3 +142,23 @@ def test_batched_prefill_is_all_or_nothing():
     finally:
         kv.close()
         gm.close()
+
+
+def test_kv_create_rejects_misaligned_buffers():
+    """The kernels read the workspace and the pools with 16-byte loads: a
+    workspace off its 256-byte alignment or a pool off 16 bytes is refused
+    before anything is allocated."""
+    cfg = configs.get("micro_bf16")
+    gm = via.Model(cfg["model"], gen.model_weights(cfg), cfg["route"])
+    kv = via.KV(gm, max_seqs=2, max_blocks_per_seq=4, blocks_full=8, blocks_slim=8, max_rows=16, max_batch=2,
+                max_drafts=4)
+    try:
+        for field, off in (("workspace", 64), ("pool_full", 8), ("pool_slim", 2)):
+            d = via.KvDesc.from_buffer_copy(kv.cd)
+            setattr(d, field, getattr(kv.cd, field) + off)
+            h = C.c_void_p()
+            assert via.via_kv_create(gm.h, C.byref(d), C.byref(h)) == via.EINVAL, field
+            assert not h.value
+    finally:
+        kv.close()
+        gm.close()
